@@ -1,0 +1,514 @@
+"""Pins of the oracle against what the paper and the mathematics fix.
+
+Nothing here calls the HIP library.  Each test names the passage or the
+mathematical fact it checks; together they are chosen so that a plausible
+mistake in the oracle (a flipped tap index, a wrong sign, a dropped term, a
+missing dilation factor, a transposed operand, a truncating instead of a
+flooring shift) fails at least one of them.
+"""
+import math
+import struct
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2501_14490_amd import workloads
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+def f32_bits(v):
+    return struct.unpack("<I", struct.pack("<f", float(v)))[0]
+
+
+def ulp_diff(a, b):
+    ia, ib = f32_bits(a), f32_bits(b)
+    if ia >> 31:
+        ia = 0x80000000 - (ia & 0x7FFFFFFF)
+    else:
+        ia = ia + 0x80000000
+    if ib >> 31:
+        ib = 0x80000000 - (ib & 0x7FFFFFFF)
+    else:
+        ib = ib + 0x80000000
+    return abs(ia - ib)
+
+
+def small_case(T=11, N=2, C=3, S=2, k=3, seed=0, s_lo=0, s_hi=4, bias_std=0.1):
+    spatial = (S,) if S > 1 else ()
+    return workloads.make_small(T, N, C, spatial, k=k, s_lo=s_lo, s_hi=s_hi, seed=seed,
+                                bias_std=bias_std)
+
+
+def tap_weights(sign, shift):
+    """Real-valued quantized weights W_q = sign * 2^-shift (double)."""
+    return sign.astype(np.float64) * np.ldexp(1.0, -shift.astype(np.int64))
+
+
+def dense_toeplitz(wq_c, T, k, d):
+    """App. A.2, time-first: A[i][j] = W_q[k-1-(i-j)/d] when
+    i - d(k-1) <= j <= i and (i-j) % d == 0, else 0."""
+    A = np.zeros((T, T))
+    for i in range(T):
+        for j in range(T):
+            if i - d * (k - 1) <= j <= i and (i - j) % d == 0:
+                A[i, j] = wq_c[k - 1 - (i - j) // d]
+    return A
+
+
+# ---------------------------------------------------------------------------
+# exp and surrogates (closed forms)
+# ---------------------------------------------------------------------------
+def test_exp_within_two_ulp_of_double_exp(orc):
+    ys = np.concatenate([np.linspace(-86.0, 88.0, 20001), -np.logspace(-8, 1.9, 2001),
+                         np.logspace(-8, 1.9, 2001), [0.0, -0.0, -1.0, 1.0, math.log(2), -math.log(2)]])
+    worst = 0
+    for y in ys.astype(np.float32):
+        got = orc.exp_f32(float(y))
+        ref = np.float32(math.exp(float(y)))
+        worst = max(worst, ulp_diff(got, ref))
+    assert worst <= 2, worst
+    assert orc.exp_f32(0.0) == np.float32(1.0)
+
+
+def test_exp_limits(orc):
+    assert orc.exp_f32(-86.5) == 0.0
+    assert orc.exp_f32(float("nan")) == 0.0
+    assert orc.exp_f32(-86.0) > 0.0 and np.isfinite(orc.exp_f32(88.0))
+    assert orc.exp_f32(1000.0) == orc.exp_f32(88.0)
+
+
+@pytest.mark.parametrize("kind,alpha,peak", [("sigmoid", 4.0, 1.0), ("sigmoid", 2.0, 0.5),
+                                             ("atan", 2.0, 1.0), ("atan", 5.0, 2.5),
+                                             ("rational", 10.0, 1.0)])
+def test_surrogate_peak_and_symmetry(orc, kind, alpha, peak):
+    # sigma'(0) = alpha/4 (sigmoid), alpha/2 (arctan), 1 (rational) exactly.
+    assert orc.surrogate(kind, alpha, 0.0) == np.float32(peak)
+    u = np.linspace(-9, 9, 1801).astype(np.float32)
+    a = orc.surrogate(kind, alpha, u)
+    b = orc.surrogate(kind, alpha, -u)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))  # even, bitwise
+    assert np.all(np.diff(a[900:]) <= 0)  # non-increasing in |u|
+
+
+@pytest.mark.parametrize("kind,alpha", [("sigmoid", 4.0), ("atan", 2.0), ("atan", 5.0), ("rational", 10.0)])
+def test_surrogate_matches_closed_form_in_double(orc, kind, alpha):
+    u = np.linspace(-6, 6, 2401).astype(np.float32)
+    got = orc.surrogate(kind, alpha, u).astype(np.float64)
+    ud = u.astype(np.float64)
+    if kind == "sigmoid":
+        # alpha s(1-s) with s = sigmoid(alpha u), in the cancellation-free form
+        e = np.exp(-alpha * np.abs(ud))
+        ref = alpha * e / (1.0 + e) ** 2
+    elif kind == "atan":
+        ref = alpha / (2.0 * (1.0 + (math.pi / 2 * alpha * ud) ** 2))
+    else:
+        ref = 1.0 / (1.0 + alpha * ud * ud)
+    rel = np.abs(got - ref) / np.maximum(np.abs(ref), 1e-30)
+    assert rel.max() < 1e-6, rel.max()
+
+
+@pytest.mark.parametrize("kind,alpha,L,closed", [
+    ("sigmoid", 4.0, 6.0, lambda a, L: 1 - 2 / (1 + math.exp(a * L))),
+    ("atan", 2.0, 6.0, lambda a, L: 2 / math.pi * math.atan(math.pi / 2 * a * L)),
+])
+def test_surrogate_integral(orc, kind, alpha, L, closed):
+    # the surrogate is the derivative of a smooth step: its integral over
+    # [-L, L] is the closed form and tends to 1.
+    u = np.linspace(-L, L, 120001)
+    v = orc.surrogate(kind, alpha, u.astype(np.float32)).astype(np.float64)
+    integral = np.trapezoid(v, u)
+    assert abs(integral - closed(alpha, L)) < 1e-5
+    assert closed(alpha, L) > 0.9
+
+
+# ---------------------------------------------------------------------------
+# quantizer (Eq. round_w) against exact rational arithmetic
+# ---------------------------------------------------------------------------
+def exact_round_log2(v: float) -> int:
+    q = abs(Fraction(v))
+    m = 0
+    while q >= 2:
+        q /= 2
+        m += 1
+    while q < 1:
+        q *= 2
+        m -= 1
+    # q in [1, 2): round(log2 q) is 1 iff q^2 >= 2
+    return m + (1 if q * q >= 2 else 0)
+
+
+def test_quantizer_matches_fraction(orc):
+    rng = np.random.default_rng(7)
+    w = np.concatenate([rng.standard_normal(4000) * 0.3, rng.standard_normal(500) * 1e-3,
+                        rng.standard_normal(500) * 50]).astype(np.float32)
+    sign, shift = orc.quantize(w, -20, 40)
+    for v, sg, sh in zip(w, sign, shift):
+        assert sg == (-1 if v < 0 else 1)
+        e = exact_round_log2(float(v))
+        assert sh == min(max(-e, -20), 40), (v, sh, e)
+
+
+def test_quantizer_boundaries_near_sqrt2(orc):
+    # the floats adjacent to sqrt(2) * 2^m round to m (below) and m+1 (above);
+    # exact powers of two are fixed points; zero and clamps follow the reading.
+    for m in range(-10, 6):
+        t = np.float32(math.sqrt(2) * 2.0 ** m)
+        below = np.nextafter(t, np.float32(0)) if float(t) > math.sqrt(2) * 2.0 ** m else t
+        above = np.nextafter(below, np.float32(np.inf))
+        assert float(below) < math.sqrt(2) * 2.0 ** m < float(above)
+        s, sh = orc.quantize(np.array([below, above, -above, np.float32(2.0 ** m)]), -64, 64)
+        assert list(sh) == [-m, -(m + 1), -(m + 1), -m]
+        assert list(s) == [1, 1, -1, 1]
+    s, sh = orc.quantize(np.array([0.0, -0.0, 1e-30, 100.0, np.inf, np.nan], np.float32), 0, 7)
+    assert list(s) == [1, 1, 1, 1, 1, 1]
+    assert list(sh) == [7, 7, 7, 0, 0, 7]
+
+
+def test_log2f_rounding_would_be_wrong(orc):
+    # the reading of round(log2|W|) is the exact one: the float log2 of the
+    # float just below 2*sqrt(2) rounds to 1.5 and then to 2, the exact answer is 1.
+    v = np.float32(2.8284270763)
+    assert float(v) < 2 * math.sqrt(2)
+    _, sh = orc.quantize(np.array([v]), -8, 8)
+    assert sh[0] == -1
+
+
+# ---------------------------------------------------------------------------
+# forward: closed forms, textbook routines, dense Toeplitz, invariants
+# ---------------------------------------------------------------------------
+def test_order_one_is_per_channel_scaling(orc):
+    c = small_case(k=1, s_lo=-3, s_hi=6)
+    H, spk = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], 1, 3, 0.25)
+    C = c["x"].shape[2]
+    w = (c["sign"].reshape(C).astype(np.float32) *
+         np.ldexp(np.float32(1), -c["shift"].reshape(C).astype(np.int32)).astype(np.float32))
+    wb = w.reshape(1, 1, C, 1)
+    ref = (c["x"] * wb).astype(np.float32) + c["bias"].reshape(1, 1, C, 1)
+    assert np.array_equal(H, ref.astype(np.float32))
+    assert np.array_equal(spk, (ref >= np.float32(0.25)).astype(np.uint8))
+
+
+def test_shared_taps_undilated_is_sliding_psn_convolution(orc):
+    # Eq. SlidingPSN-charge: H[t] = sum_i W[i] X[t-k+1+i] (X[j<0] = 0) with the
+    # same taps in every channel and d = 1; textbook routine np.convolve.
+    T, N, C, k = 40, 3, 4, 6
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((T, N, C)).astype(np.float32)
+    sign1 = np.where(rng.integers(0, 2, k) == 0, -1, 1).astype(np.int8)
+    shift1 = rng.integers(0, 6, k).astype(np.int8)
+    sign = np.tile(sign1, (C, 1))
+    shift = np.tile(shift1, (C, 1))
+    H, _ = orc.forward_f32(x, sign, shift, np.zeros(C, np.float32), k, 1, 1.0)
+    w = tap_weights(sign1, shift1)
+    for n in range(N):
+        for c in range(C):
+            ref = np.convolve(x[:, n, c].astype(np.float64), w[::-1])[:T]
+            bound = k * 2.0 ** -24 * np.convolve(np.abs(x[:, n, c]).astype(np.float64), np.abs(w[::-1]))[:T]
+            assert np.all(np.abs(H[:, n, c] - ref) <= bound + 1e-30)
+
+
+@pytest.mark.parametrize("d", [1, 2, 3])
+def test_dense_toeplitz_forward_and_transposed_backward(orc, d):
+    # App. A.2: H[c] = A[c] X[c] (time-first) and, being linear, grad_x = A^T dH.
+    k = 4
+    c = small_case(T=17, N=2, C=3, S=2, k=k, seed=11)
+    x, sign, shift, bias = c["x"], c["sign"], c["shift"], c["bias"]
+    T, N, C, S = x.shape
+    H, _ = orc.forward_f32(x, sign, shift, bias, k, d, 0.5)
+    out = orc.backward_f32(x, c["grad_spikes"], sign, shift, bias, k, d, 0.5, "sigmoid", 4.0)
+    assert np.array_equal(out["H"], H)
+    for ch in range(C):
+        A = dense_toeplitz(tap_weights(sign[ch], shift[ch]), T, k, d)
+        Aabs = np.abs(A)
+        for n in range(N):
+            for s in range(S):
+                xv = x[:, n, ch, s].astype(np.float64)
+                ref = A @ xv + float(bias[ch])
+                bound = (k + 1) * 2.0 ** -24 * (Aabs @ np.abs(xv) + abs(float(bias[ch])))
+                assert np.all(np.abs(H[:, n, ch, s] - ref) <= bound)
+                dh = out["dH"][:, n, ch, s].astype(np.float64)
+                gref = A.T @ dh
+                gbound = k * 2.0 ** -24 * (Aabs.T @ np.abs(dh))
+                assert np.all(np.abs(out["grad_x"][:, n, ch, s] - gref) <= gbound + 1e-30)
+
+
+def test_forward_bruteforce_fraction_exact_sum(orc):
+    # exact rational sum of the taps bounds the float result; each term is
+    # exactly sign * x * 2^-shift.
+    k, d = 5, 2
+    c = small_case(T=9, N=1, C=2, S=1, k=k, seed=5, s_lo=-2, s_hi=9)
+    x, sign, shift, bias = c["x"], c["sign"], c["shift"], c["bias"]
+    H, _ = orc.forward_f32(x, sign, shift, bias, k, d, 0.0)
+    T, N, C = x.shape
+    for t in range(T):
+        for ch in range(C):
+            exact = Fraction(0)
+            absum = Fraction(0)
+            for i in range(k):
+                tau = t - (k - 1 - i) * d
+                if tau < 0:
+                    continue
+                term = Fraction(float(x[tau, 0, ch])) * Fraction(2) ** (-int(shift[ch, i]))
+                term = -term if sign[ch, i] < 0 else term
+                exact += term
+                absum += abs(term)
+            exact += Fraction(float(bias[ch]))
+            absum += abs(Fraction(float(bias[ch])))
+            err = abs(Fraction(float(H[t, 0, ch])) - exact)
+            assert err <= (k + 1) * Fraction(1, 2 ** 24) * absum
+
+
+def test_causality_bitwise(orc):
+    c = small_case(T=20, k=4, seed=2)
+    x = c["x"].copy()
+    H0, S0 = orc.forward_f32(x, c["sign"], c["shift"], c["bias"], 4, 2, 0.3)
+    t0 = 9
+    x[t0 + 1:] = np.random.default_rng(1).standard_normal(x[t0 + 1:].shape).astype(np.float32) * 5
+    H1, S1 = orc.forward_f32(x, c["sign"], c["shift"], c["bias"], 4, 2, 0.3)
+    assert np.array_equal(H0[:t0 + 1].view(np.uint32), H1[:t0 + 1].view(np.uint32))
+    assert np.array_equal(S0[:t0 + 1], S1[:t0 + 1])
+    assert not np.array_equal(H0[t0 + 1:], H1[t0 + 1:])
+
+
+@pytest.mark.parametrize("m", [1, 3, 7])
+def test_time_shift_equivariance(orc, m):
+    c = small_case(T=15, k=3, seed=4)
+    x = c["x"]
+    H0, S0 = orc.forward_f32(x, c["sign"], c["shift"], c["bias"], 3, 2, 0.2)
+    xs = np.concatenate([np.zeros((m,) + x.shape[1:], np.float32), x])
+    H1, S1 = orc.forward_f32(xs, c["sign"], c["shift"], c["bias"], 3, 2, 0.2)
+    assert np.array_equal(H1[m:], H0)
+    assert np.array_equal(S1[m:], S0)
+    assert np.array_equal(H1[:m], np.broadcast_to(c["bias"].reshape(1, 1, -1, 1), H1[:m].shape))
+
+
+def test_zero_input_and_zero_gradient(orc):
+    c = small_case(T=10, k=3, seed=6)
+    z = np.zeros_like(c["x"])
+    H, _ = orc.forward_f32(z, c["sign"], c["shift"], c["bias"], 3, 2, 0.5)
+    assert np.array_equal(H, np.broadcast_to(c["bias"].reshape(1, 1, -1, 1), H.shape))
+    out = orc.backward_f32(z, c["grad_spikes"], c["sign"], c["shift"], c["bias"], 3, 2, 0.5)
+    assert np.all(out["grad_w"] == 0)
+    out = orc.backward_f32(c["x"], np.zeros_like(c["x"]), c["sign"], c["shift"], c["bias"], 3, 2, 0.5)
+    assert np.all(out["grad_x"] == 0) and np.all(out["grad_w"] == 0) and np.all(out["grad_b"] == 0)
+
+
+@pytest.mark.parametrize("p", [-3, 1, 5])
+def test_power_of_two_scaling_bitwise(orc, p):
+    c = small_case(T=13, k=4, seed=8)
+    b0 = np.zeros_like(c["bias"])
+    H0, _ = orc.forward_f32(c["x"], c["sign"], c["shift"], b0, 4, 3, 1.0)
+    H1, _ = orc.forward_f32(np.ldexp(c["x"], p).astype(np.float32), c["sign"], c["shift"], b0, 4, 3, 1.0)
+    assert np.array_equal(H1, np.ldexp(H0, p).astype(np.float32))
+
+
+def test_op_count_matches_table_formula(orc):
+    # Table "params and shape": ((T + (1-k)/2) k) SHIFT per neuron at d = 1;
+    # with dilation the omitted (negative-time) taps are sum_i max(0, (k-1-i) d) ... counted directly.
+    for T, k, d in [(32, 16, 1), (20, 5, 1), (9, 9, 1), (30, 4, 3), (7, 3, 4)]:
+        x = np.ones((T, 1, 1), np.float32)
+        _, _, taps = orc.forward_f32(x, np.ones((1, k), np.int8), np.zeros((1, k), np.int8),
+                                     np.zeros(1, np.float32), k, d, 1.0, with_tap_count=True)
+        assert taps == sum(max(0, T - (k - 1 - i) * d) for i in range(k))
+        if d == 1:
+            assert Fraction(taps) == (Fraction(T) + Fraction(1 - k, 2)) * k
+
+
+# ---------------------------------------------------------------------------
+# backward: finite differences of the smoothed loss, adjoint identity
+# ---------------------------------------------------------------------------
+def primitive(kind, alpha, u):
+    """A primitive of the surrogate derivative (a smooth step), in double."""
+    if kind == "sigmoid":
+        return 1.0 / (1.0 + np.exp(-alpha * u))
+    if kind == "atan":
+        return np.arctan(math.pi / 2 * alpha * u) / math.pi + 0.5
+    return np.arctan(math.sqrt(alpha) * u) / math.sqrt(alpha)
+
+
+def smooth_loss(x, g, wq, bias, k, d, v_th, kind, alpha):
+    """L = sum g * sigma(H - v_th) with H the exact (double) charge; its
+    derivative is the surrogate-gradient backward of the neuron."""
+    T = x.shape[0]
+    H = np.zeros(x.shape)
+    for i in range(k):
+        lag = (k - 1 - i) * d
+        if lag >= T:
+            continue
+        w = wq[:, i].reshape(1, 1, -1, 1)
+        H[lag:] += w * x[:T - lag]
+    H += bias.reshape(1, 1, -1, 1)
+    return float(np.sum(g * primitive(kind, alpha, H - v_th)))
+
+
+@pytest.mark.parametrize("kind,alpha,d", [("sigmoid", 4.0, 2), ("atan", 2.0, 3), ("rational", 10.0, 1)])
+def test_backward_matches_finite_differences(orc, kind, alpha, d):
+    k = 3
+    c = small_case(T=12, N=2, C=3, S=2, k=k, seed=21)
+    x = c["x"].astype(np.float64)
+    g = c["grad_spikes"].astype(np.float64)
+    wq = tap_weights(c["sign"], c["shift"])
+    b = c["bias"].astype(np.float64)
+    v_th = 0.3
+    out = orc.backward_f32(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, v_th, kind, alpha)
+    h = 1e-6
+
+    def L(xx=x, ww=wq, bb=b):
+        return smooth_loss(xx, g, ww, bb, k, d, v_th, kind, alpha)
+
+    scale_w = np.abs(out["grad_w"]).max()
+    for ch in range(wq.shape[0]):
+        for i in range(k):
+            wp, wm = wq.copy(), wq.copy()
+            wp[ch, i] += h
+            wm[ch, i] -= h
+            fd = (L(ww=wp) - L(ww=wm)) / (2 * h)
+            assert abs(fd - out["grad_w"][ch, i]) <= 2e-4 * scale_w + 1e-6, (ch, i, fd, out["grad_w"][ch, i])
+        bp, bm = b.copy(), b.copy()
+        bp[ch] += h
+        bm[ch] -= h
+        fd = (L(bb=bp) - L(bb=bm)) / (2 * h)
+        assert abs(fd - out["grad_b"][ch]) <= 2e-4 * np.abs(out["grad_b"]).max() + 1e-6
+    rng = np.random.default_rng(0)
+    scale_x = np.abs(out["grad_x"]).max()
+    for _ in range(40):
+        idx = tuple(int(rng.integers(0, s)) for s in x.shape)
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (L(xx=xp) - L(xx=xm)) / (2 * h)
+        assert abs(fd - out["grad_x"][idx]) <= 2e-4 * scale_x + 1e-6, (idx, fd, out["grad_x"][idx])
+
+
+def test_grad_w_exact_in_double_against_fraction(orc):
+    # grad_w sums products of two floats, each exact in double; the double sum
+    # of a few hundred terms is within n*eps of the exact rational sum.
+    k, d = 3, 2
+    c = small_case(T=10, N=2, C=2, S=3, k=k, seed=9)
+    out = orc.backward_f32(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, 0.4)
+    x, dH = c["x"], out["dH"]
+    T = x.shape[0]
+    for ch in range(2):
+        for i in range(k):
+            lag = (k - 1 - i) * d
+            exact = Fraction(0)
+            ab = Fraction(0)
+            for t in range(lag, T):
+                for n in range(2):
+                    for s in range(3):
+                        p = Fraction(float(x[t - lag, n, ch, s])) * Fraction(float(dH[t, n, ch, s]))
+                        exact += p
+                        ab += abs(p)
+            assert abs(Fraction(out["grad_w"][ch, i]) - exact) <= 64 * Fraction(1, 2 ** 53) * ab
+        gb = sum(Fraction(float(v)) for v in dH[:, :, ch, :].ravel())
+        assert abs(Fraction(out["grad_b"][ch]) - gb) <= Fraction(1, 2 ** 40)
+
+
+def test_adjoint_identity(orc):
+    # <A x, y> = <x, A^T y> for the charge operator without bias, in double.
+    k, d = 4, 2
+    c = small_case(T=16, k=k, seed=13)
+    zero_b = np.zeros_like(c["bias"])
+    y = np.random.default_rng(5).standard_normal(c["x"].shape).astype(np.float32)
+    H, _ = orc.forward_f32(c["x"], c["sign"], c["shift"], zero_b, k, d, 0.0)
+    # grad_x of the rational surrogate with alpha = 0 has sigma' = 1, so dH = g
+    out = orc.backward_f32(c["x"], y, c["sign"], c["shift"], zero_b, k, d, 0.0, "rational", 0.0)
+    assert np.array_equal(out["dH"], y)
+    lhs = float(np.sum(H.astype(np.float64) * y))
+    rhs = float(np.sum(c["x"].astype(np.float64) * out["grad_x"]))
+    assert abs(lhs - rhs) <= 1e-5 * (np.abs(H).sum() * np.abs(y).max())
+
+
+# ---------------------------------------------------------------------------
+# Q8.8 fixed point
+# ---------------------------------------------------------------------------
+def test_q88_forward_bruteforce_python_ints(orc):
+    # Python's >> on ints is the arithmetic (flooring) shift.
+    k, d = 4, 3
+    c = workloads.make_small(14, 2, 3, (2,), k=k, s_lo=0, s_hi=9, dtype="q8_8", seed=17)
+    x, sign, shift, bias = c["x"], c["sign"], c["shift"], c["bias"]
+    H, spk = orc.forward_q88(x, sign, shift, bias, k, d, 256)
+    T, N, C, S = x.shape
+    for t in range(T):
+        for n in range(N):
+            for ch in range(C):
+                for s in range(S):
+                    acc = int(bias[ch])
+                    for i in range(k):
+                        tau = t - (k - 1 - i) * d
+                        if tau >= 0:
+                            y = int(x[tau, n, ch, s]) >> int(shift[ch, i])
+                            acc += -y if sign[ch, i] < 0 else y
+                    assert H[t, n, ch, s] == acc
+                    assert spk[t, n, ch, s] == (1 if acc >= 256 else 0)
+
+
+def test_q88_backward_bruteforce_python_ints(orc):
+    k, d = 3, 2
+    c = workloads.make_small(12, 2, 2, (3,), k=k, s_lo=0, s_hi=7, dtype="q8_8", seed=19)
+    x, g, sign, shift, bias = c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"]
+    out = orc.backward_q88(x, g, sign, shift, bias, k, d, 256, "sigmoid", 4.0)
+    H, dH = out["H"], out["dH"]
+    T, N, C, S = x.shape
+    L = orc.surrogate_q15("sigmoid", 4.0, (H - 256).ravel()).reshape(H.shape)
+    ref_dH = (g.astype(object) * L.astype(object))
+    ref_dH = np.vectorize(lambda v: int(v) >> 15)(ref_dH)
+    assert np.array_equal(dH, ref_dH.astype(np.int32))
+    for ch in range(C):
+        for i in range(k):
+            lag = (k - 1 - i) * d
+            s = sum(int(x[t - lag, n, ch, sp]) * int(dH[t, n, ch, sp])
+                    for t in range(lag, T) for n in range(N) for sp in range(S))
+            assert out["grad_w"][ch, i] == s
+        assert out["grad_b"][ch] == int(dH[:, :, ch, :].astype(np.int64).sum())
+    for t in range(T):
+        for n in range(N):
+            for ch in range(C):
+                for sp in range(S):
+                    acc = 0
+                    for i in range(k):
+                        tau = t + (k - 1 - i) * d
+                        if tau < T:
+                            y = int(dH[tau, n, ch, sp]) >> int(shift[ch, i])
+                            acc += -y if sign[ch, i] < 0 else y
+                    assert out["grad_x"][t, n, ch, sp] == acc
+
+
+def test_q88_surrogate_factor(orc):
+    # L(0) = 2^15 * alpha/4 for the sigmoid, symmetric, and the float value it rounds.
+    assert orc.surrogate_q15("sigmoid", 4.0, 0) == 32768
+    u = np.arange(-3000, 3001)
+    Lq = orc.surrogate_q15("sigmoid", 4.0, u)
+    assert np.array_equal(Lq, Lq[::-1])
+    ref = np.rint(orc.surrogate("sigmoid", 4.0, (u / 256.0).astype(np.float32)) * 32768.0)
+    assert np.array_equal(Lq, ref.astype(np.int32))
+
+
+def test_q88_matches_float_path_when_shifts_are_exact(orc):
+    # for inputs that are multiples of 2^s_max the floor shift is exact, so the
+    # Q8.8 potential equals 256 times the float potential (cross-path invariant).
+    k, d, s_hi = 4, 2, 5
+    c = workloads.make_small(16, 2, 3, (), k=k, s_lo=0, s_hi=s_hi, dtype="q8_8", seed=23)
+    xq = ((c["x"].astype(np.int32) >> s_hi) << s_hi).astype(np.int16)
+    bq = (c["bias"] >> 0).astype(np.int32)
+    Hq, _ = orc.forward_q88(xq, c["sign"], c["shift"], bq, k, d, 256)
+    xf = (xq.astype(np.float32) / np.float32(256))
+    Hf, _ = orc.forward_f32(xf, c["sign"], c["shift"], (bq / 256).astype(np.float32), k, d, 1.0)
+    assert np.array_equal(Hq.astype(np.float64), Hf.astype(np.float64) * 256)
+
+
+# ---------------------------------------------------------------------------
+# bf16 storage
+# ---------------------------------------------------------------------------
+def test_bf16_rounding_matches_torch(orc):
+    import torch
+    rng = np.random.default_rng(1)
+    a = np.concatenate([rng.standard_normal(3000).astype(np.float32),
+                        np.array([0.0, -0.0, 1e-40, 3.4e38, -3.4e38, np.inf, -np.inf], np.float32)])
+    ref = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(orc.f32_to_bf16_bits(a), ref)
+    assert np.array_equal(orc.f32_to_bf16_bits_vec(a), ref)
+    assert np.array_equal(orc.bf16_bits_to_f32(ref), torch.from_numpy(ref.view(np.int16)).view(
+        torch.bfloat16).float().numpy())
