@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of the mul-free channel-wise PSN training step on one MI355X.
+
+A step is one training pass of a sawtooth stack of P neuron layers over one
+batch: the forward of every layer (dilations d = 1..P in layer order), then
+the backward of every layer in reverse order, as autograd would run them.
+Each layer reads its own x and grad_spikes tensors (the batch rolled along N),
+so no layer finds another layer's inputs in cache.  Inputs are resident in
+HBM when the timed region starts.
+
+Prints ONE JSON line on stdout (everything else goes to stderr):
+  value      = P * T*N*C*S / step time   (elements/s, whole job)
+  roofline   = the backward kernel (the dominant one): algorithmic bytes per
+               launch (read x, read grad_spikes, write grad_x) / its average
+               duration from HIP events recorded on the launch stream inside
+               the timed region, against 8 TB/s
+  cpu_baseline = the oracle (single-threaded C) timed on this host on a
+               channel slice of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def alg_bytes(wl):
+    """Algorithmic HBM bytes per element (forward, backward)."""
+    es = {"f32": 4, "bf16": 2, "q8_8": 2}[wl.dtype]
+    gxs = {"f32": 4, "bf16": 2, "q8_8": 4}[wl.dtype]
+    return es + 1, es + es + gxs
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("mfpsn_kernels.hip", "mfpsn_api.cpp", "mfpsn_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2501_14490_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(wl_name):
+    """HBM bytes per backward launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "bwd_traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(wl_name)
+    if not ent or ent.get("kernel_source") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, case, channels: int):
+    import oracle
+
+    oracle.build()
+    sub = {n: (np.ascontiguousarray(v[:, :, :channels]) if n in ("x", "grad_spikes") else v[:channels])
+           for n, v in case.items()}
+    t0 = time.perf_counter()
+    for d in wl.dilations:
+        if wl.dtype == "q8_8":
+            oracle.forward_q88(sub["x"], sub["sign"], sub["shift"], sub["bias"], wl.k, d, wl.v_th_q, 0, wl.s_max)
+            oracle.backward_q88(sub["x"], sub["grad_spikes"], sub["sign"], sub["shift"], sub["bias"], wl.k, d,
+                                wl.v_th_q, wl.surrogate, wl.alpha, 0, wl.s_max)
+        elif wl.dtype == "bf16":
+            oracle.forward_bf16(sub["x"], sub["sign"], sub["shift"], sub["bias"], wl.k, d, wl.v_th,
+                                shift_lo=0, shift_hi=wl.s_max)
+            oracle.backward_bf16(sub["x"], sub["grad_spikes"], sub["sign"], sub["shift"], sub["bias"], wl.k, d,
+                                 wl.v_th, surrogate_kind=wl.surrogate, alpha=wl.alpha, shift_lo=0,
+                                 shift_hi=wl.s_max)
+        else:
+            oracle.forward_f32(sub["x"], sub["sign"], sub["shift"], sub["bias"], wl.k, d, wl.v_th, 0, wl.s_max)
+            oracle.backward_f32(sub["x"], sub["grad_spikes"], sub["sign"], sub["shift"], sub["bias"], wl.k, d,
+                                wl.v_th, wl.surrogate, wl.alpha, 0, wl.s_max)
+    dt = time.perf_counter() - t0
+    elems = wl.T * wl.N * channels * wl.S * len(wl.dilations)
+    return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
+            "sample": f"{channels} of {wl.C} channels ({elems} element-layers, every dilation), "
+                      f"fwd+bwd in {dt:.1f} s on {platform.processor() or platform.machine()} "
+                      f"(nproc {os.cpu_count()})"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2, help="1..5 (default 2: audio-spike-shaped)")
+    ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the neuron layer "
+              f"shards over the batch with one all-reduce of grad_w/grad_b per layer, not built here)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2501_14490_amd import mfpsn, workloads
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS[args.workload]
+    log(f"workload {wl.wid}: {wl.describe()}  dilations {wl.dilations}")
+    t0 = time.time()
+    case = workloads.make_inputs(wl)
+    log(f"inputs drawn in {time.time() - t0:.1f}s")
+
+    def dev_tensor(a, storage):
+        if wl.dtype == "bf16" and storage:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x0 = dev_tensor(case["x"], True)
+    g0 = dev_tensor(case["grad_spikes"], True)
+    sign = dev_tensor(case["sign"], False)
+    shift = dev_tensor(case["shift"], False)
+    bias = dev_tensor(case["bias"], False)
+    P = len(wl.dilations)
+    layers = []
+    for li, d in enumerate(wl.dilations):
+        x = torch.roll(x0, shifts=7 * li, dims=1).contiguous() if li else x0
+        g = torch.roll(g0, shifts=11 * li, dims=1).contiguous() if li else g0
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        ws = torch.empty(max(mfpsn.mfpsn_backward_workspace_size(desc), 8), dtype=torch.uint8, device=dev)
+        layers.append({
+            "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
+            "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
+            "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
+            "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+            "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+        })
+    del x0, g0
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        for li, L in enumerate(layers):
+            if events is not None:
+                events[("fwd", li)][0].record(stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], None, stream)
+            if events is not None:
+                events[("fwd", li)][1].record(stream)
+        for li in reversed(range(P)):
+            L = layers[li]
+            if events is not None:
+                events[("bwd", li)][0].record(stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], sign, shift, bias, L["gx"], L["gw"], L["gb"],
+                                 L["ws"], stream=stream)
+            if events is not None:
+                events[("bwd", li)][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = {(kind, li): [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+                       for _ in range(args.steps)] for kind in ("fwd", "bwd") for li in range(P)}
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for s in range(args.steps):
+        step({key: ev[key][s] for key in ev})
+        if s % 5 == 4:
+            log(f"  step {s + 1}/{args.steps}")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    def avg_ms(kind, li):
+        return float(np.mean([a.elapsed_time(b) for a, b in ev[(kind, li)]]))
+
+    per = {f"{kind}_d{layers[li]['d']}_us": round(avg_ms(kind, li) * 1e3, 2)
+           for kind in ("fwd", "bwd") for li in range(P)}
+    bwd_ms = float(np.mean([avg_ms("bwd", li) for li in range(P)]))
+    fwd_ms = float(np.mean([avg_ms("fwd", li) for li in range(P)]))
+    fb, bb = alg_bytes(wl)
+    elems = wl.elements
+    bwd_bytes = elems * bb
+    achieved = bwd_bytes / (bwd_ms * 1e-3) / 1e9
+    fwd_achieved = elems * fb / (fwd_ms * 1e-3) / 1e9
+    value = P * elems / (elapsed / args.steps)
+    log(f"step {ms_per_step:.3f} ms   fwd {fwd_ms * 1e3:.1f} us ({fwd_achieved:.0f} GB/s alg)   "
+        f"bwd {bwd_ms * 1e3:.1f} us ({achieved:.0f} GB/s alg)   {value / 1e9:.2f} G elements/s")
+    log("per call (us):", per)
+
+    result = {
+        "metric": "neuron fwd+bwd elements/s (T*N*C*S) and achieved HBM GB/s vs MI355X peak",
+        "value": value,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f32": "f32", "bf16": "bf16", "q8_8": "int16 Q8.8 / int32"}[wl.dtype],
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: x[{','.join(map(str, wl.shape))}] {wl.dtype}, k={wl.k}, "
+                        f"sawtooth period {P} (one layer per d={wl.dilations}), forward of every layer "
+                        f"then backward of every layer",
+            "elements_per_layer": elems,
+            "layers_per_step": P,
+            "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
+            "v_th": wl.v_th,
+        },
+        "roofline": {
+            "kernel": "mfpsn_backward (bwd_kernel + finalize)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": measured_traffic(wl.name),
+            "alg_bytes_per_launch": bwd_bytes,
+            "avg_launch_us": bwd_ms * 1e3,
+        },
+        "forward": {"alg_bytes_per_launch": elems * fb, "avg_launch_us": fwd_ms * 1e3,
+                    "achieved_GBs": fwd_achieved, "frac": fwd_achieved / HBM_PEAK_GBS},
+        "per_call_us": per,
+    }
+    if not args.no_cpu_baseline:
+        channels = args.cpu_channels or {1: 128, 2: 24, 3: 16, 4: 2, 5: 12}[wl.wid]
+        log(f"oracle baseline on {channels} channels ...")
+        result["cpu_baseline"] = cpu_baseline(wl, case, channels)
+        log(f"oracle: {result['cpu_baseline']['value'] / 1e6:.2f} M elements/s")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,165 @@
+/*
+ * mfpsn.h — C ABI of libmfpsn.so, the gfx950 (MI355X) implementation of the
+ * training step of the mul-free channel-wise Parallel Spiking Neuron
+ * (arXiv 2501.14490, "Multiplication-Free Parallelizable Spiking Neurons with
+ * Efficient Spatio-Temporal Dynamics").
+ *
+ * Problem statement (Sec. 4.1 Eq. GPSN-charge, Sec. 4.2 Eqs. round_w,
+ * mfdpsn_charge, mfdpsn_fire; App. A.3 Eqs. forward_H, backward_X/W/b):
+ *
+ *   H[t,n,c,s] = sum_{i=0..k-1, t-(k-1-i)d >= 0} sign[c,i] * 2^-shift[c,i] * x[t-(k-1-i)d, n,c,s]
+ *                + bias[c]
+ *   spikes     = (H >= v_th)                       (Heaviside, Theta(0) = 1)
+ *   dH         = grad_spikes * sigma'(H - v_th)    (surrogate gradient)
+ *   grad_x[t]  = sum_{i, t+(k-1-i)d < T} sign[c,i] * 2^-shift[c,i] * dH[t+(k-1-i)d]
+ *   grad_w[c,i]= sum_{t,n,s} x[t-(k-1-i)d] * dH[t]  (gradient of the quantized
+ *                weight, passed unchanged to the latent weight by the
+ *                whole-quantizer straight-through estimator)
+ *   grad_b[c]  = sum_{t,n,s} dH[t]                  (minus the gradient of a
+ *                per-channel threshold)
+ *
+ * Every product by a tap is a power-of-two scaling: an exponent move (ldexp)
+ * for float data, an arithmetic right shift (floor) for Q8.8 integers
+ * (Sec. 4.2, Eq. bitshift).  Float sums run in ascending tap order from +0,
+ * bias last, each add rounded to nearest; grad_w and grad_b are accumulated
+ * from exact double-precision products and rounded once.
+ *
+ * Layouts (all device memory, owned by the caller, dense, row-major):
+ *   x, grad_spikes, spikes, h_out, grad_x : [T][N][C][S]   time-first; S is the
+ *                                            product of the spatial dimensions
+ *   sign, shift : int8 [C][k]   weight = sign * 2^-shift (sign < 0 means -1,
+ *                               anything else +1; shift is clamped into
+ *                               [shift_lo, shift_hi])
+ *   bias        : float [C] (F32, BF16) or int32 [C] Q8.8 (Q8_8)
+ *   grad_w      : float [C][k] (F32, BF16) or int64 [C][k] Q16.16 (Q8_8)
+ *   grad_b      : float [C]    (F32, BF16) or int64 [C] Q8.8 (Q8_8)
+ * Storage types per dtype:
+ *   MFPSN_F32  : x, grad_spikes, grad_x float; h_out float
+ *   MFPSN_BF16 : x, grad_spikes, grad_x bfloat16 (arithmetic in float, grad_x
+ *                rounded to nearest even); h_out float
+ *   MFPSN_Q8_8 : x, grad_spikes int16 Q8.8; grad_x int32 Q8.8; h_out int32 Q8.8
+ *
+ * Error behaviour: every entry point validates its arguments on the host
+ * before touching the GPU; on error it returns a negative mfpsn_status and
+ * launches nothing.  Launch failures return MFPSN_ERR_HIP.  All work is
+ * enqueued asynchronously on `stream` (a hipStream_t; NULL is the null
+ * stream).  Outputs are overwritten, never accumulated into.  The library
+ * keeps no per-call state and allocates no device memory; calls on different
+ * streams with disjoint outputs may overlap.
+ */
+#ifndef MFPSN_H
+#define MFPSN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MFPSN_ABI_VERSION 1
+#define MFPSN_MAX_K 32
+
+typedef enum mfpsn_status {
+    MFPSN_OK = 0,
+    MFPSN_ERR_NULL = -1,      /* a required pointer is NULL                      */
+    MFPSN_ERR_SHAPE = -2,     /* a size is negative or too large                 */
+    MFPSN_ERR_PARAM = -3,     /* k, dilation, shift range, v_th or alpha invalid */
+    MFPSN_ERR_DTYPE = -4,     /* unknown dtype or surrogate                      */
+    MFPSN_ERR_WORKSPACE = -5, /* workspace too small or misaligned               */
+    MFPSN_ERR_ALIGN = -6,     /* a tensor pointer is misaligned for its type     */
+    MFPSN_ERR_HIP = -7        /* the HIP runtime reported an error               */
+} mfpsn_status;
+
+typedef enum mfpsn_dtype {
+    MFPSN_F32 = 0,
+    MFPSN_BF16 = 1,
+    MFPSN_Q8_8 = 2
+} mfpsn_dtype;
+
+/* Surrogate derivative sigma'(u) used by the backward (Sec. 1 and App. E):
+ *   SIGMOID : alpha*e/(1+e)^2, e = exp(-alpha*|u|)   (derivative of sigmoid(alpha*u))
+ *   ATAN    : alpha / (2 (1 + (pi/2 * alpha * u)^2))
+ *   RATIONAL: 1 / (1 + alpha * u^2)
+ * Evaluated in float with a fixed operation sequence (own exp: Cody-Waite
+ * reduction, degree-7 Taylor polynomial); the Q8.8 path uses the integer
+ * factor L(u) = round_half_even(2^15 * sigma'(u/256)) and
+ * dH = floor(grad_spikes * L / 2^15). */
+typedef enum mfpsn_surrogate {
+    MFPSN_SG_SIGMOID = 0,
+    MFPSN_SG_ATAN = 1,
+    MFPSN_SG_RATIONAL = 2
+} mfpsn_surrogate;
+
+typedef struct mfpsn_desc {
+    int32_t T, N, C, S;  /* sizes, each >= 0; N*C*S*elem_bytes < 2^31        */
+    int32_t k;           /* order, 1..MFPSN_MAX_K                              */
+    int32_t dilation;    /* this layer's d >= 1 (see mfpsn_sawtooth_dilation)  */
+    int32_t dtype;       /* mfpsn_dtype                                        */
+    int32_t surrogate;   /* mfpsn_surrogate                                    */
+    float alpha;         /* surrogate parameter, 0 <= alpha <= 1024            */
+    float v_th;          /* threshold, float paths                             */
+    int32_t v_th_q;      /* threshold, Q8.8 path (256 == 1.0)                  */
+    int32_t shift_lo;    /* shifts are clamped into [shift_lo, shift_hi];      */
+    int32_t shift_hi;    /* float: -126..126, Q8.8: 0..31                      */
+} mfpsn_desc;
+
+/* Forward: charge (Eq. mfdpsn_charge) and fire (Eq. mfdpsn_fire).
+ *   x      : [T][N][C][S] storage type of desc->dtype
+ *   sign, shift : int8 [C][k];  bias : float[C] or int32[C] (Q8.8)
+ *   spikes : uint8 [T][N][C][S], 1 where H >= v_th else 0 (NaN -> 0)
+ *   h_out  : optional (may be NULL) membrane potential H, float (F32, BF16)
+ *            or int32 (Q8.8), [T][N][C][S]
+ * Alignment: x 4 bytes (F32) / 2 bytes (BF16, Q8.8); h_out, bias 4 bytes. */
+int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
+                  const void* bias, uint8_t* spikes, void* h_out, void* stream);
+
+/* Bytes of device workspace mfpsn_backward needs for this problem (per-block
+ * partial sums of grad_w and grad_b, in double).  Returns a status; *bytes is
+ * written on success. */
+int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
+
+/* Backward: H is recomputed from x (not stored), then dH, grad_x (App. A.3
+ * Eq. backward_X), grad_w (Eq. backward_W) and grad_b (Eq. backward_b).
+ *   grad_spikes : [T][N][C][S] storage type of desc->dtype (the upstream
+ *                 gradient of the spikes)
+ *   grad_x      : [T][N][C][S] float (F32), bfloat16 (BF16), int32 (Q8.8)
+ *   grad_w      : float [C][k] or int64 [C][k] (Q8.8, Q16.16)
+ *   grad_b      : float [C]    or int64 [C]    (Q8.8)
+ *   workspace   : >= mfpsn_backward_workspace_size bytes, 8-byte aligned;
+ *                 contents on entry are ignored (every word used is written)
+ * grad_w and grad_b do not depend on the order in which the GPU runs its
+ * blocks: partial sums are reduced in a fixed order, so repeated calls give
+ * identical bits.  The Q8.8 path is exact (integers below 2^53); the call
+ * fails with MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^53. */
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes,
+                   const int8_t* sign, const int8_t* shift, const void* bias,
+                   void* grad_x, void* grad_w, void* grad_b,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Power-of-two quantizer Q(W) = sign(W) * 2^round(log2|W|) (Sec. 4.2,
+ * Eq. round_w), applied elementwise to `count` (< 2^31) floats w (device):
+ *   sign  = -1 if w < 0 else +1 (so sign(0) = +1)
+ *   shift = clamp(-round(log2|w|), shift_lo, shift_hi), with the exact
+ *           rounding of the real logarithm (|w| = f 2^m, f in [1,2):
+ *           m + (f >= sqrt 2)); w = 0 or NaN -> shift_hi; +-Inf -> shift_lo.
+ * The gradient of the latent weight is grad_w itself (straight-through). */
+int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int32_t shift_hi,
+                           int8_t* sign, int8_t* shift, void* stream);
+
+/* Sawtooth dilation of layer `layer` (0-based) for a period P (Sec. 4.1,
+ * Eq. d with P = 3): d^0 = 1, d^{l+1} = d^l mod P + 1, i.e. (layer mod P) + 1.
+ * Returns 0 if layer < 0 or period < 1. */
+int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period);
+
+/* Static description of a status code. */
+const char* mfpsn_status_string(int status);
+
+/* MFPSN_ABI_VERSION of the loaded library. */
+int32_t mfpsn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MFPSN_H */

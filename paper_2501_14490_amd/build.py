@@ -1,0 +1,114 @@
+"""Build ``libmfpsn.so`` (gfx950) from ``csrc/`` with hipcc.
+
+The kernel source is compiled once per storage type and range of orders k so
+the (large, fully unrolled) instantiations build in parallel, then linked
+with the C-ABI layer into ``paper_2501_14490_amd/libmfpsn.so``.
+
+    python -m paper_2501_14490_amd.build [--jobs N] [--force]
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+import time
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(PKG, "_build")
+LIB = os.path.join(PKG, "libmfpsn.so")
+ARCH = "gfx950"
+
+HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+
+# Device code: IEEE single precision with denormals, no FMA contraction (the
+# float sums are pinned to a sequential order), packed-FP32 instructions off.
+DEVICE_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC", "-ffp-contract=off",
+    "-fno-gpu-flush-denormals-to-zero", "-fno-fast-math",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+HOST_FLAGS = ["-O2", "-std=c++20", "-fPIC", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+              "-I/opt/rocm/include"]
+
+K_RANGES = [(1, 8), (9, 16), (17, 22), (23, 27), (28, 32)]
+DTYPES = [0, 1, 2]  # f32, bf16, q8.8
+
+
+def _units():
+    src = os.path.join(CSRC, "mfpsn_kernels.hip")
+    units = []
+    for dt in DTYPES:
+        for lo, hi in K_RANGES:
+            obj = os.path.join(BUILD, f"kernels_d{dt}_k{lo}-{hi}.o")
+            units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
+                                f"-DMFPSN_TU_DTYPE={dt}", f"-DMFPSN_TU_KLO={lo}",
+                                f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj]))
+    obj = os.path.join(BUILD, "kernels_misc.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
+                        "-c", src, "-o", obj]))
+    for name in ("mfpsn_api.cpp", "mfpsn_dispatch.cpp"):
+        obj = os.path.join(BUILD, name.replace(".cpp", ".o"))
+        units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+                            os.path.join(CSRC, name), "-o", obj]))
+    return units
+
+
+def _sources():
+    return [os.path.join(CSRC, f) for f in os.listdir(CSRC)] + [os.path.join(INCLUDE, "mfpsn.h")]
+
+
+def build(jobs: int | None = None, force: bool = True, verbose: bool = False) -> str:
+    """Compile every translation unit and link libmfpsn.so; returns its path.
+    With force=False, units whose object is newer than every source are kept."""
+    os.makedirs(BUILD, exist_ok=True)
+    newest_src = max(os.path.getmtime(p) for p in _sources())
+    todo = []
+    for obj, cmd in _units():
+        if force or not os.path.exists(obj) or os.path.getmtime(obj) < newest_src:
+            todo.append((obj, cmd))
+    jobs = jobs or min(8, os.cpu_count() or 1)
+    t0 = time.time()
+
+    def run(item):
+        obj, cmd = item
+        t = time.time()
+        p = subprocess.run(cmd, capture_output=True, text=True)
+        out = "\n".join(l for l in (p.stdout + p.stderr).splitlines()
+                        if "packed-fp32-ops" not in l)
+        if p.returncode != 0:
+            raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{out}")
+        if verbose:
+            print(f"  built {os.path.basename(obj)} in {time.time() - t:.1f}s", flush=True)
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        list(ex.map(run, todo))
+    objs = [obj for obj, _ in _units()]
+    tmp = LIB + f".tmp{os.getpid()}"
+    link = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    p = subprocess.run(link, capture_output=True, text=True)
+    if p.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(link)}\n{p.stdout}{p.stderr}")
+    os.replace(tmp, LIB)
+    if verbose:
+        print(f"libmfpsn.so linked ({len(todo)} units compiled, {time.time() - t0:.1f}s)", flush=True)
+    return LIB
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--jobs", type=int, default=None)
+    ap.add_argument("--force", action="store_true")
+    args = ap.parse_args(argv)
+    build(args.jobs, force=args.force, verbose=True)
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,279 @@
+// C ABI of libmfpsn.so: argument validation, launch planning and dispatch.
+// Declarations and the contract of every entry point are in include/mfpsn.h.
+#include "mfpsn.h"
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "mfpsn_internal.h"
+
+using namespace mfpsn;
+
+namespace {
+
+constexpr int64_t kTargetWaves = 4096;  // >= 4 waves per CU on 256 CUs
+constexpr int kMaxItemsPerWave = 32;
+
+int elem_bytes(int dtype) { return dtype == MFPSN_F32 ? 4 : 2; }
+int grad_x_bytes(int dtype) { return dtype == MFPSN_BF16 ? 2 : 4; }
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Largest |dH| the Q8.8 backward can produce: |grad_spikes| <= 2^15 times the
+// integer surrogate factor, which is at most 2^15 * max sigma' (+1 for rounding).
+double q88_max_dh(const mfpsn_desc* d)
+{
+    double peak;
+    switch (d->surrogate) {
+    case MFPSN_SG_SIGMOID: peak = d->alpha / 4.0; break;
+    case MFPSN_SG_ATAN: peak = d->alpha / 2.0; break;
+    default: peak = 1.0; break;
+    }
+    return ceil(32768.0 * peak) + 1.0;
+}
+
+int validate(const mfpsn_desc* d)
+{
+    if (!d)
+        return MFPSN_ERR_NULL;
+    if (d->dtype != MFPSN_F32 && d->dtype != MFPSN_BF16 && d->dtype != MFPSN_Q8_8)
+        return MFPSN_ERR_DTYPE;
+    if (d->surrogate != MFPSN_SG_SIGMOID && d->surrogate != MFPSN_SG_ATAN &&
+        d->surrogate != MFPSN_SG_RATIONAL)
+        return MFPSN_ERR_DTYPE;
+    if (d->T < 0 || d->N < 0 || d->C < 0 || d->S < 0)
+        return MFPSN_ERR_SHAPE;
+    if (d->k < 1 || d->k > MFPSN_MAX_K || d->dilation < 1)
+        return MFPSN_ERR_PARAM;
+    if ((int64_t)(d->k - 1) * d->dilation > (int64_t)1 << 30)
+        return MFPSN_ERR_PARAM;
+    const int64_t M = (int64_t)d->N * d->C * d->S;
+    if (M * 4 >= ((int64_t)1 << 31))  // one time step of any tensor fits a 31-bit offset
+        return MFPSN_ERR_SHAPE;
+    if (d->C > 65535 && !(d->S == 1))  // plane mode puts one channel per grid row
+        return MFPSN_ERR_SHAPE;
+    if (d->shift_lo > d->shift_hi)
+        return MFPSN_ERR_PARAM;
+    if (d->dtype == MFPSN_Q8_8) {
+        if (d->shift_lo < 0 || d->shift_hi > 31)
+            return MFPSN_ERR_PARAM;
+    } else {
+        if (d->shift_lo < -126 || d->shift_hi > 126)
+            return MFPSN_ERR_PARAM;
+        if (!isfinite(d->v_th))
+            return MFPSN_ERR_PARAM;
+    }
+    if (!(d->alpha >= 0.0f && d->alpha <= 1024.0f))
+        return MFPSN_ERR_PARAM;
+    return MFPSN_OK;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Launch geometry.  Lanes walk residue classes; when the columns alone give
+// too few waves, each class is cut into chunks of at least 4k steps.
+Geom plan(const mfpsn_desc* d, bool backward)
+{
+    Geom g;
+    memset(&g, 0, sizeof(g));
+    g.T = d->T;
+    g.N = d->N;
+    g.C = d->C;
+    g.S = d->S;
+    g.k = d->k;
+    g.d = d->dilation;
+    g.M = (uint32_t)((int64_t)d->N * d->C * d->S);
+    g.esize = elem_bytes(d->dtype);
+    g.shift_lo = d->shift_lo;
+    g.shift_hi = d->shift_hi;
+    g.sg = d->surrogate;
+    g.alpha = d->alpha;
+    g.v_th = d->v_th;
+    g.v_th_q = d->v_th_q;
+    if (d->S == 1 && d->C >= 64) {
+        g.mode = kLaneChannel;
+        g.groups = (int32_t)ceil_div(d->C, 64);
+        g.spw = 1;
+        g.gpw = 1;
+        g.tiles = d->N;
+    } else {
+        g.mode = kPlane;
+        g.groups = d->C;
+        if (d->S >= 64) {
+            g.spw = (int32_t)ceil_div(d->S, 64);
+            g.gpw = 1;
+            g.tiles = d->N * g.spw;
+        } else {
+            g.spw = 1;
+            g.gpw = d->S > 0 ? 64 / d->S : 1;
+            g.tiles = (int32_t)ceil_div(d->N, g.gpw);
+        }
+    }
+    const int64_t class_len = d->T > 0 ? ceil_div(d->T, d->dilation) : 0;
+    const int64_t base = (int64_t)g.groups * g.tiles * g.d;
+    int64_t chunk = class_len > 0 ? class_len : 1;
+    int64_t nchunks = 1;
+    const int64_t min_chunk = 4 * (int64_t)d->k;
+    while (base * nchunks < kTargetWaves && chunk / 2 >= min_chunk) {
+        chunk = ceil_div(chunk, 2);
+        nchunks = ceil_div(class_len, chunk);
+    }
+    g.chunk = (int32_t)chunk;
+    g.nchunks = (int32_t)nchunks;
+    g.items = (int64_t)g.tiles * g.d * g.nchunks;
+    int64_t R = 1;
+    if (backward) {
+        const int64_t total = g.items * g.groups;
+        R = total / kTargetWaves;
+        if (R < 1)
+            R = 1;
+        if (R > kMaxItemsPerWave)
+            R = kMaxItemsPerWave;
+    }
+    g.R = (int32_t)R;
+    g.blocks = (int32_t)ceil_div(g.items, (int64_t)kWaves * R);
+    return g;
+}
+
+size_t workspace_bytes(const Geom& g)
+{
+    return (size_t)g.blocks * (size_t)(g.k + 1) * (size_t)g.C * sizeof(double);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mfpsn_abi_version(void) { return MFPSN_ABI_VERSION; }
+
+const char* mfpsn_status_string(int status)
+{
+    switch (status) {
+    case MFPSN_OK: return "ok";
+    case MFPSN_ERR_NULL: return "a required pointer is NULL";
+    case MFPSN_ERR_SHAPE: return "a size is negative or too large";
+    case MFPSN_ERR_PARAM: return "invalid order, dilation, shift range, threshold or alpha";
+    case MFPSN_ERR_DTYPE: return "unknown dtype or surrogate";
+    case MFPSN_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case MFPSN_ERR_ALIGN: return "tensor pointer misaligned for its element type";
+    case MFPSN_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period)
+{
+    if (layer < 0 || period < 1)
+        return 0;
+    return (layer % period) + 1;
+}
+
+int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
+                  const void* bias, uint8_t* spikes, void* h_out, void* stream)
+{
+    int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
+    if (total > 0 && (!x || !spikes))
+        return MFPSN_ERR_NULL;
+    if (desc->C > 0 && (!sign || !shift || !bias))
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, elem_bytes(desc->dtype)) || !aligned(bias, 4) || !aligned(h_out, 4))
+        return MFPSN_ERR_ALIGN;
+    if (total == 0)
+        return MFPSN_OK;
+    FwdArgs a;
+    a.g = plan(desc, false);
+    a.x = x;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.spikes = spikes;
+    a.h_out = h_out;
+    if (launch_forward(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
+{
+    int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (!bytes)
+        return MFPSN_ERR_NULL;
+    const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
+    *bytes = total > 0 ? workspace_bytes(plan(desc, true)) : 0;
+    return MFPSN_OK;
+}
+
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes,
+                   const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
+                   void* grad_w, void* grad_b, void* workspace, size_t ws_bytes, void* stream)
+{
+    int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
+    if (total > 0 && (!x || !grad_spikes || !grad_x))
+        return MFPSN_ERR_NULL;
+    if (desc->C > 0 && (!sign || !shift || !bias || !grad_w || !grad_b))
+        return MFPSN_ERR_NULL;
+    const int es = elem_bytes(desc->dtype);
+    if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, grad_x_bytes(desc->dtype)) ||
+        !aligned(bias, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
+        !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
+        return MFPSN_ERR_ALIGN;
+    if (desc->dtype == MFPSN_Q8_8) {
+        // every partial sum of grad_w must stay an exact integer in double
+        const double reach = (double)desc->T * desc->N * desc->S * 32768.0 * q88_max_dh(desc);
+        if (reach >= 9007199254740992.0)
+            return MFPSN_ERR_SHAPE;
+    }
+    BwdArgs a;
+    a.g = plan(desc, true);
+    const size_t need = total > 0 ? workspace_bytes(a.g) : 0;
+    if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
+        return MFPSN_ERR_WORKSPACE;
+    a.x = x;
+    a.gs = grad_spikes;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.grad_x = grad_x;
+    a.partial = (double*)workspace;
+    hipStream_t s = (hipStream_t)stream;
+    if (total > 0 && launch_backward(a, desc->dtype, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    FinArgs f;
+    f.C = desc->C;
+    f.k = desc->k;
+    f.blocks = total > 0 ? a.g.blocks : 0;
+    f.dtype = desc->dtype;
+    f.partial = (const double*)workspace;
+    f.grad_w = grad_w;
+    f.grad_b = grad_b;
+    if (launch_finalize(f, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int32_t shift_hi,
+                           int8_t* sign, int8_t* shift, void* stream)
+{
+    if (count < 0 || count >= ((int64_t)1 << 31))
+        return MFPSN_ERR_SHAPE;
+    if (shift_lo > shift_hi || shift_lo < -128 || shift_hi > 127)
+        return MFPSN_ERR_PARAM;
+    if (count > 0 && (!w || !sign || !shift))
+        return MFPSN_ERR_NULL;
+    if (!aligned(w, 4))
+        return MFPSN_ERR_ALIGN;
+    if (launch_quantize(w, count, shift_lo, shift_hi, sign, shift, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+}  // extern "C"

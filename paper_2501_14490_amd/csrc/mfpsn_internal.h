@@ -1,0 +1,84 @@
+// Internal interface between the C-ABI layer (mfpsn_api.cpp) and the gfx950
+// kernels (mfpsn_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace mfpsn {
+
+enum Dtype : int32_t { kF32 = 0, kBF16 = 1, kQ88 = 2 };
+
+// How the 64 lanes of a wave map onto the columns (n, c, s) of x[T][N][C][S].
+//   kLaneChannel (S == 1, C >= 64): lane l is channel 64*g + l of one sample n;
+//       a wave's loads are 64 consecutive channels (coalesced) and every lane
+//       owns a different channel, so grad_w needs no cross-lane reduction.
+//   kPlane (S >= 2, or C < 64): every lane of a block shares one channel c
+//       (taps are wave-uniform); lanes cover 64 consecutive spatial positions
+//       (S >= 64, the last chunk of a plane partly masked) or 64/S whole rows
+//       of S positions for 64/S samples (S < 64).
+enum Mode : int32_t { kLaneChannel = 0, kPlane = 1 };
+
+// Launch geometry, computed on the host by plan() and passed by value.
+struct Geom {
+    int32_t T, N, C, S;
+    int32_t k, d;
+    int32_t mode;
+    int32_t spw;       // plane mode: 64-wide chunks per plane row (S >= 64), else 1
+    int32_t gpw;       // plane mode with S < 64: samples per wave (64 / S), else 1
+    int32_t tiles;     // tiles per group: lane-channel N; plane N*spw or ceil(N/gpw)
+    int32_t nchunks;   // time chunks per residue class
+    int32_t chunk;     // class steps per chunk
+    int32_t R;         // items per wave
+    int32_t groups;    // gridDim.y: channel groups (lane-channel) or channels (plane)
+    int32_t blocks;    // gridDim.x: blocks per group
+    int64_t items;     // items per group = tiles * d * nchunks
+    uint32_t M;        // N*C*S, columns per time step
+    int32_t esize;     // bytes per stored element of x / grad_spikes
+    int32_t shift_lo, shift_hi;
+    int32_t sg;        // surrogate kind
+    float alpha, v_th;
+    int32_t v_th_q;
+};
+
+constexpr int kWaves = 4;          // waves per block
+constexpr int kThreads = 64 * kWaves;
+
+struct FwdArgs {
+    Geom g;
+    const void* x;
+    const int8_t* sign;
+    const int8_t* shift;
+    const void* bias;
+    uint8_t* spikes;
+    void* h_out;
+};
+
+struct BwdArgs {
+    Geom g;
+    const void* x;
+    const void* gs;
+    const int8_t* sign;
+    const int8_t* shift;
+    const void* bias;
+    void* grad_x;
+    double* partial;   // [blocks][k+1][C]
+};
+
+struct FinArgs {
+    int32_t C, k, blocks, dtype;
+    const double* partial;
+    void* grad_w;
+    void* grad_b;
+};
+
+template <int K, int DT> hipError_t fwd_k(const FwdArgs& a, hipStream_t stream);
+template <int K, int DT> hipError_t bwd_k(const BwdArgs& a, hipStream_t stream);
+
+hipError_t launch_forward(const FwdArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_backward(const BwdArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_finalize(const FinArgs& a, hipStream_t stream);
+hipError_t launch_quantize(const float* w, int64_t count, int32_t lo, int32_t hi, int8_t* sign,
+                           int8_t* shift, hipStream_t stream);
+
+}  // namespace mfpsn

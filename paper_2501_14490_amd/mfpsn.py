@@ -1,0 +1,218 @@
+"""Python binding of libmfpsn.so (declared in include/mfpsn.h).
+
+Argument marshalling only: every step of the neuron's training step runs in
+the library's HIP kernels.  PyTorch supplies device memory and the stream.
+Importing this module loads the library and raises if it is missing (build
+it with ``python -m paper_2501_14490_amd.build``); there is no fallback.
+
+The functions named like the C entry points take tensors for the C
+pointers; ``forward``/``backward``/``quantize`` additionally allocate their
+outputs, and ``MfPSNFunction`` wires quantize -> forward -> backward into
+autograd with the straight-through estimator of the quantizer (Sec. 4.2).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmfpsn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2501_14490_amd.build`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+MFPSN_OK = 0
+MFPSN_F32, MFPSN_BF16, MFPSN_Q8_8 = 0, 1, 2
+MFPSN_SG_SIGMOID, MFPSN_SG_ATAN, MFPSN_SG_RATIONAL = 0, 1, 2
+MFPSN_MAX_K = 32
+
+DTYPES = {"f32": MFPSN_F32, "bf16": MFPSN_BF16, "q8_8": MFPSN_Q8_8}
+SURROGATES = {"sigmoid": MFPSN_SG_SIGMOID, "atan": MFPSN_SG_ATAN, "arctan": MFPSN_SG_ATAN,
+              "rational": MFPSN_SG_RATIONAL}
+STORAGE = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.bfloat16, MFPSN_Q8_8: torch.int16}
+GRAD_X = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.bfloat16, MFPSN_Q8_8: torch.int32}
+H_OUT = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int32}
+BIAS = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int32}
+GRAD_WB = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int64}
+
+
+class MfpsnDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("N", ctypes.c_int32), ("C", ctypes.c_int32),
+                ("S", ctypes.c_int32), ("k", ctypes.c_int32), ("dilation", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("surrogate", ctypes.c_int32), ("alpha", ctypes.c_float),
+                ("v_th", ctypes.c_float), ("v_th_q", ctypes.c_int32), ("shift_lo", ctypes.c_int32),
+                ("shift_hi", ctypes.c_int32)]
+
+
+_P = ctypes.c_void_p
+_DP = ctypes.POINTER(MfpsnDesc)
+_lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_forward.restype = ctypes.c_int
+_lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
+_lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
+_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_backward.restype = ctypes.c_int
+_lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
+_lib.mfpsn_quantize_weights.restype = ctypes.c_int
+_lib.mfpsn_sawtooth_dilation.argtypes = [ctypes.c_int32, ctypes.c_int32]
+_lib.mfpsn_sawtooth_dilation.restype = ctypes.c_int32
+_lib.mfpsn_status_string.argtypes = [ctypes.c_int]
+_lib.mfpsn_status_string.restype = ctypes.c_char_p
+_lib.mfpsn_abi_version.argtypes = []
+_lib.mfpsn_abi_version.restype = ctypes.c_int32
+
+
+class MfpsnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {mfpsn_status_string(status)} (status {status})")
+        self.status = status
+
+
+def _check(status: int, where: str):
+    if status != MFPSN_OK:
+        raise MfpsnError(status, where)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def make_desc(shape, k: int, dilation: int, dtype="f32", surrogate="sigmoid", alpha: float = 4.0,
+              v_th: float = 1.0, v_th_q: int = 256, shift_lo: int = 0, shift_hi: int = 7) -> MfpsnDesc:
+    """Descriptor for x of shape [T, N, C, *spatial]."""
+    T, N, C = (int(v) for v in shape[:3])
+    S = 1
+    for v in shape[3:]:
+        S *= int(v)
+    dt = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+    sg = SURROGATES[surrogate] if isinstance(surrogate, str) else int(surrogate)
+    return MfpsnDesc(T, N, C, S, int(k), int(dilation), dt, sg, float(alpha), float(v_th), int(v_th_q),
+                     int(shift_lo), int(shift_hi))
+
+
+# ---------------------------------------------------------------------------
+# the C entry points
+# ---------------------------------------------------------------------------
+def mfpsn_abi_version() -> int:
+    return int(_lib.mfpsn_abi_version())
+
+
+def mfpsn_status_string(status: int) -> str:
+    return _lib.mfpsn_status_string(int(status)).decode()
+
+
+def mfpsn_sawtooth_dilation(layer: int, period: int) -> int:
+    return int(_lib.mfpsn_sawtooth_dilation(int(layer), int(period)))
+
+
+def mfpsn_forward(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, stream=None) -> None:
+    _check(_lib.mfpsn_forward(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias),
+                              _ptr(spikes), _ptr(h_out), _stream(stream)), "mfpsn_forward")
+
+
+def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.mfpsn_backward_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
+           "mfpsn_backward_workspace_size")
+    return int(n.value)
+
+
+def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b,
+                   workspace, workspace_bytes=None, stream=None) -> None:
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(sign), _ptr(shift),
+                               _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b), _ptr(workspace),
+                               int(workspace_bytes), _stream(stream)), "mfpsn_backward")
+
+
+def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=None) -> None:
+    _check(_lib.mfpsn_quantize_weights(_ptr(w), int(w.numel()), int(shift_lo), int(shift_hi), _ptr(sign),
+                                       _ptr(shift), _stream(stream)), "mfpsn_quantize_weights")
+
+
+# ---------------------------------------------------------------------------
+# allocating wrappers
+# ---------------------------------------------------------------------------
+def _expect(t, dtype, device, name):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, stream=None):
+    dev = x.device
+    _expect(x, STORAGE[desc.dtype], dev, "x")
+    _expect(bias, BIAS[desc.dtype], dev, "bias")
+    spikes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
+    h = torch.empty(x.shape, dtype=H_OUT[desc.dtype], device=dev) if want_h else None
+    mfpsn_forward(desc, x, sign, shift, bias, spikes, h, stream)
+    return (spikes, h) if want_h else spikes
+
+
+def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None):
+    dev = x.device
+    _expect(x, STORAGE[desc.dtype], dev, "x")
+    _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
+    grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
+    grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
+    grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
+    need = mfpsn_backward_workspace_size(desc)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
+    mfpsn_backward(desc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
+                   stream=stream)
+    return grad_x, grad_w, grad_b
+
+
+def quantize(w, shift_lo: int, shift_hi: int, stream=None):
+    _expect(w, torch.float32, w.device, "w")
+    sign = torch.empty(w.shape, dtype=torch.int8, device=w.device)
+    shift = torch.empty(w.shape, dtype=torch.int8, device=w.device)
+    mfpsn_quantize_weights(w, shift_lo, shift_hi, sign, shift, stream)
+    return sign, shift
+
+
+class MfPSNFunction(torch.autograd.Function):
+    """spikes = Theta(conv_{Q(W)}(x) + b - v_th) with the surrogate-gradient
+    backward.  grad of W is the grad of Q(W) (whole-quantizer straight-through
+    estimator, Sec. 4.2); the grad of b is the per-channel dH sum.  Float
+    storage paths only (f32, bf16)."""
+
+    @staticmethod
+    def forward(ctx, x, w, b, k, dilation, v_th, surrogate, alpha, shift_lo, shift_hi):
+        dtype = "bf16" if x.dtype == torch.bfloat16 else "f32"
+        desc = make_desc(x.shape, k, dilation, dtype, surrogate, alpha, v_th, 0, shift_lo, shift_hi)
+        sign, shift = quantize(w.detach().contiguous(), shift_lo, shift_hi)
+        xc = x.detach().contiguous()
+        bc = b.detach().float().contiguous()
+        spikes = forward(desc, xc, sign, shift, bc)
+        ctx.save_for_backward(xc, sign, shift, bc)
+        ctx.desc = desc
+        return spikes.to(x.dtype)
+
+    @staticmethod
+    def backward(ctx, grad_spikes):
+        xc, sign, shift, bc = ctx.saved_tensors
+        g = grad_spikes.to(xc.dtype).contiguous()
+        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc)
+        return grad_x, grad_w, grad_b, None, None, None, None, None, None, None

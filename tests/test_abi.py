@@ -1,0 +1,153 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, and
+rejects invalid arguments on the host before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mfpsn.h")
+LIB = os.path.join(ROOT, "paper_2501_14490_amd", "libmfpsn.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libmfpsn.so not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mfpsn_[a-z_0-9]+)\s*\(", text)))
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("T", "N", "C", "S", "k", "dilation", "dtype", "surrogate")] + [
+        ("alpha", ctypes.c_float), ("v_th", ctypes.c_float), ("v_th_q", ctypes.c_int32),
+        ("shift_lo", ctypes.c_int32), ("shift_hi", ctypes.c_int32)]
+
+
+def good_desc(**kw):
+    d = dict(T=16, N=2, C=64, S=1, k=4, dilation=2, dtype=0, surrogate=0, alpha=4.0, v_th=1.0, v_th_q=256,
+             shift_lo=0, shift_hi=7)
+    d.update(kw)
+    return Desc(**d)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    L = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    DP = ctypes.POINTER(Desc)
+    L.mfpsn_forward.argtypes = [DP, P, P, P, P, P, P, P]
+    L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
+    L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    L.mfpsn_status_string.restype = ctypes.c_char_p
+    return L
+
+
+def test_header_declares_the_three_entry_points():
+    fns = declared_functions()
+    for name in ("mfpsn_forward", "mfpsn_backward", "mfpsn_quantize_weights"):
+        assert name in fns
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_struct_layout_matches_header():
+    # 13 four-byte fields, no padding
+    assert ctypes.sizeof(Desc) == 52
+    text = open(HEADER).read()
+    body = text[text.index("typedef struct mfpsn_desc"):text.index("} mfpsn_desc;")]
+    names = re.findall(r"\b(?:int32_t|float)\s+([A-Za-z_, 0-9]+);", body)
+    flat = [n.strip() for group in names for n in group.split(",")]
+    assert flat == [f[0] for f in Desc._fields_]
+
+
+def test_version_and_status_strings(lib):
+    assert lib.mfpsn_abi_version() == 1
+    for s in range(-7, 1):
+        assert lib.mfpsn_status_string(s)
+    assert lib.mfpsn_status_string(-99) == b"unknown status"
+
+
+def test_sawtooth_matches_schedule(lib):
+    assert [lib.mfpsn_sawtooth_dilation(l, 3) for l in range(7)] == [1, 2, 3, 1, 2, 3, 1]
+    assert lib.mfpsn_sawtooth_dilation(-1, 3) == 0 and lib.mfpsn_sawtooth_dilation(2, 0) == 0
+
+
+FAKE = 0x100000  # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), -3), (dict(k=33), -3), (dict(dilation=0), -3), (dict(T=-1), -2), (dict(C=-5), -2),
+    (dict(dtype=7), -4), (dict(surrogate=3), -4), (dict(shift_lo=3, shift_hi=2), -3),
+    (dict(dtype=2, shift_lo=-1), -3), (dict(dtype=2, shift_hi=32), -3), (dict(shift_hi=127), -3),
+    (dict(alpha=-1.0), -3), (dict(alpha=float("nan")), -3), (dict(v_th=float("inf")), -3),
+    (dict(N=1 << 20, C=1 << 10), -2),
+])
+def test_forward_rejects_bad_descriptors(lib, kw, status):
+    d = good_desc(**kw)
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == status
+
+
+def test_forward_rejects_null_and_misaligned(lib):
+    assert lib.mfpsn_forward(None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    d = good_desc()
+    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, None) == -1
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE + 2, FAKE, FAKE, FAKE, FAKE, None, None) == -6
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE + 1, FAKE, None, None) == -6
+    d16 = good_desc(dtype=1)
+    assert lib.mfpsn_forward(ctypes.byref(d16), FAKE + 1, FAKE, FAKE, FAKE, FAKE, None, None) == -6
+
+
+def test_empty_forward_is_a_no_op(lib):
+    d = good_desc(T=0)
+    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, None, None, None) == 0
+
+
+def test_backward_workspace_and_validation(lib):
+    d = good_desc()
+    n = ctypes.c_size_t(0)
+    assert lib.mfpsn_backward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert n.value > 0 and n.value % 8 == 0
+    assert lib.mfpsn_backward_workspace_size(ctypes.byref(d), None) == -1
+    e = good_desc(T=0)
+    assert lib.mfpsn_backward_workspace_size(ctypes.byref(e), ctypes.byref(n)) == 0 and n.value == 0
+    # too small / misaligned / missing workspace
+    need = ctypes.c_size_t(0)
+    lib.mfpsn_backward_workspace_size(ctypes.byref(d), ctypes.byref(need))
+    args = [FAKE] * 8
+    assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE, need.value - 8, None) == -5
+    assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE + 4, need.value, None) == -5
+    assert lib.mfpsn_backward(ctypes.byref(d), *args, None, need.value, None) == -5
+    # null tensors
+    bad = list(args)
+    bad[6] = None  # grad_w
+    assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -1
+    # Q8.8 exactness bound on the grad_w sums
+    q = good_desc(dtype=2, T=1 << 14, N=1 << 14, C=1, S=1)
+    assert lib.mfpsn_backward(ctypes.byref(q), *args, FAKE, 1 << 40, None) == -2
+
+
+def test_quantize_validation(lib):
+    assert lib.mfpsn_quantize_weights(FAKE, -1, 0, 7, FAKE, FAKE, None) == -2
+    assert lib.mfpsn_quantize_weights(FAKE, 10, 5, 4, FAKE, FAKE, None) == -3
+    assert lib.mfpsn_quantize_weights(None, 10, 0, 7, FAKE, FAKE, None) == -1
+    assert lib.mfpsn_quantize_weights(FAKE + 2, 10, 0, 7, FAKE, FAKE, None) == -6
+    assert lib.mfpsn_quantize_weights(None, 0, 0, 7, None, None, None) == 0
+
+
+def test_workspace_grows_with_problem(lib):
+    sizes = []
+    for N in (16, 64, 256):
+        d = good_desc(T=250, N=N, C=512, k=16, dilation=4)
+        n = ctypes.c_size_t(0)
+        assert lib.mfpsn_backward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+        sizes.append(n.value)
+    assert sizes == sorted(sizes)
+    # bounded: per-block partial rows stay far below the size of x
+    assert sizes[-1] < 250 * 256 * 512 * 4 // 8

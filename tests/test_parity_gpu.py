@@ -1,0 +1,242 @@
+"""Parity of the HIP path (through the C ABI) with the oracle, on the GPU.
+
+Bar: spikes, Q8.8 potentials and all Q8.8 gradients bit-exact; float
+potentials and grad_x bit-exact (both sides follow the same pinned float
+sequence); bf16 grad_x bit-exact after round-to-nearest-even; grad_w and
+grad_b within 1e-6 absolute + 1e-5 relative of the oracle's double sums
+(only the order of the double additions differs).
+"""
+import numpy as np
+import pytest
+
+from paper_2501_14490_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2501_14490_amd import mfpsn  # noqa: E402  (loads libmfpsn.so or raises)
+
+DEV = torch.device("cuda:0")
+GW_ABS, GW_REL = 1e-6, 1e-5
+
+
+def to_dev(a, dtype):
+    if dtype == "bf16" and a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256):
+    x = to_dev(case["x"], dtype)
+    g = to_dev(case["grad_spikes"], dtype)
+    sign = to_dev(case["sign"], None)
+    shift = to_dev(case["shift"], None)
+    bias = to_dev(case["bias"], None)
+    desc = mfpsn.make_desc(case["x"].shape, k, d, dtype, surrogate, alpha, v_th, v_th_q, lo, hi)
+    spikes, h = mfpsn.forward(desc, x, sign, shift, bias, want_h=True)
+    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias)
+    torch.cuda.synchronize()
+    out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "grad_w": gw.cpu().numpy(),
+           "grad_b": gb.cpu().numpy()}
+    if dtype == "bf16":
+        out["grad_x_bits"] = gx.view(torch.int16).cpu().numpy().view(np.uint16)
+    else:
+        out["grad_x"] = gx.cpu().numpy()
+    return out
+
+
+def oracle_run(orc, case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256):
+    if dtype == "q8_8":
+        H, spk = orc.forward_q88(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th_q, lo, hi)
+        b = orc.backward_q88(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
+                             v_th_q, surrogate, alpha, lo, hi)
+    elif dtype == "bf16":
+        H, spk = orc.forward_bf16(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th,
+                                  shift_lo=lo, shift_hi=hi)
+        b = orc.backward_bf16(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
+                              v_th, surrogate_kind=surrogate, alpha=alpha, shift_lo=lo, shift_hi=hi)
+    else:
+        H, spk = orc.forward_f32(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th, lo, hi)
+        b = orc.backward_f32(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
+                             v_th, surrogate, alpha, lo, hi)
+    b["spikes"], b["Hf"] = spk, H
+    return b
+
+
+def compare(got, ref, dtype, label):
+    assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
+    if dtype == "q8_8":
+        assert np.array_equal(got["H"], ref["Hf"]), f"{label}: H differs"
+        assert np.array_equal(got["grad_x"], ref["grad_x"]), f"{label}: grad_x differs"
+        assert np.array_equal(got["grad_w"], ref["grad_w"]), f"{label}: grad_w differs"
+        assert np.array_equal(got["grad_b"], ref["grad_b"]), f"{label}: grad_b differs"
+        return
+    assert np.array_equal(got["H"].view(np.uint32), ref["Hf"].view(np.uint32)), (
+        f"{label}: H differs, max |diff| {np.abs(got['H'] - ref['Hf']).max()}")
+    if dtype == "bf16":
+        assert np.array_equal(got["grad_x_bits"], ref["grad_x_bits"]), f"{label}: bf16 grad_x differs"
+    else:
+        diff = np.abs(got["grad_x"].astype(np.float64) - ref["grad_x"])
+        assert np.array_equal(got["grad_x"].view(np.uint32), ref["grad_x"].view(np.uint32)), (
+            f"{label}: grad_x differs, max |diff| {diff.max()}")
+    for name in ("grad_w", "grad_b"):
+        g = got[name].astype(np.float64)
+        r = ref[name]
+        err = np.abs(g - r)
+        bound = GW_ABS + GW_REL * np.abs(r)
+        assert np.all(err <= bound), f"{label}: {name} max err {err.max()} (rel {(err / np.maximum(np.abs(r), 1e-30)).max()})"
+
+
+# ---------------------------------------------------------------------------
+# small shapes: every lane mapping, ragged tails, several tiles, T chunking
+# ---------------------------------------------------------------------------
+SHAPES = [
+    # (T, N, C, spatial)        mapping exercised
+    ((37, 3, 130, ()), "lane-channel, ragged channel group"),
+    ((20, 70, 7, ()), "plane, S=1 with C<64 (64 samples per wave)"),
+    ((13, 5, 3, (100,)), "plane, S>=64 with a partial chunk"),
+    ((19, 9, 4, (3,)), "plane, S<64 not dividing 64"),
+    ((11, 6, 5, (32,)), "plane, S=32"),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
+@pytest.mark.parametrize("shape_i", range(len(SHAPES)))
+@pytest.mark.parametrize("k,d", [(1, 1), (2, 3), (3, 2), (5, 1), (8, 4), (16, 2)])
+def test_small_shapes(orc, dtype, shape_i, k, d):
+    (T, N, C, sp), label = SHAPES[shape_i]
+    case = workloads.make_small(T, N, C, sp, k=k, s_lo=0, s_hi=7, dtype=dtype, seed=100 + k * 7 + d)
+    v_th = 0.5
+    got = gpu_run(case, k, d, dtype, v_th)
+    ref = oracle_run(orc, case, k, d, dtype, v_th)
+    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "q8_8"])
+@pytest.mark.parametrize("k", [4, 7, 12, 17, 24, 31, 32])
+def test_orders(orc, dtype, k):
+    d = 1 + k % 3
+    case = workloads.make_small(3 * k + 5, 4, 70, (), k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
+    ref = oracle_run(orc, case, k, d, dtype, 0.75)
+    got = gpu_run(case, k, d, dtype, 0.75)
+    compare(got, ref, dtype, f"k={k} d={d} {dtype}")
+
+
+@pytest.mark.parametrize("surrogate,alpha", [("atan", 2.0), ("atan", 5.0), ("rational", 10.0), ("sigmoid", 1.5)])
+@pytest.mark.parametrize("dtype", ["f32", "q8_8"])
+def test_surrogates(orc, surrogate, alpha, dtype):
+    case = workloads.make_small(40, 3, 66, (), k=4, dtype=dtype, seed=5)
+    got = gpu_run(case, 4, 2, dtype, 0.2, surrogate, alpha, v_th_q=51)
+    ref = oracle_run(orc, case, 4, 2, dtype, 0.2, surrogate, alpha, v_th_q=51)
+    compare(got, ref, dtype, f"{surrogate} {alpha} {dtype}")
+
+
+def test_negative_and_wide_shifts(orc):
+    case = workloads.make_small(25, 2, 65, (), k=6, s_lo=-4, s_hi=12, dtype="f32", seed=3)
+    got = gpu_run(case, 6, 3, "f32", 0.1, lo=-3, hi=10)
+    ref = oracle_run(orc, case, 6, 3, "f32", 0.1, lo=-3, hi=10)
+    compare(got, ref, "f32", "shift clamp [-3, 10]")
+
+
+@pytest.mark.parametrize("T", [1, 2, 5])
+def test_short_sequences(orc, T):
+    # T shorter than the receptive field (k-1)d + 1
+    case = workloads.make_small(T, 3, 64, (), k=8, dtype="f32", seed=T)
+    got = gpu_run(case, 8, 3, "f32", 0.0)
+    ref = oracle_run(orc, case, 8, 3, "f32", 0.0)
+    compare(got, ref, "f32", f"T={T}")
+
+
+def test_long_sequence_is_chunked(orc):
+    # few columns and a long time axis: the planner cuts each residue class into chunks
+    case = workloads.make_small(1500, 2, 64, (), k=8, dtype="q8_8", seed=9)
+    got = gpu_run(case, 8, 3, "q8_8", 0.0)
+    ref = oracle_run(orc, case, 8, 3, "q8_8", 0.0)
+    compare(got, ref, "q8_8", "chunked")
+    case = workloads.make_small(1500, 2, 64, (), k=8, dtype="f32", seed=9)
+    compare(gpu_run(case, 8, 3, "f32", 0.3), oracle_run(orc, case, 8, 3, "f32", 0.3), "f32", "chunked f32")
+
+
+def test_zero_input_gives_bias(orc):
+    case = workloads.make_small(12, 3, 70, (), k=5, dtype="f32", seed=1)
+    case["x"][:] = 0
+    got = gpu_run(case, 5, 2, "f32", 0.0)
+    assert np.array_equal(got["H"], np.broadcast_to(case["bias"].reshape(1, 1, -1), got["H"].shape))
+    assert np.all(got["grad_w"] == 0)
+
+
+def test_empty_inputs():
+    for shape in [(0, 3, 70), (5, 0, 70)]:
+        desc = mfpsn.make_desc(shape, 4, 2, "f32")
+        x = torch.zeros(shape, dtype=torch.float32, device=DEV)
+        sign = torch.ones((70, 4), dtype=torch.int8, device=DEV)
+        shift = torch.zeros((70, 4), dtype=torch.int8, device=DEV)
+        bias = torch.zeros(70, dtype=torch.float32, device=DEV)
+        mfpsn.forward(desc, x, sign, shift, bias)
+        gx, gw, gb = mfpsn.backward(desc, x, x, sign, shift, bias)
+        torch.cuda.synchronize()
+        assert gx.numel() == 0 or torch.all(gx == 0)
+        assert torch.all(gw == 0) and torch.all(gb == 0)
+
+
+def test_backward_is_deterministic():
+    case = workloads.make_small(64, 40, 96, (), k=8, dtype="f32", seed=2)
+    x = to_dev(case["x"], "f32")
+    g = to_dev(case["grad_spikes"], "f32")
+    args = [to_dev(case[n], None) for n in ("sign", "shift", "bias")]
+    desc = mfpsn.make_desc(case["x"].shape, 8, 3, "f32")
+    r1 = mfpsn.backward(desc, x, g, *args)
+    r2 = mfpsn.backward(desc, x, g, *args)
+    torch.cuda.synchronize()
+    for a, b in zip(r1, r2):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def test_quantizer_matches_oracle(orc):
+    rng = np.random.default_rng(0)
+    w = np.concatenate([rng.standard_normal(5000) * 0.2, rng.standard_normal(100) * 1e-30,
+                        [0.0, -0.0, np.inf, -np.inf, np.nan, 1.0, 2 ** -7, -(2 ** -8)]]).astype(np.float32)
+    for lo, hi in [(0, 7), (-5, 20), (0, 5)]:
+        s, sh = mfpsn.quantize(torch.from_numpy(w).to(DEV), lo, hi)
+        rs, rsh = orc.quantize(w, lo, hi)
+        assert np.array_equal(s.cpu().numpy(), rs)
+        assert np.array_equal(sh.cpu().numpy(), rsh)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads at full size, every dilation of their period: sampled
+# channels are compared in full (all t, n, s) against the oracle run on the
+# channel slice; the launch is the one bench.py times.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_workloads_full_size(orc, wid):
+    wl = workloads.WORKLOADS[wid]
+    case = workloads.make_inputs(wl)
+    dev = {n: to_dev(case[n], wl.dtype if n in ("x", "grad_spikes") else None) for n in case}
+    rng = np.random.default_rng(wid)
+    chans = np.sort(rng.choice(wl.C, size=min(wl.C, 6), replace=False))
+    chans_t = torch.from_numpy(chans).to(DEV)
+    for d in wl.dilations:
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        spikes, h = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True)
+        gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"])
+        torch.cuda.synchronize()
+        got = {"spikes": spikes.index_select(2, chans_t).cpu().numpy(),
+               "H": h.index_select(2, chans_t).cpu().numpy(),
+               "grad_w": gw.index_select(0, chans_t).cpu().numpy(),
+               "grad_b": gb.index_select(0, chans_t).cpu().numpy()}
+        gxs = gx.index_select(2, chans_t)
+        if wl.dtype == "bf16":
+            got["grad_x_bits"] = gxs.view(torch.int16).cpu().numpy().view(np.uint16)
+        else:
+            got["grad_x"] = gxs.cpu().numpy()
+        sub = {"x": np.ascontiguousarray(case["x"][:, :, chans]),
+               "grad_spikes": np.ascontiguousarray(case["grad_spikes"][:, :, chans]),
+               "sign": case["sign"][chans], "shift": case["shift"][chans], "bias": case["bias"][chans]}
+        ref = oracle_run(orc, sub, wl.k, d, wl.dtype, wl.v_th, wl.surrogate, wl.alpha, 0, wl.s_max, wl.v_th_q)
+        compare(got, ref, wl.dtype, f"{wl.name} d={d}")
+        del spikes, h, gx, gw, gb
