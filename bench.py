@@ -105,6 +105,10 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (default 2: audio-spike-shaped)")
     ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--recompute", action="store_true",
+                    help="backward recomputes H from x instead of reading the forward's saved H")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -121,6 +125,16 @@ def main():
         log("no GPU visible")
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        n = 1 << 28  # 2^28 floats = 1 GiB read + 1 GiB written per copy
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": 4 * n, "calibrate_copy_bytes_written": 4 * n,
+                          "copies": 5}), flush=True)
+        return
     wl = workloads.WORKLOADS[args.workload]
     log(f"workload {wl.wid}: {wl.describe()}  dilations {wl.dilations}")
     t0 = time.time()
@@ -149,6 +163,7 @@ def main():
             "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
             "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
             "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
+            "h": None if args.recompute else torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev),
             "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
             "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
         })
@@ -159,15 +174,15 @@ def main():
         for li, L in enumerate(layers):
             if events is not None:
                 events[("fwd", li)][0].record(stream)
-            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], None, stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], stream)
             if events is not None:
                 events[("fwd", li)][1].record(stream)
         for li in reversed(range(P)):
             L = layers[li]
             if events is not None:
                 events[("bwd", li)][0].record(stream)
-            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], sign, shift, bias, L["gx"], L["gw"], L["gb"],
-                                 L["ws"], stream=stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["h"], sign, shift, bias, L["gx"], L["gw"],
+                                 L["gb"], L["ws"], stream=stream)
             if events is not None:
                 events[("bwd", li)][1].record(stream)
 
@@ -223,6 +238,7 @@ def main():
             "elements_per_layer": elems,
             "layers_per_step": P,
             "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
+            "backward_H": "recomputed from x" if args.recompute else "saved by the forward",
             "v_th": wl.v_th,
         },
         "roofline": {
@@ -241,7 +257,7 @@ def main():
         "per_call_us": per,
     }
     if not args.no_cpu_baseline:
-        channels = args.cpu_channels or {1: 128, 2: 24, 3: 16, 4: 2, 5: 12}[wl.wid]
+        channels = args.cpu_channels or {1: 128, 2: 320, 3: 64, 4: 8, 5: 48}[wl.wid]
         log(f"oracle baseline on {channels} channels ...")
         result["cpu_baseline"] = cpu_baseline(wl, case, channels)
         log(f"oracle: {result['cpu_baseline']['value'] / 1e6:.2f} M elements/s")

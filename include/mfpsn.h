@@ -119,10 +119,15 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
  * written on success. */
 int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
 
-/* Backward: H is recomputed from x (not stored), then dH, grad_x (App. A.3
- * Eq. backward_X), grad_w (Eq. backward_W) and grad_b (Eq. backward_b).
+/* Backward: dH, grad_x (App. A.3 Eq. backward_X), grad_w (Eq. backward_W)
+ * and grad_b (Eq. backward_b).
  *   grad_spikes : [T][N][C][S] storage type of desc->dtype (the upstream
  *                 gradient of the spikes)
+ *   h           : optional (may be NULL) membrane potential H of this x, taps
+ *                 and bias as written by mfpsn_forward's h_out (float, or
+ *                 int32 for Q8.8); when NULL, H is recomputed from x.  Both
+ *                 give identical results; passing H trades 4 bytes per
+ *                 element of memory traffic for the recomputation.
  *   grad_x      : [T][N][C][S] float (F32), bfloat16 (BF16), int32 (Q8.8)
  *   grad_w      : float [C][k] or int64 [C][k] (Q8.8, Q16.16)
  *   grad_b      : float [C]    or int64 [C]    (Q8.8)
@@ -132,7 +137,7 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
  * blocks: partial sums are reduced in a fixed order, so repeated calls give
  * identical bits.  The Q8.8 path is exact (integers below 2^53); the call
  * fails with MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^53. */
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes,
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
                    const int8_t* sign, const int8_t* shift, const void* bias,
                    void* grad_x, void* grad_w, void* grad_b,
                    void* workspace, size_t workspace_bytes, void* stream);

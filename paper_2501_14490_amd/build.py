@@ -37,7 +37,7 @@ DEVICE_FLAGS = [
 HOST_FLAGS = ["-O2", "-std=c++20", "-fPIC", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
               "-I/opt/rocm/include"]
 
-K_RANGES = [(1, 8), (9, 16), (17, 22), (23, 27), (28, 32)]
+K_RANGES = [(1, 8), (9, 12), (13, 16), (17, 20), (21, 23), (24, 26), (27, 29), (30, 31), (32, 32)]
 DTYPES = [0, 1, 2]  # f32, bf16, q8.8
 
 

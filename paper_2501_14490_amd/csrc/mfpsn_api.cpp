@@ -3,6 +3,7 @@
 #include "mfpsn.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -12,8 +13,6 @@ using namespace mfpsn;
 
 namespace {
 
-constexpr int64_t kTargetWaves = 4096;  // >= 4 waves per CU on 256 CUs
-constexpr int kMaxItemsPerWave = 32;
 
 int elem_bytes(int dtype) { return dtype == MFPSN_F32 ? 4 : 2; }
 int grad_x_bytes(int dtype) { return dtype == MFPSN_BF16 ? 2 : 4; }
@@ -73,7 +72,19 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Launch geometry.  Lanes walk residue classes; when the columns alone give
 // too few waves, each class is cut into chunks of at least 4k steps.
-Geom plan(const mfpsn_desc* d, bool backward)
+// Target number of (wave-sized) work items, overridable for tuning with the
+// MFPSN_TARGET_WAVES environment variable.
+int64_t target_waves()
+{
+    static int64_t v = [] {
+        const char* e = getenv("MFPSN_TARGET_WAVES");
+        const long long x = e ? atoll(e) : 0;
+        return (int64_t)(x > 0 ? x : 2048);
+    }();
+    return v;
+}
+
+Geom plan(const mfpsn_desc* d)
 {
     Geom g;
     memset(&g, 0, sizeof(g));
@@ -91,48 +102,49 @@ Geom plan(const mfpsn_desc* d, bool backward)
     g.alpha = d->alpha;
     g.v_th = d->v_th;
     g.v_th_q = d->v_th_q;
+    {
+        // x * 2^-s stays a normal float for every s in [lo, hi] when its
+        // exponent field E satisfies max(1, hi+1) <= E <= 254 + min(0, lo)
+        const int emin = d->shift_hi + 1 > 1 ? d->shift_hi + 1 : 1;
+        const int emax = 254 + (d->shift_lo < 0 ? d->shift_lo : 0);
+        if (emin > emax) {
+            g.fast_lo = INFINITY;
+            g.fast_hi = 0.0f;
+        } else {
+            g.fast_lo = ldexpf(1.0f, emin - 127);
+            g.fast_hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
+        }
+    }
     if (d->S == 1 && d->C >= 64) {
         g.mode = kLaneChannel;
         g.groups = (int32_t)ceil_div(d->C, 64);
-        g.spw = 1;
-        g.gpw = 1;
         g.tiles = d->N;
     } else {
         g.mode = kPlane;
         g.groups = d->C;
-        if (d->S >= 64) {
-            g.spw = (int32_t)ceil_div(d->S, 64);
-            g.gpw = 1;
-            g.tiles = d->N * g.spw;
-        } else {
-            g.spw = 1;
-            g.gpw = d->S > 0 ? 64 / d->S : 1;
-            g.tiles = (int32_t)ceil_div(d->N, g.gpw);
-        }
+        g.tiles = (int32_t)ceil_div((int64_t)d->N * d->S, 64);
     }
+    // Cut each residue class into chunks (of at least 4k steps) only while
+    // the columns alone give fewer items than the target number of waves.
     const int64_t class_len = d->T > 0 ? ceil_div(d->T, d->dilation) : 0;
     const int64_t base = (int64_t)g.groups * g.tiles * g.d;
     int64_t chunk = class_len > 0 ? class_len : 1;
     int64_t nchunks = 1;
     const int64_t min_chunk = 4 * (int64_t)d->k;
-    while (base * nchunks < kTargetWaves && chunk / 2 >= min_chunk) {
+    const int64_t target = target_waves();
+    while (base * nchunks < target && chunk / 2 >= min_chunk) {
         chunk = ceil_div(chunk, 2);
         nchunks = ceil_div(class_len, chunk);
     }
     g.chunk = (int32_t)chunk;
     g.nchunks = (int32_t)nchunks;
     g.items = (int64_t)g.tiles * g.d * g.nchunks;
-    int64_t R = 1;
-    if (backward) {
-        const int64_t total = g.items * g.groups;
-        R = total / kTargetWaves;
-        if (R < 1)
-            R = 1;
-        if (R > kMaxItemsPerWave)
-            R = kMaxItemsPerWave;
-    }
-    g.R = (int32_t)R;
-    g.blocks = (int32_t)ceil_div(g.items, (int64_t)kWaves * R);
+    // upper bound of the persistent grid (the launcher picks the actual size)
+    int64_t blocks = ceil_div(kMaxResidentBlocks, g.groups);
+    const int64_t need = ceil_div(g.items, kWaves);
+    if (blocks > need)
+        blocks = need;
+    g.blocks = (int32_t)(blocks > 0 ? blocks : 1);
     return g;
 }
 
@@ -185,7 +197,7 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     if (total == 0)
         return MFPSN_OK;
     FwdArgs a;
-    a.g = plan(desc, false);
+    a.g = plan(desc);
     a.x = x;
     a.sign = sign;
     a.shift = shift;
@@ -205,11 +217,11 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
     if (!bytes)
         return MFPSN_ERR_NULL;
     const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
-    *bytes = total > 0 ? workspace_bytes(plan(desc, true)) : 0;
+    *bytes = total > 0 ? workspace_bytes(plan(desc)) : 0;
     return MFPSN_OK;
 }
 
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes,
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
                    const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
                    void* grad_w, void* grad_b, void* workspace, size_t ws_bytes, void* stream)
 {
@@ -223,7 +235,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         return MFPSN_ERR_NULL;
     const int es = elem_bytes(desc->dtype);
     if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, grad_x_bytes(desc->dtype)) ||
-        !aligned(bias, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
+        !aligned(bias, 4) || !aligned(h, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
         !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
         return MFPSN_ERR_ALIGN;
     if (desc->dtype == MFPSN_Q8_8) {
@@ -233,12 +245,13 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
             return MFPSN_ERR_SHAPE;
     }
     BwdArgs a;
-    a.g = plan(desc, true);
+    a.g = plan(desc);
     const size_t need = total > 0 ? workspace_bytes(a.g) : 0;
     if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
         return MFPSN_ERR_WORKSPACE;
     a.x = x;
     a.gs = grad_spikes;
+    a.h = h;
     a.sign = sign;
     a.shift = shift;
     a.bias = bias;

@@ -10,7 +10,7 @@ namespace mfpsn {
 namespace {
 
 template <int DT, int... Ks>
-hipError_t fwd_dispatch(int k, const FwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
+hipError_t fwd_dispatch(int k, FwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
 {
     hipError_t e = hipErrorInvalidValue;
     (void)((k == Ks + 1 ? (e = fwd_k<Ks + 1, DT>(a, st), true) : false) || ...);
@@ -18,7 +18,7 @@ hipError_t fwd_dispatch(int k, const FwdArgs& a, hipStream_t st, std::integer_se
 }
 
 template <int DT, int... Ks>
-hipError_t bwd_dispatch(int k, const BwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
+hipError_t bwd_dispatch(int k, BwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
 {
     hipError_t e = hipErrorInvalidValue;
     (void)((k == Ks + 1 ? (e = bwd_k<Ks + 1, DT>(a, st), true) : false) || ...);
@@ -29,7 +29,7 @@ using Orders = std::make_integer_sequence<int, MFPSN_MAX_K>;
 
 }  // namespace
 
-hipError_t launch_forward(const FwdArgs& a, int dtype, hipStream_t st)
+hipError_t launch_forward(FwdArgs& a, int dtype, hipStream_t st)
 {
     switch (dtype) {
     case kF32: return fwd_dispatch<kF32>(a.g.k, a, st, Orders{});
@@ -39,7 +39,7 @@ hipError_t launch_forward(const FwdArgs& a, int dtype, hipStream_t st)
     }
 }
 
-hipError_t launch_backward(const BwdArgs& a, int dtype, hipStream_t st)
+hipError_t launch_backward(BwdArgs& a, int dtype, hipStream_t st)
 {
     switch (dtype) {
     case kF32: return bwd_dispatch<kF32>(a.g.k, a, st, Orders{});

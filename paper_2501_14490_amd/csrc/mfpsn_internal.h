@@ -14,9 +14,8 @@ enum Dtype : int32_t { kF32 = 0, kBF16 = 1, kQ88 = 2 };
 //       a wave's loads are 64 consecutive channels (coalesced) and every lane
 //       owns a different channel, so grad_w needs no cross-lane reduction.
 //   kPlane (S >= 2, or C < 64): every lane of a block shares one channel c
-//       (taps are wave-uniform); lanes cover 64 consecutive spatial positions
-//       (S >= 64, the last chunk of a plane partly masked) or 64/S whole rows
-//       of S positions for 64/S samples (S < 64).
+//       (taps are wave-uniform); a wave covers 64 consecutive positions
+//       n*S + s of the channel's (n, s) plane.
 enum Mode : int32_t { kLaneChannel = 0, kPlane = 1 };
 
 // Launch geometry, computed on the host by plan() and passed by value.
@@ -24,14 +23,12 @@ struct Geom {
     int32_t T, N, C, S;
     int32_t k, d;
     int32_t mode;
-    int32_t spw;       // plane mode: 64-wide chunks per plane row (S >= 64), else 1
-    int32_t gpw;       // plane mode with S < 64: samples per wave (64 / S), else 1
-    int32_t tiles;     // tiles per group: lane-channel N; plane N*spw or ceil(N/gpw)
+    int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/64)
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk
-    int32_t R;         // items per wave
     int32_t groups;    // gridDim.y: channel groups (lane-channel) or channels (plane)
-    int32_t blocks;    // gridDim.x: blocks per group
+    int32_t blocks;    // gridDim.x: blocks per group (set by the launcher; the
+                       // planner's value is the upper bound the workspace is sized for)
     int64_t items;     // items per group = tiles * d * nchunks
     uint32_t M;        // N*C*S, columns per time step
     int32_t esize;     // bytes per stored element of x / grad_spikes
@@ -39,10 +36,19 @@ struct Geom {
     int32_t sg;        // surrogate kind
     float alpha, v_th;
     int32_t v_th_q;
+    // Float taps move the exponent with one integer add when the input is a
+    // normal number far enough from the exponent limits: fast_lo <= |x| <
+    // fast_hi (derived from [shift_lo, shift_hi]); other inputs (zero,
+    // subnormal, infinite, NaN, near-limit) take the exact ldexp path.
+    float fast_lo, fast_hi;
 };
 
 constexpr int kWaves = 4;          // waves per block
 constexpr int kThreads = 64 * kWaves;
+// Upper bound of blocks resident on one GPU at once (8 blocks of 4 waves per
+// CU is 8 waves per SIMD; 320 CUs covers every CDNA part): the persistent grid
+// never exceeds it, so it also bounds the backward's partial rows.
+constexpr int kMaxResidentBlocks = 8 * 320;
 
 struct FwdArgs {
     Geom g;
@@ -58,6 +64,7 @@ struct BwdArgs {
     Geom g;
     const void* x;
     const void* gs;
+    const void* h;     // H saved by the forward (nullable: recompute from x)
     const int8_t* sign;
     const int8_t* shift;
     const void* bias;
@@ -72,11 +79,13 @@ struct FinArgs {
     void* grad_b;
 };
 
-template <int K, int DT> hipError_t fwd_k(const FwdArgs& a, hipStream_t stream);
-template <int K, int DT> hipError_t bwd_k(const BwdArgs& a, hipStream_t stream);
+// The launchers size the persistent grid from the kernel's occupancy and
+// store the blocks per group they launched in a.g.blocks.
+template <int K, int DT> hipError_t fwd_k(FwdArgs& a, hipStream_t stream);
+template <int K, int DT> hipError_t bwd_k(BwdArgs& a, hipStream_t stream);
 
-hipError_t launch_forward(const FwdArgs& a, int dtype, hipStream_t stream);
-hipError_t launch_backward(const BwdArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_forward(FwdArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_backward(BwdArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_finalize(const FinArgs& a, hipStream_t stream);
 hipError_t launch_quantize(const float* w, int64_t count, int32_t lo, int32_t hi, int8_t* sign,
                            int8_t* shift, hipStream_t stream);

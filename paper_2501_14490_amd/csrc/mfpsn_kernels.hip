@@ -10,21 +10,25 @@
 // restricted to a chunk [j0, j1) of class steps.  The lane keeps the last k
 // inputs of its walk in a register ring, so every input is read from HBM once
 // per pass (plus a (k-1)-step halo per chunk).  The ring is indexed with
-// compile-time slots: the walk is unrolled by k, and class step j lives in
-// slot (j - j0 + k - 1) mod k.
+// compile-time slots: the walk is unrolled by k.  The grid is persistent:
+// as many blocks as fit on the GPU at once, each wave striding over items
+// (column tile, residue class, chunk).
 //
-// Taps never multiply: a float tap is an exact exponent move (v_ldexp_f32)
-// followed by a sign flip (xor of the sign bit) and one rounded add; a Q8.8
-// tap is an arithmetic right shift and an xor-add (the -1 that xor-negation
-// leaves per negative tap is folded into the starting value).  Sums run in
-// ascending tap order from +0 with the bias added last, so the float
-// potentials are bit-identical to a sequential evaluation of the definition.
+// Taps never multiply: a float tap moves the exponent, either with one
+// integer add of ((-shift) << 23) ^ sign-bit to the bit pattern (normal
+// inputs whose result stays normal) or with v_ldexp_f32 and a sign flip (any
+// other input: zero, subnormal, infinite, NaN); a Q8.8 tap is an arithmetic
+// right shift and an xor-add (the -1 that xor-negation leaves per negative
+// tap is folded into the starting value).  Sums run in ascending tap order
+// from +0 with the bias added last, so the float potentials are
+// bit-identical to a sequential evaluation of the definition.
 //
-// The backward recomputes H from the x ring (H is not stored), evaluates the
-// surrogate, pushes dH into a second ring, emits grad_x (k-1) class steps
-// late (when the last dH it needs exists), and accumulates grad_w / grad_b
-// from exact double products (Q8.8: exact integers in double).  Per-lane sums
-// are reduced inside the block in a fixed order and written as per-block
+// The backward walks each class backwards in time: the dH ring then already
+// holds the future values grad_x needs, so grad_x of step j is emitted at
+// step j.  H comes from the forward's saved potentials when the caller
+// passes them, else it is recomputed from the x ring.  grad_w / grad_b are
+// accumulated from exact double products (Q8.8: exact integers in double),
+// reduced inside the block in a fixed order and written as per-block
 // partials; a finalize kernel adds the partials in block order, so the
 // gradients are bitwise reproducible.
 #include <hip/hip_runtime.h>
@@ -39,35 +43,47 @@
 namespace mfpsn {
 namespace {
 
-constexpr uint32_t kOutOfRange = 0x80000000u;  // buffer offset past every num_records we use
-constexpr int kRsrcWord3 = 0x00020000;         // raw (untyped) buffer, gfx9 family
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint64_t byte_off,
-                                                       uint32_t nbytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)base + byte_off), (short)0,
-                                             (int)nbytes, kRsrcWord3);
-}
-
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Loads run P class steps ahead of their use.  P divides k so that the
+// prefetch slot of a step is a compile-time index inside the k-step unrolled
+// block; orders with no divisor in [2, 8] fall back to one step ahead.
+constexpr int prefetch_depth(int K, int cap = 8)
+{
+    if (K <= cap)
+        return K;
+    for (int p = cap; p >= 2; --p)
+        if (K % p == 0)
+            return p;
+    return 1;
+}
+
 // ---------------------------------------------------------------------------
-// storage types
+// storage types.  Every access is (row: uniform 64-bit address of one time
+// step of a tensor, rbytes: that step's size) + (lane byte offset): a raw
+// buffer access whose descriptor the scalar unit rebuilds from the row.
 // ---------------------------------------------------------------------------
+constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_at(uint64_t row, uint32_t rbytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, (int)rbytes, kRsrcWord3);
+}
+
 template <int DT> struct IO;
 
 template <> struct IO<kF32> {
     using V = float;    // register value of x / grad_spikes
     using D = float;    // dH
     static constexpr int es = 4;
-    __device__ static V load(__amdgpu_buffer_rsrc_t r, uint32_t vo)
-    {
-        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, vo, 0, 0));
-    }
     static constexpr int gx_es = 4;
-    __device__ static void store_gx(__amdgpu_buffer_rsrc_t r, uint32_t vo, D v)
+    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
     {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, vo, 0, 0);
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc_at(row, rb), off, 0, 0));
+    }
+    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc_at(row, rb), off, 0, 0);
     }
 };
 
@@ -75,16 +91,17 @@ template <> struct IO<kBF16> {
     using V = float;
     using D = float;
     static constexpr int es = 2;
-    __device__ static V load(__amdgpu_buffer_rsrc_t r, uint32_t vo)
+    static constexpr int gx_es = 2;
+    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
     {
-        uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(r, vo, 0, 0);
+        const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rsrc_at(row, rb), off, 0, 0);
         return __builtin_bit_cast(float, h << 16);
     }
-    static constexpr int gx_es = 2;
-    __device__ static void store_gx(__amdgpu_buffer_rsrc_t r, uint32_t vo, D v)
+    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
     {
-        __bf16 h = (__bf16)v;  // round to nearest even (v_cvt_pk_bf16_f32)
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), r, vo, 0, 0);
+        const __bf16 h = (__bf16)v;  // round to nearest even (v_cvt_pk_bf16_f32)
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rsrc_at(row, rb), off, 0,
+                                              0);
     }
 };
 
@@ -92,17 +109,34 @@ template <> struct IO<kQ88> {
     using V = int32_t;
     using D = int32_t;
     static constexpr int es = 2;
-    __device__ static V load(__amdgpu_buffer_rsrc_t r, uint32_t vo)
+    static constexpr int gx_es = 4;
+    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
     {
-        uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(r, vo, 0, 0);
+        const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rsrc_at(row, rb), off, 0, 0);
         return (int32_t)(int16_t)(uint16_t)h;
     }
-    static constexpr int gx_es = 4;
-    __device__ static void store_gx(__amdgpu_buffer_rsrc_t r, uint32_t vo, D v)
+    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
     {
-        __builtin_amdgcn_raw_buffer_store_b32((uint32_t)v, r, vo, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32((uint32_t)v, rsrc_at(row, rb), off, 0, 0);
     }
 };
+
+// 32-bit words (H, saved or stored) and bytes (spikes)
+__device__ __forceinline__ uint32_t load_w(uint64_t row, uint32_t rb, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(rsrc_at(row, rb), off, 0, 0);
+}
+__device__ __forceinline__ void store_w(uint64_t row, uint32_t rb, uint32_t off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, rsrc_at(row, rb), off, 0, 0);
+}
+__device__ __forceinline__ void store_b(uint64_t row, uint32_t rb, uint32_t off, uint8_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b8(v, rsrc_at(row, rb), off, 0, 0);
+}
+
+// H as saved by the forward: float for the float paths, int32 for Q8.8
+template <int DT> using HVal = typename IO<DT>::V;
 
 // ---------------------------------------------------------------------------
 // taps: weight sign * 2^-shift
@@ -110,23 +144,36 @@ template <> struct IO<kQ88> {
 template <int K, int DT> struct Taps;
 
 template <int K> struct TapsF {
-    int nsh[K];        // -shift
-    uint32_t sm[K];    // sign bit to xor in
+    static constexpr bool kHasFast = true;
+    // ((-shift) << 23) ^ (sign bit of a negative tap): the value added to a
+    // float's bit pattern to scale it by sign * 2^-shift (shift in -126..126)
+    uint32_t kc[K];
     __device__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
     {
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             int s = shift[c * K + i];
             s = s < lo ? lo : (s > hi ? hi : s);
-            nsh[i] = -s;
-            sm[i] = sign[c * K + i] < 0 ? 0x80000000u : 0u;
+            kc[i] = ((uint32_t)(-s) << 23) ^ (sign[c * K + i] < 0 ? 0x80000000u : 0u);
         }
     }
-    // sign * 2^-shift * v: exact exponent move, then sign flip.
+    // sign * 2^-shift * v for any float: exact exponent move (v_ldexp_f32),
+    // then sign flip.  Bits 23..30 of kc are -shift (sign-extended); bit 31 of
+    // ((-shift) << 23) alone is set exactly when shift > 0, so the tap's sign
+    // bit is bit 31 of kc xor (shift > 0).
     __device__ __forceinline__ float apply(float v, int i) const
     {
-        float y = ldexpf(v, nsh[i]);
-        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, y) ^ sm[i]);
+        const int nsh = (int)(kc[i] << 1) >> 24;
+        const uint32_t neg = (kc[i] ^ (nsh < 0 ? 0x80000000u : 0u)) & 0x80000000u;
+        float y = ldexpf(v, nsh);
+        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, y) ^ neg);
+    }
+    // The same value for a normal v whose result stays normal: adding kc to
+    // the bit pattern subtracts the shift from the exponent field and flips
+    // the sign bit.
+    __device__ __forceinline__ float apply_fast(float v, int i) const
+    {
+        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, v) + kc[i]);
     }
 };
 template <int K> struct Taps<K, kF32> : TapsF<K> {};
@@ -148,9 +195,11 @@ template <int K> struct Taps<K, kQ88> {
             cneg -= m[i];
         }
     }
+    static constexpr bool kHasFast = false;
     // (v >> s) ^ m equals +(v >> s) or -(v >> s) - 1; the -1s are cancelled by
     // starting the sum at cneg.
     __device__ __forceinline__ int apply(int v, int i) const { return (v >> sh[i]) ^ m[i]; }
+    __device__ __forceinline__ int apply_fast(int v, int i) const { return apply(v, i); }
 };
 
 // ---------------------------------------------------------------------------
@@ -226,14 +275,33 @@ __device__ __forceinline__ int32_t delta_h(const Surrogate& sg, int32_t g, int32
     return (int32_t)(p >> 15);
 }
 
+// True (wave-uniform) when some active lane's value is outside the range in
+// which the exponent-add tap is exact (lane masks straight from v_cmp).
+__device__ __forceinline__ bool any_slow(float v, const Geom& g, uint64_t act)
+{
+    const float m = __builtin_fabsf(v);
+    const uint64_t ok = __builtin_amdgcn_fcmpf(m, g.fast_lo, 3 /* >= */) &
+                        __builtin_amdgcn_fcmpf(m, g.fast_hi, 4 /* < */);
+    return (act & ~ok) != 0;
+}
+__device__ __forceinline__ bool any_slow(int, const Geom&, uint64_t) { return false; }
+
 // ---------------------------------------------------------------------------
-// lane -> column
+// lane -> column.  Lane-channel tiles: 64 consecutive channels of one sample.
+// Plane tiles: 64 consecutive positions p = n*S + s of one channel's (n, s)
+// plane, so every lane is busy except in the plane's last tile.  A lane whose
+// column does not exist reads and writes the column of the last existing
+// lane of its wave: it computes that lane's values, so its stores duplicate
+// that lane's in the same instruction.  Its grad_w / grad_b contribution is
+// dropped: lane-channel lanes past C write no partial row; in a partial plane
+// tile the backward zeroes the lane's dH before accumulating.
 // ---------------------------------------------------------------------------
 struct Item {
     int r;        // residue class
     int Lr;       // class length
     int j0, j1;   // class-step chunk
     bool active;  // this lane's column exists
+    bool partial; // plane tile with missing columns (wave-uniform)
     uint32_t col; // column index in [0, M)
 };
 
@@ -251,24 +319,26 @@ __device__ __forceinline__ Item decode_item(const Geom& g, int64_t q, int grp, i
     if (MODE == kLaneChannel) {
         const int c = grp * 64 + lane;
         it.active = c < g.C;
-        it.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)c;
-    } else if (g.S >= 64) {
-        const int n = tile / g.spw;
-        const int s = (tile % g.spw) * 64 + lane;
-        it.active = s < g.S;
-        it.col = ((uint32_t)n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + (uint32_t)s;
+        it.partial = false;
+        it.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)min(c, g.C - 1);
     } else {
-        const int n = tile * g.gpw + lane / g.S;
-        const int s = lane % g.S;
-        it.active = (lane < g.gpw * g.S) && (n < g.N);
-        it.col = ((uint32_t)n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + (uint32_t)s;
+        const uint32_t NS = (uint32_t)g.N * (uint32_t)g.S;
+        const uint32_t pos = (uint32_t)tile * 64u + (uint32_t)lane;
+        it.active = pos < NS;
+        it.partial = (uint32_t)tile * 64u + 64u > NS;
+        const uint32_t pc = min(pos, NS - 1u);
+        const uint32_t n = pc / (uint32_t)g.S, s = pc % (uint32_t)g.S;
+        it.col = (n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + s;
     }
     return it;
 }
 
-__device__ __forceinline__ uint32_t voff(const Item& it, int es)
+// addr += inc, kept opaque so the compiler updates one running SGPR pair per
+// stream instead of precomputing (and spilling) an address per unrolled step
+__device__ __forceinline__ void advance(uint64_t& addr, int64_t inc)
 {
-    return it.active ? it.col * (uint32_t)es : kOutOfRange;
+    addr += (uint64_t)inc;
+    asm volatile("" : "+s"(addr));
 }
 
 // ---------------------------------------------------------------------------
@@ -278,13 +348,16 @@ template <int K, int DT, int MODE>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
 {
     using V = typename IO<DT>::V;
+    using TP = Taps<K, DT>;
+    constexpr int P = prefetch_depth(K);
+    constexpr int es = IO<DT>::es;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
     const int grp = blockIdx.y;
     const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
 
-    Taps<K, DT> tp;
+    TP tp;
     tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
     V start;  // value the tap sum starts from
     V bias;
@@ -295,79 +368,103 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
         bias = ((const float*)a.bias)[c];
         start = 0.0f;
     }
-    const uint32_t xstep = g.M * (uint32_t)IO<DT>::es;
-    const uint32_t hstep = g.M * 4u;
+    const int64_t xrow = (int64_t)g.M * es;  // bytes per time step
+    const uint32_t xrb = (uint32_t)xrow, srb = g.M, hrb = g.M * 4u;
+    const int want_h = a.h_out != nullptr ? 1 : 0;
+    const int64_t stride = (int64_t)gridDim.x * kWaves;
 
-    for (int rep = 0; rep < g.R; ++rep) {
-        const int64_t q = ((int64_t)blockIdx.x * kWaves + wave) * g.R + rep;
-        if (q >= g.items)
-            break;
+    for (int64_t q = (int64_t)blockIdx.x * kWaves + wave; q < g.items; q += stride) {
         const Item it = decode_item<MODE>(g, q, grp, lane);
         if (it.j0 >= it.j1)
             continue;
-        const uint32_t vx = voff(it, IO<DT>::es);
-        const uint32_t v1 = voff(it, 1);
-        const uint32_t v4 = voff(it, 4);
-        const int r = it.r, d = g.d;
+        const uint32_t ox = it.col * es, o1 = it.col, o4 = it.col * 4u;
+        const uint64_t act = __builtin_amdgcn_ballot_w64(it.active);
+        const int r = it.r, d = g.d, j0 = it.j0, j1 = it.j1, Lr = it.Lr;
 
-        auto xat = [&](int j) -> V {
-            const int t = r + j * d;
-            return IO<DT>::load(rsrc(a.x, (uint64_t)t * xstep, xstep), vx);
-        };
-        auto out = [&](int j, V h) {
-            const int t = r + j * d;
-            bool fire;
-            if constexpr (DT == kQ88)
-                fire = h >= g.v_th_q;
-            else
-                fire = h >= g.v_th;
-            __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(fire ? 1 : 0),
-                                                 rsrc(a.spikes, (uint64_t)t * g.M, g.M), v1, 0, 0);
-            if (a.h_out)
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, h),
-                                                      rsrc(a.h_out, (uint64_t)t * hstep, hstep), v4,
-                                                      0, 0);
-        };
+        const int64_t xcls = d * xrow, scls = (int64_t)d * g.M, hcls = (int64_t)d * g.M * 4;
+        const uint64_t x0 = (uint64_t)a.x + (uint64_t)(r * xrow);
+        auto xat = [&](int j) -> V { return IO<DT>::load(x0 + (uint64_t)(j * xcls), xrb, ox); };
+        uint64_t xnext = x0 + (uint64_t)((j0 + P) * xcls);  // prefetch of step j + P
+        uint64_t srow = (uint64_t)a.spikes + (uint64_t)(r * (int64_t)g.M + j0 * scls);
+        uint64_t hrow = (uint64_t)a.h_out + (uint64_t)((r * (int64_t)g.M + j0 * scls) * 4);
 
         V ring[K];
+        int slow = 0;  // steps left before every ring entry is in the fast range
 #pragma unroll
         for (int m = 0; m < K - 1; ++m) {
-            const int j = it.j0 - (K - 1) + m;
+            const int j = j0 - (K - 1) + m;
             const V v = xat(max(j, 0));  // never address before the tensor
             ring[m] = j >= 0 ? v : V(0);
+            if (TP::kHasFast && any_slow(ring[m], g, act))
+                slow = m + 1;
         }
-        // one block = K class steps; its K loads are issued before any use
-        // (indices clamped into the chunk) so their latencies overlap.
-        auto block = [&](int jb, auto full_c) {
+        V pf[P];
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            pf[p] = xat(min(j0 + p, Lr - 1));
+
+        // one step: take the prefetched input into the ring, sum the taps,
+        // fire, store; full blocks need no index checks and no clamping
+        auto step = [&](auto uc, int j, auto full_c) __attribute__((always_inline)) {
+            constexpr int u = decltype(uc)::value;
             constexpr bool full = decltype(full_c)::value;
-            V xin[K];
+            const V xv = pf[u % P];
+            if constexpr (full)
+                pf[u % P] = IO<DT>::load(xnext, xrb, ox);
+            else
+                pf[u % P] = xat(min(j + P, Lr - 1));
+            advance(xnext, xcls);
+            ring[(u + K - 1) % K] = xv;
+            V acc = start;
+            if constexpr (TP::kHasFast) {
+                if (any_slow(xv, g, act))
+                    slow = K;
+                if (__builtin_expect(slow > 0, 0)) {
 #pragma unroll
-            for (int u = 0; u < K; ++u)
-                xin[u] = xat(min(jb + u, it.j1 - 1));
-            [&]<int... U>(std::integer_sequence<int, U...>) {
-                (([&] {
-                     constexpr int u = U;
-                     if (!full && jb + u >= it.j1)
-                         return;
-                     ring[(u + K - 1) % K] = xin[u];
-                     V acc = start;
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + tp.apply(ring[(u + i) % K], i);
+                    --slow;
+                } else {
 #pragma unroll
-                     for (int i = 0; i < K; ++i)
-                         acc = acc + tp.apply(ring[(u + i) % K], i);
-                     V h;
-                     if constexpr (DT == kQ88)
-                         h = acc;
-                     else
-                         h = acc + bias;
-                     out(jb + u, h);
-                 }()),
-                 ...);
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + tp.apply_fast(ring[(u + i) % K], i);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    acc = acc + tp.apply(ring[(u + i) % K], i);
+            }
+            V h;
+            bool fire;
+            if constexpr (DT == kQ88) {
+                h = acc;
+                fire = h >= g.v_th_q;
+            } else {
+                h = acc + bias;
+                fire = h >= g.v_th;
+            }
+            store_b(srow, srb, o1, fire ? 1 : 0);
+            if (want_h != 0)
+                store_w(hrow, hrb, o4, __builtin_bit_cast(uint32_t, h));
+            advance(srow, scls);
+            advance(hrow, hcls);
+        };
+        auto block = [&](int jb, auto full_c) __attribute__((always_inline)) {
+            constexpr bool full = decltype(full_c)::value;
+            [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
+                (void)((full || jb + U < j1
+                            ? (step(std::integral_constant<int, U>{}, jb + U, full_c), true)
+                            : false) &&
+                       ...);
             }(std::make_integer_sequence<int, K>{});
         };
-        int j = it.j0;
-        for (; j + K <= it.j1; j += K)
-            block(j, std::true_type{});
-        if (j < it.j1)
+        // orders above 16 keep a single (checked) copy of the block to bound
+        // the code size
+        int j = j0;
+        if constexpr (K <= 16)
+            for (; j + K <= j1 && j + K + P <= Lr; j += K)
+                block(j, std::true_type{});
+        for (; j < j1; j += K)
             block(j, std::false_type{});
     }
 }
@@ -383,11 +480,23 @@ __device__ __forceinline__ double wave_sum(double v)
     return v;
 }
 
-template <int K, int DT, int MODE>
+// Reverse walk over class steps j = jtop, jtop-1, ..., j0 (walk index
+// s = jtop - j, slot u = s mod k).  Rings: x[t] for t in [j-k+1, j] at slot
+// (jtop - t) mod k; dH[t] for t in [j, j+k-1] at slot (jtop - t) mod k, zero
+// for t past the sequence.  Steps above j1 - 1 are the halo of a lower chunk:
+// only their dH is computed.
+template <int K, int DT, int MODE, bool HS>
 __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 {
     using V = typename IO<DT>::V;
     using D = typename IO<DT>::D;
+    using TP = Taps<K, DT>;
+    constexpr int P = prefetch_depth(K, 4);  // three streams: keep the queues short
+    constexpr int es = IO<DT>::es;
+    constexpr int gxs = IO<DT>::gx_es;
+    constexpr bool kRecompute = !HS;
+    // x stays a float ring; each grad_w product widens its x operand at use
+    constexpr bool kWide = false;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
@@ -395,7 +504,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     const int c_lane = (MODE == kLaneChannel) ? grp * 64 + lane : grp;
     const int c = min(c_lane, g.C - 1);
 
-    Taps<K, DT> tp;
+    TP tp;
     tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
     V start, bias;
     D dstart;
@@ -413,8 +522,9 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     sg.alpha = g.alpha;
     sg.c_atan = 0x1.921fb6p+0f * g.alpha;
 
-    const uint32_t xstep = g.M * (uint32_t)IO<DT>::es;
-    const uint32_t gxstep = g.M * (uint32_t)IO<DT>::gx_es;
+    const int64_t xrow = (int64_t)g.M * es, gxrow = (int64_t)g.M * gxs, hrow = (int64_t)g.M * 4;
+    const uint32_t xrb = (uint32_t)xrow, gxrb = (uint32_t)gxrow, hrb = (uint32_t)hrow;
+    const int64_t stride = (int64_t)gridDim.x * kWaves;
 
     double gw[K];
 #pragma unroll
@@ -422,98 +532,185 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         gw[i] = 0.0;
     double gb = 0.0;
 
-    for (int rep = 0; rep < g.R; ++rep) {
-        const int64_t q = ((int64_t)blockIdx.x * kWaves + wave) * g.R + rep;
-        if (q >= g.items)
-            break;
+    for (int64_t q = (int64_t)blockIdx.x * kWaves + wave; q < g.items; q += stride) {
         const Item it = decode_item<MODE>(g, q, grp, lane);
         if (it.j0 >= it.j1)
             continue;
-        const uint32_t vx = voff(it, IO<DT>::es);
-        const uint32_t vgx = voff(it, IO<DT>::gx_es);
+        const uint32_t ox = it.col * es, ogx = it.col * gxs, oh = it.col * 4u;
+        const uint64_t act = __builtin_amdgcn_ballot_w64(it.active);
         const int r = it.r, d = g.d;
         const int j0 = it.j0, j1 = it.j1, Lr = it.Lr;
+        const int jtop = min(j1 + K - 1, Lr) - 1;
 
-        auto at = [&](const void* base, int j) -> V {
-            const int t = r + j * d;
-            return IO<DT>::load(rsrc(base, (uint64_t)t * xstep, xstep), vx);
+        const int64_t xcls = d * xrow, gxcls = d * gxrow, hcls = d * hrow;
+        const uint64_t x0 = (uint64_t)a.x + (uint64_t)(r * xrow);
+        const uint64_t g0 = (uint64_t)a.gs + (uint64_t)(r * xrow);
+        const uint64_t h0 = (uint64_t)a.h + (uint64_t)(r * hrow);
+        auto xat = [&](int j) -> V { return IO<DT>::load(x0 + (uint64_t)(j * xcls), xrb, ox); };
+        auto gat = [&](int j) -> V { return IO<DT>::load(g0 + (uint64_t)(j * xcls), xrb, ox); };
+        auto hat = [&](int j) -> V {
+            return __builtin_bit_cast(V, load_w(h0 + (uint64_t)(j * hcls), hrb, oh));
         };
+        // running addresses: prefetch of walk index s + P (step j - P, its
+        // x-ring entry j - P - k + 1) and the grad_x row of step j
+        uint64_t gnext = g0 + (uint64_t)((jtop - P) * xcls);
+        uint64_t hnext = h0 + (uint64_t)((jtop - P) * hcls);
+        uint64_t xnext = x0 + (uint64_t)((jtop - P - K + 1) * xcls);
+        uint64_t gxrow_j = (uint64_t)a.grad_x + (uint64_t)(r * gxrow + (int64_t)jtop * gxcls);
 
         V xr[K];
-        double xd[K];
+        double xd[kWide ? K : 1];
         D dr[K];
+        int slow_x = 0;      // steps left on the exact recompute path
+        int slow_d = K - 1;  // steps left on the exact grad_x path (the zero dH past the top)
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            dr[i] = D(0);
 #pragma unroll
         for (int m = 0; m < K - 1; ++m) {
-            const int j = j0 - (K - 1) + m;
-            const V v = at(a.x, max(j, 0));  // never address before the tensor
-            xr[m] = j >= 0 ? v : V(0);
-            xd[m] = (double)xr[m];
+            const int t = jtop - m;
+            const V v0 = xat(max(t, 0));  // never address before the tensor
+            const V v = t >= 0 ? v0 : V(0);
+            xr[m] = v;
+            if constexpr (kWide)
+                xd[m] = (double)v;
+            if (kRecompute && TP::kHasFast && any_slow(v, g, act))
+                slow_x = m + 1;
         }
-        const int jend = j1 + K - 1;
-        auto block = [&](int jb, auto full_c) {
+        V pfx[P], pfg[P], pfh[HS ? P : 1];
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int jp = max(jtop - p, 0);
+            pfg[p] = gat(jp);
+            if constexpr (HS)
+                pfh[p] = hat(jp);
+            pfx[p] = xat(max(jtop - p - K + 1, 0));
+        }
+
+        auto step = [&](auto uc, int j, auto full_c) __attribute__((always_inline)) {
+            constexpr int u = decltype(uc)::value;
             constexpr bool full = decltype(full_c)::value;
-            V xin[K], gin[K];
-#pragma unroll
-            for (int u = 0; u < K; ++u) {
-                const int jl = min(jb + u, Lr - 1);
-                xin[u] = at(a.x, jl);
-                gin[u] = at(a.gs, jl);
+            constexpr int xslot = (u + K - 1) % K;
+            const V gv = pfg[u % P];
+            V xv = pfx[u % P];
+            V hv = V(0);
+            if constexpr (HS)
+                hv = pfh[u % P];
+            if constexpr (full) {
+                pfg[u % P] = IO<DT>::load(gnext, xrb, ox);
+                if constexpr (HS)
+                    pfh[u % P] = __builtin_bit_cast(V, load_w(hnext, hrb, oh));
+                pfx[u % P] = IO<DT>::load(xnext, xrb, ox);
+            } else {
+                const int jn = max(j - P, 0);
+                pfg[u % P] = gat(jn);
+                if constexpr (HS)
+                    pfh[u % P] = hat(jn);
+                pfx[u % P] = xat(max(j - P - K + 1, 0));
+                if (j - K + 1 < 0)  // x ring entry before the start of time
+                    xv = V(0);
             }
-            [&]<int... U>(std::integer_sequence<int, U...>) {
-                (([&] {
-                     constexpr int u = U;
-                     constexpr int slot = (u + K - 1) % K;
-                     const int j = jb + u;
-                     if (!full && j >= jend)
-                         return;
-                     D dh = D(0);
-                     if (full || j < Lr) {
-                         xr[slot] = xin[u];
-                         xd[slot] = (double)xin[u];
-                         V acc = start;
+            advance(gnext, -xcls);
+            if constexpr (HS)
+                advance(hnext, -hcls);
+            advance(xnext, -xcls);
+            xr[xslot] = xv;
+            if constexpr (kWide)
+                xd[xslot] = (double)xv;
+            V h;
+            if constexpr (kRecompute) {
+                V acc = start;
+                if constexpr (TP::kHasFast) {
+                    if (any_slow(xv, g, act))
+                        slow_x = K;
+                    if (__builtin_expect(slow_x > 0, 0)) {
 #pragma unroll
-                         for (int i = 0; i < K; ++i)
-                             acc = acc + tp.apply(xr[(u + i) % K], i);
-                         V h;
-                         if constexpr (DT == kQ88)
-                             h = acc;
-                         else
-                             h = acc + bias;
-                         dh = delta_h(sg, gin[u], h, g.v_th, g.v_th_q);
-                     } else {
-                         xr[slot] = V(0);
-                         xd[slot] = 0.0;
-                     }
-                     dr[slot] = dh;
-                     if (full || j < j1) {
-                         const double dd = (double)dh;
+                        for (int i = 0; i < K; ++i)
+                            acc = acc + tp.apply(xr[(u + K - 1 - i) % K], i);
+                        --slow_x;
+                    } else {
 #pragma unroll
-                         for (int i = 0; i < K; ++i)
-                             gw[i] = __builtin_fma(xd[(u + i) % K], dd, gw[i]);
-                         gb += dd;
-                     }
-                     if (full || j >= j0 + K - 1) {
-                         D acc = dstart;
+                        for (int i = 0; i < K; ++i)
+                            acc = acc + tp.apply_fast(xr[(u + K - 1 - i) % K], i);
+                    }
+                } else {
 #pragma unroll
-                         for (int i = 0; i < K; ++i)
-                             acc = acc + tp.apply(dr[(u + K - 1 - i) % K], i);
-                         const int t = r + (j - (K - 1)) * d;
-                         IO<DT>::store_gx(rsrc(a.grad_x, (uint64_t)t * gxstep, gxstep), vgx, acc);
-                     }
-                 }()),
-                 ...);
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + tp.apply(xr[(u + K - 1 - i) % K], i);
+                }
+                if constexpr (DT == kQ88)
+                    h = acc;
+                else
+                    h = acc + bias;
+            } else {
+                h = hv;
+            }
+            const D dh = delta_h(sg, gv, h, g.v_th, g.v_th_q);
+            dr[u] = dh;
+            if (TP::kHasFast && any_slow(dh, g, act))
+                slow_d = K;
+            if (full || j < j1) {
+                double dd = (double)dh;
+                if (!full && it.partial)
+                    dd = it.active ? dd : 0.0;  // no contribution from shadow lanes
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    double xi;
+                    if constexpr (kWide)
+                        xi = xd[(u + K - 1 - i) % K];
+                    else
+                        xi = (double)xr[(u + K - 1 - i) % K];
+                    gw[i] = __builtin_fma(xi, dd, gw[i]);
+                }
+                gb += dd;
+                D acc = dstart;
+                if constexpr (TP::kHasFast) {
+                    if (__builtin_expect(slow_d > 0, 0)) {
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            acc = acc + tp.apply(dr[(u + 1 + i) % K], i);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            acc = acc + tp.apply_fast(dr[(u + 1 + i) % K], i);
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + tp.apply(dr[(u + 1 + i) % K], i);
+                }
+                IO<DT>::store_gx(gxrow_j, gxrb, ogx, acc);
+            }
+            advance(gxrow_j, -gxcls);
+            if (slow_d > 0)
+                --slow_d;
+            // keep the scheduler from hoisting later steps' loads above this
+            // step (which would hold them in registers for a whole block)
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        auto block = [&](int jb, auto full_c) __attribute__((always_inline)) {
+            constexpr bool full = decltype(full_c)::value;
+            [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
+                (void)((full || jb - U >= j0
+                            ? (step(std::integral_constant<int, U>{}, jb - U, full_c), true)
+                            : false) &&
+                       ...);
             }(std::make_integer_sequence<int, K>{});
         };
-        // blocks strictly inside [j0 + K - 1, j1) need no per-step checks
-        int j = j0;
-        block(j, std::false_type{});
-        j += K;
-        for (; j + K <= j1; j += K)
-            block(j, std::true_type{});
-        for (; j < jend; j += K)
-            block(j, std::false_type{});
+        // full blocks: every step owned (j < j1, j >= j0), x-ring entries and
+        // prefetches at or after the start of time.  The first block holds the
+        // halo (or the zero dH past the top); orders above 16 keep one
+        // checked copy only.
+        int jb = jtop;
+        block(jb, std::false_type{});
+        jb -= K;
+        if constexpr (K <= 16)
+            if (!it.partial)
+                for (; jb - K + 1 >= j0 && jb < j1 && jb >= 2 * K - 2 + P; jb -= K)
+                    block(jb, std::true_type{});
+        for (; jb >= j0; jb -= K)
+            block(jb, std::false_type{});
     }
-
     // block reduction in a fixed order, then one partial row per block
     const int C = g.C;
     if constexpr (MODE == kLaneChannel) {
@@ -559,24 +756,52 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 // ---------------------------------------------------------------------------
 // finalize: grad_w[c,i] = sum_b partial[b][i][c], grad_b[c] = sum_b partial[b][k][c]
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void fin_kernel(FinArgs a)
+// One block of 16 waves per 64 outputs: wave w adds the partial rows of a
+// fixed contiguous range of blocks, then wave 0 adds the 16 sums in order,
+// so the result does not depend on scheduling.
+constexpr int kFinWaves = 16;
+
+__global__ __launch_bounds__(64 * kFinWaves) void fin_kernel(FinArgs a)
 {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    const int kk = a.k + 1;
-    if (e >= kk * a.C)
-        return;
-    const int i = e / a.C, c = e % a.C;
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int n_out = (a.k + 1) * a.C;
+    const int e = blockIdx.x * 64 + lane;
+    const bool ok = e < n_out;
+    const int ec = ok ? e : n_out - 1;  // loads stay inside the workspace
+    const int per = (a.blocks + kFinWaves - 1) / kFinWaves;
+    const int b0 = min(w * per, a.blocks);
+    const int b1 = min(b0 + per, a.blocks);
     double s = 0.0;
-    for (int b = 0; b < a.blocks; ++b)
-        s += a.partial[((size_t)b * kk + i) * a.C + c];
+    int b = b0;
+    for (; b + 8 <= b1; b += 8) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = a.partial[(size_t)(b + u) * n_out + ec];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            s += v[u];
+    }
+    for (; b < b1; ++b)
+        s += a.partial[(size_t)b * n_out + ec];
+    __shared__ double red[kFinWaves][64];
+    red[w][lane] = s;
+    __syncthreads();
+    if (w != 0 || !ok)
+        return;
+    double t = red[0][lane];
+    for (int q = 1; q < kFinWaves; ++q)
+        t += red[q][lane];
+    const int i = e / a.C, c = e % a.C;
     if (a.dtype == kQ88) {
-        const int64_t v = (int64_t)s;
+        const int64_t v = (int64_t)t;
         if (i < a.k)
             ((int64_t*)a.grad_w)[c * a.k + i] = v;
         else
             ((int64_t*)a.grad_b)[c] = v;
     } else {
-        const float v = (float)s;
+        const float v = (float)t;
         if (i < a.k)
             ((float*)a.grad_w)[c * a.k + i] = v;
         else
@@ -630,32 +855,69 @@ __global__ __launch_bounds__(256) void quant_kernel(const float* w, int64_t coun
 // ---------------------------------------------------------------------------
 }  // namespace
 
-template <int K, int DT>
-hipError_t fwd_k(const FwdArgs& a, hipStream_t st)
+// Blocks of `kern` that fit on the current device at once (cached per kernel
+// and device).
+template <typename Kern>
+int resident_blocks(Kern kern, int (&cache)[16])
 {
-    dim3 grid(a.g.blocks, a.g.groups), block(kThreads);
-    if (a.g.mode == kLaneChannel)
-        hipLaunchKernelGGL((fwd_kernel<K, DT, kLaneChannel>), grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL((fwd_kernel<K, DT, kPlane>), grid, block, 0, st, a);
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        dev = 0;
+    const int slot = dev & 15;
+    if (cache[slot] == 0) {
+        int per_cu = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kThreads, 0) != hipSuccess)
+            per_cu = 1;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            cus = 1;
+        cache[slot] = (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
+    }
+    return cache[slot];
+}
+
+// Persistent grid: as many blocks per group as fit at once, at most one per
+// kWaves items and never more than the planner's bound.
+inline int persistent_blocks(const Geom& g, int resident)
+{
+    int64_t per_group = resident / g.groups;
+    if (per_group < 1)
+        per_group = 1;
+    const int64_t need = (g.items + kWaves - 1) / kWaves;
+    if (per_group > need)
+        per_group = need;
+    if (per_group > g.blocks)
+        per_group = g.blocks;
+    return (int)(per_group > 0 ? per_group : 1);
+}
+
+template <int K, int DT>
+hipError_t fwd_k(FwdArgs& a, hipStream_t st)
+{
+    static int cache[2][16];
+    const bool lc = a.g.mode == kLaneChannel;
+    auto kern = lc ? fwd_kernel<K, DT, kLaneChannel> : fwd_kernel<K, DT, kPlane>;
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[lc ? 0 : 1]));
+    hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
 
 template <int K, int DT>
-hipError_t bwd_k(const BwdArgs& a, hipStream_t st)
+hipError_t bwd_k(BwdArgs& a, hipStream_t st)
 {
-    dim3 grid(a.g.blocks, a.g.groups), block(kThreads);
-    if (a.g.mode == kLaneChannel)
-        hipLaunchKernelGGL((bwd_kernel<K, DT, kLaneChannel>), grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL((bwd_kernel<K, DT, kPlane>), grid, block, 0, st, a);
+    static int cache[4][16];
+    const bool lc = a.g.mode == kLaneChannel;
+    const bool hs = a.h != nullptr;
+    auto kern = lc ? (hs ? bwd_kernel<K, DT, kLaneChannel, true> : bwd_kernel<K, DT, kLaneChannel, false>)
+                   : (hs ? bwd_kernel<K, DT, kPlane, true> : bwd_kernel<K, DT, kPlane, false>);
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[(lc ? 0 : 2) + (hs ? 1 : 0)]));
+    hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
 
 #ifdef MFPSN_TU_DTYPE
 #define MFPSN_INST(K)                                                                      \
-    template hipError_t fwd_k<K, MFPSN_TU_DTYPE>(const FwdArgs&, hipStream_t);           \
-    template hipError_t bwd_k<K, MFPSN_TU_DTYPE>(const BwdArgs&, hipStream_t);
+    template hipError_t fwd_k<K, MFPSN_TU_DTYPE>(FwdArgs&, hipStream_t);                 \
+    template hipError_t bwd_k<K, MFPSN_TU_DTYPE>(BwdArgs&, hipStream_t);
 #define MFPSN_IN_TU(K) (MFPSN_TU_KLO <= (K) && (K) <= MFPSN_TU_KHI)
 #if MFPSN_IN_TU(1)
 MFPSN_INST(1)
@@ -761,7 +1023,7 @@ hipError_t launch_finalize(const FinArgs& a, hipStream_t st)
     const int n = (a.k + 1) * a.C;
     if (n == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(fin_kernel, dim3((n + 255) / 256), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(fin_kernel, dim3((n + 63) / 64), dim3(64 * kFinWaves), 0, st, a);
     return hipGetLastError();
 }
 

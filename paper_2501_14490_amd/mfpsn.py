@@ -54,7 +54,7 @@ _lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_forward.restype = ctypes.c_int
 _lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
-_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
@@ -133,13 +133,13 @@ def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
     return int(n.value)
 
 
-def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b,
+def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sign, shift, bias, grad_x, grad_w, grad_b,
                    workspace, workspace_bytes=None, stream=None) -> None:
     if workspace_bytes is None:
         workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(sign), _ptr(shift),
-                               _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b), _ptr(workspace),
-                               int(workspace_bytes), _stream(stream)), "mfpsn_backward")
+    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(h), _ptr(sign),
+                               _ptr(shift), _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
+                               _ptr(workspace), int(workspace_bytes), _stream(stream)), "mfpsn_backward")
 
 
 def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=None) -> None:
@@ -169,17 +169,20 @@ def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, stream=
     return (spikes, h) if want_h else spikes
 
 
-def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None):
+def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, h=None):
+    """h: optional saved potentials from forward(..., want_h=True)."""
     dev = x.device
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
+    if h is not None:
+        _expect(h, H_OUT[desc.dtype], dev, "h")
     grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
     grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
     grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
     need = mfpsn_backward_workspace_size(desc)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
-    mfpsn_backward(desc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
+    mfpsn_backward(desc, x, grad_spikes, h, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
                    stream=stream)
     return grad_x, grad_w, grad_b
 
@@ -205,14 +208,14 @@ class MfPSNFunction(torch.autograd.Function):
         sign, shift = quantize(w.detach().contiguous(), shift_lo, shift_hi)
         xc = x.detach().contiguous()
         bc = b.detach().float().contiguous()
-        spikes = forward(desc, xc, sign, shift, bc)
-        ctx.save_for_backward(xc, sign, shift, bc)
+        spikes, h = forward(desc, xc, sign, shift, bc, want_h=True)
+        ctx.save_for_backward(xc, sign, shift, bc, h)
         ctx.desc = desc
         return spikes.to(x.dtype)
 
     @staticmethod
     def backward(ctx, grad_spikes):
-        xc, sign, shift, bc = ctx.saved_tensors
+        xc, sign, shift, bc, h = ctx.saved_tensors
         g = grad_spikes.to(xc.dtype).contiguous()
-        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc)
+        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, h=h)
         return grad_x, grad_w, grad_b, None, None, None, None, None, None, None

@@ -29,7 +29,7 @@ def to_dev(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256):
+def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved_h=False):
     x = to_dev(case["x"], dtype)
     g = to_dev(case["grad_spikes"], dtype)
     sign = to_dev(case["sign"], None)
@@ -37,7 +37,7 @@ def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7,
     bias = to_dev(case["bias"], None)
     desc = mfpsn.make_desc(case["x"].shape, k, d, dtype, surrogate, alpha, v_th, v_th_q, lo, hi)
     spikes, h = mfpsn.forward(desc, x, sign, shift, bias, want_h=True)
-    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias)
+    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, h=h if saved_h else None)
     torch.cuda.synchronize()
     out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "grad_w": gw.cpu().numpy(),
            "grad_b": gb.cpu().numpy()}
@@ -103,26 +103,28 @@ SHAPES = [
 ]
 
 
+@pytest.mark.parametrize("saved_h", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
 @pytest.mark.parametrize("shape_i", range(len(SHAPES)))
 @pytest.mark.parametrize("k,d", [(1, 1), (2, 3), (3, 2), (5, 1), (8, 4), (16, 2)])
-def test_small_shapes(orc, dtype, shape_i, k, d):
+def test_small_shapes(orc, dtype, shape_i, k, d, saved_h):
     (T, N, C, sp), label = SHAPES[shape_i]
     case = workloads.make_small(T, N, C, sp, k=k, s_lo=0, s_hi=7, dtype=dtype, seed=100 + k * 7 + d)
     v_th = 0.5
-    got = gpu_run(case, k, d, dtype, v_th)
+    got = gpu_run(case, k, d, dtype, v_th, saved_h=saved_h)
     ref = oracle_run(orc, case, k, d, dtype, v_th)
-    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype}")
+    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_h={saved_h}")
 
 
+@pytest.mark.parametrize("saved_h", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "q8_8"])
 @pytest.mark.parametrize("k", [4, 7, 12, 17, 24, 31, 32])
-def test_orders(orc, dtype, k):
+def test_orders(orc, dtype, k, saved_h):
     d = 1 + k % 3
     case = workloads.make_small(3 * k + 5, 4, 70, (), k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
     ref = oracle_run(orc, case, k, d, dtype, 0.75)
-    got = gpu_run(case, k, d, dtype, 0.75)
-    compare(got, ref, dtype, f"k={k} d={d} {dtype}")
+    got = gpu_run(case, k, d, dtype, 0.75, saved_h=saved_h)
+    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_h={saved_h}")
 
 
 @pytest.mark.parametrize("surrogate,alpha", [("atan", 2.0), ("atan", 5.0), ("rational", 10.0), ("sigmoid", 1.5)])
@@ -150,14 +152,63 @@ def test_short_sequences(orc, T):
     compare(got, ref, "f32", f"T={T}")
 
 
-def test_long_sequence_is_chunked(orc):
-    # few columns and a long time axis: the planner cuts each residue class into chunks
-    case = workloads.make_small(1500, 2, 64, (), k=8, dtype="q8_8", seed=9)
-    got = gpu_run(case, 8, 3, "q8_8", 0.0)
-    ref = oracle_run(orc, case, 8, 3, "q8_8", 0.0)
+@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("k,d", [(8, 3), (16, 1), (5, 7)])
+def test_long_sequence_is_chunked(orc, k, d, saved_h):
+    # few columns and a long time axis: the planner cuts each residue class
+    # into chunks whose halos are recomputed
+    case = workloads.make_small(1500, 2, 64, (), k=k, dtype="q8_8", seed=9)
+    got = gpu_run(case, k, d, "q8_8", 0.0, saved_h=saved_h)
+    ref = oracle_run(orc, case, k, d, "q8_8", 0.0)
     compare(got, ref, "q8_8", "chunked")
-    case = workloads.make_small(1500, 2, 64, (), k=8, dtype="f32", seed=9)
-    compare(gpu_run(case, 8, 3, "f32", 0.3), oracle_run(orc, case, 8, 3, "f32", 0.3), "f32", "chunked f32")
+    case = workloads.make_small(1500, 2, 64, (), k=k, dtype="f32", seed=9)
+    compare(gpu_run(case, k, d, "f32", 0.3, saved_h=saved_h), oracle_run(orc, case, k, d, "f32", 0.3),
+            "f32", "chunked f32")
+
+
+def compare_nan_aware(got, ref, label):
+    """Like compare() for f32, but NaN equals NaN whatever its payload."""
+    assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
+    for name, r in (("H", ref["Hf"]), ("grad_x", ref["grad_x"])):
+        g = got[name]
+        nan = np.isnan(r)
+        assert np.array_equal(np.isnan(g), nan), f"{label}: {name} NaN pattern differs"
+        assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: {name} differs"
+
+
+@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("k,d", [(8, 1), (16, 2), (5, 3), (24, 1)])
+def test_special_values_take_the_exact_path(orc, k, d, saved_h):
+    # zeros, subnormals, values at the edge of the exponent-add range, huge
+    # values, infinities: every tap must still equal the exact ldexp result
+    case = workloads.make_small(60, 3, 80, (), k=k, s_lo=0, s_hi=7, dtype="f32", seed=k + d)
+    x = case["x"]
+    rng = np.random.default_rng(k)
+    specials = np.array([0.0, -0.0, 1e-40, -3e-39, 2.0 ** -119, -(2.0 ** -119), 2.0 ** -120,
+                         np.nextafter(np.float32(2.0 ** -119), np.float32(0)), 3e38, -3e38, 1e30],
+                        np.float32)
+    idx = rng.integers(0, x.size, size=400)
+    x.ravel()[idx] = specials[rng.integers(0, specials.size, size=idx.size)]
+    x[5:9, 1, :] = 0.0  # whole rows of zeros inside the walk
+    got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
+    ref = oracle_run(orc, case, k, d, "f32", 0.25)
+    compare_nan_aware(got, ref, f"specials k={k} d={d}")
+    case["x"].ravel()[rng.integers(0, x.size, size=20)] = np.float32(np.inf)
+    case["grad_spikes"].ravel()[rng.integers(0, x.size, size=200)] = 0.0
+    got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
+    ref = oracle_run(orc, case, k, d, "f32", 0.25)
+    compare_nan_aware(got, ref, f"specials+inf k={k} d={d}")
+
+
+def test_negative_shifts_near_overflow(orc):
+    # left shifts (negative shift) push large inputs toward overflow; the
+    # fast range shrinks accordingly and the exact path takes the rest
+    case = workloads.make_small(30, 2, 64, (), k=4, s_lo=-6, s_hi=3, dtype="f32", seed=4)
+    case["x"].ravel()[::7] = np.float32(2.0 ** 124)
+    case["x"].ravel()[3::11] = np.float32(-(2.0 ** 127))
+    got = gpu_run(case, 4, 2, "f32", 1.0, lo=-6, hi=3)
+    ref = oracle_run(orc, case, 4, 2, "f32", 1.0, lo=-6, hi=3)
+    compare_nan_aware(got, ref, "near overflow")
 
 
 def test_zero_input_gives_bias(orc):
@@ -223,7 +274,9 @@ def test_workloads_full_size(orc, wid):
         desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
                                wl.s_max)
         spikes, h = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True)
-        gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"])
+        saved = d % 2 == 1  # odd dilations read the saved H, even ones recompute it
+        gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"],
+                                    h=h if saved else None)
         torch.cuda.synchronize()
         got = {"spikes": spikes.index_select(2, chans_t).cpu().numpy(),
                "H": h.index_select(2, chans_t).cpu().numpy(),
