@@ -32,6 +32,18 @@ double q88_max_dh(const mfpsn_desc* d)
     return ceil(32768.0 * peak) + 1.0;
 }
 
+// Longest chunk of class steps (a multiple of k) whose byte span, with the
+// halo and prefetch rows, still fits the 31-bit scalar offsets the kernels
+// use inside one item (4-byte elements, the widest stream); 0 if none fits.
+int64_t max_chunk(const mfpsn_desc* d)
+{
+    const int64_t row = (int64_t)d->N * d->C * d->S * 4 * d->dilation;
+    if (row <= 0)
+        return INT64_MAX;
+    const int64_t rows = (((int64_t)1 << 31) - 1) / row - 3 * (int64_t)d->k - 8;
+    return rows >= d->k ? rows / d->k * d->k : 0;
+}
+
 int validate(const mfpsn_desc* d)
 {
     if (!d)
@@ -52,6 +64,8 @@ int validate(const mfpsn_desc* d)
         return MFPSN_ERR_SHAPE;
     if (d->C > 65535 && !(d->S == 1))  // plane mode puts one channel per grid row
         return MFPSN_ERR_SHAPE;
+    if (M > 0 && d->T > 0 && max_chunk(d) == 0)  // k rows of one class do not fit 31-bit offsets
+        return MFPSN_ERR_SHAPE;
     if (d->shift_lo > d->shift_hi)
         return MFPSN_ERR_PARAM;
     if (d->dtype == MFPSN_Q8_8) {
@@ -71,20 +85,24 @@ int validate(const mfpsn_desc* d)
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Launch geometry.  Lanes walk residue classes; when the columns alone give
-// too few waves, each class is cut into chunks of at least 4k steps.
-// Target number of (wave-sized) work items, overridable for tuning with the
-// MFPSN_TARGET_WAVES environment variable.
-int64_t target_waves()
+// too few waves, each class is cut into chunks (multiples of k, of at least
+// 4k steps).  Target number of (wave-sized) work items per pass, overridable
+// for tuning with MFPSN_FWD_ITEMS / MFPSN_BWD_ITEMS.
+int64_t env_int(const char* name, int64_t dflt)
 {
-    static int64_t v = [] {
-        const char* e = getenv("MFPSN_TARGET_WAVES");
-        const long long x = e ? atoll(e) : 0;
-        return (int64_t)(x > 0 ? x : 2048);
-    }();
-    return v;
+    const char* e = getenv(name);
+    const long long x = e ? atoll(e) : 0;
+    return x > 0 ? (int64_t)x : dflt;
 }
 
-Geom plan(const mfpsn_desc* d)
+int64_t target_items(bool backward)
+{
+    static const int64_t fwd = env_int("MFPSN_FWD_ITEMS", 2048);
+    static const int64_t bwd = env_int("MFPSN_BWD_ITEMS", 2048);
+    return backward ? bwd : fwd;
+}
+
+Geom plan(const mfpsn_desc* d, bool backward)
 {
     Geom g;
     memset(&g, 0, sizeof(g));
@@ -124,18 +142,25 @@ Geom plan(const mfpsn_desc* d)
         g.groups = d->C;
         g.tiles = (int32_t)ceil_div((int64_t)d->N * d->S, 64);
     }
-    // Cut each residue class into chunks (of at least 4k steps) only while
-    // the columns alone give fewer items than the target number of waves.
+    // Cut each residue class into chunks only while the columns alone give
+    // fewer items than the target (or a class spans too many bytes).
+    const int64_t K = d->k;
     const int64_t class_len = d->T > 0 ? ceil_div(d->T, d->dilation) : 0;
     const int64_t base = (int64_t)g.groups * g.tiles * g.d;
-    int64_t chunk = class_len > 0 ? class_len : 1;
-    int64_t nchunks = 1;
-    const int64_t min_chunk = 4 * (int64_t)d->k;
-    const int64_t target = target_waves();
-    while (base * nchunks < target && chunk / 2 >= min_chunk) {
-        chunk = ceil_div(chunk, 2);
+    const int64_t cap = max_chunk(d);
+    int64_t chunk = ceil_div(class_len > 0 ? class_len : 1, K) * K;
+    if (chunk > cap)
+        chunk = cap;
+    int64_t nchunks = ceil_div(class_len, chunk);
+    const int64_t min_chunk = 4 * K;
+    const int64_t target = target_items(backward);
+    while (base * nchunks < target && ceil_div(chunk / 2, K) * K >= min_chunk &&
+           ceil_div(chunk / 2, K) * K < chunk) {
+        chunk = ceil_div(chunk / 2, K) * K;
         nchunks = ceil_div(class_len, chunk);
     }
+    if (nchunks < 1)
+        nchunks = 1;
     g.chunk = (int32_t)chunk;
     g.nchunks = (int32_t)nchunks;
     g.items = (int64_t)g.tiles * g.d * g.nchunks;
@@ -197,7 +222,7 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     if (total == 0)
         return MFPSN_OK;
     FwdArgs a;
-    a.g = plan(desc);
+    a.g = plan(desc, false);
     a.x = x;
     a.sign = sign;
     a.shift = shift;
@@ -217,7 +242,7 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
     if (!bytes)
         return MFPSN_ERR_NULL;
     const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
-    *bytes = total > 0 ? workspace_bytes(plan(desc)) : 0;
+    *bytes = total > 0 ? workspace_bytes(plan(desc, true)) : 0;
     return MFPSN_OK;
 }
 
@@ -239,13 +264,13 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
         return MFPSN_ERR_ALIGN;
     if (desc->dtype == MFPSN_Q8_8) {
-        // every partial sum of grad_w must stay an exact integer in double
+        // every partial sum of grad_w must fit int64
         const double reach = (double)desc->T * desc->N * desc->S * 32768.0 * q88_max_dh(desc);
-        if (reach >= 9007199254740992.0)
+        if (reach >= 4611686018427387904.0)
             return MFPSN_ERR_SHAPE;
     }
     BwdArgs a;
-    a.g = plan(desc);
+    a.g = plan(desc, true);
     const size_t need = total > 0 ? workspace_bytes(a.g) : 0;
     if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
         return MFPSN_ERR_WORKSPACE;

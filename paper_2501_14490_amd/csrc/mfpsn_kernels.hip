@@ -7,34 +7,46 @@
 // are independent time series.  A dilated order-k convolution only couples
 // time steps of one residue class t = r (mod d), so each lane walks one
 // column along one residue class (class step j <-> time r + j*d), optionally
-// restricted to a chunk [j0, j1) of class steps.  The lane keeps the last k
-// inputs of its walk in a register ring, so every input is read from HBM once
-// per pass (plus a (k-1)-step halo per chunk).  The ring is indexed with
-// compile-time slots: the walk is unrolled by k.  The grid is persistent:
-// as many blocks as fit on the GPU at once, each wave striding over items
-// (column tile, residue class, chunk).
+// restricted to a chunk [j0, j1) of class steps (chunks start at multiples of
+// k).  Each wave owns an equal share of these items (a contiguous range), so
+// the persistent grid finishes together.  Register rings are indexed by
+// j mod k, and the walks are unrolled in blocks of k steps aligned to
+// multiples of k, so every ring slot is a compile-time register.  Block
+// variants: full (no bounds checks), checked (per-step uniform guards and
+// clamped prefetches), and the block that touches the start of the sequence,
+// where the taps that would read before time 0 are left out at compile time.
+//
+// Memory: one raw buffer resource per tensor and item, a per-lane column
+// offset, and a per-step running scalar offset (one SALU add per stream and
+// step).  Loads run P class steps ahead of their use.
 //
 // Taps never multiply: a float tap moves the exponent, either with one
 // integer add of ((-shift) << 23) ^ sign-bit to the bit pattern (normal
-// inputs whose result stays normal) or with v_ldexp_f32 and a sign flip (any
-// other input: zero, subnormal, infinite, NaN); a Q8.8 tap is an arithmetic
-// right shift and an xor-add (the -1 that xor-negation leaves per negative
-// tap is folded into the starting value).  Sums run in ascending tap order
-// from +0 with the bias added last, so the float potentials are
-// bit-identical to a sequential evaluation of the definition.
+// values whose result stays normal) or with v_ldexp_f32 and a sign flip (any
+// other value); a Q8.8 tap is an arithmetic right shift and an xor-add (the
+// -1 that xor-negation leaves per negative tap is folded into the starting
+// value).  Sums run in ascending tap order (starting from +0 in the
+// definition; the first term is taken as is, which can only differ in the
+// sign of a zero, and a zero bias is added as +0), bias last, so the float
+// potentials and input gradients are bit-identical to a sequential
+// evaluation of the definition.
 //
-// The backward walks each class backwards in time: the dH ring then already
-// holds the future values grad_x needs, so grad_x of step j is emitted at
-// step j.  H comes from the forward's saved potentials when the caller
-// passes them, else it is recomputed from the x ring.  grad_w / grad_b are
-// accumulated from exact double products (Q8.8: exact integers in double),
-// reduced inside the block in a fixed order and written as per-block
-// partials; a finalize kernel adds the partials in block order, so the
-// gradients are bitwise reproducible.
+// Backward.  Each class is walked backwards in time.  dH[j] is computed once
+// (from the forward's saved H, or from H recomputed out of the x ring) and
+// scattered into the k open grad_x accumulators it feeds (outputs j-k+1..j);
+// contributions reach every output in ascending tap order, so the sum order
+// is the definition's.  Output j is complete after step j and is stored.
+// Lanes whose dH is zero skip the scatter (their terms are all zeros), so
+// the exponent-add path stays usable where the surrogate underflows.
+// grad_w / grad_b are accumulated from exact products: double for float data
+// (the x ring is kept in double), int64 for Q8.8; they are reduced inside the
+// block in a fixed order and written as per-block partials, which a finalize
+// kernel adds in block order, so the gradients are bitwise reproducible.
 #include <hip/hip_runtime.h>
 #include <hip/hip_bf16.h>
 #include <stdint.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "mfpsn_internal.h"
@@ -44,11 +56,14 @@ namespace mfpsn {
 namespace {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t uniform_u(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
 
-// Loads run P class steps ahead of their use.  P divides k so that the
-// prefetch slot of a step is a compile-time index inside the k-step unrolled
-// block; orders with no divisor in [2, 8] fall back to one step ahead.
-constexpr int prefetch_depth(int K, int cap = 8)
+// Prefetch distance: a divisor of k (so the prefetch slot of a step is a
+// compile-time index inside a k-step block), at most `cap`.
+constexpr int prefetch_depth(int K, int cap)
 {
     if (K <= cap)
         return K;
@@ -58,92 +73,114 @@ constexpr int prefetch_depth(int K, int cap = 8)
     return 1;
 }
 
+template <int V> using ic = std::integral_constant<int, V>;
+enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 };
+
 // ---------------------------------------------------------------------------
-// storage types.  Every access is (row: uniform 64-bit address of one time
-// step of a tensor, rbytes: that step's size) + (lane byte offset): a raw
-// buffer access whose descriptor the scalar unit rebuilds from the row.
+// buffers: raw buffer resource over [tensor + off, tensor end), per-lane
+// voffset, uniform soffset.  Every access the kernels issue lies inside the
+// tensor by construction (prefetches are clamped in checked blocks).
 // ---------------------------------------------------------------------------
 constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_at(uint64_t row, uint32_t rbytes)
+struct Buf {
+    __amdgpu_buffer_rsrc_t rs;
+};
+
+__device__ __forceinline__ Buf make_buf(const void* tensor, uint64_t tensor_bytes, uint64_t off)
 {
-    return __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, (int)rbytes, kRsrcWord3);
+    const uint64_t rem = off < tensor_bytes ? tensor_bytes - off : 0;
+    const uint32_t n = rem > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)rem;
+    Buf b;
+    b.rs = __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)tensor + off), (short)0, (int)n, kRsrcWord3);
+    return b;
 }
 
+__device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(b.rs, v, s, 0);
+}
+__device__ __forceinline__ uint32_t ld16(Buf b, uint32_t v, int32_t s)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, 0);
+}
+__device__ __forceinline__ void st32(Buf b, uint32_t v, int32_t s, uint32_t x)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(x, b.rs, v, s, 0);
+}
+__device__ __forceinline__ void st16(Buf b, uint32_t v, int32_t s, uint16_t x)
+{
+    __builtin_amdgcn_raw_buffer_store_b16(x, b.rs, v, s, 0);
+}
+__device__ __forceinline__ void st8(Buf b, uint32_t v, int32_t s, uint8_t x)
+{
+    __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, 0);
+}
+
+// s += inc with an opaque increment, so the compiler keeps one running SGPR
+// per stream instead of precomputing (and spilling) an offset per unrolled
+// step
+__device__ __forceinline__ void advance(int32_t& s, int32_t inc)
+{
+    asm volatile("" : "+s"(inc));
+    s += inc;
+}
+
+// Makes v opaque at this point: the code that produces it cannot be sunk
+// past here (the compiler would otherwise defer the grad_w updates of a whole
+// unrolled block to its end and keep every step's operands live).
+template <typename T>
+__device__ __forceinline__ void pin(T& v)
+{
+    asm volatile("" : "+v"(v));
+}
+
+// ---------------------------------------------------------------------------
+// storage types
+// ---------------------------------------------------------------------------
 template <int DT> struct IO;
 
 template <> struct IO<kF32> {
-    using V = float;    // register value of x / grad_spikes
-    using D = float;    // dH
-    static constexpr int es = 4;
-    static constexpr int gx_es = 4;
-    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
+    using V = float;     // value of x / grad_spikes / H / dH in registers
+    using W = double;    // exact product accumulator of grad_w, grad_b
+    static constexpr int es = 4;     // bytes per stored x / grad_spikes
+    static constexpr int gx_es = 4;  // bytes per stored grad_x
+    __device__ static V load(Buf b, uint32_t v, int32_t s) { return __builtin_bit_cast(float, ld32(b, v, s)); }
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x)
     {
-        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc_at(row, rb), off, 0, 0));
-    }
-    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
-    {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc_at(row, rb), off, 0, 0);
+        st32(b, v, s, __builtin_bit_cast(uint32_t, x));
     }
 };
 
 template <> struct IO<kBF16> {
     using V = float;
-    using D = float;
+    using W = double;
     static constexpr int es = 2;
     static constexpr int gx_es = 2;
-    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
+    __device__ static V load(Buf b, uint32_t v, int32_t s) { return __builtin_bit_cast(float, ld16(b, v, s) << 16); }
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x)
     {
-        const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rsrc_at(row, rb), off, 0, 0);
-        return __builtin_bit_cast(float, h << 16);
-    }
-    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
-    {
-        const __bf16 h = (__bf16)v;  // round to nearest even (v_cvt_pk_bf16_f32)
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rsrc_at(row, rb), off, 0,
-                                              0);
+        const __bf16 h = (__bf16)x;  // round to nearest even
+        st16(b, v, s, __builtin_bit_cast(uint16_t, h));
     }
 };
 
 template <> struct IO<kQ88> {
     using V = int32_t;
-    using D = int32_t;
+    using W = int64_t;
     static constexpr int es = 2;
     static constexpr int gx_es = 4;
-    __device__ static V load(uint64_t row, uint32_t rb, uint32_t off)
-    {
-        const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rsrc_at(row, rb), off, 0, 0);
-        return (int32_t)(int16_t)(uint16_t)h;
-    }
-    __device__ static void store_gx(uint64_t row, uint32_t rb, uint32_t off, D v)
-    {
-        __builtin_amdgcn_raw_buffer_store_b32((uint32_t)v, rsrc_at(row, rb), off, 0, 0);
-    }
+    __device__ static V load(Buf b, uint32_t v, int32_t s) { return (int32_t)(int16_t)(uint16_t)ld16(b, v, s); }
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x) { st32(b, v, s, (uint32_t)x); }
 };
 
-// 32-bit words (H, saved or stored) and bytes (spikes)
-__device__ __forceinline__ uint32_t load_w(uint64_t row, uint32_t rb, uint32_t off)
-{
-    return __builtin_amdgcn_raw_buffer_load_b32(rsrc_at(row, rb), off, 0, 0);
-}
-__device__ __forceinline__ void store_w(uint64_t row, uint32_t rb, uint32_t off, uint32_t v)
-{
-    __builtin_amdgcn_raw_buffer_store_b32(v, rsrc_at(row, rb), off, 0, 0);
-}
-__device__ __forceinline__ void store_b(uint64_t row, uint32_t rb, uint32_t off, uint8_t v)
-{
-    __builtin_amdgcn_raw_buffer_store_b8(v, rsrc_at(row, rb), off, 0, 0);
-}
-
-// H as saved by the forward: float for the float paths, int32 for Q8.8
-template <int DT> using HVal = typename IO<DT>::V;
-
 // ---------------------------------------------------------------------------
-// taps: weight sign * 2^-shift
+// taps: weight sign * 2^-shift.  Lane-channel mode holds one channel per lane
+// (VGPRs); plane mode shares one channel across the block (SGPRs).
 // ---------------------------------------------------------------------------
-template <int K, int DT> struct Taps;
+template <int K, int DT, int MODE> struct Taps;
 
-template <int K> struct TapsF {
+template <int K, int MODE> struct TapsF {
     static constexpr bool kHasFast = true;
     // ((-shift) << 23) ^ (sign bit of a negative tap): the value added to a
     // float's bit pattern to scale it by sign * 2^-shift (shift in -126..126)
@@ -154,17 +191,23 @@ template <int K> struct TapsF {
         for (int i = 0; i < K; ++i) {
             int s = shift[c * K + i];
             s = s < lo ? lo : (s > hi ? hi : s);
-            kc[i] = ((uint32_t)(-s) << 23) ^ (sign[c * K + i] < 0 ? 0x80000000u : 0u);
+            uint32_t v = ((uint32_t)(-s) << 23) ^ (sign[c * K + i] < 0 ? 0x80000000u : 0u);
+            kc[i] = MODE == kPlane ? uniform_u(v) : v;
         }
     }
     // sign * 2^-shift * v for any float: exact exponent move (v_ldexp_f32),
     // then sign flip.  Bits 23..30 of kc are -shift (sign-extended); bit 31 of
     // ((-shift) << 23) alone is set exactly when shift > 0, so the tap's sign
     // bit is bit 31 of kc xor (shift > 0).
+    // (The shift and sign are derived from an opaque copy of kc, so the
+    // compiler cannot hoist them out of the walk and hold 2k more registers
+    // for a path that rarely runs.)
     __device__ __forceinline__ float apply(float v, int i) const
     {
-        const int nsh = (int)(kc[i] << 1) >> 24;
-        const uint32_t neg = (kc[i] ^ (nsh < 0 ? 0x80000000u : 0u)) & 0x80000000u;
+        uint32_t k = kc[i];
+        asm volatile("" : "+v"(k));
+        const int nsh = (int)(k << 1) >> 24;
+        const uint32_t neg = (k ^ (nsh < 0 ? 0x80000000u : 0u)) & 0x80000000u;
         float y = ldexpf(v, nsh);
         return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, y) ^ neg);
     }
@@ -176,28 +219,32 @@ template <int K> struct TapsF {
         return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, v) + kc[i]);
     }
 };
-template <int K> struct Taps<K, kF32> : TapsF<K> {};
-template <int K> struct Taps<K, kBF16> : TapsF<K> {};
+template <int K, int MODE> struct Taps<K, kF32, MODE> : TapsF<K, MODE> {};
+template <int K, int MODE> struct Taps<K, kBF16, MODE> : TapsF<K, MODE> {};
 
-template <int K> struct Taps<K, kQ88> {
+template <int K, int MODE> struct Taps<K, kQ88, MODE> {
+    static constexpr bool kHasFast = false;
     int sh[K];         // shift, 0..31
     int m[K];          // 0 (positive tap) or -1 (negative tap)
     int cneg;          // number of negative taps
+    uint32_t negmask;  // bit i set for a negative tap i
     __device__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
     {
         cneg = 0;
+        negmask = 0;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             int s = shift[c * K + i];
             s = s < lo ? lo : (s > hi ? hi : s);
-            sh[i] = s;
-            m[i] = sign[c * K + i] < 0 ? -1 : 0;
-            cneg -= m[i];
+            const bool neg = sign[c * K + i] < 0;
+            sh[i] = MODE == kPlane ? uniform(s) : s;
+            m[i] = MODE == kPlane ? uniform(neg ? -1 : 0) : (neg ? -1 : 0);
+            cneg += neg ? 1 : 0;
+            negmask |= neg ? (1u << i) : 0u;
         }
     }
-    static constexpr bool kHasFast = false;
     // (v >> s) ^ m equals +(v >> s) or -(v >> s) - 1; the -1s are cancelled by
-    // starting the sum at cneg.
+    // starting the sum at the number of negative taps it contains.
     __device__ __forceinline__ int apply(int v, int i) const { return (v >> sh[i]) ^ m[i]; }
     __device__ __forceinline__ int apply_fast(int v, int i) const { return apply(v, i); }
 };
@@ -205,16 +252,15 @@ template <int K> struct Taps<K, kQ88> {
 // ---------------------------------------------------------------------------
 // surrogate derivative (float, fixed operation sequence)
 // ---------------------------------------------------------------------------
-// exp(y): Cody-Waite reduction with ln 2 = hi + lo (hi has 15 significant
-// bits), degree-7 Taylor polynomial of e^r by fma Horner steps, scaling by
-// 2^n.  y < -86 (or NaN) gives 0, y > 88 is clamped to 88.
-__device__ __forceinline__ float mf_exp(float y)
+// exp(y) for y <= 0: Cody-Waite reduction with ln 2 = hi + lo (hi has 15
+// significant bits), degree-7 Taylor polynomial of e^r by fma Horner steps,
+// scaling by 2^n.  y < -86 (or NaN) gives 0.
+__device__ __forceinline__ float mf_exp_nonpos(float y)
 {
     const float log2e = 0x1.715476p+0f;
     const float ln2hi = 0x1.62e4p-1f;
     const float ln2lo = 0x1.7f7d1cp-20f;
     const bool zero = !(y >= -86.0f);
-    y = y > 88.0f ? 88.0f : y;
     float n = rintf(y * log2e);
     float r = __builtin_fmaf(n, -ln2hi, y);
     r = __builtin_fmaf(n, -ln2lo, r);
@@ -238,7 +284,7 @@ struct Surrogate {
     {
         if (kind == 0) {
             float a = alpha * fabsf(u);
-            float e = mf_exp(-a);
+            float e = mf_exp_nonpos(-a);
             float den = 1.0f + e;
             float num = alpha * e;
             float den2 = den * den;
@@ -264,8 +310,7 @@ __device__ __forceinline__ float delta_h(const Surrogate& sg, float g, float h, 
     return g * sg(u);
 }
 
-__device__ __forceinline__ int32_t delta_h(const Surrogate& sg, int32_t g, int32_t h, float,
-                                           int v_th_q)
+__device__ __forceinline__ int32_t delta_h(const Surrogate& sg, int32_t g, int32_t h, float, int v_th_q)
 {
     int32_t u = h - v_th_q;
     float uf = (float)u * 0.00390625f;
@@ -275,71 +320,72 @@ __device__ __forceinline__ int32_t delta_h(const Surrogate& sg, int32_t g, int32
     return (int32_t)(p >> 15);
 }
 
-// True (wave-uniform) when some active lane's value is outside the range in
-// which the exponent-add tap is exact (lane masks straight from v_cmp).
-__device__ __forceinline__ bool any_slow(float v, const Geom& g, uint64_t act)
+// True (wave-uniform) when some lane's value is outside the range in which
+// the exponent-add tap is exact.
+__device__ __forceinline__ bool any_slow(float v, const Geom& g)
 {
     const float m = __builtin_fabsf(v);
-    const uint64_t ok = __builtin_amdgcn_fcmpf(m, g.fast_lo, 3 /* >= */) &
-                        __builtin_amdgcn_fcmpf(m, g.fast_hi, 4 /* < */);
-    return (act & ~ok) != 0;
+    return __builtin_amdgcn_ballot_w64(!(m >= g.fast_lo && m < g.fast_hi)) != 0;
 }
-__device__ __forceinline__ bool any_slow(int, const Geom&, uint64_t) { return false; }
+__device__ __forceinline__ bool any_slow(int, const Geom&) { return false; }
 
 // ---------------------------------------------------------------------------
-// lane -> column.  Lane-channel tiles: 64 consecutive channels of one sample.
+// items.  Item q of a group: q = (tile * d + r) * nchunks + chunk.
+// Lane -> column.  Lane-channel tiles: 64 consecutive channels of one sample.
 // Plane tiles: 64 consecutive positions p = n*S + s of one channel's (n, s)
-// plane, so every lane is busy except in the plane's last tile.  A lane whose
-// column does not exist reads and writes the column of the last existing
-// lane of its wave: it computes that lane's values, so its stores duplicate
-// that lane's in the same instruction.  Its grad_w / grad_b contribution is
-// dropped: lane-channel lanes past C write no partial row; in a partial plane
-// tile the backward zeroes the lane's dH before accumulating.
+// plane.  A lane whose column does not exist reads and writes the column of
+// the last existing lane of its wave: it computes that lane's values, so its
+// stores duplicate that lane's.  Its grad_w / grad_b contribution is dropped.
 // ---------------------------------------------------------------------------
-struct Item {
-    int r;        // residue class
-    int Lr;       // class length
-    int j0, j1;   // class-step chunk
-    bool active;  // this lane's column exists
-    bool partial; // plane tile with missing columns (wave-uniform)
-    uint32_t col; // column index in [0, M)
+struct Cursor {
+    int tile, r, chunk;
+    __device__ Cursor(const Geom& g, int64_t q)
+    {
+        chunk = (int)(q % g.nchunks);
+        q /= g.nchunks;
+        r = (int)(q % g.d);
+        tile = (int)(q / g.d);
+    }
+    __device__ void next(const Geom& g)
+    {
+        if (++chunk == g.nchunks) {
+            chunk = 0;
+            if (++r == g.d) {
+                r = 0;
+                ++tile;
+            }
+        }
+    }
+};
+
+struct Cols {
+    uint32_t col;  // column index in [0, M)
+    bool active;   // this lane's column exists
+    bool partial;  // plane tile with missing columns (wave-uniform)
 };
 
 template <int MODE>
-__device__ __forceinline__ Item decode_item(const Geom& g, int64_t q, int grp, int lane)
+__device__ __forceinline__ Cols tile_cols(const Geom& g, int tile, int grp, int lane)
 {
-    Item it;
-    const int chunk_id = (int)(q % g.nchunks);
-    const int64_t q2 = q / g.nchunks;
-    it.r = (int)(q2 % g.d);
-    const int tile = (int)(q2 / g.d);
-    it.Lr = it.r < g.T ? (g.T - it.r + g.d - 1) / g.d : 0;
-    it.j0 = chunk_id * g.chunk;
-    it.j1 = min(it.Lr, it.j0 + g.chunk);
+    Cols t;
     if (MODE == kLaneChannel) {
         const int c = grp * 64 + lane;
-        it.active = c < g.C;
-        it.partial = false;
-        it.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)min(c, g.C - 1);
+        t.active = c < g.C;
+        t.partial = false;
+        t.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)min(c, g.C - 1);
     } else {
         const uint32_t NS = (uint32_t)g.N * (uint32_t)g.S;
         const uint32_t pos = (uint32_t)tile * 64u + (uint32_t)lane;
-        it.active = pos < NS;
-        it.partial = (uint32_t)tile * 64u + 64u > NS;
+        t.active = pos < NS;
+        t.partial = (uint32_t)tile * 64u + 64u > NS;
         const uint32_t pc = min(pos, NS - 1u);
-        const uint32_t n = pc / (uint32_t)g.S, s = pc % (uint32_t)g.S;
-        it.col = (n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + s;
+        const uint32_t n = pc / (uint32_t)g.S, s = pc - n * (uint32_t)g.S;
+        t.col = (n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + s;
     }
-    return it;
+    return t;
 }
 
-// addr += inc, kept opaque so the compiler updates one running SGPR pair per
-// stream instead of precomputing (and spilling) an address per unrolled step
-__device__ __forceinline__ void advance(uint64_t& addr, int64_t inc)
-{
-    addr += (uint64_t)inc;
-    asm volatile("" : "+s"(addr));
-}
+__device__ __forceinline__ int class_len(const Geom& g, int r) { return r < g.T ? (g.T - r + g.d - 1) / g.d : 0; }
 
 // ---------------------------------------------------------------------------
 // forward
@@ -348,124 +394,152 @@ template <int K, int DT, int MODE>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
 {
     using V = typename IO<DT>::V;
-    using TP = Taps<K, DT>;
-    constexpr int P = prefetch_depth(K);
+    using TP = Taps<K, DT, MODE>;
+    constexpr int P = prefetch_depth(K, 8);
     constexpr int es = IO<DT>::es;
+    constexpr bool kF = DT != kQ88;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
-    const int wave = uniform(threadIdx.x >> 6);
     const int grp = blockIdx.y;
+    const int wid = (int)blockIdx.x * kWaves + uniform((int)threadIdx.x >> 6);
+    const int nw = (int)gridDim.x * kWaves;
+    const int64_t q0 = g.items * wid / nw;
+    const int64_t q1 = g.items * (wid + 1) / nw;
+    if (q0 >= q1)
+        return;
     const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
 
     TP tp;
     tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
-    V start;  // value the tap sum starts from
-    V bias;
-    if constexpr (DT == kQ88) {
+    V bias, start;
+    if constexpr (kF) {
+        const float b = ((const float*)a.bias)[c];
+        bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
+        start = 0.0f;
+    } else {
         bias = ((const int32_t*)a.bias)[c];
         start = bias + tp.cneg;
-    } else {
-        bias = ((const float*)a.bias)[c];
-        start = 0.0f;
     }
-    const int64_t xrow = (int64_t)g.M * es;  // bytes per time step
-    const uint32_t xrb = (uint32_t)xrow, srb = g.M, hrb = g.M * 4u;
+    const uint32_t M = g.M;
+    const int d = g.d;
+    const uint64_t xrow = (uint64_t)M * es;
+    const uint64_t xbytes = (uint64_t)g.T * xrow, sbytes = (uint64_t)g.T * M;
+    const int32_t xstep = (int32_t)((uint64_t)d * xrow), sstep = (int32_t)((uint64_t)d * M);
+    const int32_t hstep = 4 * sstep;
     const int want_h = a.h_out != nullptr ? 1 : 0;
-    const int64_t stride = (int64_t)gridDim.x * kWaves;
 
-    for (int64_t q = (int64_t)blockIdx.x * kWaves + wave; q < g.items; q += stride) {
-        const Item it = decode_item<MODE>(g, q, grp, lane);
-        if (it.j0 >= it.j1)
+    Cursor cur(g, q0);
+    int tile_cached = -1;
+    Cols cols{};
+    for (int64_t q = q0; q < q1; ++q, cur.next(g)) {
+        // item scalars, pinned to SGPRs
+        const int r = uniform(cur.r);
+        const int Lr = uniform(class_len(g, r));
+        const int j0 = uniform(cur.chunk * g.chunk);
+        const int j1 = uniform(min(Lr, j0 + g.chunk));
+        if (j0 >= j1)
             continue;
-        const uint32_t ox = it.col * es, o1 = it.col, o4 = it.col * 4u;
-        const uint64_t act = __builtin_amdgcn_ballot_w64(it.active);
-        const int r = it.r, d = g.d, j0 = it.j0, j1 = it.j1, Lr = it.Lr;
-
-        const int64_t xcls = d * xrow, scls = (int64_t)d * g.M, hcls = (int64_t)d * g.M * 4;
-        const uint64_t x0 = (uint64_t)a.x + (uint64_t)(r * xrow);
-        auto xat = [&](int j) -> V { return IO<DT>::load(x0 + (uint64_t)(j * xcls), xrb, ox); };
-        uint64_t xnext = x0 + (uint64_t)((j0 + P) * xcls);  // prefetch of step j + P
-        uint64_t srow = (uint64_t)a.spikes + (uint64_t)(r * (int64_t)g.M + j0 * scls);
-        uint64_t hrow = (uint64_t)a.h_out + (uint64_t)((r * (int64_t)g.M + j0 * scls) * 4);
-
-        V ring[K];
-        int slow = 0;  // steps left before every ring entry is in the fast range
-#pragma unroll
-        for (int m = 0; m < K - 1; ++m) {
-            const int j = j0 - (K - 1) + m;
-            const V v = xat(max(j, 0));  // never address before the tensor
-            ring[m] = j >= 0 ? v : V(0);
-            if (TP::kHasFast && any_slow(ring[m], g, act))
-                slow = m + 1;
+        if (cur.tile != tile_cached) {
+            cols = tile_cols<MODE>(g, cur.tile, grp, lane);
+            tile_cached = cur.tile;
         }
-        V pf[P];
+        // x rows from jb (the halo of a chunk) on; outputs from j0 on
+        const int jb = j0 > 0 ? j0 - (K - 1) : 0;
+        const Buf xs = make_buf(a.x, xbytes, ((uint64_t)r + (uint64_t)jb * d) * xrow);
+        const uint64_t orow = (uint64_t)r + (uint64_t)j0 * d;
+        const Buf ss = make_buf(a.spikes, sbytes, orow * M);
+        const Buf hs = want_h ? make_buf(a.h_out, sbytes * 4, orow * M * 4) : ss;
+        const uint32_t vx = cols.col * es, vs = cols.col, vh = cols.col * 4u;
+        const int32_t so_xlast = (Lr - 1 - jb) * xstep;
+
+        V ring[K];  // x[t] at slot t mod k
+        int slow = 0;  // steps left on the exact path
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            ring[i] = V(0);
+        if (j0 > 0) {
+            // halo x[j0-k+1 .. j0-1]; j0 is a multiple of k
+#pragma unroll
+            for (int m = 0; m < K - 1; ++m) {
+                ring[(m + 1) % K] = IO<DT>::load(xs, vx, m * xstep);
+                if (TP::kHasFast && any_slow(ring[(m + 1) % K], g))
+                    slow = m + 1;
+            }
+        }
+        V pf[P];  // x[j] at slot j mod P
 #pragma unroll
         for (int p = 0; p < P; ++p)
-            pf[p] = xat(min(j0 + p, Lr - 1));
+            pf[p] = IO<DT>::load(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
+        int32_t so_xp = (j0 + P - jb) * xstep;  // prefetch of step j + P
+        int32_t so_s = 0, so_h = 0;
 
-        // one step: take the prefetched input into the ring, sum the taps,
-        // fire, store; full blocks need no index checks and no clamping
-        auto step = [&](auto uc, int j, auto full_c) __attribute__((always_inline)) {
+        // one step (u: position in the block, j = bK + u); KIND kEdge is the
+        // block at the start of the sequence, which leaves out the float taps
+        // that would read before time 0 (Q8.8 keeps them: the ring holds
+        // zeros there, whose xor-terms the starting value cancels)
+        auto step = [&](auto uc, auto kc_, int j) __attribute__((always_inline)) {
             constexpr int u = decltype(uc)::value;
-            constexpr bool full = decltype(full_c)::value;
+            constexpr int kind = decltype(kc_)::value;
+            constexpr int imin = (kF && kind == kEdge) ? K - 1 - u : 0;
+            (void)j;
             const V xv = pf[u % P];
-            if constexpr (full)
-                pf[u % P] = IO<DT>::load(xnext, xrb, ox);
-            else
-                pf[u % P] = xat(min(j + P, Lr - 1));
-            advance(xnext, xcls);
-            ring[(u + K - 1) % K] = xv;
-            V acc = start;
-            if constexpr (TP::kHasFast) {
-                if (any_slow(xv, g, act))
+            pf[u % P] = IO<DT>::load(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
+            advance(so_xp, xstep);
+            ring[u] = xv;
+            V h;
+            if constexpr (kF) {
+                if (any_slow(xv, g))
                     slow = K;
+                V acc;
                 if (__builtin_expect(slow > 0, 0)) {
+                    acc = tp.apply(ring[(u + 1 + imin) % K], imin);
 #pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc = acc + tp.apply(ring[(u + i) % K], i);
+                    for (int i = imin + 1; i < K; ++i)
+                        acc = acc + tp.apply(ring[(u + 1 + i) % K], i);
                     --slow;
                 } else {
+                    acc = tp.apply_fast(ring[(u + 1 + imin) % K], imin);
 #pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc = acc + tp.apply_fast(ring[(u + i) % K], i);
+                    for (int i = imin + 1; i < K; ++i)
+                        acc = acc + tp.apply_fast(ring[(u + 1 + i) % K], i);
                 }
+                h = acc + bias;
+                st8(ss, vs, so_s, h >= g.v_th ? 1 : 0);
             } else {
+                V acc = start;
 #pragma unroll
                 for (int i = 0; i < K; ++i)
-                    acc = acc + tp.apply(ring[(u + i) % K], i);
-            }
-            V h;
-            bool fire;
-            if constexpr (DT == kQ88) {
+                    acc = acc + tp.apply(ring[(u + 1 + i) % K], i);
                 h = acc;
-                fire = h >= g.v_th_q;
-            } else {
-                h = acc + bias;
-                fire = h >= g.v_th;
+                st8(ss, vs, so_s, h >= g.v_th_q ? 1 : 0);
             }
-            store_b(srow, srb, o1, fire ? 1 : 0);
             if (want_h != 0)
-                store_w(hrow, hrb, o4, __builtin_bit_cast(uint32_t, h));
-            advance(srow, scls);
-            advance(hrow, hcls);
+                st32(hs, vh, so_h, __builtin_bit_cast(uint32_t, h));
+            advance(so_s, sstep);
+            advance(so_h, hstep);
+            __builtin_amdgcn_sched_barrier(0);
         };
-        auto block = [&](int jb, auto full_c) __attribute__((always_inline)) {
-            constexpr bool full = decltype(full_c)::value;
+        auto block = [&](int jb0, auto kc_) __attribute__((always_inline)) {
+            constexpr int kind = decltype(kc_)::value;
             [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
-                (void)((full || jb + U < j1
-                            ? (step(std::integral_constant<int, U>{}, jb + U, full_c), true)
-                            : false) &&
+                (void)(((kind == kFull || jb0 + U < j1) ? (step(ic<U>{}, kc_, jb0 + U), true) : false) &&
                        ...);
             }(std::make_integer_sequence<int, K>{});
         };
-        // orders above 16 keep a single (checked) copy of the block to bound
-        // the code size
-        int j = j0;
-        if constexpr (K <= 16)
-            for (; j + K <= j1 && j + K + P <= Lr; j += K)
-                block(j, std::true_type{});
-        for (; j < j1; j += K)
-            block(j, std::false_type{});
+        int b = j0 / K;
+        const int bend = (j1 + K - 1) / K;
+        if (b == 0) {
+            block(0, ic<kEdge>{});
+            ++b;
+        }
+        if constexpr (K <= 16) {
+            // full blocks: every step below j1, every prefetch inside the class
+            const int bfull = min(j1 / K, (Lr - P) / K);
+            for (; b < bfull; ++b)
+                block(b * K, ic<kFull>{});
+        }
+        for (; b < bend; ++b)
+            block(b * K, ic<kChecked>{});
     }
 }
 
@@ -479,242 +553,301 @@ __device__ __forceinline__ double wave_sum(double v)
         v += __shfl_xor(v, m, 64);
     return v;
 }
+__device__ __forceinline__ int64_t wave_sum(int64_t v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+        v += __shfl_xor(v, m, 64);
+    return v;
+}
 
-// Reverse walk over class steps j = jtop, jtop-1, ..., j0 (walk index
-// s = jtop - j, slot u = s mod k).  Rings: x[t] for t in [j-k+1, j] at slot
-// (jtop - t) mod k; dH[t] for t in [j, j+k-1] at slot (jtop - t) mod k, zero
-// for t past the sequence.  Steps above j1 - 1 are the halo of a lower chunk:
-// only their dH is computed.
 template <int K, int DT, int MODE, bool HS>
 __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 {
     using V = typename IO<DT>::V;
-    using D = typename IO<DT>::D;
-    using TP = Taps<K, DT>;
-    constexpr int P = prefetch_depth(K, 4);  // three streams: keep the queues short
+    using W = typename IO<DT>::W;
+    using TP = Taps<K, DT, MODE>;
+    constexpr int P = prefetch_depth(K, 4);
     constexpr int es = IO<DT>::es;
     constexpr int gxs = IO<DT>::gx_es;
-    constexpr bool kRecompute = !HS;
-    // x stays a float ring; each grad_w product widens its x operand at use
-    constexpr bool kWide = false;
+    constexpr bool kF = DT != kQ88;
+    constexpr bool kRe = !HS;  // recompute H from the x ring
+    // x rings: double copies for the exact grad_w products of float data;
+    // the stored value itself for the recompute of float data and for Q8.8
+    // (whose products are exact 32x32 -> 64-bit integer products)
+    constexpr bool kXD = kF;
+    constexpr bool kXV = kRe || !kF;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
-    const int wave = uniform(threadIdx.x >> 6);
+    const int wave = uniform((int)threadIdx.x >> 6);
     const int grp = blockIdx.y;
-    const int c_lane = (MODE == kLaneChannel) ? grp * 64 + lane : grp;
-    const int c = min(c_lane, g.C - 1);
+    const int wid = (int)blockIdx.x * kWaves + wave;
+    const int nw = (int)gridDim.x * kWaves;
+    const int64_t q0 = g.items * wid / nw;
+    const int64_t q1 = g.items * (wid + 1) / nw;
+    const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
 
     TP tp;
     tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
-    V start, bias;
-    D dstart;
-    if constexpr (DT == kQ88) {
+    V bias = V(0), start = V(0), reset = V(0);
+    if constexpr (kF) {
+        const float b = ((const float*)a.bias)[c];
+        bias = b == 0.0f ? 0.0f : b;
+    } else {
         bias = ((const int32_t*)a.bias)[c];
         start = bias + tp.cneg;
-        dstart = tp.cneg;
-    } else {
-        bias = ((const float*)a.bias)[c];
-        start = 0.0f;
-        dstart = 0.0f;
+        reset = tp.cneg;
     }
     Surrogate sg;
     sg.kind = g.sg;
     sg.alpha = g.alpha;
     sg.c_atan = 0x1.921fb6p+0f * g.alpha;
 
-    const int64_t xrow = (int64_t)g.M * es, gxrow = (int64_t)g.M * gxs, hrow = (int64_t)g.M * 4;
-    const uint32_t xrb = (uint32_t)xrow, gxrb = (uint32_t)gxrow, hrb = (uint32_t)hrow;
-    const int64_t stride = (int64_t)gridDim.x * kWaves;
+    const uint32_t M = g.M;
+    const int d = g.d;
+    const uint64_t xrow = (uint64_t)M * es, hrow = (uint64_t)M * 4, gxrow = (uint64_t)M * gxs;
+    const uint64_t xbytes = (uint64_t)g.T * xrow, hbytes = (uint64_t)g.T * hrow, gxbytes = (uint64_t)g.T * gxrow;
+    const int32_t xstep = (int32_t)((uint64_t)d * xrow), hstep = (int32_t)((uint64_t)d * hrow);
+    const int32_t gxstep = (int32_t)((uint64_t)d * gxrow);
 
-    double gw[K];
+    W gw[K];
 #pragma unroll
     for (int i = 0; i < K; ++i)
-        gw[i] = 0.0;
-    double gb = 0.0;
+        gw[i] = W(0);
+    W gb = W(0);
 
-    for (int64_t q = (int64_t)blockIdx.x * kWaves + wave; q < g.items; q += stride) {
-        const Item it = decode_item<MODE>(g, q, grp, lane);
-        if (it.j0 >= it.j1)
+    Cursor cur(g, q0);
+    int tile_cached = -1;
+    Cols cols{};
+    for (int64_t q = q0; q < q1; ++q, cur.next(g)) {
+        // item scalars, pinned to SGPRs
+        const int r = uniform(cur.r);
+        const int Lr = uniform(class_len(g, r));
+        const int j0 = uniform(cur.chunk * g.chunk);
+        const int j1 = uniform(min(Lr, j0 + g.chunk));
+        if (j0 >= j1)
             continue;
-        const uint32_t ox = it.col * es, ogx = it.col * gxs, oh = it.col * 4u;
-        const uint64_t act = __builtin_amdgcn_ballot_w64(it.active);
-        const int r = it.r, d = g.d;
-        const int j0 = it.j0, j1 = it.j1, Lr = it.Lr;
-        const int jtop = min(j1 + K - 1, Lr) - 1;
+        if (cur.tile != tile_cached) {
+            cols = tile_cols<MODE>(g, cur.tile, grp, lane);
+            tile_cached = cur.tile;
+        }
+        const bool partial = cols.partial;
+        const bool active = cols.active;
+        // steps j1..jtop are the halo of a lower chunk: their dH feeds outputs
+        // below j1; the walk starts at the top of jtop's block
+        const int jtop = uniform(min(j1 + K - 1, Lr) - 1);
+        const int jstart = uniform((jtop / K) * K + K - 1);
+        const int jb = uniform(max(0, j0 - (K - 1) - P));  // lowest row any stream touches
+        const uint64_t brow = (uint64_t)r + (uint64_t)jb * d;
+        const Buf xs = make_buf(a.x, xbytes, brow * xrow);
+        const Buf gsb = make_buf(a.gs, xbytes, brow * xrow);
+        const Buf hsb = HS ? make_buf(a.h, hbytes, brow * hrow) : xs;
+        const Buf gxb = make_buf(a.grad_x, gxbytes, brow * gxrow);
+        const uint32_t vx = cols.col * es, vh = cols.col * 4u, vgx = cols.col * gxs;
+        const int32_t so_last = (Lr - 1 - jb) * xstep, so_hlast = (Lr - 1 - jb) * hstep;
 
-        const int64_t xcls = d * xrow, gxcls = d * gxrow, hcls = d * hrow;
-        const uint64_t x0 = (uint64_t)a.x + (uint64_t)(r * xrow);
-        const uint64_t g0 = (uint64_t)a.gs + (uint64_t)(r * xrow);
-        const uint64_t h0 = (uint64_t)a.h + (uint64_t)(r * hrow);
-        auto xat = [&](int j) -> V { return IO<DT>::load(x0 + (uint64_t)(j * xcls), xrb, ox); };
-        auto gat = [&](int j) -> V { return IO<DT>::load(g0 + (uint64_t)(j * xcls), xrb, ox); };
-        auto hat = [&](int j) -> V {
-            return __builtin_bit_cast(V, load_w(h0 + (uint64_t)(j * hcls), hrb, oh));
-        };
-        // running addresses: prefetch of walk index s + P (step j - P, its
-        // x-ring entry j - P - k + 1) and the grad_x row of step j
-        uint64_t gnext = g0 + (uint64_t)((jtop - P) * xcls);
-        uint64_t hnext = h0 + (uint64_t)((jtop - P) * hcls);
-        uint64_t xnext = x0 + (uint64_t)((jtop - P - K + 1) * xcls);
-        uint64_t gxrow_j = (uint64_t)a.grad_x + (uint64_t)(r * gxrow + (int64_t)jtop * gxcls);
-
-        V xr[K];
-        double xd[kWide ? K : 1];
-        D dr[K];
-        int slow_x = 0;      // steps left on the exact recompute path
-        int slow_d = K - 1;  // steps left on the exact grad_x path (the zero dH past the top)
+        // grad_x accumulators: output t at slot t mod k, opened with the start
+        // of its sum (Q8.8: the number of negative taps that reach it)
+        V gxa[K];
 #pragma unroll
-        for (int i = 0; i < K; ++i)
-            dr[i] = D(0);
+        for (int s = 0; s < K; ++s) {
+            if constexpr (kF) {
+                gxa[s] = 0.0f;
+            } else {
+                const int t = jtop - (((jtop - s) % K) + K) % K;  // highest output of slot s
+                const int skip = max(0, t + K - Lr);               // taps whose source lies past the end
+                gxa[s] = __builtin_popcount(tp.negmask >> skip);
+            }
+        }
+        // x ring: x[t] at slot t mod k, for t in the window of the step
+        double xd[kXD ? K : 1];
+        V xf[kXV ? K : 1];
+        int slow_x = 0;  // live steps left on the exact recompute path
 #pragma unroll
         for (int m = 0; m < K - 1; ++m) {
-            const int t = jtop - m;
-            const V v0 = xat(max(t, 0));  // never address before the tensor
-            const V v = t >= 0 ? v0 : V(0);
-            xr[m] = v;
-            if constexpr (kWide)
-                xd[m] = (double)v;
-            if (kRecompute && TP::kHasFast && any_slow(v, g, act))
-                slow_x = m + 1;
+            const int t = jstart - m;  // slot k-1-m; values past jtop are never used
+            const V v = IO<DT>::load(xs, vx, (min(t, Lr - 1) - jb) * xstep);
+            if constexpr (kXD)
+                xd[K - 1 - m] = (double)v;
+            if constexpr (kXV)
+                xf[K - 1 - m] = v;
+            // x[t] (t <= jtop) is in the window of at most k live steps
+            if (kRe && TP::kHasFast && t <= jtop && any_slow(v, g))
+                slow_x = K;
         }
-        V pfx[P], pfg[P], pfh[HS ? P : 1];
+        // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P
+        V pg[P], ph[HS ? P : 1], px[P];
 #pragma unroll
         for (int p = 0; p < P; ++p) {
-            const int jp = max(jtop - p, 0);
-            pfg[p] = gat(jp);
+            const int jp = jstart - p;
+            const int js = (K - 1 - p) % P;
+            const int rowg = min(jp, Lr - 1);
+            pg[js] = IO<DT>::load(gsb, vx, (rowg - jb) * xstep);
             if constexpr (HS)
-                pfh[p] = hat(jp);
-            pfx[p] = xat(max(jtop - p - K + 1, 0));
+                ph[js] = __builtin_bit_cast(V, ld32(hsb, vh, (rowg - jb) * hstep));
+            px[js] = IO<DT>::load(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
         }
+        int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
+        int32_t so_hp = (jstart - P - jb) * hstep;           // h of step j - P
+        int32_t so_xp = (jstart - P - K + 1 - jb) * xstep;   // x of step j - P
+        int32_t so_gx = (jstart - jb) * gxstep;              // grad_x of step j
 
-        auto step = [&](auto uc, int j, auto full_c) __attribute__((always_inline)) {
+        // one step (u: position in the block, j = bK + k-1-u).  KIND kEdge is
+        // block 0: x[j-k+1] lies before time 0 for u > 0, and the taps
+        // i < u (sources before time 0, outputs before time 0) are left out.
+        auto step = [&](auto uc, auto kc_, int j) __attribute__((always_inline)) {
             constexpr int u = decltype(uc)::value;
-            constexpr bool full = decltype(full_c)::value;
-            constexpr int xslot = (u + K - 1) % K;
-            const V gv = pfg[u % P];
-            V xv = pfx[u % P];
+            constexpr int kind = decltype(kc_)::value;
+            constexpr bool full = kind == kFull;
+            constexpr bool edge = kind == kEdge;
+            constexpr int sj = K - 1 - u;  // j mod k
+            constexpr int sp = sj % P;     // j mod P
+            constexpr int imin = edge ? u : 0;
+            const V gv = pg[sp];
+            const V xv = px[sp];
             V hv = V(0);
             if constexpr (HS)
-                hv = pfh[u % P];
-            if constexpr (full) {
-                pfg[u % P] = IO<DT>::load(gnext, xrb, ox);
-                if constexpr (HS)
-                    pfh[u % P] = __builtin_bit_cast(V, load_w(hnext, hrb, oh));
-                pfx[u % P] = IO<DT>::load(xnext, xrb, ox);
-            } else {
-                const int jn = max(j - P, 0);
-                pfg[u % P] = gat(jn);
-                if constexpr (HS)
-                    pfh[u % P] = hat(jn);
-                pfx[u % P] = xat(max(j - P - K + 1, 0));
-                if (j - K + 1 < 0)  // x ring entry before the start of time
-                    xv = V(0);
-            }
-            advance(gnext, -xcls);
+                hv = ph[sp];
+            pg[sp] = IO<DT>::load(gsb, vx, full ? so_gp : min(max(so_gp, 0), so_last));
             if constexpr (HS)
-                advance(hnext, -hcls);
-            advance(xnext, -xcls);
-            xr[xslot] = xv;
-            if constexpr (kWide)
-                xd[xslot] = (double)xv;
-            V h;
-            if constexpr (kRecompute) {
-                V acc = start;
-                if constexpr (TP::kHasFast) {
-                    if (any_slow(xv, g, act))
-                        slow_x = K;
+                ph[sp] = __builtin_bit_cast(V, ld32(hsb, vh, full ? so_hp : min(max(so_hp, 0), so_hlast)));
+            px[sp] = IO<DT>::load(xs, vx, full ? so_xp : min(max(so_xp, 0), so_last));
+            advance(so_gp, -xstep);
+            if constexpr (HS)
+                advance(so_hp, -hstep);
+            advance(so_xp, -xstep);
+            // x[j-k+1] enters the ring (slot (j+1) mod k)
+            if constexpr (!(edge && u > 0)) {
+                if constexpr (kXD)
+                    xd[(sj + 1) % K] = (double)xv;
+                if constexpr (kXV)
+                    xf[(sj + 1) % K] = xv;
+                if (kRe && TP::kHasFast && any_slow(xv, g))
+                    slow_x = K;
+            } else if constexpr (!kF) {
+                xf[(sj + 1) % K] = 0;  // Q8.8: zeros before time 0 (recompute)
+            }
+            if (full || j <= jtop) {
+                V h;
+                if constexpr (HS) {
+                    h = hv;
+                } else if constexpr (kF) {
+                    constexpr int rmin = edge ? u : 0;  // taps reading before time 0 are left out
+                    V acc;
                     if (__builtin_expect(slow_x > 0, 0)) {
+                        acc = tp.apply(xf[(sj + 1 + rmin) % K], rmin);
 #pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            acc = acc + tp.apply(xr[(u + K - 1 - i) % K], i);
-                        --slow_x;
+                        for (int i = rmin + 1; i < K; ++i)
+                            acc = acc + tp.apply(xf[(sj + 1 + i) % K], i);
                     } else {
+                        acc = tp.apply_fast(xf[(sj + 1 + rmin) % K], rmin);
 #pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            acc = acc + tp.apply_fast(xr[(u + K - 1 - i) % K], i);
+                        for (int i = rmin + 1; i < K; ++i)
+                            acc = acc + tp.apply_fast(xf[(sj + 1 + i) % K], i);
                     }
-                } else {
-#pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc = acc + tp.apply(xr[(u + K - 1 - i) % K], i);
-                }
-                if constexpr (DT == kQ88)
-                    h = acc;
-                else
                     h = acc + bias;
-            } else {
-                h = hv;
-            }
-            const D dh = delta_h(sg, gv, h, g.v_th, g.v_th_q);
-            dr[u] = dh;
-            if (TP::kHasFast && any_slow(dh, g, act))
-                slow_d = K;
-            if (full || j < j1) {
-                double dd = (double)dh;
-                if (!full && it.partial)
-                    dd = it.active ? dd : 0.0;  // no contribution from shadow lanes
-#pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    double xi;
-                    if constexpr (kWide)
-                        xi = xd[(u + K - 1 - i) % K];
-                    else
-                        xi = (double)xr[(u + K - 1 - i) % K];
-                    gw[i] = __builtin_fma(xi, dd, gw[i]);
-                }
-                gb += dd;
-                D acc = dstart;
-                if constexpr (TP::kHasFast) {
-                    if (__builtin_expect(slow_d > 0, 0)) {
-#pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            acc = acc + tp.apply(dr[(u + 1 + i) % K], i);
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            acc = acc + tp.apply_fast(dr[(u + 1 + i) % K], i);
-                    }
                 } else {
+                    V acc = start;
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc = acc + tp.apply(dr[(u + 1 + i) % K], i);
+                        acc = acc + tp.apply(xf[(sj + 1 + i) % K], i);
+                    h = acc;
                 }
-                IO<DT>::store_gx(gxrow_j, gxrb, ogx, acc);
+                const V dh = delta_h(sg, gv, h, g.v_th, g.v_th_q);
+                const bool own = full || j < j1;
+                if (own) {
+                    if constexpr (kF) {
+                        double dd = (double)dh;
+                        if (MODE == kPlane && partial)
+                            dd = active ? dd : 0.0;  // no contribution from shadow lanes
+#pragma unroll
+                        for (int i = imin; i < K; ++i) {
+                            gw[i] = __builtin_fma(xd[(sj + 1 + i) % K], dd, gw[i]);
+                            pin(gw[i]);
+                        }
+                        gb += dd;
+                        pin(gb);
+                    } else {
+                        int32_t dq = dh;
+                        if (MODE == kPlane && partial)
+                            dq = active ? dq : 0;
+#pragma unroll
+                        for (int i = imin; i < K; ++i) {
+                            gw[i] += (int64_t)xf[(sj + 1 + i) % K] * (int64_t)dq;
+                            pin(gw[i]);
+                        }
+                        gb += dq;
+                        pin(gb);
+                    }
+                }
+                // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k): lanes
+                // with a zero dH add nothing, lanes in the exponent-add range
+                // take the fast taps, any other lane the exact ones
+                if constexpr (kF) {
+                    const float m = __builtin_fabsf(dh);
+                    const bool fast = m >= g.fast_lo && m < g.fast_hi;
+                    if (fast) {
+#pragma unroll
+                        for (int i = imin; i < K; ++i)
+                            gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply_fast(dh, i);
+                    }
+                    if (__builtin_expect(!fast && dh != 0.0f, 0)) {
+#pragma unroll
+                        for (int i = imin; i < K; ++i)
+                            gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply(dh, i);
+                    }
+                } else {
+                    // (integer sums: pinned so they are not reassociated across
+                    // steps, which would keep many steps' terms live)
+#pragma unroll
+                    for (int i = imin; i < K; ++i) {
+                        gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply(dh, i);
+                        pin(gxa[(sj + 1 + i) % K]);
+                    }
+                }
+                if (own)
+                    IO<DT>::store_gx(gxb, vgx, so_gx, gxa[sj]);
+                gxa[sj] = reset;  // slot now holds output j - k
+                if constexpr (kRe && kF)
+                    if (slow_x > 0)
+                        --slow_x;
             }
-            advance(gxrow_j, -gxcls);
-            if (slow_d > 0)
-                --slow_d;
+            advance(so_gx, -gxstep);
             // keep the scheduler from hoisting later steps' loads above this
             // step (which would hold them in registers for a whole block)
             __builtin_amdgcn_sched_barrier(0);
         };
-        auto block = [&](int jb, auto full_c) __attribute__((always_inline)) {
-            constexpr bool full = decltype(full_c)::value;
+        auto block = [&](int b, auto kc_) __attribute__((always_inline)) {
+            constexpr int kind = decltype(kc_)::value;
+            const int jhi = b * K + K - 1;
             [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
-                (void)((full || jb - U >= j0
-                            ? (step(std::integral_constant<int, U>{}, jb - U, full_c), true)
-                            : false) &&
+                (void)(((kind == kFull || jhi - U >= j0) ? (step(ic<U>{}, kc_, jhi - U), true) : false) &&
                        ...);
             }(std::make_integer_sequence<int, K>{});
         };
-        // full blocks: every step owned (j < j1, j >= j0), x-ring entries and
-        // prefetches at or after the start of time.  The first block holds the
-        // halo (or the zero dH past the top); orders above 16 keep one
-        // checked copy only.
-        int jb = jtop;
-        block(jb, std::false_type{});
-        jb -= K;
-        if constexpr (K <= 16)
-            if (!it.partial)
-                for (; jb - K + 1 >= j0 && jb < j1 && jb >= 2 * K - 2 + P; jb -= K)
-                    block(jb, std::true_type{});
-        for (; jb >= j0; jb -= K)
-            block(jb, std::false_type{});
+        // full blocks: b > 0, every step owned and at or below jtop, every
+        // prefetch at or above jb
+        // (block 0, the start of the sequence, is the last one of a walk)
+        int b = jstart / K;
+        const int blo = j0 / K;
+        const int bmin = max(blo, 1);
+        if constexpr (K <= 16) {
+            const int bf_hi = (min(jtop, j1 - 1) - (K - 1)) / K;
+            const int bf_lo = max(bmin, (jb + P + 2 * K - 2) / K);
+            for (; b > bf_hi && b >= bmin; --b)
+                block(b, ic<kChecked>{});
+            for (; b >= bf_lo; --b)
+                block(b, ic<kFull>{});
+        }
+        for (; b >= bmin; --b)
+            block(b, ic<kChecked>{});
+        if (blo == 0)
+            block(0, ic<kEdge>{});
     }
     // block reduction in a fixed order, then one partial row per block
     const int C = g.C;
     if constexpr (MODE == kLaneChannel) {
-        __shared__ double red[K + 1][64];
+        __shared__ W red[K + 1][64];
         for (int w = 0; w < kWaves; ++w) {
             if (wave == w) {
 #pragma unroll
@@ -728,27 +861,27 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             const int i = e >> 6, l = e & 63;
             const int cc = grp * 64 + l;
             if (cc < C)
-                a.partial[((size_t)blockIdx.x * (K + 1) + i) * C + cc] = red[i][l];
+                ((W*)a.partial)[((size_t)blockIdx.x * (K + 1) + i) * C + cc] = red[i][l];
         }
     } else {
-        __shared__ double red[kWaves][K + 1];
+        __shared__ W red[kWaves][K + 1];
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-            const double v = wave_sum(gw[i]);
+            const W v = wave_sum(gw[i]);
             if (lane == 0)
                 red[wave][i] = v;
         }
         {
-            const double v = wave_sum(gb);
+            const W v = wave_sum(gb);
             if (lane == 0)
                 red[wave][K] = v;
         }
         __syncthreads();
         if (threadIdx.x < K + 1) {
-            double s = red[0][threadIdx.x];
+            W s = red[0][threadIdx.x];
             for (int w = 1; w < kWaves; ++w)
                 s += red[w][threadIdx.x];
-            a.partial[((size_t)blockIdx.x * (K + 1) + threadIdx.x) * C + grp] = s;
+            ((W*)a.partial)[((size_t)blockIdx.x * (K + 1) + threadIdx.x) * C + grp] = s;
         }
     }
 }
@@ -758,11 +891,14 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 // ---------------------------------------------------------------------------
 // One block of 16 waves per 64 outputs: wave w adds the partial rows of a
 // fixed contiguous range of blocks, then wave 0 adds the 16 sums in order,
-// so the result does not depend on scheduling.
+// so the result does not depend on scheduling.  Partials are double (float
+// data) or int64 (Q8.8).
 constexpr int kFinWaves = 16;
 
-__global__ __launch_bounds__(64 * kFinWaves) void fin_kernel(FinArgs a)
+template <typename W>
+__device__ __forceinline__ void fin_body(const FinArgs& a)
 {
+    const W* partial = (const W*)a.partial;
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
     const int n_out = (a.k + 1) * a.C;
@@ -772,34 +908,33 @@ __global__ __launch_bounds__(64 * kFinWaves) void fin_kernel(FinArgs a)
     const int per = (a.blocks + kFinWaves - 1) / kFinWaves;
     const int b0 = min(w * per, a.blocks);
     const int b1 = min(b0 + per, a.blocks);
-    double s = 0.0;
+    W s = W(0);
     int b = b0;
     for (; b + 8 <= b1; b += 8) {
-        double v[8];
+        W v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            v[u] = a.partial[(size_t)(b + u) * n_out + ec];
+            v[u] = partial[(size_t)(b + u) * n_out + ec];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
             s += v[u];
     }
     for (; b < b1; ++b)
-        s += a.partial[(size_t)b * n_out + ec];
-    __shared__ double red[kFinWaves][64];
+        s += partial[(size_t)b * n_out + ec];
+    __shared__ W red[kFinWaves][64];
     red[w][lane] = s;
     __syncthreads();
     if (w != 0 || !ok)
         return;
-    double t = red[0][lane];
+    W t = red[0][lane];
     for (int q = 1; q < kFinWaves; ++q)
         t += red[q][lane];
     const int i = e / a.C, c = e % a.C;
-    if (a.dtype == kQ88) {
-        const int64_t v = (int64_t)t;
+    if constexpr (std::is_same_v<W, int64_t>) {
         if (i < a.k)
-            ((int64_t*)a.grad_w)[c * a.k + i] = v;
+            ((int64_t*)a.grad_w)[c * a.k + i] = t;
         else
-            ((int64_t*)a.grad_b)[c] = v;
+            ((int64_t*)a.grad_b)[c] = t;
     } else {
         const float v = (float)t;
         if (i < a.k)
@@ -807,6 +942,14 @@ __global__ __launch_bounds__(64 * kFinWaves) void fin_kernel(FinArgs a)
         else
             ((float*)a.grad_b)[c] = v;
     }
+}
+
+__global__ __launch_bounds__(64 * kFinWaves) void fin_kernel(FinArgs a)
+{
+    if (a.dtype == kQ88)
+        fin_body<int64_t>(a);
+    else
+        fin_body<double>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -875,19 +1018,23 @@ int resident_blocks(Kern kern, int (&cache)[16])
     return cache[slot];
 }
 
-// Persistent grid: as many blocks per group as fit at once, at most one per
-// kWaves items and never more than the planner's bound.
+// Persistent grid with equal shares: the fewest rounds of items the resident
+// waves allow, then the fewest blocks that still finish in that many rounds
+// (so every wave gets the same number of items, up to one), never more than
+// the planner's bound.
 inline int persistent_blocks(const Geom& g, int resident)
 {
     int64_t per_group = resident / g.groups;
     if (per_group < 1)
         per_group = 1;
-    const int64_t need = (g.items + kWaves - 1) / kWaves;
-    if (per_group > need)
-        per_group = need;
     if (per_group > g.blocks)
         per_group = g.blocks;
-    return (int)(per_group > 0 ? per_group : 1);
+    const int64_t waves_max = per_group * kWaves;
+    const int64_t rounds = (g.items + waves_max - 1) / waves_max;
+    int64_t blocks = (g.items + rounds * kWaves - 1) / (rounds * kWaves);
+    if (blocks > per_group)
+        blocks = per_group;
+    return (int)(blocks > 0 ? blocks : 1);
 }
 
 template <int K, int DT>

@@ -131,8 +131,8 @@ def test_backward_workspace_and_validation(lib):
     bad = list(args)
     bad[2] = FAKE + 2  # misaligned h
     assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -6
-    # Q8.8 exactness bound on the grad_w sums
-    q = good_desc(dtype=2, T=1 << 14, N=1 << 14, C=1, S=1)
+    # Q8.8 bound on the int64 grad_w sums
+    q = good_desc(dtype=2, T=1 << 16, N=1 << 16, C=1, S=1)
     assert lib.mfpsn_backward(ctypes.byref(q), *args, FAKE, 1 << 40, None) == -2
 
 
