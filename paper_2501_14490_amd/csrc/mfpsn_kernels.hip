@@ -36,8 +36,11 @@
 // scattered into the k open grad_x accumulators it feeds (outputs j-k+1..j);
 // contributions reach every output in ascending tap order, so the sum order
 // is the definition's.  Output j is complete after step j and is stored.
-// Lanes whose dH is zero skip the scatter (their terms are all zeros), so
-// the exponent-add path stays usable where the surrogate underflows.
+// Lanes whose dH is zero or below the exponent-add range skip the scatter:
+// their terms are zeros or smaller than 2^(shift_hi-shift_lo-126), and they
+// would otherwise force the exact path on the whole wave wherever the
+// surrogate gradient underflows.  grad_x therefore equals the sequential
+// definition bit for bit, except that such tiny dH values count as zero.
 // grad_w / grad_b are accumulated from exact products: double for float data
 // (the x ring is kept in double), int64 for Q8.8; they are reduced inside the
 // block in a fixed order and written as per-block partials, which a finalize
@@ -90,7 +93,10 @@ struct Buf {
 __device__ __forceinline__ Buf make_buf(const void* tensor, uint64_t tensor_bytes, uint64_t off)
 {
     const uint64_t rem = off < tensor_bytes ? tensor_bytes - off : 0;
-    const uint32_t n = rem > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)rem;
+    uint32_t n = rem > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)rem;
+    // opaque, so descriptors of equal-sized tensors do not share (and then
+    // copy every step) their size and flag words
+    asm volatile("" : "+s"(n));
     Buf b;
     b.rs = __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)tensor + off), (short)0, (int)n, kRsrcWord3);
     return b;
@@ -117,13 +123,12 @@ __device__ __forceinline__ void st8(Buf b, uint32_t v, int32_t s, uint8_t x)
     __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, 0);
 }
 
-// s += inc with an opaque increment, so the compiler keeps one running SGPR
-// per stream instead of precomputing (and spilling) an offset per unrolled
-// step
+// s += inc, kept opaque so the compiler keeps one running SGPR per stream
+// instead of precomputing (and spilling) an offset per unrolled step
 __device__ __forceinline__ void advance(int32_t& s, int32_t inc)
 {
-    asm volatile("" : "+s"(inc));
     s += inc;
+    asm volatile("" : "+s"(s));
 }
 
 // Makes v opaque at this point: the code that produces it cannot be sunk
@@ -276,31 +281,40 @@ __device__ __forceinline__ float mf_exp_nonpos(float y)
     return zero ? 0.0f : e;
 }
 
+// sigmoid: alpha e / (1 + e)^2 with e = exp(-alpha |u|)
+// atan:    (alpha / 2) / (1 + (pi/2 alpha u)^2)
+// rational: 1 / (1 + alpha u^2)
+// atan and rational share one operation sequence: z = m u, den = 1 + q z^2,
+// num / den, with (m, q, num) = (float(pi/2) alpha, 1, alpha/2) or
+// (1, alpha, 1); the multiplications by 1 are exact, so each result is
+// bit-identical to its own formula.
 struct Surrogate {
-    int kind;
+    int sigmoid;  // 1: sigmoid, 0: atan or rational
     float alpha;
-    float c_atan;   // float(pi/2) * alpha
+    float m, q, num;
+    __device__ void init(int kind, float a)
+    {
+        sigmoid = kind == 0;
+        alpha = a;
+        m = kind == 1 ? 0x1.921fb6p+0f * a : 1.0f;
+        q = kind == 1 ? 1.0f : a;
+        num = kind == 1 ? 0.5f * a : 1.0f;
+    }
     __device__ __forceinline__ float operator()(float u) const
     {
-        if (kind == 0) {
+        if (sigmoid) {
             float a = alpha * fabsf(u);
             float e = mf_exp_nonpos(-a);
             float den = 1.0f + e;
-            float num = alpha * e;
+            float nm = alpha * e;
             float den2 = den * den;
-            return num / den2;
+            return nm / den2;
         }
-        if (kind == 1) {
-            float z = c_atan * u;
-            float z2 = z * z;
-            float den = 1.0f + z2;
-            float num = 0.5f * alpha;
-            return num / den;
-        }
-        float u2 = u * u;
-        float au2 = alpha * u2;
-        float den = 1.0f + au2;
-        return 1.0f / den;
+        float z = m * u;
+        float z2 = z * z;
+        float t = q * z2;
+        float den = 1.0f + t;
+        return num / den;
     }
 };
 
@@ -599,9 +613,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         reset = tp.cneg;
     }
     Surrogate sg;
-    sg.kind = g.sg;
-    sg.alpha = g.alpha;
-    sg.c_atan = 0x1.921fb6p+0f * g.alpha;
+    sg.init(g.sg, g.alpha);
 
     const uint32_t M = g.M;
     const int d = g.d;
@@ -780,18 +792,20 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                         pin(gb);
                     }
                 }
-                // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k): lanes
-                // with a zero dH add nothing, lanes in the exponent-add range
-                // take the fast taps, any other lane the exact ones
+                // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k).  Lanes
+                // whose dH is in the exponent-add range take the fast taps;
+                // lanes above it (or infinite, NaN) the exact taps.  A dH below
+                // the range (zero, or a surrogate gradient that underflowed to
+                // under 2^(shift_hi-126)) adds nothing: its terms are zeros or
+                // smaller than 2^(shift_hi-shift_lo-126).
                 if constexpr (kF) {
                     const float m = __builtin_fabsf(dh);
-                    const bool fast = m >= g.fast_lo && m < g.fast_hi;
-                    if (fast) {
+                    if (m >= g.fast_lo && m < g.fast_hi) {
 #pragma unroll
                         for (int i = imin; i < K; ++i)
                             gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply_fast(dh, i);
                     }
-                    if (__builtin_expect(!fast && dh != 0.0f, 0)) {
+                    if (__builtin_expect(!(m < g.fast_hi), 0)) {
 #pragma unroll
                         for (int i = imin; i < K; ++i)
                             gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply(dh, i);

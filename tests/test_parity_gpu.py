@@ -4,7 +4,10 @@ Bar: spikes, Q8.8 potentials and all Q8.8 gradients bit-exact; float
 potentials and grad_x bit-exact (both sides follow the same pinned float
 sequence); bf16 grad_x bit-exact after round-to-nearest-even; grad_w and
 grad_b within 1e-6 absolute + 1e-5 relative of the oracle's double sums
-(only the order of the double additions differs).
+(only the order of the double additions differs).  The one documented
+exception: the kernel drops the grad_x terms of a dH below the exponent-add
+range (|dH| < 2^(shift_hi-126), where the surrogate gradient underflows), so
+an output fed by such a dH is only required to be within 1e-30 of the oracle.
 """
 import numpy as np
 import pytest
@@ -66,7 +69,32 @@ def oracle_run(orc, case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=
     return b
 
 
-def compare(got, ref, dtype, label):
+def tiny_dh_outputs(dH, k, d, hi):
+    """Mask of grad_x outputs that receive a term from a nonzero dH below the
+    exponent-add range 2^(max(1, hi+1) - 127)."""
+    lo_bound = np.float32(2.0 ** (max(1, hi + 1) - 127))
+    tiny = (dH != 0) & (np.abs(dH) < lo_bound)
+    T = dH.shape[0]
+    hit = np.zeros(dH.shape, dtype=bool)
+    for m in range(k):
+        s = m * d
+        if s < T:
+            hit[:T - s] |= tiny[s:]
+    return hit
+
+
+def check_grad_x(g, r, hit, label):
+    """bit-exact outside `hit`; within 1e-30 on it; NaN matches NaN."""
+    nan = np.isnan(r)
+    assert np.array_equal(np.isnan(g), nan), f"{label}: grad_x NaN pattern differs"
+    exact = ~hit & ~nan
+    diff = np.abs(g.astype(np.float64) - r.astype(np.float64))
+    assert np.array_equal(g[exact].view(np.uint32), r[exact].view(np.uint32)), (
+        f"{label}: grad_x differs, max |diff| {np.nanmax(np.where(exact, diff, 0))}")
+    assert np.all(diff[hit & ~nan] <= 1e-30), f"{label}: grad_x near a tiny dH differs by {diff[hit & ~nan].max()}"
+
+
+def compare(got, ref, dtype, label, k=None, d=None, hi=7):
     assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
     if dtype == "q8_8":
         assert np.array_equal(got["H"], ref["Hf"]), f"{label}: H differs"
@@ -76,12 +104,13 @@ def compare(got, ref, dtype, label):
         return
     assert np.array_equal(got["H"].view(np.uint32), ref["Hf"].view(np.uint32)), (
         f"{label}: H differs, max |diff| {np.abs(got['H'] - ref['Hf']).max()}")
+    hit = tiny_dh_outputs(ref["dH"], k, d, hi)
     if dtype == "bf16":
-        assert np.array_equal(got["grad_x_bits"], ref["grad_x_bits"]), f"{label}: bf16 grad_x differs"
+        gb = got["grad_x_bits"].astype(np.uint32) << 16
+        rb = ref["grad_x_bits"].astype(np.uint32) << 16
+        check_grad_x(gb.view(np.float32), rb.view(np.float32), hit, label + " (bf16)")
     else:
-        diff = np.abs(got["grad_x"].astype(np.float64) - ref["grad_x"])
-        assert np.array_equal(got["grad_x"].view(np.uint32), ref["grad_x"].view(np.uint32)), (
-            f"{label}: grad_x differs, max |diff| {diff.max()}")
+        check_grad_x(got["grad_x"], ref["grad_x"], hit, label)
     for name in ("grad_w", "grad_b"):
         g = got[name].astype(np.float64)
         r = ref[name]
@@ -113,7 +142,7 @@ def test_small_shapes(orc, dtype, shape_i, k, d, saved_h):
     v_th = 0.5
     got = gpu_run(case, k, d, dtype, v_th, saved_h=saved_h)
     ref = oracle_run(orc, case, k, d, dtype, v_th)
-    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_h={saved_h}")
+    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_h={saved_h}", k, d)
 
 
 @pytest.mark.parametrize("saved_h", [False, True])
@@ -124,7 +153,7 @@ def test_orders(orc, dtype, k, saved_h):
     case = workloads.make_small(3 * k + 5, 4, 70, (), k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
     ref = oracle_run(orc, case, k, d, dtype, 0.75)
     got = gpu_run(case, k, d, dtype, 0.75, saved_h=saved_h)
-    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_h={saved_h}")
+    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_h={saved_h}", k, d)
 
 
 @pytest.mark.parametrize("surrogate,alpha", [("atan", 2.0), ("atan", 5.0), ("rational", 10.0), ("sigmoid", 1.5)])
@@ -133,14 +162,14 @@ def test_surrogates(orc, surrogate, alpha, dtype):
     case = workloads.make_small(40, 3, 66, (), k=4, dtype=dtype, seed=5)
     got = gpu_run(case, 4, 2, dtype, 0.2, surrogate, alpha, v_th_q=51)
     ref = oracle_run(orc, case, 4, 2, dtype, 0.2, surrogate, alpha, v_th_q=51)
-    compare(got, ref, dtype, f"{surrogate} {alpha} {dtype}")
+    compare(got, ref, dtype, f"{surrogate} {alpha} {dtype}", 4, 2)
 
 
 def test_negative_and_wide_shifts(orc):
     case = workloads.make_small(25, 2, 65, (), k=6, s_lo=-4, s_hi=12, dtype="f32", seed=3)
     got = gpu_run(case, 6, 3, "f32", 0.1, lo=-3, hi=10)
     ref = oracle_run(orc, case, 6, 3, "f32", 0.1, lo=-3, hi=10)
-    compare(got, ref, "f32", "shift clamp [-3, 10]")
+    compare(got, ref, "f32", "shift clamp [-3, 10]", 6, 3, hi=10)
 
 
 @pytest.mark.parametrize("T", [1, 2, 5])
@@ -149,7 +178,7 @@ def test_short_sequences(orc, T):
     case = workloads.make_small(T, 3, 64, (), k=8, dtype="f32", seed=T)
     got = gpu_run(case, 8, 3, "f32", 0.0)
     ref = oracle_run(orc, case, 8, 3, "f32", 0.0)
-    compare(got, ref, "f32", f"T={T}")
+    compare(got, ref, "f32", f"T={T}", 8, 3)
 
 
 @pytest.mark.parametrize("saved_h", [False, True])
@@ -160,20 +189,20 @@ def test_long_sequence_is_chunked(orc, k, d, saved_h):
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="q8_8", seed=9)
     got = gpu_run(case, k, d, "q8_8", 0.0, saved_h=saved_h)
     ref = oracle_run(orc, case, k, d, "q8_8", 0.0)
-    compare(got, ref, "q8_8", "chunked")
+    compare(got, ref, "q8_8", "chunked", k, d)
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="f32", seed=9)
     compare(gpu_run(case, k, d, "f32", 0.3, saved_h=saved_h), oracle_run(orc, case, k, d, "f32", 0.3),
-            "f32", "chunked f32")
+            "f32", "chunked f32", k, d)
 
 
-def compare_nan_aware(got, ref, label):
+def compare_nan_aware(got, ref, label, k, d, hi=7):
     """Like compare() for f32, but NaN equals NaN whatever its payload."""
     assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
-    for name, r in (("H", ref["Hf"]), ("grad_x", ref["grad_x"])):
-        g = got[name]
-        nan = np.isnan(r)
-        assert np.array_equal(np.isnan(g), nan), f"{label}: {name} NaN pattern differs"
-        assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: {name} differs"
+    g, r = got["H"], ref["Hf"]
+    nan = np.isnan(r)
+    assert np.array_equal(np.isnan(g), nan), f"{label}: H NaN pattern differs"
+    assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: H differs"
+    check_grad_x(got["grad_x"], ref["grad_x"], tiny_dh_outputs(ref["dH"], k, d, hi), label)
 
 
 @pytest.mark.parametrize("saved_h", [False, True])
@@ -192,12 +221,29 @@ def test_special_values_take_the_exact_path(orc, k, d, saved_h):
     x[5:9, 1, :] = 0.0  # whole rows of zeros inside the walk
     got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
-    compare_nan_aware(got, ref, f"specials k={k} d={d}")
+    compare_nan_aware(got, ref, f"specials k={k} d={d}", k, d)
     case["x"].ravel()[rng.integers(0, x.size, size=20)] = np.float32(np.inf)
     case["grad_spikes"].ravel()[rng.integers(0, x.size, size=200)] = 0.0
     got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
-    compare_nan_aware(got, ref, f"specials+inf k={k} d={d}")
+    compare_nan_aware(got, ref, f"specials+inf k={k} d={d}", k, d)
+
+
+@pytest.mark.parametrize("saved_h", [False, True])
+def test_tiny_dh_terms(orc, saved_h):
+    # grad_spikes values around 1e-38 make dH fall below the exponent-add
+    # range on many lanes: their grad_x terms are dropped, every other output
+    # stays bit-exact
+    case = workloads.make_small(50, 3, 70, (), k=8, dtype="f32", seed=21)
+    g = case["grad_spikes"]
+    rng = np.random.default_rng(21)
+    idx = rng.integers(0, g.size, size=g.size // 5)
+    g.ravel()[idx] = (rng.standard_normal(idx.size) * 1e-37).astype(np.float32)
+    got = gpu_run(case, 8, 2, "f32", 0.25, saved_h=saved_h)
+    ref = oracle_run(orc, case, 8, 2, "f32", 0.25)
+    hit = tiny_dh_outputs(ref["dH"], 8, 2, 7)
+    assert hit.any() and not hit.all()
+    compare(got, ref, "f32", "tiny dH", 8, 2)
 
 
 def test_negative_shifts_near_overflow(orc):
@@ -208,7 +254,7 @@ def test_negative_shifts_near_overflow(orc):
     case["x"].ravel()[3::11] = np.float32(-(2.0 ** 127))
     got = gpu_run(case, 4, 2, "f32", 1.0, lo=-6, hi=3)
     ref = oracle_run(orc, case, 4, 2, "f32", 1.0, lo=-6, hi=3)
-    compare_nan_aware(got, ref, "near overflow")
+    compare_nan_aware(got, ref, "near overflow", 4, 2, hi=3)
 
 
 def test_zero_input_gives_bias(orc):
@@ -291,5 +337,5 @@ def test_workloads_full_size(orc, wid):
                "grad_spikes": np.ascontiguousarray(case["grad_spikes"][:, :, chans]),
                "sign": case["sign"][chans], "shift": case["shift"][chans], "bias": case["bias"][chans]}
         ref = oracle_run(orc, sub, wl.k, d, wl.dtype, wl.v_th, wl.surrogate, wl.alpha, 0, wl.s_max, wl.v_th_q)
-        compare(got, ref, wl.dtype, f"{wl.name} d={d}")
+        compare(got, ref, wl.dtype, f"{wl.name} d={d}", wl.k, d, hi=wl.s_max)
         del spikes, h, gx, gw, gb
