@@ -106,7 +106,8 @@ def main():
     ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--recompute", action="store_true",
-                    help="backward recomputes H from x instead of reading the forward's saved H")
+                    help="backward recomputes H and the surrogate factor from x instead of reading the "
+                         "factor the forward saved")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -163,7 +164,7 @@ def main():
             "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
             "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
             "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
-            "h": None if args.recompute else torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev),
+            "sg": None if args.recompute else torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev),
             "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
             "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
         })
@@ -174,14 +175,14 @@ def main():
         for li, L in enumerate(layers):
             if events is not None:
                 events[("fwd", li)][0].record(stream)
-            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], None, L["sg"], stream)
             if events is not None:
                 events[("fwd", li)][1].record(stream)
         for li in reversed(range(P)):
             L = layers[li]
             if events is not None:
                 events[("bwd", li)][0].record(stream)
-            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["h"], sign, shift, bias, L["gx"], L["gw"],
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["sg"], sign, shift, bias, L["gx"], L["gw"],
                                  L["gb"], L["ws"], stream=stream)
             if events is not None:
                 events[("bwd", li)][1].record(stream)
@@ -238,7 +239,8 @@ def main():
             "elements_per_layer": elems,
             "layers_per_step": P,
             "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
-            "backward_H": "recomputed from x" if args.recompute else "saved by the forward",
+            "backward_surrogate": ("H and sigma' recomputed from x" if args.recompute
+                                   else "sigma'(H - v_th) saved by the forward"),
             "v_th": wl.v_th,
         },
         "roofline": {

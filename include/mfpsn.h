@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 1
+#define MFPSN_ABI_VERSION 2
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -110,34 +110,44 @@ typedef struct mfpsn_desc {
  *   spikes : uint8 [T][N][C][S], 1 where H >= v_th else 0 (NaN -> 0)
  *   h_out  : optional (may be NULL) membrane potential H, float (F32, BF16)
  *            or int32 (Q8.8), [T][N][C][S]
- * Alignment: x 4 bytes (F32) / 2 bytes (BF16, Q8.8); h_out, bias 4 bytes. */
+ *   sg_out : optional (may be NULL) surrogate factor of H, [T][N][C][S]:
+ *            float sigma'(H - v_th) (F32, BF16), or int32
+ *            L = round_half_even(2^15 * sigma'((H - v_th_q) / 256)) (Q8.8).
+ *            Passed to mfpsn_backward, it spares the backward the charge and
+ *            the surrogate (dH = grad_spikes * factor there).
+ * Alignment: x 4 bytes (F32) / 2 bytes (BF16, Q8.8); h_out, sg_out, bias
+ * 4 bytes. */
 int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
-                  const void* bias, uint8_t* spikes, void* h_out, void* stream);
+                  const void* bias, uint8_t* spikes, void* h_out, void* sg_out, void* stream);
 
 /* Bytes of device workspace mfpsn_backward needs for this problem (per-block
- * partial sums of grad_w and grad_b, in double).  Returns a status; *bytes is
- * written on success. */
+ * partial sums of grad_w and grad_b: double, or int64 for Q8.8).  Returns a
+ * status; *bytes is written on success. */
 int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
 
 /* Backward: dH, grad_x (App. A.3 Eq. backward_X), grad_w (Eq. backward_W)
  * and grad_b (Eq. backward_b).
  *   grad_spikes : [T][N][C][S] storage type of desc->dtype (the upstream
  *                 gradient of the spikes)
- *   h           : optional (may be NULL) membrane potential H of this x, taps
- *                 and bias as written by mfpsn_forward's h_out (float, or
- *                 int32 for Q8.8); when NULL, H is recomputed from x.  Both
- *                 give identical results; passing H trades 4 bytes per
+ *   sg          : optional (may be NULL) surrogate factor of this x, taps,
+ *                 bias and surrogate, as written by mfpsn_forward's sg_out;
+ *                 when NULL, H and the factor are recomputed from x.  Both
+ *                 give identical results; passing it trades 4 bytes per
  *                 element of memory traffic for the recomputation.
  *   grad_x      : [T][N][C][S] float (F32), bfloat16 (BF16), int32 (Q8.8)
  *   grad_w      : float [C][k] or int64 [C][k] (Q8.8, Q16.16)
  *   grad_b      : float [C]    or int64 [C]    (Q8.8)
  *   workspace   : >= mfpsn_backward_workspace_size bytes, 8-byte aligned;
  *                 contents on entry are ignored (every word used is written)
+ * grad_x follows the sum of the definition exactly, except that a float dH
+ * below 2^(shift_hi - 126) in magnitude (a surrogate factor that underflowed)
+ * contributes nothing to it: each of its terms is smaller than
+ * 2^(shift_hi - shift_lo - 126).
  * grad_w and grad_b do not depend on the order in which the GPU runs its
  * blocks: partial sums are reduced in a fixed order, so repeated calls give
- * identical bits.  The Q8.8 path is exact (integers below 2^53); the call
- * fails with MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^53. */
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
+ * identical bits.  The Q8.8 path is exact (int64 sums); the call fails with
+ * MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^62. */
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* sg,
                    const int8_t* sign, const int8_t* shift, const void* bias,
                    void* grad_x, void* grad_w, void* grad_b,
                    void* workspace, size_t workspace_bytes, void* stream);

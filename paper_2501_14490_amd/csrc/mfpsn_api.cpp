@@ -207,7 +207,7 @@ int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period)
 }
 
 int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
-                  const void* bias, uint8_t* spikes, void* h_out, void* stream)
+                  const void* bias, uint8_t* spikes, void* h_out, void* sg_out, void* stream)
 {
     int st = validate(desc);
     if (st != MFPSN_OK)
@@ -217,7 +217,8 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
         return MFPSN_ERR_NULL;
     if (desc->C > 0 && (!sign || !shift || !bias))
         return MFPSN_ERR_NULL;
-    if (!aligned(x, elem_bytes(desc->dtype)) || !aligned(bias, 4) || !aligned(h_out, 4))
+    if (!aligned(x, elem_bytes(desc->dtype)) || !aligned(bias, 4) || !aligned(h_out, 4) ||
+        !aligned(sg_out, 4))
         return MFPSN_ERR_ALIGN;
     if (total == 0)
         return MFPSN_OK;
@@ -229,6 +230,7 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     a.bias = bias;
     a.spikes = spikes;
     a.h_out = h_out;
+    a.sg_out = sg_out;
     if (launch_forward(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
@@ -246,7 +248,7 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
     return MFPSN_OK;
 }
 
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* sg,
                    const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
                    void* grad_w, void* grad_b, void* workspace, size_t ws_bytes, void* stream)
 {
@@ -260,7 +262,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         return MFPSN_ERR_NULL;
     const int es = elem_bytes(desc->dtype);
     if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, grad_x_bytes(desc->dtype)) ||
-        !aligned(bias, 4) || !aligned(h, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
+        !aligned(bias, 4) || !aligned(sg, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
         !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
         return MFPSN_ERR_ALIGN;
     if (desc->dtype == MFPSN_Q8_8) {
@@ -276,7 +278,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         return MFPSN_ERR_WORKSPACE;
     a.x = x;
     a.gs = grad_spikes;
-    a.h = h;
+    a.sg = sg;
     a.sign = sign;
     a.shift = shift;
     a.bias = bias;

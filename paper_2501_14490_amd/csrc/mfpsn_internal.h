@@ -57,14 +57,15 @@ struct FwdArgs {
     const int8_t* shift;
     const void* bias;
     uint8_t* spikes;
-    void* h_out;
+    void* h_out;       // nullable: potentials H
+    void* sg_out;      // nullable: surrogate factor of H
 };
 
 struct BwdArgs {
     Geom g;
     const void* x;
     const void* gs;
-    const void* h;     // H saved by the forward (nullable: recompute from x)
+    const void* sg;    // surrogate factor saved by the forward (nullable: recompute from x)
     const int8_t* sign;
     const int8_t* shift;
     const void* bias;

@@ -31,8 +31,13 @@
 // potentials and input gradients are bit-identical to a sequential
 // evaluation of the definition.
 //
+// The forward can also save the surrogate factor sigma'(H - v_th) (Q8.8: the
+// integer factor L); the backward then needs only dH = grad_spikes * factor,
+// which moves the surrogate evaluation into the pass that is bound by memory
+// traffic rather than by arithmetic.
+//
 // Backward.  Each class is walked backwards in time.  dH[j] is computed once
-// (from the forward's saved H, or from H recomputed out of the x ring) and
+// (from the forward's saved factor, or from H recomputed out of the x ring) and
 // scattered into the k open grad_x accumulators it feeds (outputs j-k+1..j);
 // contributions reach every output in ascending tap order, so the sum order
 // is the definition's.  Output j is complete after step j and is stored.
@@ -75,6 +80,17 @@ constexpr int prefetch_depth(int K, int cap)
             return p;
     return 1;
 }
+
+// Loads in flight per wave decide how close a pass gets to HBM bandwidth:
+// the forward has one input stream, the backward three.
+#ifndef MFPSN_FWD_PREFETCH
+#define MFPSN_FWD_PREFETCH 16
+#endif
+#ifndef MFPSN_BWD_PREFETCH
+#define MFPSN_BWD_PREFETCH 8
+#endif
+constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
+constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
 
 template <int V> using ic = std::integral_constant<int, V>;
 enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 };
@@ -318,18 +334,24 @@ struct Surrogate {
     }
 };
 
-__device__ __forceinline__ float delta_h(const Surrogate& sg, float g, float h, float v_th, int)
+// Surrogate factor of a potential: float sigma'(H - v_th); Q8.8 the integer
+// L = round-half-even(2^15 sigma'((H - v_th) / 256)).
+__device__ __forceinline__ float sg_factor(const Surrogate& sg, float h, float v_th, int)
 {
     float u = h - v_th;
-    return g * sg(u);
+    return sg(u);
 }
-
-__device__ __forceinline__ int32_t delta_h(const Surrogate& sg, int32_t g, int32_t h, float, int v_th_q)
+__device__ __forceinline__ int32_t sg_factor(const Surrogate& sg, int32_t h, float, int v_th_q)
 {
     int32_t u = h - v_th_q;
     float uf = (float)u * 0.00390625f;
     float s = sg(uf);
-    int32_t L = (int32_t)rintf(s * 32768.0f);
+    return (int32_t)rintf(s * 32768.0f);
+}
+// dH = grad_spikes * factor (Q8.8: floor((g * L) / 2^15))
+__device__ __forceinline__ float delta_h(float g, float f) { return g * f; }
+__device__ __forceinline__ int32_t delta_h(int32_t g, int32_t L)
+{
     int64_t p = (int64_t)g * (int64_t)L;
     return (int32_t)(p >> 15);
 }
@@ -409,7 +431,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
 {
     using V = typename IO<DT>::V;
     using TP = Taps<K, DT, MODE>;
-    constexpr int P = prefetch_depth(K, 8);
+    constexpr int P = prefetch_depth(K, kFwdPrefetch);
     constexpr int es = IO<DT>::es;
     constexpr bool kF = DT != kQ88;
     const Geom& g = a.g;
@@ -441,6 +463,9 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
     const int32_t xstep = (int32_t)((uint64_t)d * xrow), sstep = (int32_t)((uint64_t)d * M);
     const int32_t hstep = 4 * sstep;
     const int want_h = a.h_out != nullptr ? 1 : 0;
+    const int want_sg = a.sg_out != nullptr ? 1 : 0;
+    Surrogate sg;
+    sg.init(g.sg, g.alpha);
 
     Cursor cur(g, q0);
     int tile_cached = -1;
@@ -463,6 +488,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
         const uint64_t orow = (uint64_t)r + (uint64_t)j0 * d;
         const Buf ss = make_buf(a.spikes, sbytes, orow * M);
         const Buf hs = want_h ? make_buf(a.h_out, sbytes * 4, orow * M * 4) : ss;
+        const Buf gs = want_sg ? make_buf(a.sg_out, sbytes * 4, orow * M * 4) : ss;
         const uint32_t vx = cols.col * es, vs = cols.col, vh = cols.col * 4u;
         const int32_t so_xlast = (Lr - 1 - jb) * xstep;
 
@@ -529,6 +555,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
             }
             if (want_h != 0)
                 st32(hs, vh, so_h, __builtin_bit_cast(uint32_t, h));
+            if (want_sg != 0)
+                st32(gs, vh, so_h, __builtin_bit_cast(uint32_t, sg_factor(sg, h, g.v_th, g.v_th_q)));
             advance(so_s, sstep);
             advance(so_h, hstep);
             __builtin_amdgcn_sched_barrier(0);
@@ -581,11 +609,11 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     using V = typename IO<DT>::V;
     using W = typename IO<DT>::W;
     using TP = Taps<K, DT, MODE>;
-    constexpr int P = prefetch_depth(K, 4);
+    constexpr int P = prefetch_depth(K, kBwdPrefetch);
     constexpr int es = IO<DT>::es;
     constexpr int gxs = IO<DT>::gx_es;
     constexpr bool kF = DT != kQ88;
-    constexpr bool kRe = !HS;  // recompute H from the x ring
+    constexpr bool kRe = !HS;  // no saved factor: recompute H from the x ring
     // x rings: double copies for the exact grad_w products of float data;
     // the stored value itself for the recompute of float data and for Q8.8
     // (whose products are exact 32x32 -> 64-bit integer products)
@@ -653,7 +681,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         const uint64_t brow = (uint64_t)r + (uint64_t)jb * d;
         const Buf xs = make_buf(a.x, xbytes, brow * xrow);
         const Buf gsb = make_buf(a.gs, xbytes, brow * xrow);
-        const Buf hsb = HS ? make_buf(a.h, hbytes, brow * hrow) : xs;
+        const Buf hsb = HS ? make_buf(a.sg, hbytes, brow * hrow) : xs;
         const Buf gxb = make_buf(a.grad_x, gxbytes, brow * gxrow);
         const uint32_t vx = cols.col * es, vh = cols.col * 4u, vgx = cols.col * gxs;
         const int32_t so_last = (Lr - 1 - jb) * xstep, so_hlast = (Lr - 1 - jb) * hstep;
@@ -700,7 +728,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             px[js] = IO<DT>::load(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
         }
         int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
-        int32_t so_hp = (jstart - P - jb) * hstep;           // h of step j - P
+        int32_t so_hp = (jstart - P - jb) * hstep;           // factor of step j - P
         int32_t so_xp = (jstart - P - K + 1 - jb) * xstep;   // x of step j - P
         int32_t so_gx = (jstart - jb) * gxstep;              // grad_x of step j
 
@@ -740,10 +768,12 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 xf[(sj + 1) % K] = 0;  // Q8.8: zeros before time 0 (recompute)
             }
             if (full || j <= jtop) {
-                V h;
+                V dh;
                 if constexpr (HS) {
-                    h = hv;
-                } else if constexpr (kF) {
+                    dh = delta_h(gv, hv);  // hv: the saved factor
+                } else {
+                V h;
+                if constexpr (kF) {
                     constexpr int rmin = edge ? u : 0;  // taps reading before time 0 are left out
                     V acc;
                     if (__builtin_expect(slow_x > 0, 0)) {
@@ -765,7 +795,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                         acc = acc + tp.apply(xf[(sj + 1 + i) % K], i);
                     h = acc;
                 }
-                const V dh = delta_h(sg, gv, h, g.v_th, g.v_th_q);
+                dh = delta_h(gv, sg_factor(sg, h, g.v_th, g.v_th_q));
+                }
                 const bool own = full || j < j1;
                 if (own) {
                     if constexpr (kF) {
@@ -1067,7 +1098,7 @@ hipError_t bwd_k(BwdArgs& a, hipStream_t st)
 {
     static int cache[4][16];
     const bool lc = a.g.mode == kLaneChannel;
-    const bool hs = a.h != nullptr;
+    const bool hs = a.sg != nullptr;
     auto kern = lc ? (hs ? bwd_kernel<K, DT, kLaneChannel, true> : bwd_kernel<K, DT, kLaneChannel, false>)
                    : (hs ? bwd_kernel<K, DT, kPlane, true> : bwd_kernel<K, DT, kPlane, false>);
     a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[(lc ? 0 : 2) + (hs ? 1 : 0)]));

@@ -36,6 +36,7 @@ SURROGATES = {"sigmoid": MFPSN_SG_SIGMOID, "atan": MFPSN_SG_ATAN, "arctan": MFPS
 STORAGE = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.bfloat16, MFPSN_Q8_8: torch.int16}
 GRAD_X = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.bfloat16, MFPSN_Q8_8: torch.int32}
 H_OUT = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int32}
+SG_OUT = H_OUT
 BIAS = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int32}
 GRAD_WB = {MFPSN_F32: torch.float32, MFPSN_BF16: torch.float32, MFPSN_Q8_8: torch.int64}
 
@@ -50,7 +51,7 @@ class MfpsnDesc(ctypes.Structure):
 
 _P = ctypes.c_void_p
 _DP = ctypes.POINTER(MfpsnDesc)
-_lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_forward.restype = ctypes.c_int
 _lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
@@ -121,9 +122,9 @@ def mfpsn_sawtooth_dilation(layer: int, period: int) -> int:
     return int(_lib.mfpsn_sawtooth_dilation(int(layer), int(period)))
 
 
-def mfpsn_forward(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, stream=None) -> None:
+def mfpsn_forward(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, sg_out=None, stream=None) -> None:
     _check(_lib.mfpsn_forward(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias),
-                              _ptr(spikes), _ptr(h_out), _stream(stream)), "mfpsn_forward")
+                              _ptr(spikes), _ptr(h_out), _ptr(sg_out), _stream(stream)), "mfpsn_forward")
 
 
 def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
@@ -133,11 +134,11 @@ def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
     return int(n.value)
 
 
-def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sign, shift, bias, grad_x, grad_w, grad_b,
+def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, sg, sign, shift, bias, grad_x, grad_w, grad_b,
                    workspace, workspace_bytes=None, stream=None) -> None:
     if workspace_bytes is None:
         workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(h), _ptr(sign),
+    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(sg), _ptr(sign),
                                _ptr(shift), _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
                                _ptr(workspace), int(workspace_bytes), _stream(stream)), "mfpsn_backward")
 
@@ -159,30 +160,33 @@ def _expect(t, dtype, device, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, stream=None):
+def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, want_sg: bool = False, stream=None):
+    """spikes, plus H (want_h) and the surrogate factor (want_sg) in that order."""
     dev = x.device
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(bias, BIAS[desc.dtype], dev, "bias")
     spikes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
     h = torch.empty(x.shape, dtype=H_OUT[desc.dtype], device=dev) if want_h else None
-    mfpsn_forward(desc, x, sign, shift, bias, spikes, h, stream)
-    return (spikes, h) if want_h else spikes
+    sg = torch.empty(x.shape, dtype=SG_OUT[desc.dtype], device=dev) if want_sg else None
+    mfpsn_forward(desc, x, sign, shift, bias, spikes, h, sg, stream)
+    out = (spikes,) + ((h,) if want_h else ()) + ((sg,) if want_sg else ())
+    return out if len(out) > 1 else spikes
 
 
-def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, h=None):
-    """h: optional saved potentials from forward(..., want_h=True)."""
+def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, sg=None):
+    """sg: optional surrogate factor saved by forward(..., want_sg=True)."""
     dev = x.device
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
-    if h is not None:
-        _expect(h, H_OUT[desc.dtype], dev, "h")
+    if sg is not None:
+        _expect(sg, SG_OUT[desc.dtype], dev, "sg")
     grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
     grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
     grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
     need = mfpsn_backward_workspace_size(desc)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
-    mfpsn_backward(desc, x, grad_spikes, h, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
+    mfpsn_backward(desc, x, grad_spikes, sg, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
                    stream=stream)
     return grad_x, grad_w, grad_b
 
@@ -208,14 +212,14 @@ class MfPSNFunction(torch.autograd.Function):
         sign, shift = quantize(w.detach().contiguous(), shift_lo, shift_hi)
         xc = x.detach().contiguous()
         bc = b.detach().float().contiguous()
-        spikes, h = forward(desc, xc, sign, shift, bc, want_h=True)
-        ctx.save_for_backward(xc, sign, shift, bc, h)
+        spikes, sg = forward(desc, xc, sign, shift, bc, want_sg=True)
+        ctx.save_for_backward(xc, sign, shift, bc, sg)
         ctx.desc = desc
         return spikes.to(x.dtype)
 
     @staticmethod
     def backward(ctx, grad_spikes):
-        xc, sign, shift, bc, h = ctx.saved_tensors
+        xc, sign, shift, bc, sg = ctx.saved_tensors
         g = grad_spikes.to(xc.dtype).contiguous()
-        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, h=h)
+        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, sg=sg)
         return grad_x, grad_w, grad_b, None, None, None, None, None, None, None

@@ -32,18 +32,18 @@ def to_dev(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved_h=False):
+def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved_sg=False):
     x = to_dev(case["x"], dtype)
     g = to_dev(case["grad_spikes"], dtype)
     sign = to_dev(case["sign"], None)
     shift = to_dev(case["shift"], None)
     bias = to_dev(case["bias"], None)
     desc = mfpsn.make_desc(case["x"].shape, k, d, dtype, surrogate, alpha, v_th, v_th_q, lo, hi)
-    spikes, h = mfpsn.forward(desc, x, sign, shift, bias, want_h=True)
-    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, h=h if saved_h else None)
+    spikes, h, sg = mfpsn.forward(desc, x, sign, shift, bias, want_h=True, want_sg=True)
+    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, sg=sg if saved_sg else None)
     torch.cuda.synchronize()
-    out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "grad_w": gw.cpu().numpy(),
-           "grad_b": gb.cpu().numpy()}
+    out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "SG": sg.cpu().numpy(),
+           "grad_w": gw.cpu().numpy(), "grad_b": gb.cpu().numpy()}
     if dtype == "bf16":
         out["grad_x_bits"] = gx.view(torch.int16).cpu().numpy().view(np.uint16)
     else:
@@ -66,6 +66,11 @@ def oracle_run(orc, case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=
         b = orc.backward_f32(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
                              v_th, surrogate, alpha, lo, hi)
     b["spikes"], b["Hf"] = spk, H
+    # the surrogate factor the forward saves, by the oracle's own surrogate
+    if dtype == "q8_8":
+        b["SG"] = orc.surrogate_q15(surrogate, alpha, (H.astype(np.int64) - v_th_q).astype(np.int32))
+    else:
+        b["SG"] = orc.surrogate(surrogate, alpha, (H - np.float32(v_th)).astype(np.float32))
     return b
 
 
@@ -96,6 +101,14 @@ def check_grad_x(g, r, hit, label):
 
 def compare(got, ref, dtype, label, k=None, d=None, hi=7):
     assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
+    if "SG" in got:
+        g, r = got["SG"], ref["SG"]
+        if dtype == "q8_8":
+            assert np.array_equal(g, r), f"{label}: surrogate factor differs"
+        else:
+            nan = np.isnan(r)
+            assert np.array_equal(np.isnan(g), nan), f"{label}: surrogate factor NaN pattern differs"
+            assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: surrogate factor differs"
     if dtype == "q8_8":
         assert np.array_equal(got["H"], ref["Hf"]), f"{label}: H differs"
         assert np.array_equal(got["grad_x"], ref["grad_x"]), f"{label}: grad_x differs"
@@ -132,28 +145,28 @@ SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("saved_sg", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
 @pytest.mark.parametrize("shape_i", range(len(SHAPES)))
 @pytest.mark.parametrize("k,d", [(1, 1), (2, 3), (3, 2), (5, 1), (8, 4), (16, 2)])
-def test_small_shapes(orc, dtype, shape_i, k, d, saved_h):
+def test_small_shapes(orc, dtype, shape_i, k, d, saved_sg):
     (T, N, C, sp), label = SHAPES[shape_i]
     case = workloads.make_small(T, N, C, sp, k=k, s_lo=0, s_hi=7, dtype=dtype, seed=100 + k * 7 + d)
     v_th = 0.5
-    got = gpu_run(case, k, d, dtype, v_th, saved_h=saved_h)
+    got = gpu_run(case, k, d, dtype, v_th, saved_sg=saved_sg)
     ref = oracle_run(orc, case, k, d, dtype, v_th)
-    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_h={saved_h}", k, d)
+    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_sg={saved_sg}", k, d)
 
 
-@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("saved_sg", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "q8_8"])
 @pytest.mark.parametrize("k", [4, 7, 12, 17, 24, 31, 32])
-def test_orders(orc, dtype, k, saved_h):
+def test_orders(orc, dtype, k, saved_sg):
     d = 1 + k % 3
     case = workloads.make_small(3 * k + 5, 4, 70, (), k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
     ref = oracle_run(orc, case, k, d, dtype, 0.75)
-    got = gpu_run(case, k, d, dtype, 0.75, saved_h=saved_h)
-    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_h={saved_h}", k, d)
+    got = gpu_run(case, k, d, dtype, 0.75, saved_sg=saved_sg)
+    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_sg={saved_sg}", k, d)
 
 
 @pytest.mark.parametrize("surrogate,alpha", [("atan", 2.0), ("atan", 5.0), ("rational", 10.0), ("sigmoid", 1.5)])
@@ -181,17 +194,17 @@ def test_short_sequences(orc, T):
     compare(got, ref, "f32", f"T={T}", 8, 3)
 
 
-@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("saved_sg", [False, True])
 @pytest.mark.parametrize("k,d", [(8, 3), (16, 1), (5, 7)])
-def test_long_sequence_is_chunked(orc, k, d, saved_h):
+def test_long_sequence_is_chunked(orc, k, d, saved_sg):
     # few columns and a long time axis: the planner cuts each residue class
     # into chunks whose halos are recomputed
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="q8_8", seed=9)
-    got = gpu_run(case, k, d, "q8_8", 0.0, saved_h=saved_h)
+    got = gpu_run(case, k, d, "q8_8", 0.0, saved_sg=saved_sg)
     ref = oracle_run(orc, case, k, d, "q8_8", 0.0)
     compare(got, ref, "q8_8", "chunked", k, d)
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="f32", seed=9)
-    compare(gpu_run(case, k, d, "f32", 0.3, saved_h=saved_h), oracle_run(orc, case, k, d, "f32", 0.3),
+    compare(gpu_run(case, k, d, "f32", 0.3, saved_sg=saved_sg), oracle_run(orc, case, k, d, "f32", 0.3),
             "f32", "chunked f32", k, d)
 
 
@@ -203,11 +216,15 @@ def compare_nan_aware(got, ref, label, k, d, hi=7):
     assert np.array_equal(np.isnan(g), nan), f"{label}: H NaN pattern differs"
     assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: H differs"
     check_grad_x(got["grad_x"], ref["grad_x"], tiny_dh_outputs(ref["dH"], k, d, hi), label)
+    g, r = got["SG"], ref["SG"]
+    nan = np.isnan(r)
+    assert np.array_equal(np.isnan(g), nan), f"{label}: surrogate factor NaN pattern differs"
+    assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: surrogate factor differs"
 
 
-@pytest.mark.parametrize("saved_h", [False, True])
+@pytest.mark.parametrize("saved_sg", [False, True])
 @pytest.mark.parametrize("k,d", [(8, 1), (16, 2), (5, 3), (24, 1)])
-def test_special_values_take_the_exact_path(orc, k, d, saved_h):
+def test_special_values_take_the_exact_path(orc, k, d, saved_sg):
     # zeros, subnormals, values at the edge of the exponent-add range, huge
     # values, infinities: every tap must still equal the exact ldexp result
     case = workloads.make_small(60, 3, 80, (), k=k, s_lo=0, s_hi=7, dtype="f32", seed=k + d)
@@ -219,18 +236,18 @@ def test_special_values_take_the_exact_path(orc, k, d, saved_h):
     idx = rng.integers(0, x.size, size=400)
     x.ravel()[idx] = specials[rng.integers(0, specials.size, size=idx.size)]
     x[5:9, 1, :] = 0.0  # whole rows of zeros inside the walk
-    got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
+    got = gpu_run(case, k, d, "f32", 0.25, saved_sg=saved_sg)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
     compare_nan_aware(got, ref, f"specials k={k} d={d}", k, d)
     case["x"].ravel()[rng.integers(0, x.size, size=20)] = np.float32(np.inf)
     case["grad_spikes"].ravel()[rng.integers(0, x.size, size=200)] = 0.0
-    got = gpu_run(case, k, d, "f32", 0.25, saved_h=saved_h)
+    got = gpu_run(case, k, d, "f32", 0.25, saved_sg=saved_sg)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
     compare_nan_aware(got, ref, f"specials+inf k={k} d={d}", k, d)
 
 
-@pytest.mark.parametrize("saved_h", [False, True])
-def test_tiny_dh_terms(orc, saved_h):
+@pytest.mark.parametrize("saved_sg", [False, True])
+def test_tiny_dh_terms(orc, saved_sg):
     # grad_spikes values around 1e-38 make dH fall below the exponent-add
     # range on many lanes: their grad_x terms are dropped, every other output
     # stays bit-exact
@@ -239,7 +256,7 @@ def test_tiny_dh_terms(orc, saved_h):
     rng = np.random.default_rng(21)
     idx = rng.integers(0, g.size, size=g.size // 5)
     g.ravel()[idx] = (rng.standard_normal(idx.size) * 1e-37).astype(np.float32)
-    got = gpu_run(case, 8, 2, "f32", 0.25, saved_h=saved_h)
+    got = gpu_run(case, 8, 2, "f32", 0.25, saved_sg=saved_sg)
     ref = oracle_run(orc, case, 8, 2, "f32", 0.25)
     hit = tiny_dh_outputs(ref["dH"], 8, 2, 7)
     assert hit.any() and not hit.all()
@@ -319,13 +336,15 @@ def test_workloads_full_size(orc, wid):
     for d in wl.dilations:
         desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
                                wl.s_max)
-        spikes, h = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True)
-        saved = d % 2 == 1  # odd dilations read the saved H, even ones recompute it
+        spikes, h, sg = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True,
+                                      want_sg=True)
+        saved = d % 2 == 1  # odd dilations read the saved factor, even ones recompute it
         gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"],
-                                    h=h if saved else None)
+                                    sg=sg if saved else None)
         torch.cuda.synchronize()
         got = {"spikes": spikes.index_select(2, chans_t).cpu().numpy(),
                "H": h.index_select(2, chans_t).cpu().numpy(),
+               "SG": sg.index_select(2, chans_t).cpu().numpy(),
                "grad_w": gw.index_select(0, chans_t).cpu().numpy(),
                "grad_b": gb.index_select(0, chans_t).cpu().numpy()}
         gxs = gx.index_select(2, chans_t)
@@ -338,4 +357,4 @@ def test_workloads_full_size(orc, wid):
                "sign": case["sign"][chans], "shift": case["shift"][chans], "bias": case["bias"][chans]}
         ref = oracle_run(orc, sub, wl.k, d, wl.dtype, wl.v_th, wl.surrogate, wl.alpha, 0, wl.s_max, wl.v_th_q)
         compare(got, ref, wl.dtype, f"{wl.name} d={d}", wl.k, d, hi=wl.s_max)
-        del spikes, h, gx, gw, gb
+        del spikes, h, sg, gx, gw, gb
