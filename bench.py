@@ -53,7 +53,7 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(wl_name):
+def measured_traffic(wl_name, mode):
     """HBM bytes per backward launch from the committed rocprofv3 counter
     summary, if it was taken on the current kernel source; else None."""
     path = os.path.join(ROOT, "profiles", "bwd_traffic.json")
@@ -61,7 +61,7 @@ def measured_traffic(wl_name):
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    ent = rec.get(wl_name)
+    ent = rec.get(f"{wl_name}|{mode}")
     if not ent or ent.get("kernel_source") != kernel_source_hash():
         return None
     return ent.get("bytes_per_launch")
@@ -97,6 +97,31 @@ def cpu_baseline(wl, case, channels: int):
                       f"(nproc {os.cpu_count()})"}
 
 
+def memory_ceiling(torch, dev, wl):
+    """Bandwidth of torch's own elementwise kernels on float32 tensors with the
+    workload's element count: copy (8 B/el) and addcmul (3 reads + 1 write,
+    16 B/el: the saved-factor backward's mix)."""
+    n = wl.elements
+    a, b, c, o = (torch.ones(n, dtype=torch.float32, device=dev) for _ in range(4))
+    res = {}
+    for name, fn, bpe in (("copy_1r1w", lambda: o.copy_(a), 8),
+                          ("addcmul_3r1w", lambda: torch.addcmul(a, b, c, out=o), 16)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        reps = 20
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        res[name] = {"us": round(us, 2), "GB/s": round(bpe * n / (us * 1e-6) / 1e9, 1)}
+        log(f"{name}: {us:.1f} us  {res[name]['GB/s']:.0f} GB/s")
+    print(json.dumps({"memory_ceiling": res, "elements": n, "workload": wl.name}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,11 +130,15 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (default 2: audio-spike-shaped)")
     ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--recompute", action="store_true",
-                    help="backward recomputes H and the surrogate factor from x instead of reading the "
-                         "factor the forward saved")
+    ap.add_argument("--saved-factor", choices=("auto", "yes", "no"), default="auto",
+                    help="forward saves sigma'(H - v_th) for the backward (yes), or the backward "
+                         "recomputes H and the factor from x (no); auto: save when k >= 16")
+    ap.add_argument("--recompute", action="store_true", help="same as --saved-factor no")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--memory-ceiling", action="store_true",
+                    help="only time plain library streams of the workload's size (1 read + 1 write, "
+                         "3 reads + 1 write): the bandwidth a kernel with that mix can reach")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -138,6 +167,13 @@ def main():
         return
     wl = workloads.WORKLOADS[args.workload]
     log(f"workload {wl.wid}: {wl.describe()}  dilations {wl.dilations}")
+    if args.memory_ceiling:
+        memory_ceiling(torch, dev, wl)
+        return
+    if args.recompute:
+        args.saved_factor = "no"
+    saved = args.saved_factor == "yes" or (args.saved_factor == "auto" and wl.k >= 16)
+    mode = "saved" if saved else "recompute"
     t0 = time.time()
     case = workloads.make_inputs(wl)
     log(f"inputs drawn in {time.time() - t0:.1f}s")
@@ -164,7 +200,7 @@ def main():
             "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
             "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
             "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
-            "sg": None if args.recompute else torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev),
+            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if saved else None,
             "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
             "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
         })
@@ -239,8 +275,8 @@ def main():
             "elements_per_layer": elems,
             "layers_per_step": P,
             "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
-            "backward_surrogate": ("H and sigma' recomputed from x" if args.recompute
-                                   else "sigma'(H - v_th) saved by the forward"),
+            "backward_surrogate": ("sigma'(H - v_th) saved by the forward" if saved
+                                   else "H and sigma' recomputed from x"),
             "v_th": wl.v_th,
         },
         "roofline": {
@@ -250,7 +286,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": measured_traffic(wl.name),
+            "traffic": measured_traffic(wl.name, mode),
             "alg_bytes_per_launch": bwd_bytes,
             "avg_launch_us": bwd_ms * 1e3,
         },

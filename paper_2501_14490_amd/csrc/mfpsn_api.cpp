@@ -97,7 +97,9 @@ int64_t env_int(const char* name, int64_t dflt)
 
 int64_t target_items(bool backward)
 {
-    static const int64_t fwd = env_int("MFPSN_FWD_ITEMS", 2048);
+    // the forward's halo is K-1 loads, so it chunks down to about 8 waves per
+    // SIMD; the backward's halo is K-1 steps of work, so it stops at 2
+    static const int64_t fwd = env_int("MFPSN_FWD_ITEMS", 8192);
     static const int64_t bwd = env_int("MFPSN_BWD_ITEMS", 2048);
     return backward ? bwd : fwd;
 }

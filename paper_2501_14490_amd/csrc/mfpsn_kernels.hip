@@ -84,10 +84,10 @@ constexpr int prefetch_depth(int K, int cap)
 // Loads in flight per wave decide how close a pass gets to HBM bandwidth:
 // the forward has one input stream, the backward three.
 #ifndef MFPSN_FWD_PREFETCH
-#define MFPSN_FWD_PREFETCH 16
+#define MFPSN_FWD_PREFETCH 8
 #endif
 #ifndef MFPSN_BWD_PREFETCH
-#define MFPSN_BWD_PREFETCH 8
+#define MFPSN_BWD_PREFETCH 4
 #endif
 constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
 constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
