@@ -87,7 +87,7 @@ constexpr int prefetch_depth(int K, int cap)
 #define MFPSN_FWD_PREFETCH 8
 #endif
 #ifndef MFPSN_BWD_PREFETCH
-#define MFPSN_BWD_PREFETCH 4
+#define MFPSN_BWD_PREFETCH 2
 #endif
 constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
 constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
@@ -118,25 +118,33 @@ __device__ __forceinline__ Buf make_buf(const void* tensor, uint64_t tensor_byte
     return b;
 }
 
+// Cache-policy bits of the streaming accesses (every element is read or
+// written once per pass).
+#ifndef MFPSN_LD_CPOL
+#define MFPSN_LD_CPOL 0
+#endif
+#ifndef MFPSN_ST_CPOL
+#define MFPSN_ST_CPOL 2  // nt: streaming stores
+#endif
 __device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
 {
-    return __builtin_amdgcn_raw_buffer_load_b32(b.rs, v, s, 0);
+    return __builtin_amdgcn_raw_buffer_load_b32(b.rs, v, s, MFPSN_LD_CPOL);
 }
 __device__ __forceinline__ uint32_t ld16(Buf b, uint32_t v, int32_t s)
 {
-    return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, 0);
+    return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, MFPSN_LD_CPOL);
 }
 __device__ __forceinline__ void st32(Buf b, uint32_t v, int32_t s, uint32_t x)
 {
-    __builtin_amdgcn_raw_buffer_store_b32(x, b.rs, v, s, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 __device__ __forceinline__ void st16(Buf b, uint32_t v, int32_t s, uint16_t x)
 {
-    __builtin_amdgcn_raw_buffer_store_b16(x, b.rs, v, s, 0);
+    __builtin_amdgcn_raw_buffer_store_b16(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 __device__ __forceinline__ void st8(Buf b, uint32_t v, int32_t s, uint8_t x)
 {
-    __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, 0);
+    __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 
 // s += inc, kept opaque so the compiler keeps one running SGPR per stream
@@ -609,7 +617,11 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     using V = typename IO<DT>::V;
     using W = typename IO<DT>::W;
     using TP = Taps<K, DT, MODE>;
-    constexpr int P = prefetch_depth(K, kBwdPrefetch);
+    // Lane-channel waves at orders up to 16 run 4 per SIMD and stream three
+    // 256-byte rows per step: a short queue is best.  Plane waves (narrower
+    // rows) want a longer one, and high orders (2 waves per SIMD) a deep one.
+    constexpr int P = prefetch_depth(K, K >= 24 ? 8 * kBwdPrefetch
+                                                : (MODE == kLaneChannel ? kBwdPrefetch : 2 * kBwdPrefetch));
     constexpr int es = IO<DT>::es;
     constexpr int gxs = IO<DT>::gx_es;
     constexpr bool kF = DT != kQ88;
