@@ -13,7 +13,10 @@ Prints ONE JSON line on stdout (everything else goes to stderr):
   roofline   = the backward kernel (the dominant one): algorithmic bytes per
                launch (read x, read grad_spikes, write grad_x) / its average
                duration from HIP events recorded on the launch stream inside
-               the timed region, against 8 TB/s
+               the timed region, against 8 TB/s.  The events are created
+               without the system-scope fence (hipEventDisableSystemFence), so
+               recording them does not write back and invalidate the caches
+               between launches.
   cpu_baseline = the oracle (single-threaded C) timed on this host on a
                channel slice of the same workload
 """
@@ -33,6 +36,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+
+BACKWARD_INPUTS = ("recompute", "h", "sg")
+# what the forward saves for the backward in each workload (the fastest step
+# measured on MI355X)
+AUTO_BACKWARD_INPUT = {1: "recompute", 2: "sg", 3: "recompute", 4: "recompute", 5: "sg"}
 
 
 def log(*a):
@@ -65,6 +73,44 @@ def measured_traffic(wl_name, mode):
     if not ent or ent.get("kernel_source") != kernel_source_hash():
         return None
     return ent.get("bytes_per_launch")
+
+
+class HipEvents:
+    """Timing events of the HIP runtime, recorded on a given stream, created
+    without the system-scope release fence (which would add a cache write-back
+    and invalidate between the kernels they separate)."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self):
+        import ctypes
+
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def new(self):
+        e = self.ct.c_void_p()
+        rc = self.hip.hipEventCreateWithFlags(self.ct.byref(e), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+        return e
+
+    def record(self, e, stream):
+        rc = self.hip.hipEventRecord(e, self.ct.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = self.ct.c_float()
+        rc = self.hip.hipEventElapsedTime(self.ct.byref(ms), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
 
 
 def cpu_baseline(wl, case, channels: int):
@@ -130,10 +176,11 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (default 2: audio-spike-shaped)")
     ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--saved-factor", choices=("auto", "yes", "no"), default="auto",
-                    help="forward saves sigma'(H - v_th) for the backward (yes), or the backward "
-                         "recomputes H and the factor from x (no); auto: save when k >= 16")
-    ap.add_argument("--recompute", action="store_true", help="same as --saved-factor no")
+    ap.add_argument("--backward-input", choices=("auto",) + BACKWARD_INPUTS, default="auto",
+                    help="what the forward saves for the backward: nothing (recompute: the backward "
+                         "recomputes H and the surrogate factor from x), the potentials H (h), or the "
+                         "surrogate factor sigma'(H - v_th) (sg); auto: the best one measured for the "
+                         "workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--memory-ceiling", action="store_true",
@@ -170,10 +217,7 @@ def main():
     if args.memory_ceiling:
         memory_ceiling(torch, dev, wl)
         return
-    if args.recompute:
-        args.saved_factor = "no"
-    saved = args.saved_factor == "yes" or (args.saved_factor == "auto" and wl.k >= 16)
-    mode = "saved" if saved else "recompute"
+    mode = args.backward_input if args.backward_input != "auto" else AUTO_BACKWARD_INPUT[wl.wid]
     t0 = time.time()
     case = workloads.make_inputs(wl)
     log(f"inputs drawn in {time.time() - t0:.1f}s")
@@ -200,34 +244,36 @@ def main():
             "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
             "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
             "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
-            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if saved else None,
+            "h": torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev) if mode == "h" else None,
+            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if mode == "sg" else None,
             "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
             "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
         })
     del x0, g0
     stream = torch.cuda.current_stream()
+    hev = HipEvents()
 
     def step(events=None):
         for li, L in enumerate(layers):
             if events is not None:
-                events[("fwd", li)][0].record(stream)
-            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], None, L["sg"], stream)
+                hev.record(events[("fwd", li)][0], stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], L["sg"], stream)
             if events is not None:
-                events[("fwd", li)][1].record(stream)
+                hev.record(events[("fwd", li)][1], stream)
         for li in reversed(range(P)):
             L = layers[li]
             if events is not None:
-                events[("bwd", li)][0].record(stream)
-            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["sg"], sign, shift, bias, L["gx"], L["gw"],
-                                 L["gb"], L["ws"], stream=stream)
+                hev.record(events[("bwd", li)][0], stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["h"], L["sg"], sign, shift, bias, L["gx"],
+                                 L["gw"], L["gb"], L["ws"], stream=stream)
             if events is not None:
-                events[("bwd", li)][1].record(stream)
+                hev.record(events[("bwd", li)][1], stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    ev = {(kind, li): [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-                       for _ in range(args.steps)] for kind in ("fwd", "bwd") for li in range(P)}
+    ev = {(kind, li): [[hev.new(), hev.new()] for _ in range(args.steps)]
+          for kind in ("fwd", "bwd") for li in range(P)}
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for s in range(args.steps):
@@ -239,7 +285,7 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
 
     def avg_ms(kind, li):
-        return float(np.mean([a.elapsed_time(b) for a, b in ev[(kind, li)]]))
+        return float(np.mean([hev.elapsed_ms(a, b) for a, b in ev[(kind, li)]]))
 
     per = {f"{kind}_d{layers[li]['d']}_us": round(avg_ms(kind, li) * 1e3, 2)
            for kind in ("fwd", "bwd") for li in range(P)}
@@ -275,8 +321,9 @@ def main():
             "elements_per_layer": elems,
             "layers_per_step": P,
             "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
-            "backward_surrogate": ("sigma'(H - v_th) saved by the forward" if saved
-                                   else "H and sigma' recomputed from x"),
+            "backward_input": {"recompute": "H and sigma'(H - v_th) recomputed from x",
+                               "h": "H saved by the forward",
+                               "sg": "sigma'(H - v_th) saved by the forward"}[mode],
             "v_th": wl.v_th,
         },
         "roofline": {

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 2
+#define MFPSN_ABI_VERSION 3
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -109,7 +109,8 @@ typedef struct mfpsn_desc {
  *   sign, shift : int8 [C][k];  bias : float[C] or int32[C] (Q8.8)
  *   spikes : uint8 [T][N][C][S], 1 where H >= v_th else 0 (NaN -> 0)
  *   h_out  : optional (may be NULL) membrane potential H, float (F32, BF16)
- *            or int32 (Q8.8), [T][N][C][S]
+ *            or int32 (Q8.8), [T][N][C][S].  Passed to mfpsn_backward, it
+ *            spares the backward the charge.
  *   sg_out : optional (may be NULL) surrogate factor of H, [T][N][C][S]:
  *            float sigma'(H - v_th) (F32, BF16), or int32
  *            L = round_half_even(2^15 * sigma'((H - v_th_q) / 256)) (Q8.8).
@@ -129,11 +130,13 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
  * and grad_b (Eq. backward_b).
  *   grad_spikes : [T][N][C][S] storage type of desc->dtype (the upstream
  *                 gradient of the spikes)
+ *   h           : optional (may be NULL) potentials H of this x, taps and
+ *                 bias, as written by mfpsn_forward's h_out
  *   sg          : optional (may be NULL) surrogate factor of this x, taps,
- *                 bias and surrogate, as written by mfpsn_forward's sg_out;
- *                 when NULL, H and the factor are recomputed from x.  Both
- *                 give identical results; passing it trades 4 bytes per
- *                 element of memory traffic for the recomputation.
+ *                 bias and surrogate, as written by mfpsn_forward's sg_out
+ *   The backward uses sg if given, else h if given, else recomputes H and
+ *   the factor from x.  All three give identical results; a saved tensor
+ *   trades 4 bytes per element of memory traffic for the recomputation.
  *   grad_x      : [T][N][C][S] float (F32), bfloat16 (BF16), int32 (Q8.8)
  *   grad_w      : float [C][k] or int64 [C][k] (Q8.8, Q16.16)
  *   grad_b      : float [C]    or int64 [C]    (Q8.8)
@@ -147,8 +150,8 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
  * blocks: partial sums are reduced in a fixed order, so repeated calls give
  * identical bits.  The Q8.8 path is exact (int64 sums); the call fails with
  * MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^62. */
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* sg,
-                   const int8_t* sign, const int8_t* shift, const void* bias,
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
+                   const void* sg, const int8_t* sign, const int8_t* shift, const void* bias,
                    void* grad_x, void* grad_w, void* grad_b,
                    void* workspace, size_t workspace_bytes, void* stream);
 

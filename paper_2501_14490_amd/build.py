@@ -42,36 +42,36 @@ DTYPES = [0, 1, 2]  # f32, bf16, q8.8
 
 
 def _units():
+    """(object, compile command, sources it depends on) of every translation unit."""
     src = os.path.join(CSRC, "mfpsn_kernels.hip")
+    headers = [os.path.join(CSRC, "mfpsn_internal.h"), os.path.join(INCLUDE, "mfpsn.h")]
     units = []
     for dt in DTYPES:
         for lo, hi in K_RANGES:
             obj = os.path.join(BUILD, f"kernels_d{dt}_k{lo}-{hi}.o")
             units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
                                 f"-DMFPSN_TU_DTYPE={dt}", f"-DMFPSN_TU_KLO={lo}",
-                                f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj]))
+                                f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj], [src, *headers]))
     obj = os.path.join(BUILD, "kernels_misc.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
-                        "-c", src, "-o", obj]))
+                        "-c", src, "-o", obj], [src, *headers]))
     for name in ("mfpsn_api.cpp", "mfpsn_dispatch.cpp"):
         obj = os.path.join(BUILD, name.replace(".cpp", ".o"))
-        units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
-                            os.path.join(CSRC, name), "-o", obj]))
+        cpp = os.path.join(CSRC, name)
+        units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
+                      [cpp, *headers]))
     return units
-
-
-def _sources():
-    return [os.path.join(CSRC, f) for f in os.listdir(CSRC)] + [os.path.join(INCLUDE, "mfpsn.h")]
 
 
 def build(jobs: int | None = None, force: bool = True, verbose: bool = False) -> str:
     """Compile every translation unit and link libmfpsn.so; returns its path.
-    With force=False, units whose object is newer than every source are kept."""
+    With force=False, units whose object is newer than every source it
+    depends on are kept."""
     os.makedirs(BUILD, exist_ok=True)
-    newest_src = max(os.path.getmtime(p) for p in _sources())
     todo = []
-    for obj, cmd in _units():
-        if force or not os.path.exists(obj) or os.path.getmtime(obj) < newest_src:
+    for obj, cmd, deps in _units():
+        newest = max(os.path.getmtime(p) for p in deps)
+        if force or not os.path.exists(obj) or os.path.getmtime(obj) < newest:
             todo.append((obj, cmd))
     jobs = jobs or min(8, os.cpu_count() or 1)
     t0 = time.time()
@@ -90,7 +90,7 @@ def build(jobs: int | None = None, force: bool = True, verbose: bool = False) ->
 
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         list(ex.map(run, todo))
-    objs = [obj for obj, _ in _units()]
+    objs = [obj for obj, _, _ in _units()]
     tmp = LIB + f".tmp{os.getpid()}"
     link = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     p = subprocess.run(link, capture_output=True, text=True)

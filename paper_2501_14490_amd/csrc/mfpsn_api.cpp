@@ -7,6 +7,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <initializer_list>
+
 #include "mfpsn_internal.h"
 
 using namespace mfpsn;
@@ -104,7 +106,28 @@ int64_t target_items(bool backward)
     return backward ? bwd : fwd;
 }
 
-Geom plan(const mfpsn_desc* d, bool backward)
+// Two adjacent columns per lane (one 2x-wide access per stream and step):
+// plane mode with an even S (a lane's two positions share one row of S
+// columns), orders the two-column kernels are built for, and tensors aligned
+// for the wide accesses.  MFPSN_PAIR=0 turns it off.
+bool pair_layout(const mfpsn_desc* d)
+{
+    static const bool on = [] {
+        const char* e = getenv("MFPSN_PAIR");
+        return !(e && strcmp(e, "0") == 0);
+    }();
+    return on && !(d->S == 1 && d->C >= 64) && d->S % 2 == 0 && d->k <= kPairMaxK;
+}
+
+bool pair_aligned(std::initializer_list<const void*> ptrs)
+{
+    for (const void* p : ptrs)
+        if (p != nullptr && ((uintptr_t)p & 7u) != 0)
+            return false;
+    return true;
+}
+
+Geom plan(const mfpsn_desc* d, bool backward, int nv)
 {
     Geom g;
     memset(&g, 0, sizeof(g));
@@ -115,6 +138,8 @@ Geom plan(const mfpsn_desc* d, bool backward)
     g.k = d->k;
     g.d = d->dilation;
     g.M = (uint32_t)((int64_t)d->N * d->C * d->S);
+    g.tq = d->T / d->dilation;
+    g.tr = d->T % d->dilation;
     g.esize = elem_bytes(d->dtype);
     g.shift_lo = d->shift_lo;
     g.shift_hi = d->shift_hi;
@@ -137,12 +162,14 @@ Geom plan(const mfpsn_desc* d, bool backward)
     }
     if (d->S == 1 && d->C >= 64) {
         g.mode = kLaneChannel;
+        g.nv = 1;
         g.groups = (int32_t)ceil_div(d->C, 64);
         g.tiles = d->N;
     } else {
         g.mode = kPlane;
+        g.nv = nv;
         g.groups = d->C;
-        g.tiles = (int32_t)ceil_div((int64_t)d->N * d->S, 64);
+        g.tiles = (int32_t)ceil_div((int64_t)d->N * d->S, 64 * nv);
     }
     // Cut each residue class into chunks only while the columns alone give
     // fewer items than the target (or a class spans too many bytes).
@@ -178,6 +205,18 @@ Geom plan(const mfpsn_desc* d, bool backward)
 size_t workspace_bytes(const Geom& g)
 {
     return (size_t)g.blocks * (size_t)(g.k + 1) * (size_t)g.C * sizeof(double);
+}
+
+// Workspace of the backward: enough for either column layout (the layout
+// also depends on the pointers, which the size query does not see).
+size_t backward_workspace(const mfpsn_desc* d)
+{
+    size_t b = workspace_bytes(plan(d, true, 1));
+    if (pair_layout(d)) {
+        const size_t b2 = workspace_bytes(plan(d, true, 2));
+        b = b2 > b ? b2 : b;
+    }
+    return b;
 }
 
 }  // namespace
@@ -225,7 +264,7 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     if (total == 0)
         return MFPSN_OK;
     FwdArgs a;
-    a.g = plan(desc, false);
+    a.g = plan(desc, false, pair_layout(desc) && pair_aligned({x, spikes, h_out, sg_out}) ? 2 : 1);
     a.x = x;
     a.sign = sign;
     a.shift = shift;
@@ -246,12 +285,12 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
     if (!bytes)
         return MFPSN_ERR_NULL;
     const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
-    *bytes = total > 0 ? workspace_bytes(plan(desc, true)) : 0;
+    *bytes = total > 0 ? backward_workspace(desc) : 0;
     return MFPSN_OK;
 }
 
-int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* sg,
-                   const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
+int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
+                   const void* sg, const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
                    void* grad_w, void* grad_b, void* workspace, size_t ws_bytes, void* stream)
 {
     int st = validate(desc);
@@ -264,7 +303,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         return MFPSN_ERR_NULL;
     const int es = elem_bytes(desc->dtype);
     if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, grad_x_bytes(desc->dtype)) ||
-        !aligned(bias, 4) || !aligned(sg, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
+        !aligned(bias, 4) || !aligned(h, 4) || !aligned(sg, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
         !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
         return MFPSN_ERR_ALIGN;
     if (desc->dtype == MFPSN_Q8_8) {
@@ -274,12 +313,13 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
             return MFPSN_ERR_SHAPE;
     }
     BwdArgs a;
-    a.g = plan(desc, true);
-    const size_t need = total > 0 ? workspace_bytes(a.g) : 0;
+    a.g = plan(desc, true, pair_layout(desc) && pair_aligned({x, grad_spikes, h, sg, grad_x}) ? 2 : 1);
+    const size_t need = total > 0 ? backward_workspace(desc) : 0;
     if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
         return MFPSN_ERR_WORKSPACE;
     a.x = x;
     a.gs = grad_spikes;
+    a.h = h;
     a.sg = sg;
     a.sign = sign;
     a.shift = shift;

@@ -23,7 +23,9 @@ struct Geom {
     int32_t T, N, C, S;
     int32_t k, d;
     int32_t mode;
-    int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/64)
+    int32_t nv;        // adjacent columns per lane: 1, or 2 (plane mode, S even)
+    int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/(64*nv))
+    int32_t tq, tr;    // T = tq * d + tr
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk
     int32_t groups;    // gridDim.y: channel groups (lane-channel) or channels (plane)
@@ -44,6 +46,7 @@ struct Geom {
 };
 
 constexpr int kWaves = 4;          // waves per block
+constexpr int kPairMaxK = 16;      // highest order with two-column (nv = 2) kernels
 constexpr int kThreads = 64 * kWaves;
 // Upper bound of blocks resident on one GPU at once (8 blocks of 4 waves per
 // CU is 8 waves per SIMD; 320 CUs covers every CDNA part): the persistent grid
@@ -65,7 +68,8 @@ struct BwdArgs {
     Geom g;
     const void* x;
     const void* gs;
-    const void* sg;    // surrogate factor saved by the forward (nullable: recompute from x)
+    const void* h;     // potentials H saved by the forward (nullable)
+    const void* sg;    // surrogate factor saved by the forward (nullable; used if set)
     const int8_t* sign;
     const int8_t* shift;
     const void* bias;

@@ -31,10 +31,12 @@
 // potentials and input gradients are bit-identical to a sequential
 // evaluation of the definition.
 //
-// The forward can also save the surrogate factor sigma'(H - v_th) (Q8.8: the
-// integer factor L); the backward then needs only dH = grad_spikes * factor,
-// which moves the surrogate evaluation into the pass that is bound by memory
-// traffic rather than by arithmetic.
+// The forward can also save the potentials H or the surrogate factor
+// sigma'(H - v_th) (Q8.8: the integer factor L).  From saved H the backward
+// skips the recompute of the charge; from the saved factor it also skips the
+// surrogate, dH = grad_spikes * factor.  Either trades 8 bytes of traffic per
+// element for arithmetic; which pass gets the surrogate decides which pass
+// the arithmetic lands in.
 //
 // Backward.  Each class is walked backwards in time.  dH[j] is computed once
 // (from the forward's saved factor, or from H recomputed out of the x ring) and
@@ -126,6 +128,11 @@ __device__ __forceinline__ Buf make_buf(const void* tensor, uint64_t tensor_byte
 #ifndef MFPSN_ST_CPOL
 #define MFPSN_ST_CPOL 2  // nt: streaming stores
 #endif
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 ld64(Buf b, uint32_t v, int32_t s)
+{
+    return __builtin_amdgcn_raw_buffer_load_b64(b.rs, v, s, MFPSN_LD_CPOL);
+}
 __device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b32(b.rs, v, s, MFPSN_LD_CPOL);
@@ -133,6 +140,10 @@ __device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
 __device__ __forceinline__ uint32_t ld16(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, MFPSN_LD_CPOL);
+}
+__device__ __forceinline__ void st64(Buf b, uint32_t v, int32_t s, u32x2 x)
+{
+    __builtin_amdgcn_raw_buffer_store_b64(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 __device__ __forceinline__ void st32(Buf b, uint32_t v, int32_t s, uint32_t x)
 {
@@ -145,6 +156,48 @@ __device__ __forceinline__ void st16(Buf b, uint32_t v, int32_t s, uint16_t x)
 __device__ __forceinline__ void st8(Buf b, uint32_t v, int32_t s, uint8_t x)
 {
     __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, MFPSN_ST_CPOL);
+}
+
+// The NV adjacent columns a lane holds (NV = 1, or 2 in plane mode when the
+// two columns are neighbours in memory): every stream moves them with one
+// access, so a wave's access covers 64 * NV elements.
+template <typename T, int NV> struct Pk {
+    T v[NV];
+};
+// NV adjacent 32-bit words (potentials, surrogate factors, Q8.8 grad_x)
+template <int NV>
+__device__ __forceinline__ Pk<uint32_t, NV> ld_words(Buf b, uint32_t v, int32_t s)
+{
+    Pk<uint32_t, NV> r;
+    if constexpr (NV == 1) {
+        r.v[0] = ld32(b, v, s);
+    } else {
+        const u32x2 w = ld64(b, v, s);
+        r.v[0] = w.x;
+        r.v[1] = w.y;
+    }
+    return r;
+}
+template <int NV>
+__device__ __forceinline__ void st_words(Buf b, uint32_t v, int32_t s, const Pk<uint32_t, NV>& x)
+{
+    if constexpr (NV == 1) {
+        st32(b, v, s, x.v[0]);
+    } else {
+        u32x2 w;
+        w.x = x.v[0];
+        w.y = x.v[1];
+        st64(b, v, s, w);
+    }
+}
+// NV adjacent bytes, byte e in bits 8e..8e+7
+template <int NV>
+__device__ __forceinline__ void st_bytes(Buf b, uint32_t v, int32_t s, uint32_t x)
+{
+    if constexpr (NV == 1)
+        st8(b, v, s, (uint8_t)x);
+    else
+        st16(b, v, s, (uint16_t)x);
 }
 
 // s += inc, kept opaque so the compiler keeps one running SGPR per stream
@@ -174,10 +227,24 @@ template <> struct IO<kF32> {
     using W = double;    // exact product accumulator of grad_w, grad_b
     static constexpr int es = 4;     // bytes per stored x / grad_spikes
     static constexpr int gx_es = 4;  // bytes per stored grad_x
-    __device__ static V load(Buf b, uint32_t v, int32_t s) { return __builtin_bit_cast(float, ld32(b, v, s)); }
-    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x)
+    template <int NV>
+    __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
     {
-        st32(b, v, s, __builtin_bit_cast(uint32_t, x));
+        const Pk<uint32_t, NV> w = ld_words<NV>(b, v, s);
+        Pk<V, NV> r;
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            r.v[e] = __builtin_bit_cast(float, w.v[e]);
+        return r;
+    }
+    template <int NV>
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
+    {
+        Pk<uint32_t, NV> w;
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            w.v[e] = __builtin_bit_cast(uint32_t, x.v[e]);
+        st_words<NV>(b, v, s, w);
     }
 };
 
@@ -186,11 +253,30 @@ template <> struct IO<kBF16> {
     using W = double;
     static constexpr int es = 2;
     static constexpr int gx_es = 2;
-    __device__ static V load(Buf b, uint32_t v, int32_t s) { return __builtin_bit_cast(float, ld16(b, v, s) << 16); }
-    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x)
+    template <int NV>
+    __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
     {
-        const __bf16 h = (__bf16)x;  // round to nearest even
-        st16(b, v, s, __builtin_bit_cast(uint16_t, h));
+        Pk<V, NV> r;
+        if constexpr (NV == 1) {
+            r.v[0] = __builtin_bit_cast(float, ld16(b, v, s) << 16);
+        } else {
+            const uint32_t w = ld32(b, v, s);
+            r.v[0] = __builtin_bit_cast(float, w << 16);
+            r.v[1] = __builtin_bit_cast(float, w & 0xFFFF0000u);
+        }
+        return r;
+    }
+    template <int NV>
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
+    {
+        // round to nearest even
+        const uint16_t h0 = __builtin_bit_cast(uint16_t, (__bf16)x.v[0]);
+        if constexpr (NV == 1) {
+            st16(b, v, s, h0);
+        } else {
+            const uint16_t h1 = __builtin_bit_cast(uint16_t, (__bf16)x.v[1]);
+            st32(b, v, s, (uint32_t)h0 | ((uint32_t)h1 << 16));
+        }
     }
 };
 
@@ -199,8 +285,28 @@ template <> struct IO<kQ88> {
     using W = int64_t;
     static constexpr int es = 2;
     static constexpr int gx_es = 4;
-    __device__ static V load(Buf b, uint32_t v, int32_t s) { return (int32_t)(int16_t)(uint16_t)ld16(b, v, s); }
-    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, V x) { st32(b, v, s, (uint32_t)x); }
+    template <int NV>
+    __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
+    {
+        Pk<V, NV> r;
+        if constexpr (NV == 1) {
+            r.v[0] = (int32_t)(int16_t)(uint16_t)ld16(b, v, s);
+        } else {
+            const uint32_t w = ld32(b, v, s);
+            r.v[0] = (int32_t)(int16_t)(uint16_t)w;
+            r.v[1] = (int32_t)w >> 16;
+        }
+        return r;
+    }
+    template <int NV>
+    __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
+    {
+        Pk<uint32_t, NV> w;
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            w.v[e] = (uint32_t)x.v[e];
+        st_words<NV>(b, v, s, w);
+    }
 };
 
 // ---------------------------------------------------------------------------
@@ -366,12 +472,22 @@ __device__ __forceinline__ int32_t delta_h(int32_t g, int32_t L)
 
 // True (wave-uniform) when some lane's value is outside the range in which
 // the exponent-add tap is exact.
-__device__ __forceinline__ bool any_slow(float v, const Geom& g)
+template <int NV>
+__device__ __forceinline__ bool any_slow(const Pk<float, NV>& v, const Geom& g)
 {
-    const float m = __builtin_fabsf(v);
-    return __builtin_amdgcn_ballot_w64(!(m >= g.fast_lo && m < g.fast_hi)) != 0;
+    bool out = false;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        const float m = __builtin_fabsf(v.v[e]);
+        out = out || !(m >= g.fast_lo && m < g.fast_hi);
+    }
+    return __builtin_amdgcn_ballot_w64(out) != 0;
 }
-__device__ __forceinline__ bool any_slow(int, const Geom&) { return false; }
+template <int NV>
+__device__ __forceinline__ bool any_slow(const Pk<int32_t, NV>&, const Geom&)
+{
+    return false;
+}
 
 // ---------------------------------------------------------------------------
 // items.  Item q of a group: q = (tile * d + r) * nchunks + chunk.
@@ -403,12 +519,12 @@ struct Cursor {
 };
 
 struct Cols {
-    uint32_t col;  // column index in [0, M)
-    bool active;   // this lane's column exists
+    uint32_t col;  // the lane's first column, in [0, M)
+    bool active;   // this lane's columns exist
     bool partial;  // plane tile with missing columns (wave-uniform)
 };
 
-template <int MODE>
+template <int MODE, int NV>
 __device__ __forceinline__ Cols tile_cols(const Geom& g, int tile, int grp, int lane)
 {
     Cols t;
@@ -418,28 +534,32 @@ __device__ __forceinline__ Cols tile_cols(const Geom& g, int tile, int grp, int 
         t.partial = false;
         t.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)min(c, g.C - 1);
     } else {
+        // positions NV*lane .. NV*lane + NV-1 of the tile; with NV = 2, S is
+        // even, so both lie in one (n, c) row of S adjacent columns
         const uint32_t NS = (uint32_t)g.N * (uint32_t)g.S;
-        const uint32_t pos = (uint32_t)tile * 64u + (uint32_t)lane;
+        const uint32_t pos = (uint32_t)tile * (64u * NV) + (uint32_t)lane * NV;
         t.active = pos < NS;
-        t.partial = (uint32_t)tile * 64u + 64u > NS;
-        const uint32_t pc = min(pos, NS - 1u);
+        t.partial = (uint32_t)tile * (64u * NV) + 64u * NV > NS;
+        const uint32_t pc = min(pos, NS - NV);
         const uint32_t n = pc / (uint32_t)g.S, s = pc - n * (uint32_t)g.S;
         t.col = (n * (uint32_t)g.C + (uint32_t)grp) * (uint32_t)g.S + s;
     }
     return t;
 }
 
-__device__ __forceinline__ int class_len(const Geom& g, int r) { return r < g.T ? (g.T - r + g.d - 1) / g.d : 0; }
+// steps of residue class r: T = tq*d + tr, so classes below tr hold one more
+__device__ __forceinline__ int class_len(const Geom& g, int r) { return g.tq + (r < g.tr ? 1 : 0); }
 
 // ---------------------------------------------------------------------------
 // forward
 // ---------------------------------------------------------------------------
-template <int K, int DT, int MODE>
+template <int K, int DT, int MODE, int NV>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
 {
     using V = typename IO<DT>::V;
+    using PV = Pk<V, NV>;
     using TP = Taps<K, DT, MODE>;
-    constexpr int P = prefetch_depth(K, kFwdPrefetch);
+    constexpr int P = prefetch_depth(K, kFwdPrefetch / NV);
     constexpr int es = IO<DT>::es;
     constexpr bool kF = DT != kQ88;
     const Geom& g = a.g;
@@ -487,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
         if (j0 >= j1)
             continue;
         if (cur.tile != tile_cached) {
-            cols = tile_cols<MODE>(g, cur.tile, grp, lane);
+            cols = tile_cols<MODE, NV>(g, cur.tile, grp, lane);
             tile_cached = cur.tile;
         }
         // x rows from jb (the halo of a chunk) on; outputs from j0 on
@@ -500,24 +620,26 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
         const uint32_t vx = cols.col * es, vs = cols.col, vh = cols.col * 4u;
         const int32_t so_xlast = (Lr - 1 - jb) * xstep;
 
-        V ring[K];  // x[t] at slot t mod k
+        PV ring[K];  // x[t] at slot t mod k
         int slow = 0;  // steps left on the exact path
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            ring[i] = V(0);
+#pragma unroll
+            for (int e = 0; e < NV; ++e)
+                ring[i].v[e] = V(0);
         if (j0 > 0) {
             // halo x[j0-k+1 .. j0-1]; j0 is a multiple of k
 #pragma unroll
             for (int m = 0; m < K - 1; ++m) {
-                ring[(m + 1) % K] = IO<DT>::load(xs, vx, m * xstep);
+                ring[(m + 1) % K] = IO<DT>::template load<NV>(xs, vx, m * xstep);
                 if (TP::kHasFast && any_slow(ring[(m + 1) % K], g))
                     slow = m + 1;
             }
         }
-        V pf[P];  // x[j] at slot j mod P
+        PV pf[P];  // x[j] at slot j mod P
 #pragma unroll
         for (int p = 0; p < P; ++p)
-            pf[p] = IO<DT>::load(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
+            pf[p] = IO<DT>::template load<NV>(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
         int32_t so_xp = (j0 + P - jb) * xstep;  // prefetch of step j + P
         int32_t so_s = 0, so_h = 0;
 
@@ -530,41 +652,64 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
             constexpr int kind = decltype(kc_)::value;
             constexpr int imin = (kF && kind == kEdge) ? K - 1 - u : 0;
             (void)j;
-            const V xv = pf[u % P];
-            pf[u % P] = IO<DT>::load(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
+            const PV xv = pf[u % P];
+            pf[u % P] = IO<DT>::template load<NV>(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
             advance(so_xp, xstep);
             ring[u] = xv;
-            V h;
+            PV h;
+            uint32_t spk = 0;  // spike of column e in byte e
             if constexpr (kF) {
                 if (any_slow(xv, g))
                     slow = K;
-                V acc;
                 if (__builtin_expect(slow > 0, 0)) {
-                    acc = tp.apply(ring[(u + 1 + imin) % K], imin);
 #pragma unroll
-                    for (int i = imin + 1; i < K; ++i)
-                        acc = acc + tp.apply(ring[(u + 1 + i) % K], i);
+                    for (int e = 0; e < NV; ++e) {
+                        V acc = tp.apply(ring[(u + 1 + imin) % K].v[e], imin);
+#pragma unroll
+                        for (int i = imin + 1; i < K; ++i)
+                            acc = acc + tp.apply(ring[(u + 1 + i) % K].v[e], i);
+                        h.v[e] = acc + bias;
+                    }
                     --slow;
                 } else {
-                    acc = tp.apply_fast(ring[(u + 1 + imin) % K], imin);
 #pragma unroll
-                    for (int i = imin + 1; i < K; ++i)
-                        acc = acc + tp.apply_fast(ring[(u + 1 + i) % K], i);
+                    for (int e = 0; e < NV; ++e) {
+                        V acc = tp.apply_fast(ring[(u + 1 + imin) % K].v[e], imin);
+#pragma unroll
+                        for (int i = imin + 1; i < K; ++i)
+                            acc = acc + tp.apply_fast(ring[(u + 1 + i) % K].v[e], i);
+                        h.v[e] = acc + bias;
+                    }
                 }
-                h = acc + bias;
-                st8(ss, vs, so_s, h >= g.v_th ? 1 : 0);
-            } else {
-                V acc = start;
 #pragma unroll
-                for (int i = 0; i < K; ++i)
-                    acc = acc + tp.apply(ring[(u + 1 + i) % K], i);
-                h = acc;
-                st8(ss, vs, so_s, h >= g.v_th_q ? 1 : 0);
+                for (int e = 0; e < NV; ++e)
+                    spk |= (h.v[e] >= g.v_th ? 1u : 0u) << (8 * e);
+            } else {
+#pragma unroll
+                for (int e = 0; e < NV; ++e) {
+                    V acc = start;
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + tp.apply(ring[(u + 1 + i) % K].v[e], i);
+                    h.v[e] = acc;
+                    spk |= (h.v[e] >= g.v_th_q ? 1u : 0u) << (8 * e);
+                }
             }
-            if (want_h != 0)
-                st32(hs, vh, so_h, __builtin_bit_cast(uint32_t, h));
-            if (want_sg != 0)
-                st32(gs, vh, so_h, __builtin_bit_cast(uint32_t, sg_factor(sg, h, g.v_th, g.v_th_q)));
+            st_bytes<NV>(ss, vs, so_s, spk);
+            if (want_h != 0) {
+                Pk<uint32_t, NV> w;
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    w.v[e] = __builtin_bit_cast(uint32_t, h.v[e]);
+                st_words<NV>(hs, vh, so_h, w);
+            }
+            if (want_sg != 0) {
+                Pk<uint32_t, NV> w;
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
+                st_words<NV>(gs, vh, so_h, w);
+            }
             advance(so_s, sstep);
             advance(so_h, hstep);
             __builtin_amdgcn_sched_barrier(0);
@@ -611,21 +756,28 @@ __device__ __forceinline__ int64_t wave_sum(int64_t v)
     return v;
 }
 
-template <int K, int DT, int MODE, bool HS>
+// What the backward reads besides x and grad_spikes: nothing (H and the
+// surrogate factor are recomputed from the x ring), the forward's saved
+// surrogate factor, or the forward's saved potentials H.
+enum SavedKind : int { kRecompute = 0, kSavedFactor = 1, kSavedH = 2 };
+
+template <int K, int DT, int MODE, int HS, int NV>
 __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 {
     using V = typename IO<DT>::V;
     using W = typename IO<DT>::W;
+    using PV = Pk<V, NV>;
     using TP = Taps<K, DT, MODE>;
     // Lane-channel waves at orders up to 16 run 4 per SIMD and stream three
     // 256-byte rows per step: a short queue is best.  Plane waves (narrower
     // rows) want a longer one, and high orders (2 waves per SIMD) a deep one.
-    constexpr int P = prefetch_depth(K, K >= 24 ? 8 * kBwdPrefetch
-                                                : (MODE == kLaneChannel ? kBwdPrefetch : 2 * kBwdPrefetch));
+    // Lanes holding two columns move twice the bytes per access.
+    constexpr int P = prefetch_depth(
+        K, (K >= 24 ? 8 * kBwdPrefetch : (MODE == kLaneChannel ? kBwdPrefetch : 2 * kBwdPrefetch)) / NV);
     constexpr int es = IO<DT>::es;
     constexpr int gxs = IO<DT>::gx_es;
     constexpr bool kF = DT != kQ88;
-    constexpr bool kRe = !HS;  // no saved factor: recompute H from the x ring
+    constexpr bool kRe = HS == kRecompute;  // recompute H from the x ring
     // x rings: double copies for the exact grad_w products of float data;
     // the stored value itself for the recompute of float data and for Q8.8
     // (whose products are exact 32x32 -> 64-bit integer products)
@@ -680,7 +832,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         if (j0 >= j1)
             continue;
         if (cur.tile != tile_cached) {
-            cols = tile_cols<MODE>(g, cur.tile, grp, lane);
+            cols = tile_cols<MODE, NV>(g, cur.tile, grp, lane);
             tile_cached = cur.tile;
         }
         const bool partial = cols.partial;
@@ -693,34 +845,40 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         const uint64_t brow = (uint64_t)r + (uint64_t)jb * d;
         const Buf xs = make_buf(a.x, xbytes, brow * xrow);
         const Buf gsb = make_buf(a.gs, xbytes, brow * xrow);
-        const Buf hsb = HS ? make_buf(a.sg, hbytes, brow * hrow) : xs;
+        const Buf hsb = HS ? make_buf(HS == kSavedFactor ? a.sg : a.h, hbytes, brow * hrow) : xs;
         const Buf gxb = make_buf(a.grad_x, gxbytes, brow * gxrow);
         const uint32_t vx = cols.col * es, vh = cols.col * 4u, vgx = cols.col * gxs;
         const int32_t so_last = (Lr - 1 - jb) * xstep, so_hlast = (Lr - 1 - jb) * hstep;
 
         // grad_x accumulators: output t at slot t mod k, opened with the start
         // of its sum (Q8.8: the number of negative taps that reach it)
-        V gxa[K];
+        PV gxa[K];
 #pragma unroll
         for (int s = 0; s < K; ++s) {
+            V v0;
             if constexpr (kF) {
-                gxa[s] = 0.0f;
+                v0 = 0.0f;
             } else {
                 const int t = jtop - (((jtop - s) % K) + K) % K;  // highest output of slot s
                 const int skip = max(0, t + K - Lr);               // taps whose source lies past the end
-                gxa[s] = __builtin_popcount(tp.negmask >> skip);
+                v0 = __builtin_popcount(tp.negmask >> skip);
             }
+#pragma unroll
+            for (int e = 0; e < NV; ++e)
+                gxa[s].v[e] = v0;
         }
         // x ring: x[t] at slot t mod k, for t in the window of the step
-        double xd[kXD ? K : 1];
-        V xf[kXV ? K : 1];
+        Pk<double, NV> xd[kXD ? K : 1];
+        PV xf[kXV ? K : 1];
         int slow_x = 0;  // live steps left on the exact recompute path
 #pragma unroll
         for (int m = 0; m < K - 1; ++m) {
             const int t = jstart - m;  // slot k-1-m; values past jtop are never used
-            const V v = IO<DT>::load(xs, vx, (min(t, Lr - 1) - jb) * xstep);
+            const PV v = IO<DT>::template load<NV>(xs, vx, (min(t, Lr - 1) - jb) * xstep);
             if constexpr (kXD)
-                xd[K - 1 - m] = (double)v;
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    xd[K - 1 - m].v[e] = (double)v.v[e];
             if constexpr (kXV)
                 xf[K - 1 - m] = v;
             // x[t] (t <= jtop) is in the window of at most k live steps
@@ -728,19 +886,27 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 slow_x = K;
         }
         // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P
-        V pg[P], ph[HS ? P : 1], px[P];
+        PV pg[P], ph[HS ? P : 1], px[P];
+        auto load_h = [&](int32_t so) __attribute__((always_inline)) {
+            const Pk<uint32_t, NV> w = ld_words<NV>(hsb, vh, so);
+            PV v;
+#pragma unroll
+            for (int e = 0; e < NV; ++e)
+                v.v[e] = __builtin_bit_cast(V, w.v[e]);
+            return v;
+        };
 #pragma unroll
         for (int p = 0; p < P; ++p) {
             const int jp = jstart - p;
             const int js = (K - 1 - p) % P;
             const int rowg = min(jp, Lr - 1);
-            pg[js] = IO<DT>::load(gsb, vx, (rowg - jb) * xstep);
+            pg[js] = IO<DT>::template load<NV>(gsb, vx, (rowg - jb) * xstep);
             if constexpr (HS)
-                ph[js] = __builtin_bit_cast(V, ld32(hsb, vh, (rowg - jb) * hstep));
-            px[js] = IO<DT>::load(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
+                ph[js] = load_h((rowg - jb) * hstep);
+            px[js] = IO<DT>::template load<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
         }
         int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
-        int32_t so_hp = (jstart - P - jb) * hstep;           // factor of step j - P
+        int32_t so_hp = (jstart - P - jb) * hstep;           // factor or H of step j - P
         int32_t so_xp = (jstart - P - K + 1 - jb) * xstep;   // x of step j - P
         int32_t so_gx = (jstart - jb) * gxstep;              // grad_x of step j
 
@@ -755,15 +921,15 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             constexpr int sj = K - 1 - u;  // j mod k
             constexpr int sp = sj % P;     // j mod P
             constexpr int imin = edge ? u : 0;
-            const V gv = pg[sp];
-            const V xv = px[sp];
-            V hv = V(0);
+            const PV gv = pg[sp];
+            const PV xv = px[sp];
+            PV hv;
             if constexpr (HS)
                 hv = ph[sp];
-            pg[sp] = IO<DT>::load(gsb, vx, full ? so_gp : min(max(so_gp, 0), so_last));
+            pg[sp] = IO<DT>::template load<NV>(gsb, vx, full ? so_gp : min(max(so_gp, 0), so_last));
             if constexpr (HS)
-                ph[sp] = __builtin_bit_cast(V, ld32(hsb, vh, full ? so_hp : min(max(so_hp, 0), so_hlast)));
-            px[sp] = IO<DT>::load(xs, vx, full ? so_xp : min(max(so_xp, 0), so_last));
+                ph[sp] = load_h(full ? so_hp : min(max(so_hp, 0), so_hlast));
+            px[sp] = IO<DT>::template load<NV>(xs, vx, full ? so_xp : min(max(so_xp, 0), so_last));
             advance(so_gp, -xstep);
             if constexpr (HS)
                 advance(so_hp, -hstep);
@@ -771,68 +937,92 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             // x[j-k+1] enters the ring (slot (j+1) mod k)
             if constexpr (!(edge && u > 0)) {
                 if constexpr (kXD)
-                    xd[(sj + 1) % K] = (double)xv;
+#pragma unroll
+                    for (int e = 0; e < NV; ++e)
+                        xd[(sj + 1) % K].v[e] = (double)xv.v[e];
                 if constexpr (kXV)
                     xf[(sj + 1) % K] = xv;
                 if (kRe && TP::kHasFast && any_slow(xv, g))
                     slow_x = K;
             } else if constexpr (!kF) {
-                xf[(sj + 1) % K] = 0;  // Q8.8: zeros before time 0 (recompute)
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    xf[(sj + 1) % K].v[e] = 0;  // Q8.8: zeros before time 0 (recompute)
             }
             if (full || j <= jtop) {
-                V dh;
-                if constexpr (HS) {
-                    dh = delta_h(gv, hv);  // hv: the saved factor
-                } else {
-                V h;
-                if constexpr (kF) {
-                    constexpr int rmin = edge ? u : 0;  // taps reading before time 0 are left out
-                    V acc;
-                    if (__builtin_expect(slow_x > 0, 0)) {
-                        acc = tp.apply(xf[(sj + 1 + rmin) % K], rmin);
+                PV dh;
+                if constexpr (HS == kSavedFactor) {
 #pragma unroll
-                        for (int i = rmin + 1; i < K; ++i)
-                            acc = acc + tp.apply(xf[(sj + 1 + i) % K], i);
+                    for (int e = 0; e < NV; ++e)
+                        dh.v[e] = delta_h(gv.v[e], hv.v[e]);
+                } else if constexpr (HS == kSavedH) {
+#pragma unroll
+                    for (int e = 0; e < NV; ++e)
+                        dh.v[e] = delta_h(gv.v[e], sg_factor(sg, hv.v[e], g.v_th, g.v_th_q));
+                } else {
+                    PV h;
+                    if constexpr (kF) {
+                        constexpr int rmin = edge ? u : 0;  // taps reading before time 0 are left out
+                        if (__builtin_expect(slow_x > 0, 0)) {
+#pragma unroll
+                            for (int e = 0; e < NV; ++e) {
+                                V acc = tp.apply(xf[(sj + 1 + rmin) % K].v[e], rmin);
+#pragma unroll
+                                for (int i = rmin + 1; i < K; ++i)
+                                    acc = acc + tp.apply(xf[(sj + 1 + i) % K].v[e], i);
+                                h.v[e] = acc + bias;
+                            }
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < NV; ++e) {
+                                V acc = tp.apply_fast(xf[(sj + 1 + rmin) % K].v[e], rmin);
+#pragma unroll
+                                for (int i = rmin + 1; i < K; ++i)
+                                    acc = acc + tp.apply_fast(xf[(sj + 1 + i) % K].v[e], i);
+                                h.v[e] = acc + bias;
+                            }
+                        }
                     } else {
-                        acc = tp.apply_fast(xf[(sj + 1 + rmin) % K], rmin);
 #pragma unroll
-                        for (int i = rmin + 1; i < K; ++i)
-                            acc = acc + tp.apply_fast(xf[(sj + 1 + i) % K], i);
+                        for (int e = 0; e < NV; ++e) {
+                            V acc = start;
+#pragma unroll
+                            for (int i = 0; i < K; ++i)
+                                acc = acc + tp.apply(xf[(sj + 1 + i) % K].v[e], i);
+                            h.v[e] = acc;
+                        }
                     }
-                    h = acc + bias;
-                } else {
-                    V acc = start;
 #pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc = acc + tp.apply(xf[(sj + 1 + i) % K], i);
-                    h = acc;
-                }
-                dh = delta_h(gv, sg_factor(sg, h, g.v_th, g.v_th_q));
+                    for (int e = 0; e < NV; ++e)
+                        dh.v[e] = delta_h(gv.v[e], sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
                 }
                 const bool own = full || j < j1;
                 if (own) {
-                    if constexpr (kF) {
-                        double dd = (double)dh;
-                        if (MODE == kPlane && partial)
-                            dd = active ? dd : 0.0;  // no contribution from shadow lanes
 #pragma unroll
-                        for (int i = imin; i < K; ++i) {
-                            gw[i] = __builtin_fma(xd[(sj + 1 + i) % K], dd, gw[i]);
-                            pin(gw[i]);
-                        }
-                        gb += dd;
-                        pin(gb);
-                    } else {
-                        int32_t dq = dh;
-                        if (MODE == kPlane && partial)
-                            dq = active ? dq : 0;
+                    for (int e = 0; e < NV; ++e) {
+                        if constexpr (kF) {
+                            double dd = (double)dh.v[e];
+                            if (MODE == kPlane && partial)
+                                dd = active ? dd : 0.0;  // no contribution from shadow lanes
 #pragma unroll
-                        for (int i = imin; i < K; ++i) {
-                            gw[i] += (int64_t)xf[(sj + 1 + i) % K] * (int64_t)dq;
-                            pin(gw[i]);
+                            for (int i = imin; i < K; ++i) {
+                                gw[i] = __builtin_fma(xd[(sj + 1 + i) % K].v[e], dd, gw[i]);
+                                pin(gw[i]);
+                            }
+                            gb += dd;
+                            pin(gb);
+                        } else {
+                            int32_t dq = dh.v[e];
+                            if (MODE == kPlane && partial)
+                                dq = active ? dq : 0;
+#pragma unroll
+                            for (int i = imin; i < K; ++i) {
+                                gw[i] += (int64_t)xf[(sj + 1 + i) % K].v[e] * (int64_t)dq;
+                                pin(gw[i]);
+                            }
+                            gb += dq;
+                            pin(gb);
                         }
-                        gb += dq;
-                        pin(gb);
                     }
                 }
                 // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k).  Lanes
@@ -841,30 +1031,35 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 // the range (zero, or a surrogate gradient that underflowed to
                 // under 2^(shift_hi-126)) adds nothing: its terms are zeros or
                 // smaller than 2^(shift_hi-shift_lo-126).
-                if constexpr (kF) {
-                    const float m = __builtin_fabsf(dh);
-                    if (m >= g.fast_lo && m < g.fast_hi) {
 #pragma unroll
-                        for (int i = imin; i < K; ++i)
-                            gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply_fast(dh, i);
-                    }
-                    if (__builtin_expect(!(m < g.fast_hi), 0)) {
+                for (int e = 0; e < NV; ++e) {
+                    if constexpr (kF) {
+                        const float m = __builtin_fabsf(dh.v[e]);
+                        if (m >= g.fast_lo && m < g.fast_hi) {
 #pragma unroll
-                        for (int i = imin; i < K; ++i)
-                            gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply(dh, i);
-                    }
-                } else {
-                    // (integer sums: pinned so they are not reassociated across
-                    // steps, which would keep many steps' terms live)
+                            for (int i = imin; i < K; ++i)
+                                gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply_fast(dh.v[e], i);
+                        }
+                        if (__builtin_expect(!(m < g.fast_hi), 0)) {
 #pragma unroll
-                    for (int i = imin; i < K; ++i) {
-                        gxa[(sj + 1 + i) % K] = gxa[(sj + 1 + i) % K] + tp.apply(dh, i);
-                        pin(gxa[(sj + 1 + i) % K]);
+                            for (int i = imin; i < K; ++i)
+                                gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply(dh.v[e], i);
+                        }
+                    } else {
+                        // (integer sums: pinned so they are not reassociated across
+                        // steps, which would keep many steps' terms live)
+#pragma unroll
+                        for (int i = imin; i < K; ++i) {
+                            gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply(dh.v[e], i);
+                            pin(gxa[(sj + 1 + i) % K].v[e]);
+                        }
                     }
                 }
                 if (own)
-                    IO<DT>::store_gx(gxb, vgx, so_gx, gxa[sj]);
-                gxa[sj] = reset;  // slot now holds output j - k
+                    IO<DT>::template store_gx<NV>(gxb, vgx, so_gx, gxa[sj]);
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    gxa[sj].v[e] = reset;  // slot now holds output j - k
                 if constexpr (kRe && kF)
                     if (slow_x > 0)
                         --slow_x;
@@ -1097,23 +1292,58 @@ inline int persistent_blocks(const Geom& g, int resident)
 template <int K, int DT>
 hipError_t fwd_k(FwdArgs& a, hipStream_t st)
 {
-    static int cache[2][16];
-    const bool lc = a.g.mode == kLaneChannel;
-    auto kern = lc ? fwd_kernel<K, DT, kLaneChannel> : fwd_kernel<K, DT, kPlane>;
-    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[lc ? 0 : 1]));
+    static int cache[3][16];
+    void (*kern)(FwdArgs) = fwd_kernel<K, DT, kLaneChannel, 1>;
+    int slot = 0;
+    if (a.g.mode == kPlane) {
+        if (a.g.nv == 2) {
+            if constexpr (K <= kPairMaxK) {
+                kern = fwd_kernel<K, DT, kPlane, 2>;
+                slot = 2;
+            } else {
+                return hipErrorInvalidValue;
+            }
+        } else {
+            kern = fwd_kernel<K, DT, kPlane, 1>;
+            slot = 1;
+        }
+    }
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[slot]));
     hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
+}
+
+template <int K, int DT, int HS>
+void (*bwd_kernel_for(const Geom& g, int& slot))(BwdArgs)
+{
+    if (g.mode == kLaneChannel) {
+        slot = 0;
+        return bwd_kernel<K, DT, kLaneChannel, HS, 1>;
+    }
+    if (g.nv == 2) {
+        if constexpr (K <= kPairMaxK) {
+            slot = 2;
+            return bwd_kernel<K, DT, kPlane, HS, 2>;
+        } else {
+            return nullptr;
+        }
+    }
+    slot = 1;
+    return bwd_kernel<K, DT, kPlane, HS, 1>;
 }
 
 template <int K, int DT>
 hipError_t bwd_k(BwdArgs& a, hipStream_t st)
 {
-    static int cache[4][16];
-    const bool lc = a.g.mode == kLaneChannel;
-    const bool hs = a.sg != nullptr;
-    auto kern = lc ? (hs ? bwd_kernel<K, DT, kLaneChannel, true> : bwd_kernel<K, DT, kLaneChannel, false>)
-                   : (hs ? bwd_kernel<K, DT, kPlane, true> : bwd_kernel<K, DT, kPlane, false>);
-    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[(lc ? 0 : 2) + (hs ? 1 : 0)]));
+    static int cache[3][3][16];
+    const int hs = a.sg != nullptr ? kSavedFactor : (a.h != nullptr ? kSavedH : kRecompute);
+    int slot = 0;
+    void (*kern)(BwdArgs) = hs == kSavedFactor ? bwd_kernel_for<K, DT, kSavedFactor>(a.g, slot)
+                            : hs == kSavedH    ? bwd_kernel_for<K, DT, kSavedH>(a.g, slot)
+                                               : bwd_kernel_for<K, DT, kRecompute>(a.g, slot);
+    if (kern == nullptr)
+        return hipErrorInvalidValue;
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[hs][slot]));
     hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }

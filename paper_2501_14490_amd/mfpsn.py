@@ -55,7 +55,7 @@ _lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_forward.restype = ctypes.c_int
 _lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
-_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
@@ -134,11 +134,11 @@ def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
     return int(n.value)
 
 
-def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, sg, sign, shift, bias, grad_x, grad_w, grad_b,
+def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b,
                    workspace, workspace_bytes=None, stream=None) -> None:
     if workspace_bytes is None:
         workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(sg), _ptr(sign),
+    _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(h), _ptr(sg), _ptr(sign),
                                _ptr(shift), _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
                                _ptr(workspace), int(workspace_bytes), _stream(stream)), "mfpsn_backward")
 
@@ -173,20 +173,24 @@ def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, want_sg
     return out if len(out) > 1 else spikes
 
 
-def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, sg=None):
-    """sg: optional surrogate factor saved by forward(..., want_sg=True)."""
+def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, sg=None, h=None):
+    """sg: optional surrogate factor saved by forward(..., want_sg=True); h:
+    optional potentials saved by forward(..., want_h=True).  sg is used if
+    given, else h, else both are recomputed from x."""
     dev = x.device
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
     if sg is not None:
         _expect(sg, SG_OUT[desc.dtype], dev, "sg")
+    if h is not None:
+        _expect(h, H_OUT[desc.dtype], dev, "h")
     grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
     grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
     grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
     need = mfpsn_backward_workspace_size(desc)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
-    mfpsn_backward(desc, x, grad_spikes, sg, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
+    mfpsn_backward(desc, x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
                    stream=stream)
     return grad_x, grad_w, grad_b
 

@@ -38,7 +38,7 @@ def lib():
     P = ctypes.c_void_p
     DP = ctypes.POINTER(Desc)
     L.mfpsn_forward.argtypes = [DP, P, P, P, P, P, P, P, P]
-    L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
     L.mfpsn_status_string.restype = ctypes.c_char_p
@@ -67,7 +67,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 2
+    assert lib.mfpsn_abi_version() == 3
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -121,17 +121,18 @@ def test_backward_workspace_and_validation(lib):
     # too small / misaligned / missing workspace
     need = ctypes.c_size_t(0)
     lib.mfpsn_backward_workspace_size(ctypes.byref(d), ctypes.byref(need))
-    args = [FAKE] * 9  # x, grad_spikes, sg, sign, shift, bias, grad_x, grad_w, grad_b
+    args = [FAKE] * 10  # x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b
     assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE, need.value - 8, None) == -5
     assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE + 4, need.value, None) == -5
     assert lib.mfpsn_backward(ctypes.byref(d), *args, None, need.value, None) == -5
-    # null tensors (sg may be NULL; grad_w may not)
+    # null tensors (h and sg may be NULL; grad_w may not)
     bad = list(args)
-    bad[7] = None  # grad_w
+    bad[8] = None  # grad_w
     assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -1
-    bad = list(args)
-    bad[2] = FAKE + 2  # misaligned sg
-    assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -6
+    for i in (2, 3):  # misaligned h, sg
+        bad = list(args)
+        bad[i] = FAKE + 2
+        assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -6
     # Q8.8 bound on the int64 grad_w sums
     q = good_desc(dtype=2, T=1 << 16, N=1 << 16, C=1, S=1)
     assert lib.mfpsn_backward(ctypes.byref(q), *args, FAKE, 1 << 40, None) == -2

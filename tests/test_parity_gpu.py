@@ -26,21 +26,32 @@ DEV = torch.device("cuda:0")
 GW_ABS, GW_REL = 1e-6, 1e-5
 
 
-def to_dev(a, dtype):
+def to_dev(a, dtype, offset=0):
+    """Device copy of `a`; with `offset`, a contiguous view that starts
+    `offset` elements into a larger buffer (a pointer that is only
+    element-aligned)."""
     if dtype == "bf16" and a.dtype == np.uint16:
-        return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
-    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+        t = torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    if offset:
+        flat = torch.empty(t.numel() + offset, dtype=t.dtype, device=DEV)
+        flat[offset:].copy_(t.reshape(-1))
+        t = flat[offset:].view(t.shape)
+    return t
 
 
-def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved_sg=False):
-    x = to_dev(case["x"], dtype)
-    g = to_dev(case["grad_spikes"], dtype)
+def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved=None,
+            offset=0):
+    x = to_dev(case["x"], dtype, offset)
+    g = to_dev(case["grad_spikes"], dtype, offset)
     sign = to_dev(case["sign"], None)
     shift = to_dev(case["shift"], None)
     bias = to_dev(case["bias"], None)
     desc = mfpsn.make_desc(case["x"].shape, k, d, dtype, surrogate, alpha, v_th, v_th_q, lo, hi)
     spikes, h, sg = mfpsn.forward(desc, x, sign, shift, bias, want_h=True, want_sg=True)
-    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, sg=sg if saved_sg else None)
+    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, sg=sg if saved == "sg" else None,
+                                h=h if saved == "h" else None)
     torch.cuda.synchronize()
     out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "SG": sg.cpu().numpy(),
            "grad_w": gw.cpu().numpy(), "grad_b": gb.cpu().numpy()}
@@ -142,31 +153,50 @@ SHAPES = [
     ((13, 5, 3, (100,)), "plane, S>=64 with a partial chunk"),
     ((19, 9, 4, (3,)), "plane, S<64 not dividing 64"),
     ((11, 6, 5, (32,)), "plane, S=32"),
+    ((9, 5, 2, (70,)), "plane, S=70: two columns per lane, ragged last tile"),
+    ((6, 65, 3, (2,)), "plane, S=2: two columns per lane, one live lane in the last tile"),
+    ((7, 8, 2, (4, 4)), "plane, S=16: one full two-column tile"),
 ]
 
 
-@pytest.mark.parametrize("saved_sg", [False, True])
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
 @pytest.mark.parametrize("shape_i", range(len(SHAPES)))
 @pytest.mark.parametrize("k,d", [(1, 1), (2, 3), (3, 2), (5, 1), (8, 4), (16, 2)])
-def test_small_shapes(orc, dtype, shape_i, k, d, saved_sg):
+def test_small_shapes(orc, dtype, shape_i, k, d, saved):
     (T, N, C, sp), label = SHAPES[shape_i]
     case = workloads.make_small(T, N, C, sp, k=k, s_lo=0, s_hi=7, dtype=dtype, seed=100 + k * 7 + d)
     v_th = 0.5
-    got = gpu_run(case, k, d, dtype, v_th, saved_sg=saved_sg)
+    got = gpu_run(case, k, d, dtype, v_th, saved=saved)
     ref = oracle_run(orc, case, k, d, dtype, v_th)
-    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved_sg={saved_sg}", k, d)
+    compare(got, ref, dtype, f"{label} k={k} d={d} {dtype} saved={saved}", k, d)
 
 
-@pytest.mark.parametrize("saved_sg", [False, True])
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
+def test_two_column_layout_needs_alignment(orc, dtype, saved):
+    # an even S puts two adjacent columns on each lane when every tensor is
+    # 8-byte aligned; inputs that start one element into a buffer take one
+    # column per lane; both must give the oracle's results
+    case = workloads.make_small(15, 6, 3, (10,), k=5, dtype=dtype, seed=31)
+    ref = oracle_run(orc, case, 5, 2, dtype, 0.5)
+    compare(gpu_run(case, 5, 2, dtype, 0.5, saved=saved), ref, dtype, "aligned", 5, 2)
+    compare(gpu_run(case, 5, 2, dtype, 0.5, saved=saved, offset=1), ref, dtype, "one element off", 5, 2)
+
+
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
 @pytest.mark.parametrize("dtype", ["f32", "q8_8"])
-@pytest.mark.parametrize("k", [4, 7, 12, 17, 24, 31, 32])
-def test_orders(orc, dtype, k, saved_sg):
+@pytest.mark.parametrize("k", [4, 7, 12, 16, 17, 24, 31, 32])
+@pytest.mark.parametrize("spatial", [(), (6,)])
+def test_orders(orc, dtype, k, saved, spatial):
+    # (): lane-channel; (6,): plane with two columns per lane up to the
+    # highest order that has them, one column above it
     d = 1 + k % 3
-    case = workloads.make_small(3 * k + 5, 4, 70, (), k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
+    C = 70 if not spatial else 3
+    case = workloads.make_small(3 * k + 5, 4, C, spatial, k=k, s_lo=0, s_hi=7, dtype=dtype, seed=k)
     ref = oracle_run(orc, case, k, d, dtype, 0.75)
-    got = gpu_run(case, k, d, dtype, 0.75, saved_sg=saved_sg)
-    compare(got, ref, dtype, f"k={k} d={d} {dtype} saved_sg={saved_sg}", k, d)
+    got = gpu_run(case, k, d, dtype, 0.75, saved=saved)
+    compare(got, ref, dtype, f"k={k} d={d} {dtype} spatial={spatial} saved={saved}", k, d)
 
 
 @pytest.mark.parametrize("surrogate,alpha", [("atan", 2.0), ("atan", 5.0), ("rational", 10.0), ("sigmoid", 1.5)])
@@ -194,18 +224,22 @@ def test_short_sequences(orc, T):
     compare(got, ref, "f32", f"T={T}", 8, 3)
 
 
-@pytest.mark.parametrize("saved_sg", [False, True])
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
 @pytest.mark.parametrize("k,d", [(8, 3), (16, 1), (5, 7)])
-def test_long_sequence_is_chunked(orc, k, d, saved_sg):
+def test_long_sequence_is_chunked(orc, k, d, saved):
     # few columns and a long time axis: the planner cuts each residue class
     # into chunks whose halos are recomputed
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="q8_8", seed=9)
-    got = gpu_run(case, k, d, "q8_8", 0.0, saved_sg=saved_sg)
+    got = gpu_run(case, k, d, "q8_8", 0.0, saved=saved)
     ref = oracle_run(orc, case, k, d, "q8_8", 0.0)
     compare(got, ref, "q8_8", "chunked", k, d)
     case = workloads.make_small(1500, 2, 64, (), k=k, dtype="f32", seed=9)
-    compare(gpu_run(case, k, d, "f32", 0.3, saved_sg=saved_sg), oracle_run(orc, case, k, d, "f32", 0.3),
+    compare(gpu_run(case, k, d, "f32", 0.3, saved=saved), oracle_run(orc, case, k, d, "f32", 0.3),
             "f32", "chunked f32", k, d)
+    # plane mode, two columns per lane
+    case = workloads.make_small(1500, 2, 2, (6,), k=k, dtype="bf16", seed=10)
+    compare(gpu_run(case, k, d, "bf16", 0.3, saved=saved), oracle_run(orc, case, k, d, "bf16", 0.3),
+            "bf16", "chunked plane bf16", k, d)
 
 
 def compare_nan_aware(got, ref, label, k, d, hi=7):
@@ -222,9 +256,9 @@ def compare_nan_aware(got, ref, label, k, d, hi=7):
     assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: surrogate factor differs"
 
 
-@pytest.mark.parametrize("saved_sg", [False, True])
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
 @pytest.mark.parametrize("k,d", [(8, 1), (16, 2), (5, 3), (24, 1)])
-def test_special_values_take_the_exact_path(orc, k, d, saved_sg):
+def test_special_values_take_the_exact_path(orc, k, d, saved):
     # zeros, subnormals, values at the edge of the exponent-add range, huge
     # values, infinities: every tap must still equal the exact ldexp result
     case = workloads.make_small(60, 3, 80, (), k=k, s_lo=0, s_hi=7, dtype="f32", seed=k + d)
@@ -236,18 +270,18 @@ def test_special_values_take_the_exact_path(orc, k, d, saved_sg):
     idx = rng.integers(0, x.size, size=400)
     x.ravel()[idx] = specials[rng.integers(0, specials.size, size=idx.size)]
     x[5:9, 1, :] = 0.0  # whole rows of zeros inside the walk
-    got = gpu_run(case, k, d, "f32", 0.25, saved_sg=saved_sg)
+    got = gpu_run(case, k, d, "f32", 0.25, saved=saved)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
     compare_nan_aware(got, ref, f"specials k={k} d={d}", k, d)
     case["x"].ravel()[rng.integers(0, x.size, size=20)] = np.float32(np.inf)
     case["grad_spikes"].ravel()[rng.integers(0, x.size, size=200)] = 0.0
-    got = gpu_run(case, k, d, "f32", 0.25, saved_sg=saved_sg)
+    got = gpu_run(case, k, d, "f32", 0.25, saved=saved)
     ref = oracle_run(orc, case, k, d, "f32", 0.25)
     compare_nan_aware(got, ref, f"specials+inf k={k} d={d}", k, d)
 
 
-@pytest.mark.parametrize("saved_sg", [False, True])
-def test_tiny_dh_terms(orc, saved_sg):
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
+def test_tiny_dh_terms(orc, saved):
     # grad_spikes values around 1e-38 make dH fall below the exponent-add
     # range on many lanes: their grad_x terms are dropped, every other output
     # stays bit-exact
@@ -256,7 +290,7 @@ def test_tiny_dh_terms(orc, saved_sg):
     rng = np.random.default_rng(21)
     idx = rng.integers(0, g.size, size=g.size // 5)
     g.ravel()[idx] = (rng.standard_normal(idx.size) * 1e-37).astype(np.float32)
-    got = gpu_run(case, 8, 2, "f32", 0.25, saved_sg=saved_sg)
+    got = gpu_run(case, 8, 2, "f32", 0.25, saved=saved)
     ref = oracle_run(orc, case, 8, 2, "f32", 0.25)
     hit = tiny_dh_outputs(ref["dH"], 8, 2, 7)
     assert hit.any() and not hit.all()
@@ -338,9 +372,11 @@ def test_workloads_full_size(orc, wid):
                                wl.s_max)
         spikes, h, sg = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True,
                                       want_sg=True)
-        saved = d % 2 == 1  # odd dilations read the saved factor, even ones recompute it
+        # the backward recomputes H, or reads the saved factor or the saved H,
+        # by dilation
+        saved = (None, "sg", "h")[d % 3]
         gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"],
-                                    sg=sg if saved else None)
+                                    sg=sg if saved == "sg" else None, h=h if saved == "h" else None)
         torch.cuda.synchronize()
         got = {"spikes": spikes.index_select(2, chans_t).cpu().numpy(),
                "H": h.index_select(2, chans_t).cpu().numpy(),
