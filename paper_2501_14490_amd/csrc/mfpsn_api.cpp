@@ -119,6 +119,16 @@ bool pair_layout(const mfpsn_desc* d)
     return on && !(d->S == 1 && d->C >= 64) && d->S % 2 == 0 && d->k <= kPairMaxK;
 }
 
+// Line-aligned plane tiles (MFPSN_ROW_TILES=0 turns them off).
+bool row_tiles_enabled()
+{
+    static const bool on = [] {
+        const char* e = getenv("MFPSN_ROW_TILES");
+        return !(e && strcmp(e, "0") == 0);
+    }();
+    return on;
+}
+
 bool pair_aligned(std::initializer_list<const void*> ptrs)
 {
     for (const void* p : ptrs)
@@ -170,7 +180,19 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
         g.nv = nv;
         g.groups = d->C;
         g.tiles = (int32_t)ceil_div((int64_t)d->N * d->S, 64 * nv);
+        // Rows whose length is not a multiple of 128 bytes start mid-line, so
+        // tiles over the flattened plane straddle lines and neighbouring tiles
+        // fetch the shared lines twice.  Long enough rows get tiles of their
+        // own that start on lines, at the price of a few shadow lanes.
+        const int64_t width = 64 * nv, line = 128 / g.esize;
+        const int64_t per_row = ceil_div(d->S + line - 1, width);
+        if (((int64_t)d->S * g.esize) % 128 != 0 && per_row * width * 8 <= (int64_t)d->S * 9 &&
+            row_tiles_enabled()) {
+            g.row_tiles = (int32_t)per_row;
+            g.tiles = (int32_t)(per_row * d->N);
+        }
     }
+    g.line_elems = 128 / g.esize;
     // Cut each residue class into chunks only while the columns alone give
     // fewer items than the target (or a class spans too many bytes).
     const int64_t K = d->k;

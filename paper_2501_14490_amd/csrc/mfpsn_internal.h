@@ -24,7 +24,11 @@ struct Geom {
     int32_t k, d;
     int32_t mode;
     int32_t nv;        // adjacent columns per lane: 1, or 2 (plane mode, S even)
-    int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/(64*nv))
+    int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/(64*nv)),
+                       // or N * row_tiles with line-aligned rows
+    int32_t row_tiles; // plane tiles per (n, c) row when tiles follow 128-byte lines
+                       // within each row (0: tiles run over the flattened (n, s) plane)
+    int32_t line_elems;// elements per 128-byte line (128 / esize)
     int32_t tq, tr;    // T = tq * d + tr
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk

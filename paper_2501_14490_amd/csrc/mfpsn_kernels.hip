@@ -533,6 +533,20 @@ __device__ __forceinline__ Cols tile_cols(const Geom& g, int tile, int grp, int 
         t.active = c < g.C;
         t.partial = false;
         t.col = (uint32_t)tile * (uint32_t)g.C + (uint32_t)min(c, g.C - 1);
+    } else if (g.row_tiles > 0) {
+        // tiles of one (n, c) row, starting on 128-byte lines: tile m covers
+        // positions s0 .. s0 + 64*NV - 1 with s0 = m*64*NV - (elements of the
+        // row's first line that precede it); lanes outside [0, S) are shadows
+        const uint32_t S = (uint32_t)g.S;
+        const uint32_t n = (uint32_t)tile / (uint32_t)g.row_tiles;
+        const uint32_t m = (uint32_t)tile - n * (uint32_t)g.row_tiles;
+        const uint32_t row = n * (uint32_t)g.C + (uint32_t)grp;
+        const int lead = (int)((row * S) & (uint32_t)(g.line_elems - 1));
+        const int s0 = (int)(m * (64u * NV)) - lead;
+        const int sl = s0 + lane * NV;
+        t.active = sl >= 0 && sl < (int)S;
+        t.partial = s0 < 0 || s0 + 64 * NV > (int)S;
+        t.col = row * S + (uint32_t)min(max(sl, 0), (int)S - NV);
     } else {
         // positions NV*lane .. NV*lane + NV-1 of the tile; with NV = 2, S is
         // even, so both lie in one (n, c) row of S adjacent columns

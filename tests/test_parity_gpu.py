@@ -156,6 +156,8 @@ SHAPES = [
     ((9, 5, 2, (70,)), "plane, S=70: two columns per lane, ragged last tile"),
     ((6, 65, 3, (2,)), "plane, S=2: two columns per lane, one live lane in the last tile"),
     ((7, 8, 2, (4, 4)), "plane, S=16: one full two-column tile"),
+    ((9, 3, 2, (44, 44)), "plane, S=1936: tiles on 128-byte lines of each row, two columns per lane"),
+    ((7, 2, 3, (5, 387)), "plane, S=1935 (odd): tiles on 128-byte lines of each row, one column per lane"),
 ]
 
 
