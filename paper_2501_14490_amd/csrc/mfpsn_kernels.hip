@@ -455,13 +455,40 @@ __device__ __forceinline__ float sg_factor(const Surrogate& sg, float h, float v
     float u = h - v_th;
     return sg(u);
 }
-__device__ __forceinline__ int32_t sg_factor(const Surrogate& sg, int32_t h, float, int v_th_q)
+__device__ __forceinline__ int32_t sg_factor_q(const Surrogate& sg, int32_t u)
 {
-    int32_t u = h - v_th_q;
     float uf = (float)u * 0.00390625f;
     float s = sg(uf);
     return (int32_t)rintf(s * 32768.0f);
 }
+__device__ __forceinline__ int32_t sg_factor(const Surrogate& sg, int32_t h, float, int v_th_q)
+{
+    return sg_factor_q(sg, (int32_t)((uint32_t)h - (uint32_t)v_th_q));
+}
+
+// Q8.8 factors come from a table: u = H - v_th_q is an integer and L(u) is
+// even in u (the float sequence sees |u|, or u only through u*u), so each
+// block evaluates L(0 .. kQTable-1) once into LDS with the same sequence and
+// looks factors up; |u| beyond the table takes the sequence directly.
+constexpr int kQTable = 4096;
+
+struct QTable {
+    int32_t* tab;
+    __device__ void fill(const Surrogate& sg) const
+    {
+        for (int j = threadIdx.x; j < kQTable; j += kThreads)
+            tab[j] = sg_factor_q(sg, j);
+    }
+    __device__ __forceinline__ int32_t operator()(const Surrogate& sg, int32_t h, int v_th_q) const
+    {
+        const int32_t u = (int32_t)((uint32_t)h - (uint32_t)v_th_q);
+        const uint32_t au = u < 0 ? 0u - (uint32_t)u : (uint32_t)u;
+        int32_t L = tab[min(au, (uint32_t)(kQTable - 1))];
+        if (__builtin_expect(au >= (uint32_t)kQTable, 0))
+            L = sg_factor_q(sg, u);
+        return L;
+    }
+};
 // dH = grad_spikes * factor (Q8.8: floor((g * L) / 2^15))
 __device__ __forceinline__ float delta_h(float g, float f) { return g * f; }
 __device__ __forceinline__ int32_t delta_h(int32_t g, int32_t L)
@@ -568,7 +595,7 @@ __device__ __forceinline__ int class_len(const Geom& g, int r) { return g.tq + (
 // forward
 // ---------------------------------------------------------------------------
 template <int K, int DT, int MODE, int NV>
-__global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void fwd_kernel(FwdArgs a)
 {
     using V = typename IO<DT>::V;
     using PV = Pk<V, NV>;
@@ -583,6 +610,16 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
     const int nw = (int)gridDim.x * kWaves;
     const int64_t q0 = g.items * wid / nw;
     const int64_t q1 = g.items * (wid + 1) / nw;
+    Surrogate sg;
+    sg.init(g.sg, g.alpha);
+    __shared__ int32_t qtab[kF ? 1 : kQTable];
+    const QTable qt{qtab};
+    if constexpr (!kF) {
+        if (a.sg_out != nullptr) {
+            qt.fill(sg);
+            __syncthreads();
+        }
+    }
     if (q0 >= q1)
         return;
     const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
@@ -606,8 +643,6 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
     const int32_t hstep = 4 * sstep;
     const int want_h = a.h_out != nullptr ? 1 : 0;
     const int want_sg = a.sg_out != nullptr ? 1 : 0;
-    Surrogate sg;
-    sg.init(g.sg, g.alpha);
 
     Cursor cur(g, q0);
     int tile_cached = -1;
@@ -721,7 +756,10 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdArgs a)
                 Pk<uint32_t, NV> w;
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
-                    w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
+                    if constexpr (kF)
+                        w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
+                    else
+                        w.v[e] = (uint32_t)qt(sg, h.v[e], g.v_th_q);
                 st_words<NV>(gs, vh, so_h, w);
             }
             advance(so_s, sstep);
@@ -820,6 +858,19 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     }
     Surrogate sg;
     sg.init(g.sg, g.alpha);
+    constexpr bool kQT = !kF && HS != kSavedFactor;  // Q8.8 factors from the table
+    __shared__ int32_t qtab[kQT ? kQTable : 1];
+    const QTable qt{qtab};
+    if constexpr (kQT) {
+        qt.fill(sg);
+        __syncthreads();
+    }
+    auto factor = [&](V h) __attribute__((always_inline)) {
+        if constexpr (kQT)
+            return qt(sg, h, g.v_th_q);
+        else
+            return sg_factor(sg, h, g.v_th, g.v_th_q);
+    };
 
     const uint32_t M = g.M;
     const int d = g.d;
@@ -972,7 +1023,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 } else if constexpr (HS == kSavedH) {
 #pragma unroll
                     for (int e = 0; e < NV; ++e)
-                        dh.v[e] = delta_h(gv.v[e], sg_factor(sg, hv.v[e], g.v_th, g.v_th_q));
+                        dh.v[e] = delta_h(gv.v[e], factor(hv.v[e]));
                 } else {
                     PV h;
                     if constexpr (kF) {
@@ -1008,7 +1059,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                     }
 #pragma unroll
                     for (int e = 0; e < NV; ++e)
-                        dh.v[e] = delta_h(gv.v[e], sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
+                        dh.v[e] = delta_h(gv.v[e], factor(h.v[e]));
                 }
                 const bool own = full || j < j1;
                 if (own) {
