@@ -88,11 +88,19 @@ constexpr int prefetch_depth(int K, int cap)
 #ifndef MFPSN_FWD_PREFETCH
 #define MFPSN_FWD_PREFETCH 8
 #endif
+#ifndef MFPSN_FWD_PREFETCH_F32_PAIR
+#define MFPSN_FWD_PREFETCH_F32_PAIR 2
+#endif
 #ifndef MFPSN_BWD_PREFETCH
 #define MFPSN_BWD_PREFETCH 2
 #endif
+#ifndef MFPSN_BWD_PAIR_BYTES
+#define MFPSN_BWD_PAIR_BYTES 16
+#endif
 constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
+constexpr int kFwdPrefetchF32Pair = MFPSN_FWD_PREFETCH_F32_PAIR;
 constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
+constexpr int kBwdPairBytes = MFPSN_BWD_PAIR_BYTES;  // plane mode, two columns per lane
 
 template <int V> using ic = std::integral_constant<int, V>;
 enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 };
@@ -600,8 +608,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     using V = typename IO<DT>::V;
     using PV = Pk<V, NV>;
     using TP = Taps<K, DT, MODE>;
-    constexpr int P = prefetch_depth(K, kFwdPrefetch / NV);
     constexpr int es = IO<DT>::es;
+    // 8 steps of x in flight, but 2 for lanes holding two f32 columns (8
+    // bytes per access): the depths measured fastest on MI355X
+    constexpr int P = prefetch_depth(K, (NV == 2 && es == 4) ? kFwdPrefetchF32Pair : kFwdPrefetch);
     constexpr bool kF = DT != kQ88;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
@@ -820,13 +830,16 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     using W = typename IO<DT>::W;
     using PV = Pk<V, NV>;
     using TP = Taps<K, DT, MODE>;
+    constexpr int es = IO<DT>::es;
     // Lane-channel waves at orders up to 16 run 4 per SIMD and stream three
     // 256-byte rows per step: a short queue is best.  Plane waves (narrower
     // rows) want a longer one, and high orders (2 waves per SIMD) a deep one.
-    // Lanes holding two columns move twice the bytes per access.
+    // Lanes holding two columns do best with about 16 bytes per stream in
+    // flight (2 steps of f32 pairs, 4 of bf16 or Q8.8 pairs).
     constexpr int P = prefetch_depth(
-        K, (K >= 24 ? 8 * kBwdPrefetch : (MODE == kLaneChannel ? kBwdPrefetch : 2 * kBwdPrefetch)) / NV);
-    constexpr int es = IO<DT>::es;
+        K, K >= 24 ? 8 * kBwdPrefetch
+                   : (MODE == kLaneChannel ? kBwdPrefetch
+                                           : (NV == 2 ? kBwdPairBytes / (es * NV) : 2 * kBwdPrefetch)));
     constexpr int gxs = IO<DT>::gx_es;
     constexpr bool kF = DT != kQ88;
     constexpr bool kRe = HS == kRecompute;  // recompute H from the x ring
