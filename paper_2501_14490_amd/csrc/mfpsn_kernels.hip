@@ -145,7 +145,7 @@ __device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b32(b.rs, v, s, MFPSN_LD_CPOL);
 }
-__device__ __forceinline__ uint32_t ld16(Buf b, uint32_t v, int32_t s)
+__device__ __forceinline__ uint16_t ld16(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, MFPSN_LD_CPOL);
 }
@@ -235,15 +235,25 @@ template <> struct IO<kF32> {
     using W = double;    // exact product accumulator of grad_w, grad_b
     static constexpr int es = 4;     // bytes per stored x / grad_spikes
     static constexpr int gx_es = 4;  // bytes per stored grad_x
+    template <int NV> using Raw = Pk<uint32_t, NV>;
     template <int NV>
-    __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
+    __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
     {
-        const Pk<uint32_t, NV> w = ld_words<NV>(b, v, s);
+        return ld_words<NV>(b, v, s);
+    }
+    template <int NV>
+    __device__ static Pk<V, NV> cvt(const Raw<NV>& w)
+    {
         Pk<V, NV> r;
 #pragma unroll
         for (int e = 0; e < NV; ++e)
             r.v[e] = __builtin_bit_cast(float, w.v[e]);
         return r;
+    }
+    template <int NV>
+    __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
+    {
+        return cvt<NV>(load_raw<NV>(b, v, s));
     }
     template <int NV>
     __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
@@ -261,18 +271,32 @@ template <> struct IO<kBF16> {
     using W = double;
     static constexpr int es = 2;
     static constexpr int gx_es = 2;
+    // NV stored values in one 16-bit (NV = 1) or 32-bit (NV = 2) word, widened
+    // only where they are used
+    template <int NV> using Raw = Pk<std::conditional_t<NV == 1, uint16_t, uint32_t>, 1>;
+    template <int NV>
+    __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
+    {
+        Raw<NV> w;
+        if constexpr (NV == 1)
+            w.v[0] = ld16(b, v, s);
+        else
+            w.v[0] = ld32(b, v, s);
+        return w;
+    }
+    template <int NV>
+    __device__ static Pk<V, NV> cvt(const Raw<NV>& w)
+    {
+        Pk<V, NV> r;
+        r.v[0] = __builtin_bit_cast(float, (uint32_t)w.v[0] << 16);
+        if constexpr (NV == 2)
+            r.v[1] = __builtin_bit_cast(float, w.v[0] & 0xFFFF0000u);
+        return r;
+    }
     template <int NV>
     __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
     {
-        Pk<V, NV> r;
-        if constexpr (NV == 1) {
-            r.v[0] = __builtin_bit_cast(float, ld16(b, v, s) << 16);
-        } else {
-            const uint32_t w = ld32(b, v, s);
-            r.v[0] = __builtin_bit_cast(float, w << 16);
-            r.v[1] = __builtin_bit_cast(float, w & 0xFFFF0000u);
-        }
-        return r;
+        return cvt<NV>(load_raw<NV>(b, v, s));
     }
     template <int NV>
     __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
@@ -293,18 +317,30 @@ template <> struct IO<kQ88> {
     using W = int64_t;
     static constexpr int es = 2;
     static constexpr int gx_es = 4;
+    template <int NV> using Raw = Pk<std::conditional_t<NV == 1, uint16_t, uint32_t>, 1>;
+    template <int NV>
+    __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
+    {
+        Raw<NV> w;
+        if constexpr (NV == 1)
+            w.v[0] = ld16(b, v, s);
+        else
+            w.v[0] = ld32(b, v, s);
+        return w;
+    }
+    template <int NV>
+    __device__ static Pk<V, NV> cvt(const Raw<NV>& w)
+    {
+        Pk<V, NV> r;
+        r.v[0] = (int32_t)(int16_t)w.v[0];
+        if constexpr (NV == 2)
+            r.v[1] = (int32_t)w.v[0] >> 16;
+        return r;
+    }
     template <int NV>
     __device__ static Pk<V, NV> load(Buf b, uint32_t v, int32_t s)
     {
-        Pk<V, NV> r;
-        if constexpr (NV == 1) {
-            r.v[0] = (int32_t)(int16_t)(uint16_t)ld16(b, v, s);
-        } else {
-            const uint32_t w = ld32(b, v, s);
-            r.v[0] = (int32_t)(int16_t)(uint16_t)w;
-            r.v[1] = (int32_t)w >> 16;
-        }
-        return r;
+        return cvt<NV>(load_raw<NV>(b, v, s));
     }
     template <int NV>
     __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
@@ -695,10 +731,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                     slow = m + 1;
             }
         }
-        PV pf[P];  // x[j] at slot j mod P
+        // x[j] at slot j mod P, as loaded: converted in the step that uses it,
+        // so no step waits for the loads it issues itself
+        typename IO<DT>::template Raw<NV> pf[P];
 #pragma unroll
         for (int p = 0; p < P; ++p)
-            pf[p] = IO<DT>::template load<NV>(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
+            pf[p] = IO<DT>::template load_raw<NV>(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
         int32_t so_xp = (j0 + P - jb) * xstep;  // prefetch of step j + P
         int32_t so_s = 0, so_h = 0;
 
@@ -711,8 +749,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             constexpr int kind = decltype(kc_)::value;
             constexpr int imin = (kF && kind == kEdge) ? K - 1 - u : 0;
             (void)j;
-            const PV xv = pf[u % P];
-            pf[u % P] = IO<DT>::template load<NV>(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
+            const PV xv = IO<DT>::template cvt<NV>(pf[u % P]);
+            pf[u % P] = IO<DT>::template load_raw<NV>(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
             advance(so_xp, xstep);
             ring[u] = xv;
             PV h;
@@ -746,10 +784,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             } else {
 #pragma unroll
                 for (int e = 0; e < NV; ++e) {
+                    // (pinned partial sums: one shift and one xor-add per tap,
+                    // instead of the reassociated shift, xor, add3 sequence)
                     V acc = start;
 #pragma unroll
-                    for (int i = 0; i < K; ++i)
+                    for (int i = 0; i < K; ++i) {
                         acc = acc + tp.apply(ring[(u + 1 + i) % K].v[e], i);
+                        pin(acc);
+                    }
                     h.v[e] = acc;
                     spk |= (h.v[e] >= g.v_th_q ? 1u : 0u) << (8 * e);
                 }
@@ -963,8 +1005,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             if (kRe && TP::kHasFast && t <= jtop && any_slow(v, g))
                 slow_x = K;
         }
-        // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P
-        PV pg[P], ph[HS ? P : 1], px[P];
+        // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P, as loaded
+        // (converted in the step that uses them)
+        typename IO<DT>::template Raw<NV> pg[P], px[P];
+        PV ph[HS ? P : 1];
         auto load_h = [&](int32_t so) __attribute__((always_inline)) {
             const Pk<uint32_t, NV> w = ld_words<NV>(hsb, vh, so);
             PV v;
@@ -978,10 +1022,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             const int jp = jstart - p;
             const int js = (K - 1 - p) % P;
             const int rowg = min(jp, Lr - 1);
-            pg[js] = IO<DT>::template load<NV>(gsb, vx, (rowg - jb) * xstep);
+            pg[js] = IO<DT>::template load_raw<NV>(gsb, vx, (rowg - jb) * xstep);
             if constexpr (HS)
                 ph[js] = load_h((rowg - jb) * hstep);
-            px[js] = IO<DT>::template load<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
+            px[js] = IO<DT>::template load_raw<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
         }
         int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
         int32_t so_hp = (jstart - P - jb) * hstep;           // factor or H of step j - P
@@ -999,15 +1043,15 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             constexpr int sj = K - 1 - u;  // j mod k
             constexpr int sp = sj % P;     // j mod P
             constexpr int imin = edge ? u : 0;
-            const PV gv = pg[sp];
-            const PV xv = px[sp];
+            const PV gv = IO<DT>::template cvt<NV>(pg[sp]);
+            const PV xv = IO<DT>::template cvt<NV>(px[sp]);
             PV hv;
             if constexpr (HS)
                 hv = ph[sp];
-            pg[sp] = IO<DT>::template load<NV>(gsb, vx, full ? so_gp : min(max(so_gp, 0), so_last));
+            pg[sp] = IO<DT>::template load_raw<NV>(gsb, vx, full ? so_gp : min(max(so_gp, 0), so_last));
             if constexpr (HS)
                 ph[sp] = load_h(full ? so_hp : min(max(so_hp, 0), so_hlast));
-            px[sp] = IO<DT>::template load<NV>(xs, vx, full ? so_xp : min(max(so_xp, 0), so_last));
+            px[sp] = IO<DT>::template load_raw<NV>(xs, vx, full ? so_xp : min(max(so_xp, 0), so_last));
             advance(so_gp, -xstep);
             if constexpr (HS)
                 advance(so_hp, -hstep);
@@ -1065,8 +1109,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                         for (int e = 0; e < NV; ++e) {
                             V acc = start;
 #pragma unroll
-                            for (int i = 0; i < K; ++i)
+                            for (int i = 0; i < K; ++i) {
                                 acc = acc + tp.apply(xf[(sj + 1 + i) % K].v[e], i);
+                                pin(acc);
+                            }
                             h.v[e] = acc;
                         }
                     }
