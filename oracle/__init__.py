@@ -18,6 +18,9 @@ and ``tests/test_golden.py``):
   surrogate, exp  closed forms at 0, symmetry, unit integral, 2-ulp bound
                   against double exp
   sawtooth        the printed sequence and receptive-field example of Sec. 4.1
+  stream_forward  the (pinned) whole-sequence forward, bit for bit, from a
+                  history ring that starts as garbage; the exact receptive
+                  field (k-1)d+1 that sizes the ring
 """
 from __future__ import annotations
 
@@ -78,6 +81,12 @@ def _load():
             lib.orc_backward_q88.argtypes = [P, P, *geo, P, P, i32, i32, P, ctypes.c_int32, i32, f32,
                                              P, P, P, P, P]
             lib.orc_backward_q88.restype = None
+            lib.orc_stream_step_f32.argtypes = [P, i32, i32, i32, i32, i32, i64, P, P, P, i32, i32, P, f32,
+                                                P, P]
+            lib.orc_stream_step_f32.restype = None
+            lib.orc_stream_step_q88.argtypes = [P, i32, i32, i32, i32, i32, i64, P, P, P, i32, i32, P,
+                                                ctypes.c_int32, P, P]
+            lib.orc_stream_step_q88.restype = None
             lib.orc_sawtooth_dilation.argtypes = [i32, i32]
             lib.orc_sawtooth_dilation.restype = i32
             _lib = lib
@@ -195,6 +204,47 @@ def forward_q88(x, sign, shift, bias, k: int, d: int, v_th: int, shift_lo: int =
                             ctypes.byref(taps))
     if with_tap_count:
         return H, spk, int(taps.value)
+    return H, spk
+
+
+def stream_ring_steps(k: int, d: int) -> int:
+    """History slots of the step-by-step neuron: its receptive field (k-1)d+1."""
+    return (int(k) - 1) * int(d) + 1
+
+
+def stream_forward(x, sign, shift, bias, k: int, d: int, v_th, dtype: str = "f32", shift_lo: int = -127,
+                   shift_hi: int = 127):
+    """Runs the step-by-step neuron (orc_stream_step_*) over x [T, N, C, ...]
+    one time step per call, with a history ring of stream_ring_steps(k, d)
+    slots; returns H and spikes stacked over time.  dtype "f32" (float32 x),
+    "bf16" (uint16 bit patterns, arithmetic in float) or "q8_8" (int16 x)."""
+    lib = _load()
+    if dtype == "bf16":
+        x = bf16_bits_to_f32(x)
+        dtype = "f32"
+    q = dtype == "q8_8"
+    x = _c(x, np.int16 if q else np.float32)
+    T, N, C, S = _geometry(x)
+    sign = _c(sign, np.int8).reshape(C, k)
+    shift = _c(shift, np.int8).reshape(C, k)
+    bias = _c(bias, np.int32 if q else np.float32).reshape(C)
+    R = stream_ring_steps(k, d)
+    # the ring starts with garbage: no step may read a slot before writing it
+    hist = np.full((R,) + x.shape[1:], 0x5A5A if q else np.nan, dtype=np.int16 if q else np.float32)
+    H = np.empty(x.shape, np.int32 if q else np.float32)
+    spk = np.empty(x.shape, np.uint8)
+    for t in range(T):
+        xt = np.ascontiguousarray(x[t])
+        Ht = np.empty(x.shape[1:], H.dtype)
+        st = np.empty(x.shape[1:], np.uint8)
+        if q:
+            lib.orc_stream_step_q88(_ptr(xt), N, C, S, int(k), int(d), t, _ptr(hist), _ptr(sign), _ptr(shift),
+                                    int(shift_lo), int(shift_hi), _ptr(bias), int(v_th), _ptr(Ht), _ptr(st))
+        else:
+            lib.orc_stream_step_f32(_ptr(xt), N, C, S, int(k), int(d), t, _ptr(hist), _ptr(sign), _ptr(shift),
+                                    int(shift_lo), int(shift_hi), _ptr(bias), float(v_th), _ptr(Ht), _ptr(st))
+        H[t] = Ht
+        spk[t] = st
     return H, spk
 
 

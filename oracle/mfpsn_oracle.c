@@ -387,6 +387,78 @@ void orc_backward_q88(const int16_t* x, const int16_t* grad_spikes, int T, int N
     }
 }
 
+/* ------------------------------------------------------------------------ */
+/* Step-by-step inference (Sec. 3.2: the sliding PSN emits H[t] at step t;    */
+/* Sec. 5, Table "inference memory": the neuron keeps an input history whose  */
+/* length grows with its order).                                              */
+/* ------------------------------------------------------------------------ */
+
+/* One time step t of the charge and fire, for inputs that arrive one step at
+ * a time.  The neuron keeps the inputs of its receptive field in a history
+ * ring hist[R][N][C][S] with R = (k-1)*d + 1 slots, the input of time tau in
+ * slot tau mod R: tap i reads time tau = t - (k-1-i) d, and the oldest one,
+ * tap 0, reaches back (k-1) d steps.  The step first stores x_t (the inputs
+ * of time t, [N][C][S]) in slot t mod R, then evaluates the same sum as
+ * orc_forward_f32 at this t: ascending taps from +0.0f, terms with tau < 0
+ * omitted, bias last.  Calling it for t = 0, 1, ..., T-1 gives the
+ * potentials and spikes of orc_forward_f32 over the whole sequence. */
+void orc_stream_step_f32(const float* x_t, int N, int C, int S, int k, int d, int64_t t,
+                         float* hist, const int8_t* sign, const int8_t* shift, int lo, int hi,
+                         const float* bias, float v_th, float* H_t, uint8_t* spikes_t)
+{
+    const int64_t M = (int64_t)N * C * S;
+    const int64_t R = (int64_t)(k - 1) * d + 1;
+    memcpy(hist + (t % R) * M, x_t, (size_t)M * sizeof(float));
+    for (int n = 0; n < N; ++n)
+        for (int c = 0; c < C; ++c)
+            for (int s = 0; s < S; ++s) {
+                const int64_t col = ((int64_t)n * C + c) * S + s;
+                float acc = 0.0f;
+                for (int i = 0; i < k; ++i) {
+                    const int64_t tau = t - (int64_t)(k - 1 - i) * d;
+                    if (tau < 0)
+                        continue;
+                    float term = ldexpf(hist[(tau % R) * M + col], -clamp_shift(shift[c * k + i], lo, hi));
+                    if (sign[c * k + i] < 0)
+                        term = -term;
+                    acc = acc + term;
+                }
+                const float h = acc + bias[c];
+                if (H_t)
+                    H_t[col] = h;
+                if (spikes_t)
+                    spikes_t[col] = (h >= v_th) ? 1 : 0;
+            }
+}
+
+/* Q8.8 version of the step: int16 history, floor shifts, negation after the
+ * shift, int32 accumulator starting at the bias (as orc_forward_q88). */
+void orc_stream_step_q88(const int16_t* x_t, int N, int C, int S, int k, int d, int64_t t,
+                         int16_t* hist, const int8_t* sign, const int8_t* shift, int lo, int hi,
+                         const int32_t* bias, int32_t v_th, int32_t* H_t, uint8_t* spikes_t)
+{
+    const int64_t M = (int64_t)N * C * S;
+    const int64_t R = (int64_t)(k - 1) * d + 1;
+    memcpy(hist + (t % R) * M, x_t, (size_t)M * sizeof(int16_t));
+    for (int n = 0; n < N; ++n)
+        for (int c = 0; c < C; ++c)
+            for (int s = 0; s < S; ++s) {
+                const int64_t col = ((int64_t)n * C + c) * S + s;
+                int64_t acc = bias[c];
+                for (int i = 0; i < k; ++i) {
+                    const int64_t tau = t - (int64_t)(k - 1 - i) * d;
+                    if (tau < 0)
+                        continue;
+                    int64_t term = floor_div_pow2(hist[(tau % R) * M + col], clamp_shift(shift[c * k + i], lo, hi));
+                    acc += (sign[c * k + i] < 0) ? -term : term;
+                }
+                if (H_t)
+                    H_t[col] = (int32_t)acc;
+                if (spikes_t)
+                    spikes_t[col] = (acc >= v_th) ? 1 : 0;
+            }
+}
+
 /* Sawtooth dilation schedule (Sec. 4.1, Eq. d): d^0 = 1, d^{l+1} = d^l mod P + 1
  * (the paper uses P = 3), computed by iterating the recurrence. */
 int orc_sawtooth_dilation(int layer, int period)

@@ -512,3 +512,52 @@ def test_bf16_rounding_matches_torch(orc):
     assert np.array_equal(orc.f32_to_bf16_bits_vec(a), ref)
     assert np.array_equal(orc.bf16_bits_to_f32(ref), torch.from_numpy(ref.view(np.int16)).view(
         torch.bfloat16).float().numpy())
+
+
+# ---------------------------------------------------------------------------
+# step-by-step inference (Sec. 3.2: H[t] is available at step t; Sec. 5,
+# Table "inference memory": the neuron stores an input history whose length
+# grows with its order)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("k,d,T", [(1, 1, 7), (3, 1, 12), (4, 3, 20), (5, 2, 6), (2, 9, 12), (8, 4, 40)])
+def test_stream_steps_reproduce_the_parallel_forward(orc, k, d, T):
+    """Feeding one time step per call through a ring of (k-1)d+1 slots gives
+    the potentials and spikes of the whole-sequence forward bit for bit (the
+    ring starts as NaN / a garbage pattern, so a slot read before it was
+    written would show)."""
+    c = small_case(T=T, N=2, C=3, S=2, k=k, seed=40 + k * d)
+    H, S = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0.3, 0, 4)
+    Hs, Ss = orc.stream_forward(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0.3, "f32", 0, 4)
+    assert np.array_equal(H.view(np.uint32), Hs.view(np.uint32))
+    assert np.array_equal(S, Ss)
+
+
+def test_stream_steps_bf16_and_q88(orc):
+    k, d, T = 4, 2, 15
+    cb = workloads.make_small(T, 2, 5, (3,), k=k, dtype="bf16", seed=7)
+    H, S = orc.forward_bf16(cb["x"], cb["sign"], cb["shift"], cb["bias"], k, d, 0.2, shift_lo=0, shift_hi=7)
+    Hs, Ss = orc.stream_forward(cb["x"], cb["sign"], cb["shift"], cb["bias"], k, d, 0.2, "bf16", 0, 7)
+    assert np.array_equal(H.view(np.uint32), Hs.view(np.uint32)) and np.array_equal(S, Ss)
+    cq = workloads.make_small(T, 2, 5, (3,), k=k, dtype="q8_8", seed=8)
+    H, S = orc.forward_q88(cq["x"], cq["sign"], cq["shift"], cq["bias"], k, d, 100, 0, 7)
+    Hs, Ss = orc.stream_forward(cq["x"], cq["sign"], cq["shift"], cq["bias"], k, d, 100, "q8_8", 0, 7)
+    assert np.array_equal(H, Hs) and np.array_equal(S, Ss)
+
+
+@pytest.mark.parametrize("k,d", [(4, 3), (2, 5), (6, 1)])
+def test_receptive_field_is_exactly_the_ring_length(orc, k, d):
+    """H[t] depends on x[t - (k-1)d] and on nothing older (every tap is a
+    nonzero power of two), so (k-1)d + 1 inputs are the smallest history a
+    step-by-step neuron can keep."""
+    R = orc.stream_ring_steps(k, d)
+    assert R == (k - 1) * d + 1
+    T = R + 6
+    c = small_case(T=T, N=1, C=2, S=1, k=k, seed=3)
+    x = c["x"].astype(np.float32)
+    H0, _ = orc.forward_f32(x, c["sign"], c["shift"], c["bias"], k, d, 0.0, 0, 4)
+    t = T - 1
+    for age, changes in ((R - 1, True), (R, False), (R + 3, False)):
+        x1 = x.copy()
+        x1[t - age] += np.float32(64.0)
+        H1, _ = orc.forward_f32(x1, c["sign"], c["shift"], c["bias"], k, d, 0.0, 0, 4)
+        assert bool(np.any(H1[t] != H0[t])) == changes, (age, changes)
