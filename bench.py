@@ -168,6 +168,88 @@ def memory_ceiling(torch, dev, wl):
     print(json.dumps({"memory_ceiling": res, "elements": n, "workload": wl.name}), flush=True)
 
 
+def stream_inference(torch, dev, wl, case, reps: int, warmup: int):
+    """Step-by-step inference of the workload's layers (one per dilation, each
+    with its own input sequence): for t = 0..T-1, one mfpsn_stream_step per
+    layer, each layer on its own history ring of (k-1)d+1 steps.  The whole
+    sequence is captured once in a HIP graph (no slot of a fresh ring is read
+    before it is written, so every replay recomputes the sequence) and
+    replayed; value = layers * T * N*C*S / replay time."""
+    from paper_2501_14490_amd import mfpsn
+
+    def dev_tensor(a, storage):
+        if wl.dtype == "bf16" and storage:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x0 = dev_tensor(case["x"], True)
+    sign, shift, bias = (dev_tensor(case[n], False) for n in ("sign", "shift", "bias"))
+    es = {"f32": 4, "bf16": 2, "q8_8": 2}[wl.dtype]
+    M = wl.N * wl.C * wl.S
+    layers, alg_bytes, ring_bytes = [], 0, 0
+    for li, d in enumerate(wl.dilations):
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        x = torch.roll(x0, shifts=7 * li, dims=1).contiguous() if li else x0
+        st = mfpsn.StreamState(desc, x.shape[1:], sign, shift, bias)
+        ring_bytes += st.ring.numel() * st.ring.element_size()
+        spikes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
+        layers.append((st, x, spikes))
+        # per step: read x_t, store it in the ring, read the older inputs the
+        # taps reach (fewer at the start), write the spike byte
+        alg_bytes += sum(M * (2 * es + min(wl.k - 1, t // d) * es + 1) for t in range(wl.T))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+
+    def sequence():
+        for st, _, _ in layers:
+            st.t = 0
+        for t in range(wl.T):
+            for st, x, spikes in layers:
+                st.step(x[t], stream=side, out=(spikes[t], None))
+
+    with torch.cuda.stream(side):
+        sequence()  # eager run (also loads the kernels)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            sequence()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    e0, e1 = hev.new(), hev.new()
+    cur = torch.cuda.current_stream()
+    hev.record(e0, cur)
+    for _ in range(reps):
+        g.replay()
+    hev.record(e1, cur)
+    torch.cuda.synchronize()
+    ms = hev.elapsed_ms(e0, e1) / reps
+    P = len(wl.dilations)
+    calls = P * wl.T
+    value = calls * M / (ms * 1e-3)
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    log(f"stream inference: {ms * 1e3:.1f} us per sequence ({calls} steps, {ms * 1e3 / calls:.2f} us/step), "
+        f"{value / 1e9:.2f} G elements/s, {achieved:.0f} GB/s of step traffic")
+    print(json.dumps({
+        "metric": "step-by-step inference elements/s (T*N*C*S per layer)",
+        "value": value, "unit": "elements/s", "n_gpus": 1, "steps": reps, "warmup": warmup,
+        "ms_per_sequence": ms, "higher_is_better": True, "dtype": {"f32": "f32", "bf16": "bf16",
+                                                                   "q8_8": "int16 Q8.8 / int32"}[wl.dtype],
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: x[{','.join(map(str, wl.shape))}] {wl.dtype}, k={wl.k}, one layer "
+                               f"per d={wl.dilations}, one mfpsn_stream_step per layer and time step, "
+                               f"the sequence replayed from a HIP graph",
+                   "calls_per_sequence": calls, "ring_bytes_all_layers": ring_bytes},
+        "step_traffic": {"alg_bytes_per_sequence": alg_bytes, "achieved_GBs": achieved,
+                         "us_per_step": ms * 1e3 / calls,
+                         "note": "the rings are small enough to stay in the on-chip caches"},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -183,6 +265,9 @@ def main():
                          "workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--stream-inference", action="store_true",
+                    help="only time step-by-step inference (mfpsn_stream_step per layer and time step, "
+                         "the sequence replayed from a HIP graph)")
     ap.add_argument("--memory-ceiling", action="store_true",
                     help="only time plain library streams of the workload's size (1 read + 1 write, "
                          "3 reads + 1 write): the bandwidth a kernel with that mix can reach")
@@ -221,6 +306,9 @@ def main():
     t0 = time.time()
     case = workloads.make_inputs(wl)
     log(f"inputs drawn in {time.time() - t0:.1f}s")
+    if args.stream_inference:
+        stream_inference(torch, dev, wl, case, args.steps, args.warmup)
+        return
 
     def dev_tensor(a, storage):
         if wl.dtype == "bf16" and storage:

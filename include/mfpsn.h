@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 3
+#define MFPSN_ABI_VERSION 4
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -164,6 +164,36 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
  * The gradient of the latent weight is grad_w itself (straight-through). */
 int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int32_t shift_hi,
                            int8_t* sign, int8_t* shift, void* stream);
+
+/* Step-by-step (streaming) inference: one time step of the charge
+ * (Eq. mfdpsn_charge) and fire (Eq. mfdpsn_fire) per call, for inputs that
+ * arrive one step at a time (the sliding PSN emits H[t] at step t, Sec. 3.2;
+ * the input history it stores grows with the order, Sec. 5, Table
+ * "inference memory").  The neuron keeps the last (k-1)*dilation + 1 inputs
+ * of every column, its receptive field, in a history ring owned by the
+ * caller:
+ *   ring : [R][N][C][S] storage type of desc->dtype, R = (k-1)*dilation + 1;
+ *          the input of time tau is in slot tau mod R.  Never read before it
+ *          is written, so it needs no initialization.
+ * mfpsn_stream_ring_bytes writes R to *steps and the ring's size in bytes to
+ * *bytes (either pointer may be NULL, not both).  desc->T is ignored by both
+ * streaming calls; every other field means what it means above.
+ *
+ * mfpsn_stream_step, for time step t >= 0:
+ *   x_t      : [N][C][S] storage type of desc->dtype, the inputs of time t;
+ *              stored into ring slot t mod R
+ *   spikes_t : uint8 [N][C][S];  h_t : optional (NULL) float / int32 [N][C][S]
+ *   H_t = sum over taps i with t-(k-1-i)d >= 0 of sign*2^-shift*x[t-(k-1-i)d]
+ *         + bias, in the same order and arithmetic as mfpsn_forward, so
+ *   calls for t = 0, 1, ..., T-1 (in that order, on one stream, on one ring)
+ *   give mfpsn_forward's spikes and H over the sequence bit for bit.
+ * The call reads the ring slots of times t-d, t-2d, ..., so steps of one ring
+ * must not overlap: issue them in order on one stream.  Errors: t < 0 is
+ * MFPSN_ERR_PARAM; alignment as for mfpsn_forward (ring like x). */
+int mfpsn_stream_ring_bytes(const mfpsn_desc* desc, int32_t* steps, size_t* bytes);
+int mfpsn_stream_step(const mfpsn_desc* desc, int64_t t, const void* x_t, void* ring,
+                      const int8_t* sign, const int8_t* shift, const void* bias,
+                      uint8_t* spikes_t, void* h_t, void* stream);
 
 /* Sawtooth dilation of layer `layer` (0-based) for a period P (Sec. 4.1,
  * Eq. d with P = 3): d^0 = 1, d^{l+1} = d^l mod P + 1, i.e. (layer mod P) + 1.

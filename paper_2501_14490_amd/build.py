@@ -52,6 +52,10 @@ def _units():
             units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
                                 f"-DMFPSN_TU_DTYPE={dt}", f"-DMFPSN_TU_KLO={lo}",
                                 f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj], [src, *headers]))
+    stream_src = os.path.join(CSRC, "mfpsn_stream.hip")
+    obj = os.path.join(BUILD, "stream.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", stream_src, "-o", obj],
+                  [stream_src, os.path.join(CSRC, "mfpsn_stream.h"), *headers]))
     obj = os.path.join(BUILD, "kernels_misc.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
                         "-c", src, "-o", obj], [src, *headers]))
@@ -59,7 +63,7 @@ def _units():
         obj = os.path.join(BUILD, name.replace(".cpp", ".o"))
         cpp = os.path.join(CSRC, name)
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
-                      [cpp, *headers]))
+                      [cpp, os.path.join(CSRC, "mfpsn_stream.h"), *headers]))
     return units
 
 

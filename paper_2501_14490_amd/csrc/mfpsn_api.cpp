@@ -10,6 +10,7 @@
 #include <initializer_list>
 
 #include "mfpsn_internal.h"
+#include "mfpsn_stream.h"
 
 using namespace mfpsn;
 
@@ -83,6 +84,20 @@ int validate(const mfpsn_desc* d)
         return MFPSN_ERR_PARAM;
     return MFPSN_OK;
 }
+
+// The streaming step looks at one time step: the descriptor's T plays no
+// part, every other field is checked as for the whole-sequence calls.
+int validate_stream(const mfpsn_desc* d)
+{
+    if (!d)
+        return MFPSN_ERR_NULL;
+    mfpsn_desc one = *d;
+    one.T = 0;
+    return validate(&one);
+}
+
+// History slots of the streaming step: the receptive field (k-1)*d + 1.
+int64_t ring_steps(const mfpsn_desc* d) { return (int64_t)(d->k - 1) * d->dilation + 1; }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -360,6 +375,67 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     f.grad_w = grad_w;
     f.grad_b = grad_b;
     if (launch_finalize(f, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_stream_ring_bytes(const mfpsn_desc* desc, int32_t* steps, size_t* bytes)
+{
+    int st = validate_stream(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (!steps && !bytes)
+        return MFPSN_ERR_NULL;
+    const int64_t R = ring_steps(desc);
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    if (steps)
+        *steps = (int32_t)R;
+    if (bytes)
+        *bytes = (size_t)R * (size_t)M * (size_t)elem_bytes(desc->dtype);
+    return MFPSN_OK;
+}
+
+int mfpsn_stream_step(const mfpsn_desc* desc, int64_t t, const void* x_t, void* ring, const int8_t* sign,
+                      const int8_t* shift, const void* bias, uint8_t* spikes_t, void* h_t, void* stream)
+{
+    int st = validate_stream(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (t < 0)
+        return MFPSN_ERR_PARAM;
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    if (M > 0 && (!x_t || !ring || !spikes_t))
+        return MFPSN_ERR_NULL;
+    if (desc->C > 0 && (!sign || !shift || !bias))
+        return MFPSN_ERR_NULL;
+    const int es = elem_bytes(desc->dtype);
+    if (!aligned(x_t, es) || !aligned(ring, es) || !aligned(bias, 4) || !aligned(h_t, 4))
+        return MFPSN_ERR_ALIGN;
+    if (M == 0)
+        return MFPSN_OK;
+    const int64_t R = ring_steps(desc);
+    StreamArgs a;
+    a.M = M;
+    a.C = desc->C;
+    a.S = desc->S;
+    a.k = desc->k;
+    a.d = desc->dilation;
+    a.R = (int32_t)R;
+    a.slot = (int32_t)(t % R);
+    const int64_t reach = t / desc->dilation;  // taps that look back at most t steps
+    a.m_max = (int32_t)(reach < desc->k - 1 ? reach : desc->k - 1);
+    a.shift_lo = desc->shift_lo;
+    a.shift_hi = desc->shift_hi;
+    a.v_th = desc->v_th;
+    a.v_th_q = desc->v_th_q;
+    a.x_t = x_t;
+    a.ring = ring;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.spikes = spikes_t;
+    a.h_t = h_t;
+    if (launch_stream_step(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
 }

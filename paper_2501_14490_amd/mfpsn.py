@@ -59,6 +59,10 @@ _lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
+_lib.mfpsn_stream_ring_bytes.argtypes = [_DP, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
+_lib.mfpsn_stream_ring_bytes.restype = ctypes.c_int
+_lib.mfpsn_stream_step.argtypes = [_DP, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_stream_step.restype = ctypes.c_int
 _lib.mfpsn_sawtooth_dilation.argtypes = [ctypes.c_int32, ctypes.c_int32]
 _lib.mfpsn_sawtooth_dilation.restype = ctypes.c_int32
 _lib.mfpsn_status_string.argtypes = [ctypes.c_int]
@@ -148,6 +152,21 @@ def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=
                                        _ptr(shift), _stream(stream)), "mfpsn_quantize_weights")
 
 
+def mfpsn_stream_ring_bytes(desc: MfpsnDesc):
+    """(ring slots R = (k-1)*dilation + 1, ring size in bytes)."""
+    steps = ctypes.c_int32(0)
+    n = ctypes.c_size_t(0)
+    _check(_lib.mfpsn_stream_ring_bytes(ctypes.byref(desc), ctypes.byref(steps), ctypes.byref(n)),
+           "mfpsn_stream_ring_bytes")
+    return int(steps.value), int(n.value)
+
+
+def mfpsn_stream_step(desc: MfpsnDesc, t: int, x_t, ring, sign, shift, bias, spikes_t, h_t=None,
+                      stream=None) -> None:
+    _check(_lib.mfpsn_stream_step(ctypes.byref(desc), int(t), _ptr(x_t), _ptr(ring), _ptr(sign), _ptr(shift),
+                                  _ptr(bias), _ptr(spikes_t), _ptr(h_t), _stream(stream)), "mfpsn_stream_step")
+
+
 # ---------------------------------------------------------------------------
 # allocating wrappers
 # ---------------------------------------------------------------------------
@@ -201,6 +220,36 @@ def quantize(w, shift_lo: int, shift_hi: int, stream=None):
     shift = torch.empty(w.shape, dtype=torch.int8, device=w.device)
     mfpsn_quantize_weights(w, shift_lo, shift_hi, sign, shift, stream)
     return sign, shift
+
+
+class StreamState:
+    """Step-by-step inference of one neuron layer: owns the history ring of
+    the last (k-1)*dilation + 1 inputs ([R, N, C, *spatial], the storage type
+    of the layer) and the time index.  ``step(x_t)`` consumes the inputs of
+    the next time step ([N, C, *spatial]) and returns its spikes (and H with
+    want_h); over a sequence this equals ``forward`` bit for bit.  The ring
+    needs no initialization: no slot is read before it is written."""
+
+    def __init__(self, desc: MfpsnDesc, spatial_shape, sign, shift, bias, device=None):
+        self.desc = desc
+        self.shape = tuple(int(v) for v in spatial_shape)  # (N, C, *spatial)
+        self.steps, nbytes = mfpsn_stream_ring_bytes(desc)
+        dev = torch.device(device) if device is not None else bias.device
+        self.ring = torch.empty((self.steps,) + self.shape, dtype=STORAGE[desc.dtype], device=dev)
+        assert self.ring.numel() * self.ring.element_size() == nbytes
+        self.sign, self.shift, self.bias = sign, shift, bias
+        self.t = 0
+
+    def step(self, x_t, want_h: bool = False, stream=None, out=None):
+        _expect(x_t, STORAGE[self.desc.dtype], self.ring.device, "x_t")
+        if tuple(x_t.shape) != self.shape:
+            raise ValueError(f"x_t must have shape {self.shape}, got {tuple(x_t.shape)}")
+        spikes, h = out if out is not None else (
+            torch.empty(self.shape, dtype=torch.uint8, device=x_t.device),
+            torch.empty(self.shape, dtype=H_OUT[self.desc.dtype], device=x_t.device) if want_h else None)
+        mfpsn_stream_step(self.desc, self.t, x_t, self.ring, self.sign, self.shift, self.bias, spikes, h, stream)
+        self.t += 1
+        return (spikes, h) if want_h else spikes
 
 
 class MfPSNFunction(torch.autograd.Function):

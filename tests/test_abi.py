@@ -41,6 +41,8 @@ def lib():
     L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    L.mfpsn_stream_ring_bytes.argtypes = [DP, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
+    L.mfpsn_stream_step.argtypes = [DP, ctypes.c_int64, P, P, P, P, P, P, P, P]
     L.mfpsn_status_string.restype = ctypes.c_char_p
     return L
 
@@ -67,7 +69,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 3
+    assert lib.mfpsn_abi_version() == 4
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -157,3 +159,35 @@ def test_workspace_grows_with_problem(lib):
     # bounded by the resident-grid limit, not by the problem: per-block
     # partial rows stay well below the size of x
     assert sizes[-1] < 250 * 256 * 512 * 4 // 4
+
+
+@pytest.mark.parametrize("k,d,dtype,es", [(4, 2, 0, 4), (16, 4, 0, 4), (8, 3, 1, 2), (32, 8, 2, 2), (1, 5, 0, 4)])
+def test_stream_ring_size(lib, k, d, dtype, es):
+    """The ring holds the receptive field, (k-1)d + 1 steps of N*C*S inputs."""
+    desc = good_desc(T=-7 if k == 1 else 0, k=k, dilation=d, dtype=dtype, N=3, C=5, S=7)  # T is ignored
+    steps, n = ctypes.c_int32(0), ctypes.c_size_t(0)
+    assert lib.mfpsn_stream_ring_bytes(ctypes.byref(desc), ctypes.byref(steps), ctypes.byref(n)) == 0
+    assert steps.value == (k - 1) * d + 1
+    assert n.value == steps.value * 3 * 5 * 7 * es
+    assert lib.mfpsn_stream_ring_bytes(ctypes.byref(desc), None, None) == -1
+
+
+def test_stream_step_validation(lib):
+    d = good_desc()
+    args = [FAKE] * 7  # x_t, ring, sign, shift, bias, spikes_t, h_t
+    assert lib.mfpsn_stream_step(None, 0, *args, None) == -1
+    assert lib.mfpsn_stream_step(ctypes.byref(d), -1, *args, None) == -3
+    for i in (0, 1, 5):  # x_t, ring, spikes_t
+        bad = list(args)
+        bad[i] = None
+        assert lib.mfpsn_stream_step(ctypes.byref(d), 3, *bad, None) == -1
+    bad = list(args)
+    bad[1] = FAKE + 2  # misaligned float ring
+    assert lib.mfpsn_stream_step(ctypes.byref(d), 3, *bad, None) == -6
+    bad = list(args)
+    bad[6] = FAKE + 1  # misaligned h_t
+    assert lib.mfpsn_stream_step(ctypes.byref(d), 3, *bad, None) == -6
+    e = good_desc(k=40)
+    assert lib.mfpsn_stream_step(ctypes.byref(e), 3, *args, None) == -3
+    z = good_desc(N=0)
+    assert lib.mfpsn_stream_step(ctypes.byref(z), 3, None, None, FAKE, FAKE, FAKE, None, None, None) == 0
