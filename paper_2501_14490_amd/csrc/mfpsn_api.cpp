@@ -424,6 +424,12 @@ int mfpsn_stream_step(const mfpsn_desc* desc, int64_t t, const void* x_t, void* 
     a.slot = (int32_t)(t % R);
     const int64_t reach = t / desc->dilation;  // taps that look back at most t steps
     a.m_max = (int32_t)(reach < desc->k - 1 ? reach : desc->k - 1);
+    for (int m = 0; m < MFPSN_MAX_K; ++m) {
+        int64_t sl = m < desc->k ? a.slot - (int64_t)m * desc->dilation : 0;  // >= -(R-1)
+        if (sl < 0)
+            sl += R;
+        a.rows[m] = sl * M;
+    }
     a.shift_lo = desc->shift_lo;
     a.shift_hi = desc->shift_hi;
     a.v_th = desc->v_th;

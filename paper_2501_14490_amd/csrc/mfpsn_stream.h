@@ -5,6 +5,7 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "mfpsn.h"
 #include "mfpsn_internal.h"
 
 namespace mfpsn {
@@ -15,6 +16,8 @@ struct StreamArgs {
     int32_t R;           // ring slots, (k-1)*d + 1
     int32_t slot;        // t mod R: the slot x_t is stored in
     int32_t m_max;       // min(k-1, t/d): taps looking back more than t steps are left out
+    int64_t rows[MFPSN_MAX_K];  // element offset of the ring row of time t - m*d (slot mod R) for
+                                // m < k; rows[0] is x_t's slot
     int32_t shift_lo, shift_hi;
     float v_th;
     int32_t v_th_q;
