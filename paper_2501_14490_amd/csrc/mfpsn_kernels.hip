@@ -94,13 +94,24 @@ constexpr int prefetch_depth(int K, int cap)
 #ifndef MFPSN_BWD_PREFETCH
 #define MFPSN_BWD_PREFETCH 2
 #endif
+#ifndef MFPSN_BWD_PREFETCH_HIGH_K
+#define MFPSN_BWD_PREFETCH_HIGH_K 8
+#endif
 #ifndef MFPSN_BWD_PAIR_BYTES
 #define MFPSN_BWD_PAIR_BYTES 16
 #endif
 constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
 constexpr int kFwdPrefetchF32Pair = MFPSN_FWD_PREFETCH_F32_PAIR;
 constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
+constexpr int kBwdPrefetchHighK = MFPSN_BWD_PREFETCH_HIGH_K;  // orders 24 and up
 constexpr int kBwdPairBytes = MFPSN_BWD_PAIR_BYTES;  // plane mode, two columns per lane
+
+// Highest order built with unguarded full blocks (higher orders walk only
+// guarded blocks: smaller code, a few scalar instructions more per step).
+#ifndef MFPSN_FULL_BLOCK_MAX_K
+#define MFPSN_FULL_BLOCK_MAX_K 16
+#endif
+constexpr int kFullBlockMaxK = MFPSN_FULL_BLOCK_MAX_K;
 
 template <int V> using ic = std::integral_constant<int, V>;
 enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 };
@@ -831,7 +842,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             block(0, ic<kEdge>{});
             ++b;
         }
-        if constexpr (K <= 16) {
+        if constexpr (K <= kFullBlockMaxK) {
             // full blocks: every step below j1, every prefetch inside the class
             const int bfull = min(j1 / K, (Lr - P) / K);
             for (; b < bfull; ++b)
@@ -875,11 +886,12 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     constexpr int es = IO<DT>::es;
     // Lane-channel waves at orders up to 16 run 4 per SIMD and stream three
     // 256-byte rows per step: a short queue is best.  Plane waves (narrower
-    // rows) want a longer one, and high orders (2 waves per SIMD) a deep one.
+    // rows) want a longer one, and high orders 8 steps (which keeps the Q8.8
+    // order-32 saved-factor kernel at two waves per SIMD).
     // Lanes holding two columns do best with about 16 bytes per stream in
     // flight (2 steps of f32 pairs, 4 of bf16 or Q8.8 pairs).
     constexpr int P = prefetch_depth(
-        K, K >= 24 ? 8 * kBwdPrefetch
+        K, K >= 24 ? kBwdPrefetchHighK
                    : (MODE == kLaneChannel ? kBwdPrefetch
                                            : (NV == 2 ? kBwdPairBytes / (es * NV) : 2 * kBwdPrefetch)));
     constexpr int gxs = IO<DT>::gx_es;
@@ -1207,7 +1219,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         int b = jstart / K;
         const int blo = j0 / K;
         const int bmin = max(blo, 1);
-        if constexpr (K <= 16) {
+        if constexpr (K <= kFullBlockMaxK) {
             const int bf_hi = (min(jtop, j1 - 1) - (K - 1)) / K;
             const int bf_lo = max(bmin, (jb + P + 2 * K - 2) / K);
             for (; b > bf_hi && b >= bmin; --b)
@@ -1394,20 +1406,31 @@ int resident_blocks(Kern kern, int (&cache)[16])
     return cache[slot];
 }
 
-// Persistent grid with equal shares: the fewest rounds of items the resident
-// waves allow, then the fewest blocks that still finish in that many rounds
-// (so every wave gets the same number of items, up to one), never more than
-// the planner's bound.
-inline int persistent_blocks(const Geom& g, int resident)
+// Persistent grid, never more blocks than the planner's bound; waves own
+// contiguous ranges of items that differ by at most one.
+//   fill = false (forward): equal shares, the fewest rounds of items the
+//     resident waves allow, then the fewest blocks that still finish in that
+//     many rounds (fewer waves streaming at once measured faster there);
+//   fill = true (backward): every resident wave slot of the group's share of
+//     the GPU (up to one wave per item).  That never raises the largest
+//     share, and a SIMD with more waves issues faster: one wave alone issues
+//     at most one VALU instruction every few cycles and cannot cover its own
+//     dependency latencies (order-32 Q8.8 backward: 384 -> 304 us).
+inline int persistent_blocks(const Geom& g, int resident, bool fill)
 {
     int64_t per_group = resident / g.groups;
     if (per_group < 1)
         per_group = 1;
     if (per_group > g.blocks)
         per_group = g.blocks;
-    const int64_t waves_max = per_group * kWaves;
-    const int64_t rounds = (g.items + waves_max - 1) / waves_max;
-    int64_t blocks = (g.items + rounds * kWaves - 1) / (rounds * kWaves);
+    int64_t blocks;
+    if (fill) {
+        blocks = (g.items + kWaves - 1) / kWaves;
+    } else {
+        const int64_t waves_max = per_group * kWaves;
+        const int64_t rounds = (g.items + waves_max - 1) / waves_max;
+        blocks = (g.items + rounds * kWaves - 1) / (rounds * kWaves);
+    }
     if (blocks > per_group)
         blocks = per_group;
     return (int)(blocks > 0 ? blocks : 1);
@@ -1432,7 +1455,7 @@ hipError_t fwd_k(FwdArgs& a, hipStream_t st)
             slot = 1;
         }
     }
-    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[slot]));
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[slot]), false);
     hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
@@ -1467,7 +1490,7 @@ hipError_t bwd_k(BwdArgs& a, hipStream_t st)
                                                : bwd_kernel_for<K, DT, kRecompute>(a.g, slot);
     if (kern == nullptr)
         return hipErrorInvalidValue;
-    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[hs][slot]));
+    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[hs][slot]), true);
     hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
