@@ -9,6 +9,8 @@ the passage of the paper it follows in the C source.
 Functions whose results are pinned, and by what (see ``tests/test_oracle_pins.py``
 and ``tests/test_golden.py``):
   quantize        exact rational arithmetic (Fraction) around 2^(m+1/2)
+  quantizer_grad  Eq. ste_q's factor times |W| is |Wq| (exact rational check),
+                  power-of-two weights are fixed points, evenness in W
   forward_*       k=1 closed form, np.convolve (sliding PSN), dense Toeplitz
                   matrix of App. A.2, causality, time-shift, zero input,
                   power-of-two scaling, Fraction brute force, the op counts of
@@ -81,6 +83,8 @@ def _load():
             lib.orc_backward_q88.argtypes = [P, P, *geo, P, P, i32, i32, P, ctypes.c_int32, i32, f32,
                                              P, P, P, P, P]
             lib.orc_backward_q88.restype = None
+            lib.orc_quantizer_grad.argtypes = [P, P, i32, i32, P, i64, i32, P]
+            lib.orc_quantizer_grad.restype = None
             lib.orc_stream_step_f32.argtypes = [P, i32, i32, i32, i32, i32, i64, P, P, P, i32, i32, P, f32,
                                                 P, P]
             lib.orc_stream_step_f32.restype = None
@@ -164,6 +168,18 @@ def quantize(w, shift_lo: int, shift_hi: int):
     shift = np.empty(w.shape, np.int8)
     _load().orc_quantize(_ptr(w), w.size, int(shift_lo), int(shift_hi), _ptr(sign), _ptr(shift))
     return sign, shift
+
+
+def quantizer_grad(w, shift, grad_wq, mode: int, shift_lo: int, shift_hi: int) -> np.ndarray:
+    """grad of the latent weight: mode 0 whole-quantizer STE (identity),
+    mode 1 round-only STE (grad_wq * 2^-shift / |w|, Eq. ste_q)."""
+    w = _c(w, np.float32)
+    shift = _c(shift, np.int8).reshape(w.shape)
+    g = _c(grad_wq, np.float32).reshape(w.shape)
+    out = np.empty(w.shape, np.float32)
+    _load().orc_quantizer_grad(_ptr(w), _ptr(shift), int(shift_lo), int(shift_hi), _ptr(g), int(w.size),
+                               int(mode), _ptr(out))
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -160,6 +160,36 @@ void orc_quantize(const float* w, int64_t count, int lo, int hi, int8_t* sign, i
     }
 }
 
+/* Gradient of the latent weight from the gradient of the quantized weight
+ * (Sec. 4.2).  mode 0, the whole-quantizer straight-through estimator the
+ * paper trains with: dWq/dW = 1, so grad_w = grad_wq.  mode 1, the estimator
+ * that only replaces round()'s derivative by 1 (Eq. ste, Eq. ste_q):
+ * dWq/dW = 2^round(log2|W|) / |W| = |Wq| / |W|, with |Wq| = 2^-shift (the
+ * clamped shift the quantizer chose), so grad_w = grad_wq * (2^-shift / |W|),
+ * each operation one correctly rounded float operation in that order.  Where
+ * the factor is undefined or not finite (W = 0, W not finite) grad_w is 0. */
+void orc_quantizer_grad(const float* w, const int8_t* shift, int lo, int hi, const float* grad_wq,
+                        int64_t count, int mode, float* grad_w)
+{
+    for (int64_t j = 0; j < count; ++j) {
+        if (mode == 0) {
+            grad_w[j] = grad_wq[j];
+            continue;
+        }
+        const float a = fabsf(w[j]);
+        if (!(a > 0.0f) || isinf(a)) {
+            grad_w[j] = 0.0f;
+            continue;
+        }
+        int s = shift[j];
+        if (s < lo) s = lo;
+        if (s > hi) s = hi;
+        const float q = ldexpf(1.0f, -s);   /* |Wq|, exact */
+        const float f = q / a;              /* rounded once */
+        grad_w[j] = isfinite(f) ? grad_wq[j] * f : 0.0f;
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Forward: charge (Eq. mfdpsn_charge) + fire (Eq. mfdpsn_fire).             */
 /* ------------------------------------------------------------------------ */

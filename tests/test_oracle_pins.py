@@ -561,3 +561,51 @@ def test_receptive_field_is_exactly_the_ring_length(orc, k, d):
         x1[t - age] += np.float32(64.0)
         H1, _ = orc.forward_f32(x1, c["sign"], c["shift"], c["bias"], k, d, 0.0, 0, 4)
         assert bool(np.any(H1[t] != H0[t])) == changes, (age, changes)
+
+
+# ---------------------------------------------------------------------------
+# gradients of the quantizer (Sec. 4.2: Eq. ste, Eq. ste_q, and the
+# whole-quantizer straight-through estimator the paper trains with)
+# ---------------------------------------------------------------------------
+def test_quantizer_grad_whole_ste_is_identity(orc):
+    rng = np.random.default_rng(4)
+    w = rng.normal(0, 1, 200).astype(np.float32)
+    g = rng.normal(0, 1, 200).astype(np.float32)
+    _, shift = orc.quantize(w, -10, 10)
+    assert np.array_equal(orc.quantizer_grad(w, shift, g, 0, -10, 10), g)
+
+
+def test_quantizer_grad_round_only_factor_is_wq_over_w(orc):
+    """Eq. ste_q: Q'(W) = 2^round(log2|W|)/|W|.  The factor is one rounded
+    division, so factor*|W| lies within half an ulp of the factor (times |W|)
+    of |Wq| = 2^round(log2|W|), the exactly rounded power of two (checked
+    with rational arithmetic); it is even in W; powers of two inside the
+    shift range are fixed points (factor 1)."""
+    rng = np.random.default_rng(5)
+    w = (rng.normal(0, 1, 400) * np.exp2(rng.integers(-6, 6, 400))).astype(np.float32)
+    w[:10] = np.ldexp(1.0, -np.arange(10)).astype(np.float32)
+    ones = np.ones_like(w)
+    lo, hi = -20, 20
+    _, shift = orc.quantize(w, lo, hi)
+    fac = orc.quantizer_grad(w, shift, ones, 1, lo, hi)
+    for wi, f in zip(w, fac):
+        m = math.frexp(abs(float(wi)))[1] - 1        # |w| = f 2^m, f in [1, 2)
+        e = m + (1 if Fraction(abs(float(wi))) ** 2 >= Fraction(2) ** (2 * m + 1) else 0)
+        exact = Fraction(2) ** e / Fraction(abs(float(wi)))
+        ulp = Fraction(2) ** (math.frexp(float(f))[1] - 24)
+        assert abs(Fraction(float(f)) - exact) <= ulp / 2, (wi, f)
+    assert np.all(fac[:10] == 1.0)
+    assert np.array_equal(orc.quantizer_grad(-w, shift, ones, 1, lo, hi), fac)
+    g = rng.normal(0, 1, 400).astype(np.float32)
+    assert np.array_equal(orc.quantizer_grad(w, shift, g, 1, lo, hi), (g * fac).astype(np.float32))
+
+
+def test_quantizer_grad_round_only_special_values(orc):
+    w = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, 3.0], np.float32)
+    _, shift = orc.quantize(w, 0, 7)
+    out = orc.quantizer_grad(w, shift, np.ones_like(w), 1, 0, 7)
+    assert np.all(out[:5] == 0.0)
+    # 1e-45 is far below 2^-7: the clamped |Wq| = 2^-7 over |W| overflows -> 0
+    assert out[5] == 0.0
+    # Q(3) rounds to 4 (shift -2), clamped into [0, 7] to shift 0: |Wq| = 1, factor 1/3
+    assert out[6] == np.float32(1.0) / np.float32(3.0)
