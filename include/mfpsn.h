@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 4
+#define MFPSN_ABI_VERSION 5
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -164,6 +164,22 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
  * The gradient of the latent weight is grad_w itself (straight-through). */
 int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int32_t shift_hi,
                            int8_t* sign, int8_t* shift, void* stream);
+
+/* Gradient of the latent weight from the gradient of the quantized weight
+ * (Sec. 4.2), elementwise over `count` (< 2^31) weights, device memory:
+ *   MFPSN_STE_WHOLE : the whole-quantizer straight-through estimator the paper
+ *                     trains with, dWq/dW = 1: grad_w = grad_wq (w, shift unused)
+ *   MFPSN_STE_ROUND : only round()'s derivative replaced by 1 (Eq. ste), so
+ *                     dWq/dW = 2^round(log2|W|)/|W| = |Wq|/|W| (Eq. ste_q):
+ *                     grad_w = grad_wq * (2^-shift / |w|), shift clamped into
+ *                     [shift_lo, shift_hi] as by the quantizer; the quotient and
+ *                     the product each rounded once; 0 where w = 0, w is not
+ *                     finite or the quotient overflows.
+ * w, grad_wq, grad_w: float [count]; shift: int8 [count] (from
+ * mfpsn_quantize_weights).  grad_w may alias grad_wq. */
+enum { MFPSN_STE_WHOLE = 0, MFPSN_STE_ROUND = 1 };
+int mfpsn_quantizer_grad(const float* w, const int8_t* shift, int32_t shift_lo, int32_t shift_hi,
+                         const float* grad_wq, int64_t count, int32_t mode, float* grad_w, void* stream);
 
 /* Step-by-step (streaming) inference: one time step of the charge
  * (Eq. mfdpsn_charge) and fire (Eq. mfdpsn_fire) per call, for inputs that

@@ -52,6 +52,10 @@ def _units():
             units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
                                 f"-DMFPSN_TU_DTYPE={dt}", f"-DMFPSN_TU_KLO={lo}",
                                 f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj], [src, *headers]))
+    qg_src = os.path.join(CSRC, "mfpsn_qgrad.hip")
+    obj = os.path.join(BUILD, "qgrad.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
+                  [qg_src, os.path.join(CSRC, "mfpsn_qgrad.h")]))
     stream_src = os.path.join(CSRC, "mfpsn_stream.hip")
     obj = os.path.join(BUILD, "stream.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", stream_src, "-o", obj],
@@ -63,7 +67,8 @@ def _units():
         obj = os.path.join(BUILD, name.replace(".cpp", ".o"))
         cpp = os.path.join(CSRC, name)
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
-                      [cpp, os.path.join(CSRC, "mfpsn_stream.h"), *headers]))
+                      [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
+                       *headers]))
     return units
 
 

@@ -10,6 +10,7 @@
 #include <initializer_list>
 
 #include "mfpsn_internal.h"
+#include "mfpsn_qgrad.h"
 #include "mfpsn_stream.h"
 
 using namespace mfpsn;
@@ -375,6 +376,23 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     f.grad_w = grad_w;
     f.grad_b = grad_b;
     if (launch_finalize(f, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_quantizer_grad(const float* w, const int8_t* shift, int32_t shift_lo, int32_t shift_hi,
+                         const float* grad_wq, int64_t count, int32_t mode, float* grad_w, void* stream)
+{
+    if (count < 0 || count >= ((int64_t)1 << 31))
+        return MFPSN_ERR_SHAPE;
+    if (shift_lo > shift_hi || shift_lo < -128 || shift_hi > 127 || (mode != MFPSN_STE_WHOLE && mode != MFPSN_STE_ROUND))
+        return MFPSN_ERR_PARAM;
+    if (count > 0 && (!grad_wq || !grad_w || (mode == MFPSN_STE_ROUND && (!w || !shift))))
+        return MFPSN_ERR_NULL;
+    if (!aligned(w, 4) || !aligned(grad_wq, 4) || !aligned(grad_w, 4))
+        return MFPSN_ERR_ALIGN;
+    if (launch_quantizer_grad(w, shift, shift_lo, shift_hi, grad_wq, count, mode, grad_w, (hipStream_t)stream) !=
+        hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
 }

@@ -28,6 +28,8 @@ _lib = ctypes.CDLL(LIB_PATH)
 MFPSN_OK = 0
 MFPSN_F32, MFPSN_BF16, MFPSN_Q8_8 = 0, 1, 2
 MFPSN_SG_SIGMOID, MFPSN_SG_ATAN, MFPSN_SG_RATIONAL = 0, 1, 2
+MFPSN_STE_WHOLE, MFPSN_STE_ROUND = 0, 1
+STE = {"whole": MFPSN_STE_WHOLE, "round": MFPSN_STE_ROUND}
 MFPSN_MAX_K = 32
 
 DTYPES = {"f32": MFPSN_F32, "bf16": MFPSN_BF16, "q8_8": MFPSN_Q8_8}
@@ -59,6 +61,9 @@ _lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
+_lib.mfpsn_quantizer_grad.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int32, _P,
+                                      _P]
+_lib.mfpsn_quantizer_grad.restype = ctypes.c_int
 _lib.mfpsn_stream_ring_bytes.argtypes = [_DP, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
 _lib.mfpsn_stream_ring_bytes.restype = ctypes.c_int
 _lib.mfpsn_stream_step.argtypes = [_DP, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
@@ -152,6 +157,12 @@ def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=
                                        _ptr(shift), _stream(stream)), "mfpsn_quantize_weights")
 
 
+def mfpsn_quantizer_grad(w, shift, shift_lo: int, shift_hi: int, grad_wq, mode: int, grad_w, stream=None) -> None:
+    _check(_lib.mfpsn_quantizer_grad(_ptr(w), _ptr(shift), int(shift_lo), int(shift_hi), _ptr(grad_wq),
+                                     int(grad_wq.numel()), int(mode), _ptr(grad_w), _stream(stream)),
+           "mfpsn_quantizer_grad")
+
+
 def mfpsn_stream_ring_bytes(desc: MfpsnDesc):
     """(ring slots R = (k-1)*dilation + 1, ring size in bytes)."""
     steps = ctypes.c_int32(0)
@@ -222,6 +233,15 @@ def quantize(w, shift_lo: int, shift_hi: int, stream=None):
     return sign, shift
 
 
+def quantizer_grad(w, shift, grad_wq, ste="whole", shift_lo: int = 0, shift_hi: int = 7, stream=None):
+    """Latent-weight gradient: "whole" (the paper's whole-quantizer STE:
+    grad_wq unchanged) or "round" (Eq. ste_q: grad_wq * 2^-shift / |w|)."""
+    _expect(grad_wq, torch.float32, grad_wq.device, "grad_wq")
+    out = torch.empty_like(grad_wq)
+    mfpsn_quantizer_grad(w, shift, shift_lo, shift_hi, grad_wq, STE[ste], out, stream)
+    return out
+
+
 class StreamState:
     """Step-by-step inference of one neuron layer: owns the history ring of
     the last (k-1)*dilation + 1 inputs ([R, N, C, *spatial], the storage type
@@ -254,25 +274,39 @@ class StreamState:
 
 class MfPSNFunction(torch.autograd.Function):
     """spikes = Theta(conv_{Q(W)}(x) + b - v_th) with the surrogate-gradient
-    backward.  grad of W is the grad of Q(W) (whole-quantizer straight-through
-    estimator, Sec. 4.2); the grad of b is the per-channel dH sum.  Float
-    storage paths only (f32, bf16)."""
+    backward (Sec. 4.2, App. A.3).  Float storage paths (f32, bf16).
+
+    ste="whole" (default): the gradient of W is the gradient of Q(W) (the
+    whole-quantizer straight-through estimator the paper trains with);
+    ste="round": only round()'s derivative is replaced by 1, so the gradient
+    of W is that of Q(W) times |Q(W)|/|W| (Eq. ste_q).
+    v_th: a float, or a per-channel tensor [C] (the learnable channel-wise
+    threshold of Eq. mfdpsn_fire).  A per-channel threshold folds into the
+    bias, b - v_th, compared with 0; its gradient is minus the bias gradient."""
 
     @staticmethod
-    def forward(ctx, x, w, b, k, dilation, v_th, surrogate, alpha, shift_lo, shift_hi):
+    def forward(ctx, x, w, b, k, dilation, v_th, surrogate, alpha, shift_lo, shift_hi, ste="whole"):
         dtype = "bf16" if x.dtype == torch.bfloat16 else "f32"
-        desc = make_desc(x.shape, k, dilation, dtype, surrogate, alpha, v_th, 0, shift_lo, shift_hi)
-        sign, shift = quantize(w.detach().contiguous(), shift_lo, shift_hi)
-        xc = x.detach().contiguous()
+        per_channel = torch.is_tensor(v_th)
         bc = b.detach().float().contiguous()
+        if per_channel:
+            bc = (bc - v_th.detach().float().reshape(bc.shape)).contiguous()
+        desc = make_desc(x.shape, k, dilation, dtype, surrogate, alpha, 0.0 if per_channel else v_th, 0,
+                         shift_lo, shift_hi)
+        wc = w.detach().contiguous()
+        sign, shift = quantize(wc, shift_lo, shift_hi)
+        xc = x.detach().contiguous()
         spikes, sg = forward(desc, xc, sign, shift, bc, want_sg=True)
-        ctx.save_for_backward(xc, sign, shift, bc, sg)
-        ctx.desc = desc
+        ctx.save_for_backward(xc, wc, sign, shift, bc, sg)
+        ctx.desc, ctx.per_channel, ctx.ste = desc, per_channel, ste
+        ctx.shift_range = (shift_lo, shift_hi)
         return spikes.to(x.dtype)
 
     @staticmethod
     def backward(ctx, grad_spikes):
-        xc, sign, shift, bc, sg = ctx.saved_tensors
+        xc, wc, sign, shift, bc, sg = ctx.saved_tensors
         g = grad_spikes.to(xc.dtype).contiguous()
-        grad_x, grad_w, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, sg=sg)
-        return grad_x, grad_w, grad_b, None, None, None, None, None, None, None
+        grad_x, grad_wq, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, sg=sg)
+        grad_w = grad_wq if ctx.ste == "whole" else quantizer_grad(wc, shift, grad_wq, ctx.ste, *ctx.shift_range)
+        grad_vth = -grad_b if ctx.per_channel else None
+        return grad_x, grad_w, grad_b, None, None, grad_vth, None, None, None, None, None

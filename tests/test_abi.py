@@ -41,6 +41,7 @@ def lib():
     L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    L.mfpsn_quantizer_grad.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int64, ctypes.c_int32, P, P]
     L.mfpsn_stream_ring_bytes.argtypes = [DP, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_stream_step.argtypes = [DP, ctypes.c_int64, P, P, P, P, P, P, P, P]
     L.mfpsn_status_string.restype = ctypes.c_char_p
@@ -69,7 +70,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 4
+    assert lib.mfpsn_abi_version() == 5
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -191,3 +192,15 @@ def test_stream_step_validation(lib):
     assert lib.mfpsn_stream_step(ctypes.byref(e), 3, *args, None) == -3
     z = good_desc(N=0)
     assert lib.mfpsn_stream_step(ctypes.byref(z), 3, None, None, FAKE, FAKE, FAKE, None, None, None) == 0
+
+
+def test_quantizer_grad_validation(lib):
+    q = lib.mfpsn_quantizer_grad
+    assert q(FAKE, FAKE, 0, 7, FAKE, -1, 0, FAKE, None) == -2
+    assert q(FAKE, FAKE, 0, 7, FAKE, 10, 2, FAKE, None) == -3      # unknown mode
+    assert q(FAKE, FAKE, 5, 4, FAKE, 10, 1, FAKE, None) == -3
+    assert q(None, FAKE, 0, 7, FAKE, 10, 1, FAKE, None) == -1      # round-only needs w
+    assert q(FAKE, None, 0, 7, FAKE, 10, 1, FAKE, None) == -1      # ... and shift
+    assert q(FAKE, FAKE, 0, 7, None, 10, 0, FAKE, None) == -1
+    assert q(FAKE, FAKE, 0, 7, FAKE + 2, 10, 0, FAKE, None) == -6
+    assert q(None, None, 0, 7, None, 0, 1, None, None) == 0         # nothing to do
