@@ -20,6 +20,11 @@ and ``tests/test_golden.py``):
   surrogate, exp  closed forms at 0, symmetry, unit integral, 2-ulp bound
                   against double exp
   sawtooth        the printed sequence and receptive-field example of Sec. 4.1
+  bn_forward_stats, bn_backward
+                  numpy mean / biased variance of the latent convolution; the
+                  fusion identity s*(W*x) + (beta - s*mu) = BN(W*x); central
+                  finite differences of a smooth version of the whole fused
+                  step (quantizer taken as identity, Heaviside as a sigmoid)
   stream_forward  the (pinned) whole-sequence forward, bit for bit, from a
                   history ring that starts as garbage; the exact receptive
                   field (k-1)d+1 that sizes the ring
@@ -83,6 +88,10 @@ def _load():
             lib.orc_backward_q88.argtypes = [P, P, *geo, P, P, i32, i32, P, ctypes.c_int32, i32, f32,
                                              P, P, P, P, P]
             lib.orc_backward_q88.restype = None
+            lib.orc_bn_forward_stats.argtypes = [P, *geo, P, P, P, f32, P, P, P, P]
+            lib.orc_bn_forward_stats.restype = None
+            lib.orc_bn_backward.argtypes = [P, *geo, P, P, f32, P, P, P, P, P, P, P, P]
+            lib.orc_bn_backward.restype = None
             lib.orc_quantizer_grad.argtypes = [P, P, i32, i32, P, i64, i32, P]
             lib.orc_quantizer_grad.restype = None
             lib.orc_stream_step_f32.argtypes = [P, i32, i32, i32, i32, i32, i64, P, P, P, i32, i32, P, f32,
@@ -168,6 +177,45 @@ def quantize(w, shift_lo: int, shift_hi: int):
     shift = np.empty(w.shape, np.int8)
     _load().orc_quantize(_ptr(w), w.size, int(shift_lo), int(shift_hi), _ptr(sign), _ptr(shift))
     return sign, shift
+
+
+def bn_forward_stats(x, w, gamma, beta, eps: float, k: int, d: int):
+    """App. C, training mode: statistics of the latent-weight convolution and
+    the fused weight and bias.  Returns dict w_f, b_f (float32), aux [C, 4]
+    (mu, var, s, 1/sqrt(var+eps), float64), stats [C, 2] (sum, sum of squares)."""
+    x = _c(x, np.float32)
+    T, N, C, S = _geometry(x)
+    w = _c(w, np.float32).reshape(C, k)
+    gamma = _c(gamma, np.float32).reshape(C)
+    beta = _c(beta, np.float32).reshape(C)
+    w_f = np.empty((C, k), np.float32)
+    b_f = np.empty(C, np.float32)
+    aux = np.empty((C, 4), np.float64)
+    stats = np.empty((C, 2), np.float64)
+    _load().orc_bn_forward_stats(_ptr(x), T, N, C, S, int(k), int(d), _ptr(w), _ptr(gamma), _ptr(beta),
+                                 float(eps), _ptr(w_f), _ptr(b_f), _ptr(aux), _ptr(stats))
+    return {"w_f": w_f, "b_f": b_f, "aux": aux, "stats": stats}
+
+
+def bn_backward(x, w, gamma, eps: float, aux, grad_wf, grad_bf, grad_xq, k: int, d: int):
+    """Backward of the fusion and the batch statistics (App. C): returns dict
+    grad_x (grad_xq plus the statistics path), grad_w, grad_gamma, grad_beta,
+    all float64."""
+    x = _c(x, np.float32)
+    T, N, C, S = _geometry(x)
+    w = _c(w, np.float32).reshape(C, k)
+    gamma = _c(gamma, np.float32).reshape(C)
+    aux = _c(aux, np.float64).reshape(C, 4)
+    gwf = _c(grad_wf, np.float64).reshape(C, k)
+    gbf = _c(grad_bf, np.float64).reshape(C)
+    gxq = _c(grad_xq, np.float64).reshape(x.shape)
+    gx = np.empty(x.shape, np.float64)
+    gw = np.empty((C, k), np.float64)
+    gg = np.empty(C, np.float64)
+    gb = np.empty(C, np.float64)
+    _load().orc_bn_backward(_ptr(x), T, N, C, S, int(k), int(d), _ptr(w), _ptr(gamma), float(eps), _ptr(aux),
+                            _ptr(gwf), _ptr(gbf), _ptr(gxq), _ptr(gx), _ptr(gw), _ptr(gg), _ptr(gb))
+    return {"grad_x": gx, "grad_w": gw, "grad_gamma": gg, "grad_beta": gb}
 
 
 def quantizer_grad(w, shift, grad_wq, mode: int, shift_lo: int, shift_hi: int) -> np.ndarray:

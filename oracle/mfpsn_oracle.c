@@ -489,6 +489,146 @@ void orc_stream_step_q88(const int16_t* x_t, int N, int C, int S, int k, int d, 
             }
 }
 
+/* ------------------------------------------------------------------------ */
+/* Batch-normalized threshold with fused-weight quantization (App. C,        */
+/* Eqs. weight fuse, bias fuse): the training step the paper runs.            */
+/* ------------------------------------------------------------------------ */
+
+/* The convolution with the latent (real-valued) weights, the intermediate
+ * variable of App. C whose statistics the batch normalization uses:
+ *   Tv[t,n,c,s] = sum_{i, tau >= 0} W[c,i] * x[tau,n,c,s],  tau = t-(k-1-i)d,
+ * in double: each product of two floats is exact in double, the sum runs in
+ * ascending i from +0.0 (no FMA contraction). */
+static double bn_conv_value(const float* x, int64_t M, int64_t t, int64_t col, int c, int k, int d,
+                            const float* w)
+{
+    double acc = 0.0;
+    for (int i = 0; i < k; ++i) {
+        const int64_t tau = t - (int64_t)(k - 1 - i) * d;
+        if (tau < 0)
+            continue;
+        acc = acc + (double)w[c * k + i] * (double)x[tau * M + col];
+    }
+    return acc;
+}
+
+/* Training-mode statistics and fusion.  Per channel c, over all (t, n, s):
+ *   mean mu = sum Tv / n_c,  biased variance var = sum (Tv - mu)^2 / n_c,
+ *   n_c = T*N*S (the mean and biased variance of the input sequence, App. C);
+ *   s = gamma / sqrt(var + eps),  W_f = s * W,  b_f = beta - s * mu
+ * (Eq. weight fuse, Eq. bias fuse).  The sums are sequential in (t, n, s)
+ * order, in double; the variance takes the two-pass form.  W_f and b_f are
+ * rounded once to float (the quantizer and the charge consume floats); aux
+ * keeps [mu, var, s, 1/sqrt(var + eps)] per channel in double for the
+ * backward.  stats (optional) receives [sum Tv, sum Tv^2] per channel. */
+void orc_bn_forward_stats(const float* x, int T, int N, int C, int S, int k, int d, const float* w,
+                          const float* gamma, const float* beta, float eps, float* w_f, float* b_f,
+                          double* aux, double* stats)
+{
+    const int64_t M = (int64_t)N * C * S;
+    const double nc = (double)T * N * S;
+    for (int c = 0; c < C; ++c) {
+        double s1 = 0.0, s2 = 0.0;
+        for (int t = 0; t < T; ++t)
+            for (int n = 0; n < N; ++n)
+                for (int sp = 0; sp < S; ++sp) {
+                    const double v = bn_conv_value(x, M, t, ((int64_t)n * C + c) * S + sp, c, k, d, w);
+                    s1 += v;
+                    s2 += v * v;
+                }
+        const double mu = nc > 0 ? s1 / nc : 0.0;
+        double dev = 0.0;
+        for (int t = 0; t < T; ++t)
+            for (int n = 0; n < N; ++n)
+                for (int sp = 0; sp < S; ++sp) {
+                    const double v = bn_conv_value(x, M, t, ((int64_t)n * C + c) * S + sp, c, k, d, w) - mu;
+                    dev += v * v;
+                }
+        const double var = nc > 0 ? dev / nc : 0.0;
+        const double inv = 1.0 / sqrt(var + (double)eps);
+        const double sc = (double)gamma[c] * inv;
+        for (int i = 0; i < k; ++i)
+            w_f[c * k + i] = (float)(sc * (double)w[c * k + i]);
+        b_f[c] = (float)((double)beta[c] - sc * mu);
+        aux[4 * c + 0] = mu;
+        aux[4 * c + 1] = var;
+        aux[4 * c + 2] = sc;
+        aux[4 * c + 3] = inv;
+        if (stats) {
+            stats[2 * c + 0] = s1;
+            stats[2 * c + 1] = s2;
+        }
+    }
+}
+
+/* Backward of the fusion and the statistics.  Inputs: the gradients of the
+ * fused (quantized) weight and bias, grad_wf [C][k] and grad_bf [C] (the
+ * quantizer passes grad_wf to W_f unchanged, Sec. 4.2), and grad_xq, the
+ * input gradient through the quantized convolution (App. A.3 Eq. backward_X),
+ * all in double.  With n_c, mu, var, s, inv from the forward:
+ *   dL/ds   = sum_i grad_wf[c,i] W[c,i] - grad_bf[c] mu
+ *   dL/dgamma = dL/ds * inv,   dL/dbeta = grad_bf
+ *   dL/dvar = -dL/ds * s / (2 (var + eps)),   dL/dmu (through b_f) = -s grad_bf
+ *   dTv = dL/dmu / n_c + dL/dvar * 2 (Tv - mu) / n_c      (per element)
+ *   grad_x = grad_xq + sum_i W[c,i] dTv[t + (k-1-i)d]      (transposed conv, latent W)
+ *   grad_w = s grad_wf + sum_{t,n,s} dTv[t] x[t-(k-1-i)d]
+ * (the derivative of var through mu vanishes: sum (Tv - mu) = 0).  Every sum
+ * in double; grad_x, grad_w, grad_gamma, grad_beta returned in double. */
+void orc_bn_backward(const float* x, int T, int N, int C, int S, int k, int d, const float* w,
+                     const float* gamma, float eps, const double* aux, const double* grad_wf,
+                     const double* grad_bf, const double* grad_xq, double* grad_x, double* grad_w,
+                     double* grad_gamma, double* grad_beta)
+{
+    const int64_t M = (int64_t)N * C * S;
+    const double nc = (double)T * N * S;
+    (void)gamma;
+    for (int c = 0; c < C; ++c) {
+        const double mu = aux[4 * c + 0], var = aux[4 * c + 1], sc = aux[4 * c + 2], inv = aux[4 * c + 3];
+        double dsc = 0.0;
+        for (int i = 0; i < k; ++i)
+            dsc += grad_wf[c * k + i] * (double)w[c * k + i];
+        dsc -= grad_bf[c] * mu;
+        grad_gamma[c] = dsc * inv;
+        grad_beta[c] = grad_bf[c];
+        const double dvar = -dsc * sc / (2.0 * (var + (double)eps));
+        const double dmu = -sc * grad_bf[c];
+        const double b = nc > 0 ? 2.0 * dvar / nc : 0.0;
+        const double a = nc > 0 ? dmu / nc - b * mu : 0.0;
+        for (int i = 0; i < k; ++i)
+            grad_w[c * k + i] = sc * grad_wf[c * k + i];
+        for (int n = 0; n < N; ++n)
+            for (int sp = 0; sp < S; ++sp) {
+                const int64_t col = ((int64_t)n * C + c) * S + sp;
+                for (int t = 0; t < T; ++t) {
+                    /* input gradient at time t: dTv of the outputs its taps feed */
+                    double gx = 0.0;
+                    for (int i = 0; i < k; ++i) {
+                        const int64_t to = (int64_t)t + (int64_t)(k - 1 - i) * d;
+                        if (to >= T)
+                            continue;
+                        const double dtv = a + b * bn_conv_value(x, M, to, col, c, k, d, w);
+                        gx = gx + (double)w[c * k + i] * dtv;
+                    }
+                    grad_x[t * M + col] = grad_xq[t * M + col] + gx;
+                }
+            }
+        for (int i = 0; i < k; ++i) {
+            double acc = 0.0;
+            for (int t = 0; t < T; ++t)
+                for (int n = 0; n < N; ++n)
+                    for (int sp = 0; sp < S; ++sp) {
+                        const int64_t tau = (int64_t)t - (int64_t)(k - 1 - i) * d;
+                        if (tau < 0)
+                            continue;
+                        const int64_t col = ((int64_t)n * C + c) * S + sp;
+                        const double dtv = a + b * bn_conv_value(x, M, t, col, c, k, d, w);
+                        acc += dtv * (double)x[tau * M + col];
+                    }
+            grad_w[c * k + i] += acc;
+        }
+    }
+}
+
 /* Sawtooth dilation schedule (Sec. 4.1, Eq. d): d^0 = 1, d^{l+1} = d^l mod P + 1
  * (the paper uses P = 3), computed by iterating the recurrence. */
 int orc_sawtooth_dilation(int layer, int period)

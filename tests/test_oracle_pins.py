@@ -609,3 +609,130 @@ def test_quantizer_grad_round_only_special_values(orc):
     assert out[5] == 0.0
     # Q(3) rounds to 4 (shift -2), clamped into [0, 7] to shift 0: |Wq| = 1, factor 1/3
     assert out[6] == np.float32(1.0) / np.float32(3.0)
+
+
+# ---------------------------------------------------------------------------
+# batch-normalized threshold with fused-weight quantization (App. C)
+# ---------------------------------------------------------------------------
+def latent_conv(x, w, k, d):
+    """W * x in float64 with the causal, dilated taps (independent numpy form)."""
+    x = x.astype(np.float64)
+    T = x.shape[0]
+    out = np.zeros_like(x)
+    C = x.shape[2]
+    sh = (1, 1, C) + (1,) * (x.ndim - 3)
+    for i in range(k):
+        off = (k - 1 - i) * d
+        if off < T:
+            out[off:] += w[:, i].astype(np.float64).reshape(sh) * x[:T - off]
+    return out
+
+
+def bn_case(seed=60, T=13, N=3, C=4, S=2, k=3):
+    rng = np.random.default_rng(seed)
+    x = rng.normal(0.4, 1.0, (T, N, C, S)).astype(np.float32)
+    w = rng.normal(0, 0.6, (C, k)).astype(np.float32)
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = rng.normal(-1.0, 0.2, C).astype(np.float32)
+    return x, w, gamma, beta
+
+
+@pytest.mark.parametrize("d", [1, 3])
+def test_bn_statistics_are_mean_and_biased_variance(orc, d):
+    x, w, gamma, beta = bn_case()
+    k, eps = 3, 1e-5
+    r = orc.bn_forward_stats(x, w, gamma, beta, eps, k, d)
+    tv = latent_conv(x, w, k, d)
+    axes = (0, 1, 3)
+    mu, var = tv.mean(axis=axes), tv.var(axis=axes)
+    assert np.allclose(r["aux"][:, 0], mu, rtol=1e-12, atol=1e-13)
+    assert np.allclose(r["aux"][:, 1], var, rtol=1e-12, atol=1e-13)
+    assert np.allclose(r["stats"][:, 0], tv.sum(axis=axes), rtol=1e-12, atol=1e-12)
+    assert np.allclose(r["stats"][:, 1], (tv * tv).sum(axis=axes), rtol=1e-12, atol=1e-12)
+
+
+def test_bn_fusion_identity(orc):
+    """Eqs. weight fuse, bias fuse: the fused convolution plus the fused bias
+    is the batch-normalized latent convolution, gamma (Tv - mu)/sqrt(var +
+    eps) + beta; W_f and b_f are those values rounded to float."""
+    x, w, gamma, beta = bn_case(61)
+    k, d, eps = 3, 2, 1e-5
+    r = orc.bn_forward_stats(x, w, gamma, beta, eps, k, d)
+    mu, var, sc, inv = r["aux"].T
+    tv = latent_conv(x, w, k, d)
+    sh = (1, 1, 4, 1)
+    bn = gamma.astype(np.float64).reshape(sh) * (tv - mu.reshape(sh)) * inv.reshape(sh) + beta.reshape(sh)
+    fused = latent_conv(x, (sc[:, None] * w.astype(np.float64)), k, d) + (beta - sc * mu).reshape(sh)
+    assert np.allclose(fused, bn, rtol=1e-12, atol=1e-12)
+    assert np.allclose(inv, 1.0 / np.sqrt(var + eps), rtol=1e-15)
+    assert np.array_equal(r["w_f"], (sc[:, None] * w.astype(np.float64)).astype(np.float32))
+    assert np.array_equal(r["b_f"], (beta.astype(np.float64) - sc * mu).astype(np.float32))
+
+
+@pytest.mark.parametrize("d", [1, 2])
+def test_bn_backward_matches_finite_differences(orc, d):
+    """With the quantizer taken as identity (its straight-through gradient)
+    and the Heaviside replaced by a sigmoid of slope alpha, the fused step is
+    a smooth function of x, W, gamma and beta; the oracle's backward of the
+    fusion and the statistics, fed with that function's gradients of W_f,
+    b_f and the quantized-path input gradient, must equal its central finite
+    differences."""
+    x, w, gamma, beta = bn_case(62 + d)
+    k, eps, alpha = 3, 1e-5, 2.0
+    rng = np.random.default_rng(70 + d)
+    g = rng.normal(0, 1, x.shape)
+    sh = (1, 1, x.shape[2], 1)
+
+    def loss(xv, wv, gv, bv):
+        tv = latent_conv(xv, wv, k, d)
+        mu = tv.mean(axis=(0, 1, 3))
+        var = tv.var(axis=(0, 1, 3))
+        sc = gv / np.sqrt(var + eps)
+        hf = latent_conv(xv, sc[:, None] * wv, k, d) + (bv - sc * mu).reshape(sh)
+        return float(np.sum(g / (1.0 + np.exp(-alpha * hf))))
+
+    r = orc.bn_forward_stats(x, w, gamma, beta, eps, k, d)
+    mu, var, sc, inv = r["aux"].T
+    wf = sc[:, None] * w.astype(np.float64)
+    hf = latent_conv(x, wf, k, d) + (beta - sc * mu).reshape(sh)
+    sg = 1.0 / (1.0 + np.exp(-alpha * hf))
+    dh = g * alpha * sg * (1.0 - sg)
+    T = x.shape[0]
+    xd = x.astype(np.float64)
+    gwf = np.zeros((x.shape[2], k))
+    gxq = np.zeros_like(xd)
+    for i in range(k):
+        off = (k - 1 - i) * d
+        if off < T:
+            gwf[:, i] = np.sum(dh[off:] * xd[:T - off], axis=(0, 1, 3))
+            gxq[:T - off] += wf[:, i].reshape(sh) * dh[off:]
+    gbf = dh.sum(axis=(0, 1, 3))
+    b = orc.bn_backward(x, w, gamma, eps, r["aux"], gwf, gbf, gxq, k, d)
+    h = 1e-6
+    for idx in [(0, 0, 0, 0), (5, 1, 2, 1), (T - 1, 2, 3, 0), (T - 4, 0, 1, 1)]:
+        xp, xm = xd.copy(), xd.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (loss(xp, w.astype(np.float64), gamma.astype(np.float64), beta.astype(np.float64)) -
+              loss(xm, w.astype(np.float64), gamma.astype(np.float64), beta.astype(np.float64))) / (2 * h)
+        assert abs(fd - b["grad_x"][idx]) <= 1e-6 + 1e-5 * abs(fd), ("x", idx, fd, b["grad_x"][idx])
+    for c, i in [(0, 0), (2, 2), (3, 1)]:
+        wp, wm = w.astype(np.float64), w.astype(np.float64)
+        wp[c, i] += h
+        wm[c, i] -= h
+        fd = (loss(xd, wp, gamma.astype(np.float64), beta.astype(np.float64)) -
+              loss(xd, wm, gamma.astype(np.float64), beta.astype(np.float64))) / (2 * h)
+        assert abs(fd - b["grad_w"][c, i]) <= 1e-6 + 1e-5 * abs(fd), ("w", c, i, fd, b["grad_w"][c, i])
+    for c in range(x.shape[2]):
+        for name, which in (("gamma", 0), ("beta", 1)):
+            gp, gm = gamma.astype(np.float64), gamma.astype(np.float64)
+            bp, bm = beta.astype(np.float64), beta.astype(np.float64)
+            if which == 0:
+                gp[c] += h
+                gm[c] -= h
+            else:
+                bp[c] += h
+                bm[c] -= h
+            fd = (loss(xd, w.astype(np.float64), gp, bp) - loss(xd, w.astype(np.float64), gm, bm)) / (2 * h)
+            got = b["grad_gamma" if which == 0 else "grad_beta"][c]
+            assert abs(fd - got) <= 1e-6 + 1e-5 * abs(fd), (name, c, fd, got)
