@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 5
+#define MFPSN_ABI_VERSION 6
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -164,6 +164,40 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
  * The gradient of the latent weight is grad_w itself (straight-through). */
 int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int32_t shift_hi,
                            int8_t* sign, int8_t* shift, void* stream);
+
+/* Batch-normalized threshold with fused-weight quantization, the training
+ * step of App. C (Eq. weight fuse, Eq. bias fuse), for float x (MFPSN_F32):
+ * the spike rule is Theta(gamma (H - mu)/sqrt(var + eps) + beta) on the
+ * latent-weight convolution H, trained through the fused, quantized weight.
+ *   forward:  mfpsn_bn_forward_stats -> mfpsn_quantize_weights(w_f) ->
+ *             mfpsn_forward(bias = b_f, v_th = 0, saving the factor)
+ *   backward: mfpsn_backward (grad_x, grad of W_f = grad of the quantized
+ *             weight, grad of b_f) -> mfpsn_bn_backward
+ * mfpsn_bn_forward_stats: per channel c, over all (t, n, s), the mean mu and
+ * the biased variance var of Tv = latent W * x (Tv in double: exact float
+ * products, ascending taps), then s = gamma/sqrt(var + eps),
+ * w_f = s * w (float [C][k]), b_f = beta - s * mu (float [C]),
+ * aux = [mu, var, s, 1/sqrt(var + eps)] (double [C][4], for the backward),
+ * stats = [sum Tv, sum Tv^2] (double [C][2], optional).  Sums are added in a
+ * fixed order (bitwise reproducible); var = sum Tv^2/n - mu^2, at least 0.
+ * mfpsn_bn_backward: from grad_wf (float [C][k]) and grad_bf (float [C])
+ * of the fused weight and bias, adds the statistics path to grad_x (float
+ * [T][N][C][S], in: the quantized path's input gradient, out: the total)
+ * and writes grad_w (float [C][k], latent weight), grad_gamma, grad_beta
+ * (float [C]):  ds = sum_i grad_wf W - grad_bf mu, grad_gamma = ds/sqrt(var +
+ * eps), grad_beta = grad_bf, dvar = -ds s / (2 (var + eps)), dmu = -s grad_bf,
+ * dTv = dmu/n + dvar 2 (Tv - mu)/n, grad_x += W^T * dTv (latent weights,
+ * double, ascending taps), grad_w = s grad_wf + sum dTv x (n = T*N*S).
+ * Both need mfpsn_bn_workspace_size bytes of workspace (8-byte aligned;
+ * the backward keeps dTv of every element there).  eps > 0; empty batches
+ * are MFPSN_ERR_SHAPE; other dtypes MFPSN_ERR_DTYPE. */
+int mfpsn_bn_workspace_size(const mfpsn_desc* desc, size_t* bytes);
+int mfpsn_bn_forward_stats(const mfpsn_desc* desc, const float* x, const float* w, const float* gamma,
+                           const float* beta, float eps, float* w_f, float* b_f, double* aux, double* stats,
+                           void* workspace, size_t workspace_bytes, void* stream);
+int mfpsn_bn_backward(const mfpsn_desc* desc, const float* x, const float* w, const double* aux, float eps,
+                      const float* grad_wf, const float* grad_bf, float* grad_x, float* grad_w, float* grad_gamma,
+                      float* grad_beta, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Gradient of the latent weight from the gradient of the quantized weight
  * (Sec. 4.2), elementwise over `count` (< 2^31) weights, device memory:

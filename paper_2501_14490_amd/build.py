@@ -52,6 +52,10 @@ def _units():
             units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
                                 f"-DMFPSN_TU_DTYPE={dt}", f"-DMFPSN_TU_KLO={lo}",
                                 f"-DMFPSN_TU_KHI={hi}", "-c", src, "-o", obj], [src, *headers]))
+    bn_src = os.path.join(CSRC, "mfpsn_bn.hip")
+    obj = os.path.join(BUILD, "bn.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", bn_src, "-o", obj],
+                  [bn_src, os.path.join(CSRC, "mfpsn_bn.h")]))
     qg_src = os.path.join(CSRC, "mfpsn_qgrad.hip")
     obj = os.path.join(BUILD, "qgrad.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
@@ -68,7 +72,7 @@ def _units():
         cpp = os.path.join(CSRC, name)
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
                       [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
-                       *headers]))
+                       os.path.join(CSRC, "mfpsn_bn.h"), *headers]))
     return units
 
 

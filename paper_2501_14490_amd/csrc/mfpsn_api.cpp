@@ -10,6 +10,7 @@
 #include <initializer_list>
 
 #include "mfpsn_internal.h"
+#include "mfpsn_bn.h"
 #include "mfpsn_qgrad.h"
 #include "mfpsn_stream.h"
 
@@ -376,6 +377,91 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     f.grad_w = grad_w;
     f.grad_b = grad_b;
     if (launch_finalize(f, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+namespace {
+// The batch-normalization entry points take float x (MFPSN_F32) and one
+// layer's shapes; T is used.
+int validate_bn(const mfpsn_desc* d, BnGeom* g)
+{
+    const int st = validate(d);
+    if (st != MFPSN_OK)
+        return st;
+    if (d->dtype != MFPSN_F32)
+        return MFPSN_ERR_DTYPE;
+    g->T = d->T;
+    g->N = d->N;
+    g->C = d->C;
+    g->S = d->S;
+    g->k = d->k;
+    g->d = d->dilation;
+    g->M = (size_t)d->N * d->C * d->S;
+    g->tc = 32;
+    g->chunks = (d->T + g->tc - 1) / g->tc;
+    return MFPSN_OK;
+}
+}  // namespace
+
+int mfpsn_bn_workspace_size(const mfpsn_desc* desc, size_t* bytes)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!bytes)
+        return MFPSN_ERR_NULL;
+    *bytes = g.M > 0 && g.T > 0 ? bn_workspace_bytes(g) : 0;
+    return MFPSN_OK;
+}
+
+int mfpsn_bn_forward_stats(const mfpsn_desc* desc, const float* x, const float* w, const float* gamma,
+                           const float* beta, float eps, float* w_f, float* b_f, double* aux, double* stats,
+                           void* workspace, size_t workspace_bytes, void* stream)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!(eps > 0.0f) || !isfinite(eps))
+        return MFPSN_ERR_PARAM;
+    if (g.M == 0 || g.T == 0)
+        return MFPSN_ERR_SHAPE;  // statistics of an empty batch are undefined
+    if (!x || !w || !gamma || !beta || !w_f || !b_f || !aux)
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(gamma, 4) || !aligned(beta, 4) || !aligned(w_f, 4) ||
+        !aligned(b_f, 4) || !aligned(aux, 8) || !aligned(stats, 8))
+        return MFPSN_ERR_ALIGN;
+    if (!workspace || workspace_bytes < bn_workspace_bytes(g) || !aligned(workspace, 8))
+        return MFPSN_ERR_WORKSPACE;
+    if (launch_bn_forward_stats(g, x, w, gamma, beta, eps, w_f, b_f, aux, stats, workspace, (hipStream_t)stream) !=
+        hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_bn_backward(const mfpsn_desc* desc, const float* x, const float* w, const double* aux, float eps,
+                      const float* grad_wf, const float* grad_bf, float* grad_x, float* grad_w, float* grad_gamma,
+                      float* grad_beta, void* workspace, size_t workspace_bytes, void* stream)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!(eps > 0.0f) || !isfinite(eps))
+        return MFPSN_ERR_PARAM;
+    if (g.M == 0 || g.T == 0)
+        return MFPSN_ERR_SHAPE;
+    if (!x || !w || !aux || !grad_wf || !grad_bf || !grad_x || !grad_w || !grad_gamma || !grad_beta)
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(aux, 8) || !aligned(grad_wf, 4) || !aligned(grad_bf, 4) ||
+        !aligned(grad_x, 4) || !aligned(grad_w, 4) || !aligned(grad_gamma, 4) || !aligned(grad_beta, 4))
+        return MFPSN_ERR_ALIGN;
+    if (!workspace || workspace_bytes < bn_workspace_bytes(g) || !aligned(workspace, 8))
+        return MFPSN_ERR_WORKSPACE;
+    if (launch_bn_backward(g, x, w, aux, eps, grad_wf, grad_bf, grad_x, grad_w, grad_gamma, grad_beta, workspace,
+                           (hipStream_t)stream) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
 }

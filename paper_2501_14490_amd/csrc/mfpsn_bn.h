@@ -1,0 +1,26 @@
+// Internal interface of the batch-normalization kernels (mfpsn_bn.hip) for
+// the C-ABI layer.  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mfpsn {
+
+struct BnGeom {
+    int32_t T, N, C, S, k, d;
+    size_t M;        // N*C*S
+    int32_t tc;      // time steps per statistics chunk
+    int32_t chunks;  // ceil(T / tc)
+};
+
+size_t bn_workspace_bytes(const BnGeom& g);
+hipError_t launch_bn_forward_stats(const BnGeom& g, const float* x, const float* w, const float* gamma,
+                                   const float* beta, float eps, float* w_f, float* b_f, double* aux,
+                                   double* stats, void* workspace, hipStream_t stream);
+hipError_t launch_bn_backward(const BnGeom& g, const float* x, const float* w, const double* aux, float eps,
+                              const float* grad_wf, const float* grad_bf, float* grad_x, float* grad_w,
+                              float* grad_gamma, float* grad_beta, void* workspace, hipStream_t stream);
+
+}  // namespace mfpsn

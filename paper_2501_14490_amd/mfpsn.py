@@ -61,6 +61,12 @@ _lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
+_lib.mfpsn_bn_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
+_lib.mfpsn_bn_workspace_size.restype = ctypes.c_int
+_lib.mfpsn_bn_forward_stats.argtypes = [_DP, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_bn_forward_stats.restype = ctypes.c_int
+_lib.mfpsn_bn_backward.argtypes = [_DP, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_bn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantizer_grad.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int32, _P,
                                       _P]
 _lib.mfpsn_quantizer_grad.restype = ctypes.c_int
@@ -163,6 +169,28 @@ def mfpsn_quantizer_grad(w, shift, shift_lo: int, shift_hi: int, grad_wq, mode: 
            "mfpsn_quantizer_grad")
 
 
+def mfpsn_bn_workspace_size(desc: MfpsnDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.mfpsn_bn_workspace_size(ctypes.byref(desc), ctypes.byref(n)), "mfpsn_bn_workspace_size")
+    return int(n.value)
+
+
+def mfpsn_bn_forward_stats(desc: MfpsnDesc, x, w, gamma, beta, eps: float, w_f, b_f, aux, stats, workspace,
+                           stream=None) -> None:
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(_lib.mfpsn_bn_forward_stats(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(gamma), _ptr(beta), float(eps),
+                                       _ptr(w_f), _ptr(b_f), _ptr(aux), _ptr(stats), _ptr(workspace), nbytes,
+                                       _stream(stream)), "mfpsn_bn_forward_stats")
+
+
+def mfpsn_bn_backward(desc: MfpsnDesc, x, w, aux, eps: float, grad_wf, grad_bf, grad_x, grad_w, grad_gamma,
+                      grad_beta, workspace, stream=None) -> None:
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(_lib.mfpsn_bn_backward(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(aux), float(eps), _ptr(grad_wf),
+                                  _ptr(grad_bf), _ptr(grad_x), _ptr(grad_w), _ptr(grad_gamma), _ptr(grad_beta),
+                                  _ptr(workspace), nbytes, _stream(stream)), "mfpsn_bn_backward")
+
+
 def mfpsn_stream_ring_bytes(desc: MfpsnDesc):
     """(ring slots R = (k-1)*dilation + 1, ring size in bytes)."""
     steps = ctypes.c_int32(0)
@@ -242,6 +270,39 @@ def quantizer_grad(w, shift, grad_wq, ste="whole", shift_lo: int = 0, shift_hi: 
     return out
 
 
+def bn_workspace(desc: MfpsnDesc, device):
+    return torch.empty(max(mfpsn_bn_workspace_size(desc), 8), dtype=torch.uint8, device=device)
+
+
+def bn_forward_stats(desc: MfpsnDesc, x, w, gamma, beta, eps: float = 1e-5, workspace=None, stream=None,
+                     want_stats: bool = False):
+    """Fused weight and bias of App. C from the batch statistics of the
+    latent-weight convolution: (w_f, b_f, aux[, stats])."""
+    dev = x.device
+    _expect(x, torch.float32, dev, "x")
+    w_f = torch.empty((desc.C, desc.k), dtype=torch.float32, device=dev)
+    b_f = torch.empty((desc.C,), dtype=torch.float32, device=dev)
+    aux = torch.empty((desc.C, 4), dtype=torch.float64, device=dev)
+    stats = torch.empty((desc.C, 2), dtype=torch.float64, device=dev) if want_stats else None
+    ws = workspace if workspace is not None else bn_workspace(desc, dev)
+    mfpsn_bn_forward_stats(desc, x, w, gamma, beta, eps, w_f, b_f, aux, stats, ws, stream)
+    return (w_f, b_f, aux, stats) if want_stats else (w_f, b_f, aux)
+
+
+def bn_backward(desc: MfpsnDesc, x, w, aux, grad_wf, grad_bf, grad_x, eps: float = 1e-5, workspace=None,
+                stream=None):
+    """Adds the batch-statistics path to grad_x (in place) and returns
+    (grad_w, grad_gamma, grad_beta) of the latent weight and the BN affine
+    parameters."""
+    dev = x.device
+    grad_w = torch.empty((desc.C, desc.k), dtype=torch.float32, device=dev)
+    grad_gamma = torch.empty((desc.C,), dtype=torch.float32, device=dev)
+    grad_beta = torch.empty((desc.C,), dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else bn_workspace(desc, dev)
+    mfpsn_bn_backward(desc, x, w, aux, eps, grad_wf, grad_bf, grad_x, grad_w, grad_gamma, grad_beta, ws, stream)
+    return grad_w, grad_gamma, grad_beta
+
+
 class StreamState:
     """Step-by-step inference of one neuron layer: owns the history ring of
     the last (k-1)*dilation + 1 inputs ([R, N, C, *spatial], the storage type
@@ -310,3 +371,35 @@ class MfPSNFunction(torch.autograd.Function):
         grad_w = grad_wq if ctx.ste == "whole" else quantizer_grad(wc, shift, grad_wq, ctx.ste, *ctx.shift_range)
         grad_vth = -grad_b if ctx.per_channel else None
         return grad_x, grad_w, grad_b, None, None, grad_vth, None, None, None, None, None
+
+
+class MfPSNBNFunction(torch.autograd.Function):
+    """The training step of App. C: spikes = Theta(BN(W * x)) with the batch
+    statistics of the latent-weight convolution, run as
+    Theta(Q(W_f) * x + b_f) with the fused weight W_f = gamma W/sqrt(var+eps)
+    and bias b_f = beta - gamma mu/sqrt(var+eps) (Eqs. weight fuse, bias
+    fuse; the quantizer's whole straight-through estimator passes the
+    gradient of Q(W_f) to W_f).  Float x only."""
+
+    @staticmethod
+    def forward(ctx, x, w, gamma, beta, k, dilation, eps, surrogate, alpha, shift_lo, shift_hi):
+        xc = x.detach().contiguous()
+        wc = w.detach().contiguous()
+        desc = make_desc(x.shape, k, dilation, "f32", surrogate, alpha, 0.0, 0, shift_lo, shift_hi)
+        ws = bn_workspace(desc, x.device)
+        w_f, b_f, aux = bn_forward_stats(desc, xc, wc, gamma.detach().contiguous(), beta.detach().contiguous(),
+                                         eps, ws)
+        sign, shift = quantize(w_f, shift_lo, shift_hi)
+        spikes, sg = forward(desc, xc, sign, shift, b_f, want_sg=True)
+        ctx.save_for_backward(xc, wc, sign, shift, b_f, sg, aux)
+        ctx.desc, ctx.eps, ctx.ws = desc, eps, ws
+        return spikes.to(x.dtype)
+
+    @staticmethod
+    def backward(ctx, grad_spikes):
+        xc, wc, sign, shift, b_f, sg, aux = ctx.saved_tensors
+        g = grad_spikes.to(torch.float32).contiguous()
+        grad_x, grad_wf, grad_bf = backward(ctx.desc, xc, g, sign, shift, b_f, sg=sg)
+        grad_w, grad_gamma, grad_beta = bn_backward(ctx.desc, xc, wc, aux, grad_wf, grad_bf, grad_x, ctx.eps,
+                                                    ctx.ws)
+        return grad_x, grad_w, grad_gamma, grad_beta, None, None, None, None, None, None, None

@@ -41,6 +41,9 @@ def lib():
     L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    L.mfpsn_bn_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
+    L.mfpsn_bn_forward_stats.argtypes = [DP, P, P, P, P, ctypes.c_float, P, P, P, P, P, ctypes.c_size_t, P]
+    L.mfpsn_bn_backward.argtypes = [DP, P, P, P, ctypes.c_float, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_quantizer_grad.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int64, ctypes.c_int32, P, P]
     L.mfpsn_stream_ring_bytes.argtypes = [DP, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_stream_step.argtypes = [DP, ctypes.c_int64, P, P, P, P, P, P, P, P]
@@ -70,7 +73,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 5
+    assert lib.mfpsn_abi_version() == 6
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -204,3 +207,27 @@ def test_quantizer_grad_validation(lib):
     assert q(FAKE, FAKE, 0, 7, None, 10, 0, FAKE, None) == -1
     assert q(FAKE, FAKE, 0, 7, FAKE + 2, 10, 0, FAKE, None) == -6
     assert q(None, None, 0, 7, None, 0, 1, None, None) == 0         # nothing to do
+
+
+def test_bn_validation(lib):
+    d = good_desc()
+    n = ctypes.c_size_t(0)
+    assert lib.mfpsn_bn_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0 and n.value > 0
+    need = n.value
+    f = lib.mfpsn_bn_forward_stats
+    args = [FAKE] * 4  # x, w, gamma, beta
+    outs = [FAKE] * 4  # w_f, b_f, aux, stats
+    assert f(ctypes.byref(good_desc(dtype=1)), *args, 1e-5, *outs, FAKE, need, None) == -4
+    assert f(ctypes.byref(d), *args, 0.0, *outs, FAKE, need, None) == -3
+    assert f(ctypes.byref(d), *args, float("nan"), *outs, FAKE, need, None) == -3
+    assert f(ctypes.byref(good_desc(T=0)), *args, 1e-5, *outs, FAKE, need, None) == -2
+    assert f(ctypes.byref(d), None, FAKE, FAKE, FAKE, 1e-5, *outs, FAKE, need, None) == -1
+    assert f(ctypes.byref(d), *args, 1e-5, FAKE, FAKE, FAKE + 4, FAKE, FAKE, need, None) == -6
+    assert f(ctypes.byref(d), *args, 1e-5, *outs, FAKE, need - 8, None) == -5
+    b = lib.mfpsn_bn_backward
+    bargs = [FAKE] * 3  # x, w, aux
+    grads = [FAKE] * 6  # grad_wf, grad_bf, grad_x, grad_w, grad_gamma, grad_beta
+    assert b(ctypes.byref(good_desc(dtype=2)), *bargs, 1e-5, *grads, FAKE, need, None) == -4
+    assert b(ctypes.byref(d), *bargs, -1.0, *grads, FAKE, need, None) == -3
+    assert b(ctypes.byref(d), FAKE, FAKE, None, 1e-5, *grads, FAKE, need, None) == -1
+    assert b(ctypes.byref(d), *bargs, 1e-5, *grads, None, need, None) == -5
