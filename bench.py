@@ -250,6 +250,106 @@ def stream_inference(torch, dev, wl, case, reps: int, warmup: int):
     }), flush=True)
 
 
+def bn_step(torch, dev, wl, case, steps: int, warmup: int):
+    """The batch-normalized-threshold training step of App. C for the
+    workload's layers (float storage): per layer, mfpsn_bn_forward_stats
+    (statistics of the latent-weight convolution and the fusion),
+    mfpsn_quantize_weights(W_f), mfpsn_forward (bias b_f, threshold 0, saving
+    the surrogate factor); then per layer in reverse, mfpsn_backward and
+    mfpsn_bn_backward.  value = layers * T*N*C*S / step time."""
+    from paper_2501_14490_amd import mfpsn
+
+    if wl.dtype != "f32":
+        log("the batch-normalized step takes float x: choose an f32 workload")
+        sys.exit(2)
+    rng = np.random.default_rng(90)
+    x0 = torch.from_numpy(np.ascontiguousarray(case["x"])).to(dev)
+    g0 = torch.from_numpy(np.ascontiguousarray(case["grad_spikes"])).to(dev)
+    P = len(wl.dilations)
+    eps = 1e-5
+    layers = []
+    for li, d in enumerate(wl.dilations):
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, "f32", wl.surrogate, wl.alpha, 0.0, 0, 0, wl.s_max)
+        C, k = wl.C, wl.k
+        L = {"d": d, "desc": desc,
+             "x": torch.roll(x0, shifts=7 * li, dims=1).contiguous() if li else x0,
+             "g": torch.roll(g0, shifts=11 * li, dims=1).contiguous() if li else g0,
+             "w": torch.from_numpy(rng.normal(0, 0.3, (C, k)).astype(np.float32)).to(dev),
+             "gamma": torch.ones(C, dtype=torch.float32, device=dev),
+             "beta": torch.full((C,), -1.0, dtype=torch.float32, device=dev),  # the paper's initialization
+             "w_f": torch.empty((C, k), dtype=torch.float32, device=dev),
+             "b_f": torch.empty(C, dtype=torch.float32, device=dev),
+             "aux": torch.empty((C, 4), dtype=torch.float64, device=dev),
+             "sign": torch.empty((C, k), dtype=torch.int8, device=dev),
+             "shift": torch.empty((C, k), dtype=torch.int8, device=dev),
+             "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
+             "sg": torch.empty(wl.shape, dtype=torch.float32, device=dev),
+             "gx": torch.empty(wl.shape, dtype=torch.float32, device=dev),
+             "gwf": torch.empty((C, k), dtype=torch.float32, device=dev),
+             "gbf": torch.empty(C, dtype=torch.float32, device=dev),
+             "gw": torch.empty((C, k), dtype=torch.float32, device=dev),
+             "ggamma": torch.empty(C, dtype=torch.float32, device=dev),
+             "gbeta": torch.empty(C, dtype=torch.float32, device=dev),
+             "ws": torch.empty(max(mfpsn.mfpsn_backward_workspace_size(desc), 8), dtype=torch.uint8, device=dev),
+             "bnws": mfpsn.bn_workspace(desc, dev)}
+        layers.append(L)
+    del x0, g0
+    stream = torch.cuda.current_stream()
+    hev = HipEvents()
+    stages = ("stats", "quantize", "forward", "backward", "bn_backward")
+
+    def step(ev=None):
+        def mark(name, li, end):
+            if ev is not None:
+                hev.record(ev[(name, li)][end], stream)
+        for li, L in enumerate(layers):
+            mark("stats", li, 0)
+            mfpsn.mfpsn_bn_forward_stats(L["desc"], L["x"], L["w"], L["gamma"], L["beta"], eps, L["w_f"], L["b_f"],
+                                         L["aux"], None, L["bnws"], stream)
+            mark("stats", li, 1)
+            mark("quantize", li, 0)
+            mfpsn.mfpsn_quantize_weights(L["w_f"], 0, wl.s_max, L["sign"], L["shift"], stream)
+            mark("quantize", li, 1)
+            mark("forward", li, 0)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], L["sign"], L["shift"], L["b_f"], L["spikes"], None, L["sg"],
+                                stream)
+            mark("forward", li, 1)
+        for li in reversed(range(P)):
+            L = layers[li]
+            mark("backward", li, 0)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], None, L["sg"], L["sign"], L["shift"], L["b_f"], L["gx"],
+                                 L["gwf"], L["gbf"], L["ws"], stream=stream)
+            mark("backward", li, 1)
+            mark("bn_backward", li, 0)
+            mfpsn.mfpsn_bn_backward(L["desc"], L["x"], L["w"], L["aux"], eps, L["gwf"], L["gbf"], L["gx"], L["gw"],
+                                    L["ggamma"], L["gbeta"], L["bnws"], stream)
+            mark("bn_backward", li, 1)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [{(n, li): [hev.new(), hev.new()] for n in stages for li in range(P)} for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s_ in range(steps):
+        step(evs[s_])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    per_stage = {n: round(float(np.mean([hev.elapsed_ms(*e[(n, li)]) for e in evs for li in range(P)])) * 1e3, 2)
+                 for n in stages}
+    value = P * wl.elements / (elapsed / steps)
+    log(f"bn step {elapsed * 1e3 / steps:.3f} ms, {value / 1e9:.2f} G elements/s, per layer (us): {per_stage}")
+    print(json.dumps({
+        "metric": "batch-normalized-threshold training step elements/s (T*N*C*S per layer)",
+        "value": value, "unit": "elements/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": elapsed * 1e3 / steps, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: x[{','.join(map(str, wl.shape))}] f32, k={wl.k}, one layer per "
+                               f"d={wl.dilations}; statistics + fusion, quantize, forward, backward, "
+                               f"backward of the statistics",
+                   "eps": eps, "gamma_init": 1.0, "beta_init": -1.0},
+        "per_layer_us": per_stage,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -265,6 +365,8 @@ def main():
                          "workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--bn-step", action="store_true",
+                    help="only time the batch-normalized-threshold training step of App. C (float workloads)")
     ap.add_argument("--stream-inference", action="store_true",
                     help="only time step-by-step inference (mfpsn_stream_step per layer and time step, "
                          "the sequence replayed from a HIP graph)")
@@ -308,6 +410,9 @@ def main():
     log(f"inputs drawn in {time.time() - t0:.1f}s")
     if args.stream_inference:
         stream_inference(torch, dev, wl, case, args.steps, args.warmup)
+        return
+    if args.bn_step:
+        bn_step(torch, dev, wl, case, args.steps, args.warmup)
         return
 
     def dev_tensor(a, storage):

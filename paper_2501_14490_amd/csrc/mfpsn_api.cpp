@@ -398,8 +398,45 @@ int validate_bn(const mfpsn_desc* d, BnGeom* g)
     g->k = d->k;
     g->d = d->dilation;
     g->M = (size_t)d->N * d->C * d->S;
-    g->tc = 32;
-    g->chunks = (d->T + g->tc - 1) / g->tc;
+    g->tq = d->T / d->dilation;
+    g->tr = d->T % d->dilation;
+    // Walk plan: a grid of about three waves per SIMD (256 CUs x 4 SIMDs),
+    // chunks of each residue class such that each thread has two or three
+    // items (each chunk at least 2k steps), and a thread count that spreads
+    // the items evenly and keeps every thread in one channel
+    constexpr int64_t kTarget = 256 * 4 * 3 * 64;
+    const int64_t L = (d->T + d->dilation - 1) / d->dilation;
+    const int64_t walks = (int64_t)g->M * d->dilation;
+    int64_t nch = walks > 0 ? (2 * kTarget + walks - 1) / walks : 1;
+    const int64_t max_nch = L / (2 * (int64_t)d->k);
+    if (nch > max_nch)
+        nch = max_nch;
+    if (nch < 1)
+        nch = 1;
+    g->lc = L > 0 ? (int32_t)((L + nch - 1) / nch) : 1;  // an empty sequence has no chunks
+    g->nch = (int32_t)((L + g->lc - 1) / g->lc);
+    g->items = (size_t)g->nch * d->dilation * g->M;
+    const int64_t SC = (int64_t)d->S * d->C;
+    int64_t a = SC, b = kBnThreads;  // base = lcm(SC, block size)
+    while (b != 0) {
+        const int64_t t = a % b;
+        a = b;
+        b = t;
+    }
+    const int64_t base = SC / a * kBnThreads;
+    const int64_t items = (int64_t)g->items;
+    int64_t G;
+    if (items == 0)
+        G = kBnThreads;
+    else if (base > items)
+        G = (items + kBnThreads - 1) / kBnThreads * kBnThreads;  // one item per thread
+    else {
+        const int64_t per = (items + kTarget - 1) / kTarget;  // items per thread
+        G = ((items + per - 1) / per + base - 1) / base * base;
+    }
+    g->G = (size_t)G;
+    g->R = SC > 0 ? (int32_t)((G + SC - 1) / SC) : 1;
+    g->NG = (g->R + kBnRowGroup - 1) / kBnRowGroup;
     return MFPSN_OK;
 }
 }  // namespace

@@ -11,9 +11,18 @@ namespace mfpsn {
 struct BnGeom {
     int32_t T, N, C, S, k, d;
     size_t M;        // N*C*S
-    int32_t tc;      // time steps per statistics chunk
-    int32_t chunks;  // ceil(T / tc)
+    int32_t tq, tr;  // T = tq * d + tr: class r has tq + (r < tr) steps
+    int32_t lc;      // class steps per walk chunk
+    int32_t nch;     // chunks per class, ceil(ceil(T/d) / lc)
+    size_t items;    // walk items, nch * d * M
+    size_t G;        // walk threads: thread t takes items t, t + G, ...; all of
+                     // them in channel ((t mod S*C) / S) (G is a multiple of
+                     // S*C and of the block size, or no thread has two items)
+    int32_t R;       // partial rows, ceil(G / (S*C)): thread t = row * S*C + j
+    int32_t NG;      // row groups of the first reduction level, ceil(R / kBnRowGroup)
 };
+constexpr int kBnThreads = 256;
+constexpr int kBnRowGroup = 16;
 
 size_t bn_workspace_bytes(const BnGeom& g);
 hipError_t launch_bn_forward_stats(const BnGeom& g, const float* x, const float* w, const float* gamma,
