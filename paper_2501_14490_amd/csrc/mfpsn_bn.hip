@@ -241,6 +241,7 @@ __global__ __launch_bounds__(kBnThreads) void bn_coef(BnGeom g, const float* __r
         const double sc = aux[4 * (size_t)c + 2], inv = aux[4 * (size_t)c + 3];
         const double gbf = (double)grad_bf[c];
         double dsc = 0.0;
+#pragma unroll 8
         for (int i = 0; i < g.k; ++i)
             dsc += (double)grad_wf[(size_t)c * g.k + i] * (double)w[(size_t)c * g.k + i];
         dsc -= gbf * mu;
@@ -256,20 +257,29 @@ __global__ __launch_bounds__(kBnThreads) void bn_coef(BnGeom g, const float* __r
     }
 }
 
-// The statistics path's input gradient in one reverse walk per item, steps
+// The backward of the statistics path in one reverse walk per item, steps
 // jtop down to j0 (jtop: up to K-1 steps above the chunk, which only feed
-// outputs of the chunk).  Step j gives dTv[j] = a + b Tv[j] and its terms
-// W[i] dTv[j] for the outputs j-(K-1-i); each output collects its terms in
-// a register, from i = 0 to K-1 (ascending taps, as the steps descend), and
-// is complete after its own step, when grad_x[j] gets it.  Slot of class
-// step t, in the ring and among the outputs: (jtop - t) mod K.
+// outputs of the chunk).  Step j gives dTv[j] = a + b Tv[j] and
+//  - its terms W[i] dTv[j] for the input gradients j-(K-1-i): each output
+//    collects its terms in a register, from i = 0 to K-1 (ascending taps, as
+//    the steps descend), and is complete after its own step, when grad_x[j]
+//    gets it;
+//  - for a step of the chunk, its terms dTv[j] x[j-(K-1-i)] of the weight
+//    gradient, summed per thread over all its items (one channel) and
+//    written to part[i * G + t].
+// Slot of class step t, in the ring and among the outputs: (jtop - t) mod K.
 template <int K>
-__global__ __launch_bounds__(kBnThreads) void bn_gx_walk(BnGeom g, const float* __restrict__ x,
+__global__ __launch_bounds__(kBnThreads) void bn_bwd_walk(BnGeom g, const float* __restrict__ x,
                                                          const float* __restrict__ w, const double* __restrict__ coef,
-                                                         float* __restrict__ grad_x)
+                                                         float* __restrict__ grad_x, double* __restrict__ part)
 {
+    const size_t t = (size_t)blockIdx.x * kBnThreads + threadIdx.x;
+    double gw[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        gw[i] = 0.0;
     const ptrdiff_t drow = (ptrdiff_t)g.d * (ptrdiff_t)g.M;
-    for (size_t q = (size_t)blockIdx.x * kBnThreads + threadIdx.x; q < g.items; q += g.G) {
+    for (size_t q = t; q < g.items; q += g.G) {
         const WalkItem it = walk_item(g, q);
         if (it.j0 >= it.j1)
             continue;
@@ -312,8 +322,12 @@ __global__ __launch_bounds__(kBnThreads) void bn_gx_walk(BnGeom g, const float* 
                 const int o = (u + K - 1 - i) % K;
                 A[o] = A[o] + wd[i] * dtv;
             }
-            if (j < it.j1)
+            if (j < it.j1) {
                 grad_x[so] = (float)((double)gstage[u] + A[u]);
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    gw[i] = __builtin_fma(dtv, ring[(u + K - 1 - i) % K], gw[i]);
+            }
             A[u] = 0.0;
             ring[u] = j - K >= 0 ? (double)stage[u] : 0.0;
         };
@@ -330,37 +344,6 @@ __global__ __launch_bounds__(kBnThreads) void bn_gx_walk(BnGeom g, const float* 
         for (int u = 0; u < K; ++u, --j, so -= drow)
             if (u < rem)
                 step(u, j);
-    }
-}
-
-// The statistics path's weight gradient: thread t's sums over the steps of
-// all its items of dTv[j] x[j-(K-1-i)] (forward walks like the
-// statistics'), written to part[i * G + t].  Inputs before time 0 are 0 in
-// the ring and add nothing.
-template <int K>
-__global__ __launch_bounds__(kBnThreads) void bn_gw_walk(BnGeom g, const float* __restrict__ x,
-                                                         const float* __restrict__ w, const double* __restrict__ coef,
-                                                         double* __restrict__ part)
-{
-    const size_t t = (size_t)blockIdx.x * kBnThreads + threadIdx.x;
-    double gw[K];
-#pragma unroll
-    for (int i = 0; i < K; ++i)
-        gw[i] = 0.0;
-    for (size_t q = t; q < g.items; q += g.G) {
-        const WalkItem it = walk_item(g, q);
-        if (it.j1 > it.j0) {
-            const double ca = coef[2 * it.c + 0], cb = coef[2 * it.c + 1];  // oldest loads: see bn_gx_walk
-            double wd[K], ring[K];
-            load_weights<K>(w + (size_t)it.c * K, wd);
-            __builtin_amdgcn_sched_barrier(0);
-            forward_walk<K>(g, it, x, wd, ring, [&](double v, int u) {
-                const double dtv = ca + cb * v;
-#pragma unroll
-                for (int i = 0; i < K; ++i)
-                    gw[i] = __builtin_fma(dtv, ring[(u + i + 1) % K], gw[i]);
-            });
-        }
     }
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -397,8 +380,7 @@ template <int K>
 void launch_bwd_k(const BnGeom& g, const float* x, const float* w, const double* coef, float* grad_x, double* part,
                   hipStream_t st)
 {
-    hipLaunchKernelGGL(bn_gx_walk<K>, walk_grid(g), dim3(kBnThreads), 0, st, g, x, w, coef, grad_x);
-    hipLaunchKernelGGL(bn_gw_walk<K>, walk_grid(g), dim3(kBnThreads), 0, st, g, x, w, coef, part);
+    hipLaunchKernelGGL(bn_bwd_walk<K>, walk_grid(g), dim3(kBnThreads), 0, st, g, x, w, coef, grad_x, part);
 }
 template <int... Ks>
 void stats_dispatch(const BnGeom& g, const float* x, const float* w, double* part, hipStream_t st,
