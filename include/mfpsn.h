@@ -188,9 +188,12 @@ int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int3
  * eps), grad_beta = grad_bf, dvar = -ds s / (2 (var + eps)), dmu = -s grad_bf,
  * dTv = dmu/n + dvar 2 (Tv - mu)/n, grad_x += W^T * dTv (latent weights,
  * double, ascending taps), grad_w = s grad_wf + sum dTv x (n = T*N*S).
- * Both need mfpsn_bn_workspace_size bytes of workspace (8-byte aligned;
- * the backward keeps dTv of every element there).  eps > 0; empty batches
- * are MFPSN_ERR_SHAPE; other dtypes MFPSN_ERR_DTYPE. */
+ * Both need mfpsn_bn_workspace_size bytes of workspace (8-byte aligned,
+ * caller-owned, contents not kept between calls: per-thread partial sums of
+ * the reductions and the per-channel coefficients of dTv).  x, w, gamma,
+ * beta, the gradients and aux are device memory, not written except the
+ * outputs named above.  eps > 0 and finite, else MFPSN_ERR_PARAM; empty
+ * batches are MFPSN_ERR_SHAPE; dtypes other than f32 MFPSN_ERR_DTYPE. */
 int mfpsn_bn_workspace_size(const mfpsn_desc* desc, size_t* bytes);
 int mfpsn_bn_forward_stats(const mfpsn_desc* desc, const float* x, const float* w, const float* gamma,
                            const float* beta, float eps, float* w_f, float* b_f, double* aux, double* stats,

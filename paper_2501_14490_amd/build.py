@@ -67,12 +67,12 @@ def _units():
     obj = os.path.join(BUILD, "kernels_misc.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
                         "-c", src, "-o", obj], [src, *headers]))
-    for name in ("mfpsn_api.cpp", "mfpsn_dispatch.cpp"):
+    for name in ("mfpsn_api.cpp", "mfpsn_api_ext.cpp", "mfpsn_dispatch.cpp"):
         obj = os.path.join(BUILD, name.replace(".cpp", ".o"))
         cpp = os.path.join(CSRC, name)
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
                       [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
-                       os.path.join(CSRC, "mfpsn_bn.h"), *headers]))
+                       os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(CSRC, "mfpsn_validate.h"), *headers]))
     return units
 
 

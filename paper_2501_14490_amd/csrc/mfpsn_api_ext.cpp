@@ -1,0 +1,241 @@
+// C ABI of libmfpsn.so beside the training step: the batch-normalized
+// threshold with fused-weight quantization, the quantizer's latent-weight
+// gradient and step-by-step inference.  Declarations and the contract of
+// every entry point are in include/mfpsn.h.
+#include "mfpsn.h"
+
+#include <math.h>
+#include <stdint.h>
+
+#include "mfpsn_bn.h"
+#include "mfpsn_internal.h"
+#include "mfpsn_qgrad.h"
+#include "mfpsn_stream.h"
+#include "mfpsn_validate.h"
+
+using namespace mfpsn;
+
+namespace {
+
+// The streaming step looks at one time step: the descriptor's T plays no
+// part, every other field is checked as for the whole-sequence calls.
+int validate_stream(const mfpsn_desc* d)
+{
+    if (!d)
+        return MFPSN_ERR_NULL;
+    mfpsn_desc one = *d;
+    one.T = 0;
+    return validate(&one);
+}
+
+// History slots of the streaming step: the receptive field (k-1)*d + 1.
+int64_t ring_steps(const mfpsn_desc* d) { return (int64_t)(d->k - 1) * d->dilation + 1; }
+
+}  // namespace
+
+namespace {
+// The batch-normalization entry points take float x (MFPSN_F32) and one
+// layer's shapes; T is used.
+int validate_bn(const mfpsn_desc* d, BnGeom* g)
+{
+    const int st = validate(d);
+    if (st != MFPSN_OK)
+        return st;
+    if (d->dtype != MFPSN_F32)
+        return MFPSN_ERR_DTYPE;
+    g->T = d->T;
+    g->N = d->N;
+    g->C = d->C;
+    g->S = d->S;
+    g->k = d->k;
+    g->d = d->dilation;
+    g->M = (size_t)d->N * d->C * d->S;
+    g->tq = d->T / d->dilation;
+    g->tr = d->T % d->dilation;
+    // Walk plan: a grid of about three waves per SIMD (256 CUs x 4 SIMDs),
+    // chunks of each residue class such that each thread has two or three
+    // items (each chunk at least 2k steps), and a thread count that spreads
+    // the items evenly and keeps every thread in one channel
+    constexpr int64_t kTarget = 256 * 4 * 3 * 64;
+    const int64_t L = (d->T + d->dilation - 1) / d->dilation;
+    const int64_t walks = (int64_t)g->M * d->dilation;
+    int64_t nch = walks > 0 ? (2 * kTarget + walks - 1) / walks : 1;
+    const int64_t max_nch = L / (2 * (int64_t)d->k);
+    if (nch > max_nch)
+        nch = max_nch;
+    if (nch < 1)
+        nch = 1;
+    g->lc = L > 0 ? (int32_t)((L + nch - 1) / nch) : 1;  // an empty sequence has no chunks
+    g->nch = (int32_t)((L + g->lc - 1) / g->lc);
+    g->items = (size_t)g->nch * d->dilation * g->M;
+    const int64_t SC = (int64_t)d->S * d->C;
+    int64_t a = SC, b = kBnThreads;  // base = lcm(SC, block size)
+    while (b != 0) {
+        const int64_t t = a % b;
+        a = b;
+        b = t;
+    }
+    const int64_t base = SC / a * kBnThreads;
+    const int64_t items = (int64_t)g->items;
+    int64_t G;
+    if (items == 0)
+        G = kBnThreads;
+    else if (base > items)
+        G = (items + kBnThreads - 1) / kBnThreads * kBnThreads;  // one item per thread
+    else {
+        const int64_t per = (items + kTarget - 1) / kTarget;  // items per thread
+        G = ((items + per - 1) / per + base - 1) / base * base;
+    }
+    g->G = (size_t)G;
+    g->R = SC > 0 ? (int32_t)((G + SC - 1) / SC) : 1;
+    g->NG = (g->R + kBnRowGroup - 1) / kBnRowGroup;
+    return MFPSN_OK;
+}
+}  // namespace
+
+int mfpsn_bn_workspace_size(const mfpsn_desc* desc, size_t* bytes)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!bytes)
+        return MFPSN_ERR_NULL;
+    *bytes = g.M > 0 && g.T > 0 ? bn_workspace_bytes(g) : 0;
+    return MFPSN_OK;
+}
+
+int mfpsn_bn_forward_stats(const mfpsn_desc* desc, const float* x, const float* w, const float* gamma,
+                           const float* beta, float eps, float* w_f, float* b_f, double* aux, double* stats,
+                           void* workspace, size_t workspace_bytes, void* stream)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!(eps > 0.0f) || !isfinite(eps))
+        return MFPSN_ERR_PARAM;
+    if (g.M == 0 || g.T == 0)
+        return MFPSN_ERR_SHAPE;  // statistics of an empty batch are undefined
+    if (!x || !w || !gamma || !beta || !w_f || !b_f || !aux)
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(gamma, 4) || !aligned(beta, 4) || !aligned(w_f, 4) ||
+        !aligned(b_f, 4) || !aligned(aux, 8) || !aligned(stats, 8))
+        return MFPSN_ERR_ALIGN;
+    if (!workspace || workspace_bytes < bn_workspace_bytes(g) || !aligned(workspace, 8))
+        return MFPSN_ERR_WORKSPACE;
+    if (launch_bn_forward_stats(g, x, w, gamma, beta, eps, w_f, b_f, aux, stats, workspace, (hipStream_t)stream) !=
+        hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_bn_backward(const mfpsn_desc* desc, const float* x, const float* w, const double* aux, float eps,
+                      const float* grad_wf, const float* grad_bf, float* grad_x, float* grad_w, float* grad_gamma,
+                      float* grad_beta, void* workspace, size_t workspace_bytes, void* stream)
+{
+    BnGeom g;
+    const int st = validate_bn(desc, &g);
+    if (st != MFPSN_OK)
+        return st;
+    if (!(eps > 0.0f) || !isfinite(eps))
+        return MFPSN_ERR_PARAM;
+    if (g.M == 0 || g.T == 0)
+        return MFPSN_ERR_SHAPE;
+    if (!x || !w || !aux || !grad_wf || !grad_bf || !grad_x || !grad_w || !grad_gamma || !grad_beta)
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(aux, 8) || !aligned(grad_wf, 4) || !aligned(grad_bf, 4) ||
+        !aligned(grad_x, 4) || !aligned(grad_w, 4) || !aligned(grad_gamma, 4) || !aligned(grad_beta, 4))
+        return MFPSN_ERR_ALIGN;
+    if (!workspace || workspace_bytes < bn_workspace_bytes(g) || !aligned(workspace, 8))
+        return MFPSN_ERR_WORKSPACE;
+    if (launch_bn_backward(g, x, w, aux, eps, grad_wf, grad_bf, grad_x, grad_w, grad_gamma, grad_beta, workspace,
+                           (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_quantizer_grad(const float* w, const int8_t* shift, int32_t shift_lo, int32_t shift_hi,
+                         const float* grad_wq, int64_t count, int32_t mode, float* grad_w, void* stream)
+{
+    if (count < 0 || count >= ((int64_t)1 << 31))
+        return MFPSN_ERR_SHAPE;
+    if (shift_lo > shift_hi || shift_lo < -128 || shift_hi > 127 || (mode != MFPSN_STE_WHOLE && mode != MFPSN_STE_ROUND))
+        return MFPSN_ERR_PARAM;
+    if (count > 0 && (!grad_wq || !grad_w || (mode == MFPSN_STE_ROUND && (!w || !shift))))
+        return MFPSN_ERR_NULL;
+    if (!aligned(w, 4) || !aligned(grad_wq, 4) || !aligned(grad_w, 4))
+        return MFPSN_ERR_ALIGN;
+    if (launch_quantizer_grad(w, shift, shift_lo, shift_hi, grad_wq, count, mode, grad_w, (hipStream_t)stream) !=
+        hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_stream_ring_bytes(const mfpsn_desc* desc, int32_t* steps, size_t* bytes)
+{
+    int st = validate_stream(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (!steps && !bytes)
+        return MFPSN_ERR_NULL;
+    const int64_t R = ring_steps(desc);
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    if (steps)
+        *steps = (int32_t)R;
+    if (bytes)
+        *bytes = (size_t)R * (size_t)M * (size_t)elem_bytes(desc->dtype);
+    return MFPSN_OK;
+}
+
+int mfpsn_stream_step(const mfpsn_desc* desc, int64_t t, const void* x_t, void* ring, const int8_t* sign,
+                      const int8_t* shift, const void* bias, uint8_t* spikes_t, void* h_t, void* stream)
+{
+    int st = validate_stream(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (t < 0)
+        return MFPSN_ERR_PARAM;
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    if (M > 0 && (!x_t || !ring || !spikes_t))
+        return MFPSN_ERR_NULL;
+    if (desc->C > 0 && (!sign || !shift || !bias))
+        return MFPSN_ERR_NULL;
+    const int es = elem_bytes(desc->dtype);
+    if (!aligned(x_t, es) || !aligned(ring, es) || !aligned(bias, 4) || !aligned(h_t, 4))
+        return MFPSN_ERR_ALIGN;
+    if (M == 0)
+        return MFPSN_OK;
+    const int64_t R = ring_steps(desc);
+    StreamArgs a;
+    a.M = M;
+    a.C = desc->C;
+    a.S = desc->S;
+    a.k = desc->k;
+    a.d = desc->dilation;
+    a.R = (int32_t)R;
+    a.slot = (int32_t)(t % R);
+    const int64_t reach = t / desc->dilation;  // taps that look back at most t steps
+    a.m_max = (int32_t)(reach < desc->k - 1 ? reach : desc->k - 1);
+    for (int m = 0; m < MFPSN_MAX_K; ++m) {
+        int64_t sl = m < desc->k ? a.slot - (int64_t)m * desc->dilation : 0;  // >= -(R-1)
+        if (sl < 0)
+            sl += R;
+        a.rows[m] = sl * M;
+    }
+    a.shift_lo = desc->shift_lo;
+    a.shift_hi = desc->shift_hi;
+    a.v_th = desc->v_th;
+    a.v_th_q = desc->v_th_q;
+    a.x_t = x_t;
+    a.ring = ring;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.spikes = spikes_t;
+    a.h_t = h_t;
+    if (launch_stream_step(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+

@@ -100,10 +100,64 @@ def test_bn_stages_match_oracle(orc, T, N, C, S, k, d):
     run_case(orc, T, N, C, S, k, d, seed=T * 7 + k)
 
 
+@pytest.mark.parametrize("T,N,C,S,k,d", [(25, 96, 64, 16, 3, 2), (50, 48, 128, 16, 8, 1)])
+def test_bn_threads_with_several_items(orc, T, N, C, S, k, d):
+    """Shapes with more than 2^17 (chunk, class, column) items, so that each
+    thread of the walks sums two items of its channel and the partials span
+    several row groups of the reduction; classes of unequal length (T not a
+    multiple of d) and chunks that are not a multiple of k steps."""
+    run_case(orc, T, N, C, S, k, d, seed=T + k)
+
+
 def test_bn_audio_spike_shape(orc):
     """The audio-spike layer's channels and order (C=512, k=16, d=4) on a
     shorter batch, so that the oracle finishes in seconds."""
     run_case(orc, 40, 16, 512, 1, 16, 4, seed=2)
+
+
+@pytest.mark.parametrize("d", [1, 4])
+def test_bn_full_audio_spike_layer_sampled_channels(orc, d):
+    """The whole audio-spike layer (T=250, N=256, C=512, k=16), in the launch
+    configuration the bench times, checked on a sample of channels: every
+    stage of the step is independent per channel, so the oracle run on the
+    sampled channels' slices of x, W, gamma, beta and of the GPU's gradients
+    must give the GPU's values on those channels, to the bars above."""
+    T, N, C, S, k = 250, 256, 512, 1, 16
+    x, w, gamma, beta, g = make_case(T, N, C, S, k, seed=400 + d)
+    desc = mfpsn.make_desc(x.shape, k, d, "f32", "sigmoid", 4.0, 0.0, 0, 0, 7)
+    xt, wt = dev(x), dev(w)
+    ws = mfpsn.bn_workspace(desc, DEV)
+    w_f, b_f, aux, stats = mfpsn.bn_forward_stats(desc, xt, wt, dev(gamma), dev(beta), EPS, ws, want_stats=True)
+    sign, shift = mfpsn.quantize(w_f, 0, 7)
+    spikes, sg = mfpsn.forward(desc, xt, sign, shift, b_f, want_sg=True)
+    gx, gwf, gbf = mfpsn.backward(desc, xt, dev(g), sign, shift, b_f, sg=sg)
+    gxq = gx.clone()
+    grad_w, grad_gamma, grad_beta = mfpsn.bn_backward(desc, xt, wt, aux, gwf, gbf, gx, EPS, ws)
+    torch.cuda.synchronize()
+    ch = np.array([0, 1, 77, 255, 256, 300, 510, 511])
+    xs = np.ascontiguousarray(x[:, :, ch])
+    ref = orc.bn_forward_stats(xs, w[ch], gamma[ch], beta[ch], EPS, k, d)
+    a = aux.cpu().numpy()[ch]
+    rel_close(stats.cpu().numpy()[ch], ref["stats"], 1e-12, 1e-9)
+    rel_close(a[:, 0], ref["aux"][:, 0], 1e-12, 1e-12)
+    rel_close(a[:, 1], ref["aux"][:, 1], 1e-9, 1e-12)
+    rel_close(a[:, 2:], ref["aux"][:, 2:], 1e-9)
+    wf_np, bf_np = w_f.cpu().numpy()[ch], b_f.cpu().numpy()[ch]
+    rel_close(wf_np, ref["w_f"], 1e-6)
+    rel_close(bf_np, ref["b_f"], 1e-6, 1e-7)
+    s_ref, sh_ref = orc.quantize(wf_np, 0, 7)
+    assert np.array_equal(sign.cpu().numpy()[ch], s_ref) and np.array_equal(shift.cpu().numpy()[ch], sh_ref)
+    _, S_ref = orc.forward_f32(xs, s_ref, sh_ref, bf_np, k, d, 0.0, 0, 7)
+    assert np.array_equal(spikes.cpu().numpy()[:, :, ch], S_ref)
+    rb = orc.bn_backward(xs, w[ch], gamma[ch], EPS, a, gwf.cpu().numpy()[ch].astype(np.float64),
+                         gbf.cpu().numpy()[ch].astype(np.float64),
+                         np.ascontiguousarray(gxq.cpu().numpy()[:, :, ch]).astype(np.float64), k, d)
+    want_gx = rb["grad_x"].astype(np.float32)
+    got_gx = np.ascontiguousarray(gx.cpu().numpy()[:, :, ch])
+    assert np.array_equal(got_gx.view(np.uint32), want_gx.view(np.uint32))
+    rel_close(grad_gamma.cpu().numpy()[ch], rb["grad_gamma"].astype(np.float32), 1e-6, 1e-12)
+    rel_close(grad_beta.cpu().numpy()[ch], rb["grad_beta"].astype(np.float32), 0.0)
+    rel_close(grad_w.cpu().numpy()[ch], rb["grad_w"], 1e-5, 1e-6)
 
 
 def test_bn_autograd_function_equals_the_stages(orc):
