@@ -350,6 +350,82 @@ def bn_step(torch, dev, wl, case, steps: int, warmup: int):
     }), flush=True)
 
 
+def stack_step(torch, dev, wl, case, mode: str, steps: int, warmup: int):
+    """The sawtooth stack: the workload's layers (one per dilation) chained
+    through identity stateless layers.  Forward: layer l's spikes become
+    layer l+1's input (mfpsn_spikes_to_input); backward: layer l+1's grad_x is
+    layer l's grad_spikes.  Float storage types only.  value = layers *
+    T*N*C*S / step time, the casts included."""
+    from paper_2501_14490_amd import mfpsn
+
+    if wl.dtype == "q8_8":
+        log("the chained stack takes float or bfloat16 storage: choose an f32 or bf16 workload")
+        sys.exit(2)
+
+    def dev_tensor(a, storage):
+        if wl.dtype == "bf16" and storage:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x0 = dev_tensor(case["x"], True)
+    g_top = dev_tensor(case["grad_spikes"], True)
+    sign = dev_tensor(case["sign"], False)
+    shift = dev_tensor(case["shift"], False)
+    bias = dev_tensor(case["bias"], False)
+    P = len(wl.dilations)
+    layers = []
+    for li, d in enumerate(wl.dilations):
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        layers.append({
+            "d": d, "desc": desc,
+            "x": x0 if li == 0 else torch.empty(wl.shape, dtype=x0.dtype, device=dev),
+            "ws": torch.empty(max(mfpsn.mfpsn_backward_workspace_size(desc), 8), dtype=torch.uint8, device=dev),
+            "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
+            "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
+            "h": torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev) if mode == "h" else None,
+            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if mode == "sg" else None,
+            "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+            "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+        })
+    stream = torch.cuda.current_stream()
+    dt = mfpsn.DTYPES[wl.dtype]
+
+    def step():
+        for li, L in enumerate(layers):
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], L["sg"], stream)
+            if li + 1 < P:
+                mfpsn.mfpsn_spikes_to_input(L["spikes"], dt, layers[li + 1]["x"], stream)
+        g = g_top
+        for li in reversed(range(P)):
+            L = layers[li]
+            mfpsn.mfpsn_backward(L["desc"], L["x"], g, L["h"], L["sg"], sign, shift, bias, L["gx"], L["gw"],
+                                 L["gb"], L["ws"], stream=stream)
+            g = L["gx"]
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    value = P * wl.elements / (elapsed / steps)
+    rate = float(torch.cat([L["spikes"].reshape(-1)[: 1 << 20].float().mean().reshape(1) for L in layers]).mean())
+    log(f"stack step {elapsed * 1e3 / steps:.3f} ms, {value / 1e9:.2f} G elements/s, "
+        f"mean firing rate of the layers {rate:.3f}")
+    print(json.dumps({
+        "metric": "chained sawtooth stack fwd+bwd elements/s (T*N*C*S per layer)",
+        "value": value, "unit": "elements/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": elapsed * 1e3 / steps, "higher_is_better": True, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": f"{wl.name}: x[{','.join(map(str, wl.shape))}] {wl.dtype}, k={wl.k}, layers "
+                               f"d={wl.dilations} chained (spikes of one layer are the next layer's input); "
+                               f"forward of every layer, then backward in reverse",
+                   "backward_input": mode},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -367,6 +443,8 @@ def main():
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--bn-step", action="store_true",
                     help="only time the batch-normalized-threshold training step of App. C (float workloads)")
+    ap.add_argument("--stack", action="store_true",
+                    help="only time the workload's layers chained into one sawtooth stack (float workloads)")
     ap.add_argument("--stream-inference", action="store_true",
                     help="only time step-by-step inference (mfpsn_stream_step per layer and time step, "
                          "the sequence replayed from a HIP graph)")
@@ -413,6 +491,9 @@ def main():
         return
     if args.bn_step:
         bn_step(torch, dev, wl, case, args.steps, args.warmup)
+        return
+    if args.stack:
+        stack_step(torch, dev, wl, case, mode, args.steps, args.warmup)
         return
 
     def dev_tensor(a, storage):

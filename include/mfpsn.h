@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 6
+#define MFPSN_ABI_VERSION 7
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -255,6 +255,19 @@ int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period);
 
 /* Static description of a status code. */
 const char* mfpsn_status_string(int status);
+
+/* Chaining layers: one layer's spikes as the next layer's input, for a
+ * stack of neuron layers joined by identity stateless layers (the sawtooth
+ * stack of Sec. 4.1, dilations 1..P one layer after the other).
+ * x[i] = spikes[i] != 0 ? 1 : 0 in the storage type `dtype` (MFPSN_F32
+ * float 1.0, MFPSN_BF16 bfloat16 1.0, MFPSN_Q8_8 int16 256), elementwise
+ * over `count` elements of device memory (spikes uint8, x 2 or 4 bytes,
+ * aligned to its element size, not overlapping spikes).  In the backward,
+ * the next layer's grad_x is this layer's grad_spikes unchanged for the
+ * float storage types (the derivative of the identity).  Errors:
+ * MFPSN_ERR_SHAPE for count < 0, MFPSN_ERR_DTYPE, MFPSN_ERR_NULL,
+ * MFPSN_ERR_ALIGN; count = 0 does nothing. */
+int mfpsn_spikes_to_input(const uint8_t* spikes, int64_t count, int32_t dtype, void* x, void* stream);
 
 /* MFPSN_ABI_VERSION of the loaded library. */
 int32_t mfpsn_abi_version(void);

@@ -60,6 +60,10 @@ def _units():
     obj = os.path.join(BUILD, "qgrad.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
                   [qg_src, os.path.join(CSRC, "mfpsn_qgrad.h")]))
+    chain_src = os.path.join(CSRC, "mfpsn_chain.hip")
+    obj = os.path.join(BUILD, "chain.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", chain_src, "-o", obj],
+                  [chain_src, os.path.join(CSRC, "mfpsn_chain.h"), os.path.join(INCLUDE, "mfpsn.h")]))
     stream_src = os.path.join(CSRC, "mfpsn_stream.hip")
     obj = os.path.join(BUILD, "stream.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", stream_src, "-o", obj],
@@ -72,7 +76,8 @@ def _units():
         cpp = os.path.join(CSRC, name)
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
                       [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
-                       os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(CSRC, "mfpsn_validate.h"), *headers]))
+                       os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(CSRC, "mfpsn_validate.h"),
+                       os.path.join(CSRC, "mfpsn_chain.h"), *headers]))
     return units
 
 

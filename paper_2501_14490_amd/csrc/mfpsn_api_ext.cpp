@@ -1,6 +1,6 @@
 // C ABI of libmfpsn.so beside the training step: the batch-normalized
 // threshold with fused-weight quantization, the quantizer's latent-weight
-// gradient and step-by-step inference.  Declarations and the contract of
+// gradient, step-by-step inference and the chaining of layers.  Declarations and the contract of
 // every entry point are in include/mfpsn.h.
 #include "mfpsn.h"
 
@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include "mfpsn_bn.h"
+#include "mfpsn_chain.h"
 #include "mfpsn_internal.h"
 #include "mfpsn_qgrad.h"
 #include "mfpsn_stream.h"
@@ -239,3 +240,20 @@ int mfpsn_stream_step(const mfpsn_desc* desc, int64_t t, const void* x_t, void* 
     return MFPSN_OK;
 }
 
+
+int mfpsn_spikes_to_input(const uint8_t* spikes, int64_t count, int32_t dtype, void* x, void* stream)
+{
+    if (count < 0)
+        return MFPSN_ERR_SHAPE;
+    if (dtype != MFPSN_F32 && dtype != MFPSN_BF16 && dtype != MFPSN_Q8_8)
+        return MFPSN_ERR_DTYPE;
+    if (count == 0)
+        return MFPSN_OK;
+    if (!spikes || !x)
+        return MFPSN_ERR_NULL;
+    if (!aligned(x, elem_bytes(dtype)))
+        return MFPSN_ERR_ALIGN;
+    if (launch_spikes_to_input(spikes, count, dtype, x, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}

@@ -74,6 +74,8 @@ _lib.mfpsn_stream_ring_bytes.argtypes = [_DP, ctypes.POINTER(ctypes.c_int32), ct
 _lib.mfpsn_stream_ring_bytes.restype = ctypes.c_int
 _lib.mfpsn_stream_step.argtypes = [_DP, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_stream_step.restype = ctypes.c_int
+_lib.mfpsn_spikes_to_input.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, _P, _P]
+_lib.mfpsn_spikes_to_input.restype = ctypes.c_int
 _lib.mfpsn_sawtooth_dilation.argtypes = [ctypes.c_int32, ctypes.c_int32]
 _lib.mfpsn_sawtooth_dilation.restype = ctypes.c_int32
 _lib.mfpsn_status_string.argtypes = [ctypes.c_int]
@@ -167,6 +169,11 @@ def mfpsn_quantizer_grad(w, shift, shift_lo: int, shift_hi: int, grad_wq, mode: 
     _check(_lib.mfpsn_quantizer_grad(_ptr(w), _ptr(shift), int(shift_lo), int(shift_hi), _ptr(grad_wq),
                                      int(grad_wq.numel()), int(mode), _ptr(grad_w), _stream(stream)),
            "mfpsn_quantizer_grad")
+
+
+def mfpsn_spikes_to_input(spikes, dtype: int, x, stream=None) -> None:
+    _check(_lib.mfpsn_spikes_to_input(_ptr(spikes), int(spikes.numel()), int(dtype), _ptr(x), _stream(stream)),
+           "mfpsn_spikes_to_input")
 
 
 def mfpsn_bn_workspace_size(desc: MfpsnDesc) -> int:
@@ -268,6 +275,16 @@ def quantizer_grad(w, shift, grad_wq, ste="whole", shift_lo: int = 0, shift_hi: 
     out = torch.empty_like(grad_wq)
     mfpsn_quantizer_grad(w, shift, shift_lo, shift_hi, grad_wq, STE[ste], out, stream)
     return out
+
+
+def spikes_to_input(spikes, dtype: str = "f32", stream=None):
+    """One layer's spikes (uint8) as the next layer's input in storage type
+    `dtype` ("f32", "bf16": returned as torch.bfloat16, "q8_8": int16 256)."""
+    _expect(spikes, torch.uint8, spikes.device, "spikes")
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "q8_8": torch.int16}[dtype]
+    x = torch.empty(spikes.shape, dtype=tdt, device=spikes.device)
+    mfpsn_spikes_to_input(spikes, DTYPES[dtype], x, stream)
+    return x
 
 
 def bn_workspace(desc: MfpsnDesc, device):

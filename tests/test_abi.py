@@ -73,7 +73,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 6
+    assert lib.mfpsn_abi_version() == 7
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -231,3 +231,15 @@ def test_bn_validation(lib):
     assert b(ctypes.byref(d), *bargs, -1.0, *grads, FAKE, need, None) == -3
     assert b(ctypes.byref(d), FAKE, FAKE, None, 1e-5, *grads, FAKE, need, None) == -1
     assert b(ctypes.byref(d), *bargs, 1e-5, *grads, None, need, None) == -5
+
+
+def test_spikes_to_input_validation(lib):
+    f = lib.mfpsn_spikes_to_input
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert f(FAKE, -1, 0, FAKE, None) == -2                 # negative count
+    assert f(FAKE, 10, 3, FAKE, None) == -4                 # unknown storage type
+    assert f(None, 10, 0, FAKE, None) == -1
+    assert f(FAKE, 10, 0, None, None) == -1
+    assert f(FAKE, 10, 0, FAKE + 2, None) == -6             # float output 4-byte aligned
+    assert f(FAKE, 10, 1, FAKE + 1, None) == -6             # bfloat16 output 2-byte aligned
+    assert f(None, 0, 2, None, None) == 0                   # nothing to do
