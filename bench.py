@@ -426,6 +426,78 @@ def stack_step(torch, dev, wl, case, mode: str, steps: int, warmup: int):
     }), flush=True)
 
 
+def time_last(torch, dev, wl, case, steps: int, warmup: int):
+    """The forward (charge and fire, spikes only) of the workload's layers in
+    the time-last layout [N][C][S][T] (mfpsn_forward_time_last), timed beside
+    the time-first forward (mfpsn_forward, spikes only) on the same inputs.
+    value = layers * T*N*C*S / time of the time-last forwards; roofline:
+    algorithmic bytes (x read, spikes written) per launch over its average
+    duration."""
+    from paper_2501_14490_amd import mfpsn
+
+    es = {"f32": 4, "bf16": 2, "q8_8": 2}[wl.dtype]
+    x_tf = case["x"]
+    if wl.dtype == "bf16":
+        x_tf = x_tf.view(np.int16)
+    x_tl = np.ascontiguousarray(np.moveaxis(x_tf, 0, -1))
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        return t.view(torch.bfloat16) if wl.dtype == "bf16" else t
+
+    xs = {"tl": up(x_tl), "tf": up(x_tf)}
+    sign, shift, bias = (torch.from_numpy(np.ascontiguousarray(case[n])).to(dev) for n in ("sign", "shift", "bias"))
+    descs = [mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0, wl.s_max)
+             for d in wl.dilations]
+    spk = {"tl": torch.empty(x_tl.shape, dtype=torch.uint8, device=dev),
+           "tf": torch.empty(wl.shape, dtype=torch.uint8, device=dev)}
+    stream = torch.cuda.current_stream()
+    hev = HipEvents()
+
+    def run(layout, ev=None):
+        for li, desc in enumerate(descs):
+            if ev is not None:
+                hev.record(ev[li][0], stream)
+            if layout == "tl":
+                mfpsn.mfpsn_forward_time_last(desc, xs["tl"], sign, shift, bias, spk["tl"], None, stream)
+            else:
+                mfpsn.mfpsn_forward(desc, xs["tf"], sign, shift, bias, spk["tf"], None, None, stream)
+            if ev is not None:
+                hev.record(ev[li][1], stream)
+
+    out = {}
+    for layout in ("tl", "tf"):
+        for _ in range(warmup):
+            run(layout)
+        torch.cuda.synchronize()
+        evs = [[[hev.new(), hev.new()] for _ in descs] for _ in range(steps)]
+        t0 = time.perf_counter()
+        for s_ in range(steps):
+            run(layout, evs[s_])
+        torch.cuda.synchronize()
+        out[layout] = {"elapsed": (time.perf_counter() - t0) / steps,
+                       "launch_ms": float(np.mean([hev.elapsed_ms(*e) for st in evs for e in st]))}
+    same = bool(torch.equal(spk["tl"].cpu(), torch.from_numpy(np.ascontiguousarray(
+        np.moveaxis(spk["tf"].cpu().numpy(), 0, -1)))))
+    P = len(descs)
+    value = P * wl.elements / out["tl"]["elapsed"]
+    alg = wl.elements * (es + 1)
+    ach = alg / (out["tl"]["launch_ms"] * 1e-3) / 1e9
+    log(f"time-last forward {out['tl']['launch_ms'] * 1e3:.1f} us per layer ({ach:.0f} GB/s alg), time-first "
+        f"{out['tf']['launch_ms'] * 1e3:.1f} us; {value / 1e9:.2f} G elements/s; last layer's spikes equal: {same}")
+    print(json.dumps({
+        "metric": "time-last forward elements/s (T*N*C*S per layer)",
+        "value": value, "unit": "elements/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": out["tl"]["elapsed"] * 1e3, "higher_is_better": True, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": f"{wl.name}: x[{','.join(map(str, x_tl.shape))}] {wl.dtype} time last, k={wl.k}, "
+                               f"one layer per d={wl.dilations}; forward, spikes only"},
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS},
+        "time_first_forward_us_per_layer": out["tf"]["launch_ms"] * 1e3,
+        "time_last_forward_us_per_layer": out["tl"]["launch_ms"] * 1e3,
+        "spikes_equal_time_first": same,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -443,6 +515,8 @@ def main():
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--bn-step", action="store_true",
                     help="only time the batch-normalized-threshold training step of App. C (float workloads)")
+    ap.add_argument("--time-last", action="store_true",
+                    help="only time the forward in the time-last layout [N][C][S][T] beside the time-first one")
     ap.add_argument("--stack", action="store_true",
                     help="only time the workload's layers chained into one sawtooth stack (float workloads)")
     ap.add_argument("--stream-inference", action="store_true",
@@ -494,6 +568,9 @@ def main():
         return
     if args.stack:
         stack_step(torch, dev, wl, case, mode, args.steps, args.warmup)
+        return
+    if args.time_last:
+        time_last(torch, dev, wl, case, args.steps, args.warmup)
         return
 
     def dev_tensor(a, storage):

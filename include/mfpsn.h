@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 7
+#define MFPSN_ABI_VERSION 8
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -255,6 +255,19 @@ int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period);
 
 /* Static description of a status code. */
 const char* mfpsn_status_string(int status);
+
+/* Forward (Eq. mfdpsn_charge, Eq. mfdpsn_fire) in the time-last layout, time
+ * innermost (the paper's second layout):
+ *   x      : [N][C][S][T] storage type of desc->dtype
+ *   spikes : uint8 [N][C][S][T];  h_out : optional (may be NULL), [N][C][S][T]
+ *            float (F32, BF16) or int32 (Q8.8)
+ * sign, shift, bias, desc (sizes T, N, C, S as for mfpsn_forward) and the
+ * values computed are those of mfpsn_forward: the outputs are its outputs
+ * with the time axis moved last, bit for bit.  Same alignment and errors as
+ * mfpsn_forward; MFPSN_ERR_SHAPE also when N*C*S*ceil(T/256) >= 2^33.  The
+ * library keeps no state; the call is asynchronous on `stream`. */
+int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
+                            const void* bias, uint8_t* spikes, void* h_out, void* stream);
 
 /* Chaining layers: one layer's spikes as the next layer's input, for a
  * stack of neuron layers joined by identity stateless layers (the sawtooth

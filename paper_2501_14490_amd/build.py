@@ -60,6 +60,10 @@ def _units():
     obj = os.path.join(BUILD, "qgrad.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
                   [qg_src, os.path.join(CSRC, "mfpsn_qgrad.h")]))
+    tl_src = os.path.join(CSRC, "mfpsn_tl.hip")
+    obj = os.path.join(BUILD, "tl.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", tl_src, "-o", obj],
+                  [tl_src, os.path.join(CSRC, "mfpsn_tl.h"), os.path.join(INCLUDE, "mfpsn.h")]))
     chain_src = os.path.join(CSRC, "mfpsn_chain.hip")
     obj = os.path.join(BUILD, "chain.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", chain_src, "-o", obj],
@@ -77,7 +81,7 @@ def _units():
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
                       [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
                        os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(CSRC, "mfpsn_validate.h"),
-                       os.path.join(CSRC, "mfpsn_chain.h"), *headers]))
+                       os.path.join(CSRC, "mfpsn_chain.h"), os.path.join(CSRC, "mfpsn_tl.h"), *headers]))
     return units
 
 

@@ -1,6 +1,7 @@
 // C ABI of libmfpsn.so beside the training step: the batch-normalized
 // threshold with fused-weight quantization, the quantizer's latent-weight
-// gradient, step-by-step inference and the chaining of layers.  Declarations and the contract of
+// gradient, step-by-step inference, the chaining of layers and the forward
+// in the time-last layout.  Declarations and the contract of
 // every entry point are in include/mfpsn.h.
 #include "mfpsn.h"
 
@@ -12,6 +13,7 @@
 #include "mfpsn_internal.h"
 #include "mfpsn_qgrad.h"
 #include "mfpsn_stream.h"
+#include "mfpsn_tl.h"
 #include "mfpsn_validate.h"
 
 using namespace mfpsn;
@@ -254,6 +256,62 @@ int mfpsn_spikes_to_input(const uint8_t* spikes, int64_t count, int32_t dtype, v
     if (!aligned(x, elem_bytes(dtype)))
         return MFPSN_ERR_ALIGN;
     if (launch_spikes_to_input(spikes, count, dtype, x, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
+                            const void* bias, uint8_t* spikes, void* h_out, void* stream)
+{
+    const int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    // segments of 256 time steps, or of 64 for short sequences (fewer idle lanes)
+    const int spl = desc->T > 96 ? 4 : 1;
+    const int64_t nseg = ((int64_t)desc->T + 64 * spl - 1) / (64 * spl);
+    if (M * nseg >= ((int64_t)1 << 33))  // blocks of kTlWaves segments must fit the grid
+        return MFPSN_ERR_SHAPE;
+    if (M == 0 || desc->T == 0)
+        return MFPSN_OK;
+    if (!x || !sign || !shift || !bias || !spikes)
+        return MFPSN_ERR_NULL;
+    const int es = elem_bytes(desc->dtype);
+    if (!aligned(x, es) || !aligned(bias, 4) || !aligned(h_out, 4))
+        return MFPSN_ERR_ALIGN;
+    TlArgs a;
+    a.x = x;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.spikes = spikes;
+    a.h_out = h_out;
+    a.M = M;
+    a.T = desc->T;
+    a.C = desc->C;
+    a.S = desc->S;
+    a.k = desc->k;
+    a.d = desc->dilation;
+    a.steps_per_lane = spl;
+    a.nseg = (int32_t)nseg;
+    const int64_t span = (int64_t)(desc->k - 1) * desc->dilation;
+    a.halo = span <= kTlMaxHalo ? (int32_t)span : 0;
+    a.shift_lo = desc->shift_lo;
+    a.shift_hi = desc->shift_hi;
+    a.v_th = desc->v_th;
+    a.v_th_q = desc->v_th_q;
+    // x * 2^-s stays a normal float for every s in [lo, hi] when its exponent
+    // field E satisfies max(1, hi+1) <= E <= 254 + min(0, lo)
+    const int emin = desc->shift_hi + 1 > 1 ? desc->shift_hi + 1 : 1;
+    const int emax = 254 + (desc->shift_lo < 0 ? desc->shift_lo : 0);
+    if (emin > emax) {
+        a.fast_lo = INFINITY;
+        a.fast_hi = 0.0f;
+    } else {
+        a.fast_lo = ldexpf(1.0f, emin - 127);
+        a.fast_hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
+    }
+    if (launch_forward_time_last(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
 }

@@ -1,0 +1,33 @@
+// Internal interface of the time-last forward kernel (mfpsn_tl.hip) for the
+// C-ABI layer.  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace mfpsn {
+
+constexpr int kTlWaves = 4;                 // waves per block
+constexpr int kTlMaxHalo = 2048;            // longest history staged in LDS
+
+struct TlArgs {
+    const void* x;          // [N][C][S][T] storage type
+    const int8_t* sign;     // [C][k]
+    const int8_t* shift;    // [C][k]
+    const void* bias;       // float[C] or int32[C]
+    uint8_t* spikes;        // [N][C][S][T]
+    void* h_out;            // nullable, float or int32 [N][C][S][T]
+    int64_t M;              // columns, N*C*S
+    int32_t T, C, S, k, d;
+    int32_t steps_per_lane; // 1 or 4: segments of 64 or 256 time steps
+    int32_t nseg;           // segments per column, ceil(T / (64 * steps_per_lane))
+    int32_t halo;           // LDS history slots per wave (0: taps read from global memory)
+    int32_t shift_lo, shift_hi;
+    float v_th;
+    int32_t v_th_q;
+    float fast_lo, fast_hi; // range of |x| in which the exponent-add tap is exact
+};
+
+hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t stream);
+
+}  // namespace mfpsn

@@ -74,6 +74,8 @@ _lib.mfpsn_stream_ring_bytes.argtypes = [_DP, ctypes.POINTER(ctypes.c_int32), ct
 _lib.mfpsn_stream_ring_bytes.restype = ctypes.c_int
 _lib.mfpsn_stream_step.argtypes = [_DP, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_stream_step.restype = ctypes.c_int
+_lib.mfpsn_forward_time_last.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_forward_time_last.restype = ctypes.c_int
 _lib.mfpsn_spikes_to_input.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, _P, _P]
 _lib.mfpsn_spikes_to_input.restype = ctypes.c_int
 _lib.mfpsn_sawtooth_dilation.argtypes = [ctypes.c_int32, ctypes.c_int32]
@@ -169,6 +171,11 @@ def mfpsn_quantizer_grad(w, shift, shift_lo: int, shift_hi: int, grad_wq, mode: 
     _check(_lib.mfpsn_quantizer_grad(_ptr(w), _ptr(shift), int(shift_lo), int(shift_hi), _ptr(grad_wq),
                                      int(grad_wq.numel()), int(mode), _ptr(grad_w), _stream(stream)),
            "mfpsn_quantizer_grad")
+
+
+def mfpsn_forward_time_last(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, stream=None) -> None:
+    _check(_lib.mfpsn_forward_time_last(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias),
+                                        _ptr(spikes), _ptr(h_out), _stream(stream)), "mfpsn_forward_time_last")
 
 
 def mfpsn_spikes_to_input(spikes, dtype: int, x, stream=None) -> None:
@@ -275,6 +282,21 @@ def quantizer_grad(w, shift, grad_wq, ste="whole", shift_lo: int = 0, shift_hi: 
     out = torch.empty_like(grad_wq)
     mfpsn_quantizer_grad(w, shift, shift_lo, shift_hi, grad_wq, STE[ste], out, stream)
     return out
+
+
+def forward_time_last(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, stream=None):
+    """Forward for x in the time-last layout [N, C, *spatial, T]: spikes (and
+    H with want_h) in the same layout.  desc is the one of the time-first
+    shape [T, N, C, *spatial] (make_desc)."""
+    dev = x.device
+    _expect(x, STORAGE[desc.dtype], dev, "x")
+    _expect(bias, BIAS[desc.dtype], dev, "bias")
+    if x.shape[-1] != desc.T or x.numel() != desc.T * desc.N * desc.C * desc.S:
+        raise ValueError(f"x of shape {tuple(x.shape)} does not match the descriptor (time last)")
+    spikes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
+    h = torch.empty(x.shape, dtype=H_OUT[desc.dtype], device=dev) if want_h else None
+    mfpsn_forward_time_last(desc, x, sign, shift, bias, spikes, h, stream)
+    return (spikes, h) if want_h else spikes
 
 
 def spikes_to_input(spikes, dtype: str = "f32", stream=None):

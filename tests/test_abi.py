@@ -73,7 +73,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 7
+    assert lib.mfpsn_abi_version() == 8
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -243,3 +243,17 @@ def test_spikes_to_input_validation(lib):
     assert f(FAKE, 10, 0, FAKE + 2, None) == -6             # float output 4-byte aligned
     assert f(FAKE, 10, 1, FAKE + 1, None) == -6             # bfloat16 output 2-byte aligned
     assert f(None, 0, 2, None, None) == 0                   # nothing to do
+
+
+def test_forward_time_last_validation(lib):
+    f = lib.mfpsn_forward_time_last
+    f.argtypes = [ctypes.POINTER(Desc)] + [ctypes.c_void_p] * 7
+    d = good_desc()
+    assert f(None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert f(ctypes.byref(good_desc(dtype=7)), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -4
+    assert f(ctypes.byref(good_desc(k=0)), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -3
+    assert f(ctypes.byref(d), None, FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert f(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, None) == -1
+    assert f(ctypes.byref(d), FAKE + 2, FAKE, FAKE, FAKE, FAKE, None, None) == -6
+    assert f(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, None) == -6
+    assert f(ctypes.byref(good_desc(T=0)), None, None, None, None, None, None, None) == 0
