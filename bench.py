@@ -427,30 +427,42 @@ def stack_step(torch, dev, wl, case, mode: str, steps: int, warmup: int):
 
 
 def time_last(torch, dev, wl, case, steps: int, warmup: int):
-    """The forward (charge and fire, spikes only) of the workload's layers in
-    the time-last layout [N][C][S][T] (mfpsn_forward_time_last), timed beside
-    the time-first forward (mfpsn_forward, spikes only) on the same inputs.
-    value = layers * T*N*C*S / time of the time-last forwards; roofline:
-    algorithmic bytes (x read, spikes written) per launch over its average
+    """The workload's layers in the time-last layout [N][C][S][T], timed beside
+    the time-first entry points on the same inputs: the forward (charge and
+    fire, spikes only; mfpsn_forward_time_last) and, for sequences of at most
+    64 steps, the backward (mfpsn_backward_time_last, H recomputed).
+    value = layers * T*N*C*S / time of the time-last step; roofline: the
+    dominant kernel's algorithmic bytes per launch (backward: x, grad_spikes
+    read, grad_x written; forward: x read, spikes written) over its average
     duration."""
     from paper_2501_14490_amd import mfpsn
 
     es = {"f32": 4, "bf16": 2, "q8_8": 2}[wl.dtype]
-    x_tf = case["x"]
-    if wl.dtype == "bf16":
-        x_tf = x_tf.view(np.int16)
-    x_tl = np.ascontiguousarray(np.moveaxis(x_tf, 0, -1))
+    gxs = {"f32": 4, "bf16": 2, "q8_8": 4}[wl.dtype]
+    with_bwd = wl.shape[0] <= 64
+    raw = {}
+    for name in ("x", "grad_spikes"):
+        a = case[name]
+        raw[name] = a.view(np.int16) if wl.dtype == "bf16" else a
 
     def up(a):
         t = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         return t.view(torch.bfloat16) if wl.dtype == "bf16" else t
 
-    xs = {"tl": up(x_tl), "tf": up(x_tf)}
+    xs = {"tf": up(raw["x"]), "tl": up(np.moveaxis(raw["x"], 0, -1))}
+    gs = {"tf": up(raw["grad_spikes"]), "tl": up(np.moveaxis(raw["grad_spikes"], 0, -1))}
+    tl_shape = tuple(xs["tl"].shape)
     sign, shift, bias = (torch.from_numpy(np.ascontiguousarray(case[n])).to(dev) for n in ("sign", "shift", "bias"))
     descs = [mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0, wl.s_max)
              for d in wl.dilations]
-    spk = {"tl": torch.empty(x_tl.shape, dtype=torch.uint8, device=dev),
-           "tf": torch.empty(wl.shape, dtype=torch.uint8, device=dev)}
+    shapes = {"tl": tl_shape, "tf": tuple(wl.shape)}
+    spk = {lay: torch.empty(shapes[lay], dtype=torch.uint8, device=dev) for lay in shapes}
+    gx = {lay: torch.empty(shapes[lay], dtype=mfpsn.GRAD_X[descs[0].dtype], device=dev) for lay in shapes}
+    gw = torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[descs[0].dtype], device=dev)
+    gb = torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[descs[0].dtype], device=dev)
+    ws_bytes = max(max(mfpsn.mfpsn_backward_workspace_size(d), mfpsn.mfpsn_backward_time_last_workspace_size(d))
+                   for d in descs)
+    ws = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
     hev = HipEvents()
 
@@ -464,38 +476,67 @@ def time_last(torch, dev, wl, case, steps: int, warmup: int):
                 mfpsn.mfpsn_forward(desc, xs["tf"], sign, shift, bias, spk["tf"], None, None, stream)
             if ev is not None:
                 hev.record(ev[li][1], stream)
+        if not with_bwd:
+            return
+        for li in reversed(range(len(descs))):
+            desc = descs[li]
+            if ev is not None:
+                hev.record(ev[li][2], stream)
+            if layout == "tl":
+                mfpsn.mfpsn_backward_time_last(desc, xs["tl"], gs["tl"], sign, shift, bias, gx["tl"], gw, gb, ws,
+                                               stream)
+            else:
+                mfpsn.mfpsn_backward(desc, xs["tf"], gs["tf"], None, None, sign, shift, bias, gx["tf"], gw, gb, ws,
+                                     stream=stream)
+            if ev is not None:
+                hev.record(ev[li][3], stream)
 
     out = {}
     for layout in ("tl", "tf"):
         for _ in range(warmup):
             run(layout)
         torch.cuda.synchronize()
-        evs = [[[hev.new(), hev.new()] for _ in descs] for _ in range(steps)]
+        evs = [[[hev.new() for _ in range(4)] for _ in descs] for _ in range(steps)]
         t0 = time.perf_counter()
         for s_ in range(steps):
             run(layout, evs[s_])
         torch.cuda.synchronize()
         out[layout] = {"elapsed": (time.perf_counter() - t0) / steps,
-                       "launch_ms": float(np.mean([hev.elapsed_ms(*e) for st in evs for e in st]))}
+                       "fwd_ms": float(np.mean([hev.elapsed_ms(e[0], e[1]) for st in evs for e in st]))}
+        if with_bwd:
+            out[layout]["bwd_ms"] = float(np.mean([hev.elapsed_ms(e[2], e[3]) for st in evs for e in st]))
     same = bool(torch.equal(spk["tl"].cpu(), torch.from_numpy(np.ascontiguousarray(
         np.moveaxis(spk["tf"].cpu().numpy(), 0, -1)))))
     P = len(descs)
     value = P * wl.elements / out["tl"]["elapsed"]
-    alg = wl.elements * (es + 1)
-    ach = alg / (out["tl"]["launch_ms"] * 1e-3) / 1e9
-    log(f"time-last forward {out['tl']['launch_ms'] * 1e3:.1f} us per layer ({ach:.0f} GB/s alg), time-first "
-        f"{out['tf']['launch_ms'] * 1e3:.1f} us; {value / 1e9:.2f} G elements/s; last layer's spikes equal: {same}")
-    print(json.dumps({
-        "metric": "time-last forward elements/s (T*N*C*S per layer)",
+    if with_bwd:
+        alg, ms, kern = wl.elements * (2 * es + gxs), out["tl"]["bwd_ms"], "backward"
+    else:
+        alg, ms, kern = wl.elements * (es + 1), out["tl"]["fwd_ms"], "forward"
+    ach = alg / (ms * 1e-3) / 1e9
+    line = (f"time-last forward {out['tl']['fwd_ms'] * 1e3:.1f} us per layer, time-first "
+            f"{out['tf']['fwd_ms'] * 1e3:.1f} us")
+    if with_bwd:
+        line += (f"; backward {out['tl']['bwd_ms'] * 1e3:.1f} us per layer, time-first "
+                 f"{out['tf']['bwd_ms'] * 1e3:.1f} us")
+    log(f"{line}; {value / 1e9:.2f} G elements/s; {kern} {ach:.0f} GB/s alg; last layer's spikes equal: {same}")
+    rec = {
+        "metric": "time-last " + ("forward+backward" if with_bwd else "forward") + " elements/s (T*N*C*S per layer)",
         "value": value, "unit": "elements/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
         "ms_per_step": out["tl"]["elapsed"] * 1e3, "higher_is_better": True, "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": f"{wl.name}: x[{','.join(map(str, x_tl.shape))}] {wl.dtype} time last, k={wl.k}, "
-                               f"one layer per d={wl.dilations}; forward, spikes only"},
-        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS},
-        "time_first_forward_us_per_layer": out["tf"]["launch_ms"] * 1e3,
-        "time_last_forward_us_per_layer": out["tl"]["launch_ms"] * 1e3,
+        "config": {"workload": f"{wl.name}: x[{','.join(map(str, tl_shape))}] {wl.dtype} time last, k={wl.k}, "
+                               f"one layer per d={wl.dilations}; forward (spikes only)"
+                               + (" and backward (H recomputed)" if with_bwd else "")},
+        "roofline": {"bound": "hbm", "kernel": kern, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS},
+        "time_first_forward_us_per_layer": out["tf"]["fwd_ms"] * 1e3,
+        "time_last_forward_us_per_layer": out["tl"]["fwd_ms"] * 1e3,
         "spikes_equal_time_first": same,
-    }), flush=True)
+    }
+    if with_bwd:
+        rec["time_first_backward_us_per_layer"] = out["tf"]["bwd_ms"] * 1e3
+        rec["time_last_backward_us_per_layer"] = out["tl"]["bwd_ms"] * 1e3
+    print(json.dumps(rec), flush=True)
 
 
 def main():

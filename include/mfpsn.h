@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 8
+#define MFPSN_ABI_VERSION 9
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -268,6 +268,31 @@ const char* mfpsn_status_string(int status);
  * library keeps no state; the call is asynchronous on `stream`. */
 int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
                             const void* bias, uint8_t* spikes, void* h_out, void* stream);
+
+/* Bytes of device workspace mfpsn_backward_time_last needs: (k+1)*C
+ * 8-byte sums.  Returns a status; *bytes is written on success. */
+int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* bytes);
+
+/* Backward (App. A.3 Eqs. backward_X, backward_W, backward_b, with the taps
+ * dilated by d) in the time-last layout, for sequences of at most 64 steps:
+ *   x, grad_spikes : [N][C][S][T] storage type of desc->dtype
+ *   grad_x         : [N][C][S][T] float (F32), bfloat16 (BF16, rounded to
+ *                    nearest even) or int32 (Q8.8)
+ *   grad_w [C][k], grad_b [C] : float, or int64 (Q8.8: Q16.16 and Q8.8);
+ *                    overwritten
+ *   workspace      : >= mfpsn_backward_time_last_workspace_size bytes,
+ *                    8-byte aligned; contents on entry are ignored
+ * H is recomputed from x (the charge of mfpsn_forward), dH = grad_spikes *
+ * sigma'(H - v_th) with the surrogate of mfpsn_backward, and grad_x is the
+ * definition's sum over the taps in ascending order, every term included.
+ * grad_w and grad_b are sums of exact products in double (int64 for Q8.8)
+ * rounded once to float; the double sums are added in an order that can
+ * change from call to call (the Q8.8 sums are exact).  Errors as
+ * mfpsn_backward; MFPSN_ERR_SHAPE also for T > 64 or N*C*S >= 2^37.
+ * Asynchronous on `stream`. */
+int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const int8_t* sign,
+                             const int8_t* shift, const void* bias, void* grad_x, void* grad_w, void* grad_b,
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 /* Chaining layers: one layer's spikes as the next layer's input, for a
  * stack of neuron layers joined by identity stateless layers (the sawtooth

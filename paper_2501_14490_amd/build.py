@@ -44,7 +44,8 @@ DTYPES = [0, 1, 2]  # f32, bf16, q8.8
 def _units():
     """(object, compile command, sources it depends on) of every translation unit."""
     src = os.path.join(CSRC, "mfpsn_kernels.hip")
-    headers = [os.path.join(CSRC, "mfpsn_internal.h"), os.path.join(INCLUDE, "mfpsn.h")]
+    headers = [os.path.join(CSRC, "mfpsn_internal.h"), os.path.join(CSRC, "mfpsn_surrogate.h"),
+               os.path.join(INCLUDE, "mfpsn.h")]
     units = []
     for dt in DTYPES:
         for lo, hi in K_RANGES:
@@ -63,7 +64,8 @@ def _units():
     tl_src = os.path.join(CSRC, "mfpsn_tl.hip")
     obj = os.path.join(BUILD, "tl.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", tl_src, "-o", obj],
-                  [tl_src, os.path.join(CSRC, "mfpsn_tl.h"), os.path.join(INCLUDE, "mfpsn.h")]))
+                  [tl_src, os.path.join(CSRC, "mfpsn_tl.h"), os.path.join(CSRC, "mfpsn_surrogate.h"),
+                   os.path.join(INCLUDE, "mfpsn.h")]))
     chain_src = os.path.join(CSRC, "mfpsn_chain.hip")
     obj = os.path.join(BUILD, "chain.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", chain_src, "-o", obj],

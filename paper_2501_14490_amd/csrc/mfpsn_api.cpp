@@ -19,19 +19,6 @@ namespace {
 
 int grad_x_bytes(int dtype) { return dtype == MFPSN_BF16 ? 2 : 4; }
 
-// Largest |dH| the Q8.8 backward can produce: |grad_spikes| <= 2^15 times the
-// integer surrogate factor, which is at most 2^15 * max sigma' (+1 for rounding).
-double q88_max_dh(const mfpsn_desc* d)
-{
-    double peak;
-    switch (d->surrogate) {
-    case MFPSN_SG_SIGMOID: peak = d->alpha / 4.0; break;
-    case MFPSN_SG_ATAN: peak = d->alpha / 2.0; break;
-    default: peak = 1.0; break;
-    }
-    return ceil(32768.0 * peak) + 1.0;
-}
-
 // Longest chunk of class steps (a multiple of k) whose byte span, with the
 // halo and prefetch rows, still fits the 31-bit scalar offsets the kernels
 // use inside one item (4-byte elements, the widest stream); 0 if none fits.

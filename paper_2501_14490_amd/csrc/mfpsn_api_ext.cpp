@@ -94,6 +94,22 @@ int validate_bn(const mfpsn_desc* d, BnGeom* g)
     g->NG = (g->R + kBnRowGroup - 1) / kBnRowGroup;
     return MFPSN_OK;
 }
+
+// Range [lo, hi) of |v| in which v * 2^-s stays a normal float for every s
+// in [shift_lo, shift_hi]: exponent field E with max(1, hi+1) <= E <=
+// 254 + min(0, lo) (empty when no E qualifies)
+void fast_range(const mfpsn_desc* desc, float* lo, float* hi)
+{
+    const int emin = desc->shift_hi + 1 > 1 ? desc->shift_hi + 1 : 1;
+    const int emax = 254 + (desc->shift_lo < 0 ? desc->shift_lo : 0);
+    if (emin > emax) {
+        *lo = INFINITY;
+        *hi = 0.0f;
+    } else {
+        *lo = ldexpf(1.0f, emin - 127);
+        *hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
+    }
+}
 }  // namespace
 
 int mfpsn_bn_workspace_size(const mfpsn_desc* desc, size_t* bytes)
@@ -300,18 +316,92 @@ int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t*
     a.shift_hi = desc->shift_hi;
     a.v_th = desc->v_th;
     a.v_th_q = desc->v_th_q;
-    // x * 2^-s stays a normal float for every s in [lo, hi] when its exponent
-    // field E satisfies max(1, hi+1) <= E <= 254 + min(0, lo)
-    const int emin = desc->shift_hi + 1 > 1 ? desc->shift_hi + 1 : 1;
-    const int emax = 254 + (desc->shift_lo < 0 ? desc->shift_lo : 0);
-    if (emin > emax) {
-        a.fast_lo = INFINITY;
-        a.fast_hi = 0.0f;
-    } else {
-        a.fast_lo = ldexpf(1.0f, emin - 127);
-        a.fast_hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
-    }
+    fast_range(desc, &a.fast_lo, &a.fast_hi);
+    a.tdiv = desc->T >= 2 ? (uint32_t)((((uint64_t)1) << 32) / (uint64_t)desc->T + 1) : 0;
+    a.vec_x = aligned(x, 4 * es) ? 1 : 0;
+    a.vec_s = aligned(spikes, 16) ? 1 : 0;
     if (launch_forward_time_last(a, desc->dtype, (hipStream_t)stream) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    return MFPSN_OK;
+}
+
+int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* bytes)
+{
+    const int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    if (!bytes)
+        return MFPSN_ERR_NULL;
+    *bytes = (size_t)(desc->k + 1) * (size_t)desc->C * 8;
+    return MFPSN_OK;
+}
+
+int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const int8_t* sign,
+                             const int8_t* shift, const void* bias, void* grad_x, void* grad_w, void* grad_b,
+                             void* workspace, size_t ws_bytes, void* stream)
+{
+    const int st = validate(desc);
+    if (st != MFPSN_OK)
+        return st;
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    if (desc->T > kTlColsMaxT || M >= ((int64_t)1 << 37))
+        return MFPSN_ERR_SHAPE;
+    const int64_t total = M * desc->T;
+    if (total > 0 && (!x || !grad_spikes || !grad_x))
+        return MFPSN_ERR_NULL;
+    if (desc->C > 0 && (!sign || !shift || !bias || !grad_w || !grad_b))
+        return MFPSN_ERR_NULL;
+    const int es = elem_bytes(desc->dtype);
+    const size_t wb = desc->dtype == MFPSN_Q8_8 ? 8 : 4;
+    if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, desc->dtype == MFPSN_BF16 ? 2 : 4) ||
+        !aligned(bias, 4) || !aligned(grad_w, wb) || !aligned(grad_b, wb))
+        return MFPSN_ERR_ALIGN;
+    if (desc->dtype == MFPSN_Q8_8) {
+        // every partial sum of grad_w must fit int64
+        const double reach = (double)desc->T * desc->N * desc->S * 32768.0 * q88_max_dh(desc);
+        if (reach >= 4611686018427387904.0)
+            return MFPSN_ERR_SHAPE;
+    }
+    const size_t need = (size_t)(desc->k + 1) * (size_t)desc->C * 8;
+    if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
+        return MFPSN_ERR_WORKSPACE;
+    if (desc->C == 0)
+        return MFPSN_OK;
+    TlBwdArgs a;
+    a.x = x;
+    a.g = grad_spikes;
+    a.sign = sign;
+    a.shift = shift;
+    a.bias = bias;
+    a.grad_x = grad_x;
+    a.acc = workspace;
+    a.M = M;
+    a.T = desc->T;
+    a.C = desc->C;
+    a.S = desc->S;
+    a.k = desc->k;
+    a.d = desc->dilation;
+    a.shift_lo = desc->shift_lo;
+    a.shift_hi = desc->shift_hi;
+    a.v_th = desc->v_th;
+    a.v_th_q = desc->v_th_q;
+    a.sg = desc->surrogate;
+    a.alpha = desc->alpha;
+    fast_range(desc, &a.fast_lo, &a.fast_hi);
+    a.tdiv = desc->T >= 2 ? (uint32_t)((((uint64_t)1) << 32) / (uint64_t)desc->T + 1) : 0;
+    a.vec_x = aligned(x, 4 * es) && aligned(grad_spikes, 4 * es) ? 1 : 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (launch_backward_time_last(a, desc->dtype, s) != hipSuccess)
+        return MFPSN_ERR_HIP;
+    FinArgs f;
+    f.C = desc->C;
+    f.k = desc->k;
+    f.blocks = 1;
+    f.dtype = desc->dtype;
+    f.partial = (const double*)workspace;
+    f.grad_w = grad_w;
+    f.grad_b = grad_b;
+    if (launch_finalize(f, s) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;
 }

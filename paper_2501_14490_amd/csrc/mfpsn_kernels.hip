@@ -60,6 +60,7 @@
 #include <utility>
 
 #include "mfpsn_internal.h"
+#include "mfpsn_surrogate.h"
 
 
 namespace mfpsn {
@@ -439,88 +440,6 @@ template <int K, int MODE> struct Taps<K, kQ88, MODE> {
     __device__ __forceinline__ int apply_fast(int v, int i) const { return apply(v, i); }
 };
 
-// ---------------------------------------------------------------------------
-// surrogate derivative (float, fixed operation sequence)
-// ---------------------------------------------------------------------------
-// exp(y) for y <= 0: Cody-Waite reduction with ln 2 = hi + lo (hi has 15
-// significant bits), degree-7 Taylor polynomial of e^r by fma Horner steps,
-// scaling by 2^n.  y < -86 (or NaN) gives 0.
-__device__ __forceinline__ float mf_exp_nonpos(float y)
-{
-    const float log2e = 0x1.715476p+0f;
-    const float ln2hi = 0x1.62e4p-1f;
-    const float ln2lo = 0x1.7f7d1cp-20f;
-    const bool zero = !(y >= -86.0f);
-    float n = rintf(y * log2e);
-    float r = __builtin_fmaf(n, -ln2hi, y);
-    r = __builtin_fmaf(n, -ln2lo, r);
-    float p = 0x1.a01a02p-13f;
-    p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);
-    p = __builtin_fmaf(p, r, 0x1.111112p-7f);
-    p = __builtin_fmaf(p, r, 0x1.555556p-5f);
-    p = __builtin_fmaf(p, r, 0x1.555556p-3f);
-    p = __builtin_fmaf(p, r, 0.5f);
-    p = __builtin_fmaf(p, r, 1.0f);
-    p = __builtin_fmaf(p, r, 1.0f);
-    float e = ldexpf(p, (int)n);
-    return zero ? 0.0f : e;
-}
-
-// sigmoid: alpha e / (1 + e)^2 with e = exp(-alpha |u|)
-// atan:    (alpha / 2) / (1 + (pi/2 alpha u)^2)
-// rational: 1 / (1 + alpha u^2)
-// atan and rational share one operation sequence: z = m u, den = 1 + q z^2,
-// num / den, with (m, q, num) = (float(pi/2) alpha, 1, alpha/2) or
-// (1, alpha, 1); the multiplications by 1 are exact, so each result is
-// bit-identical to its own formula.
-struct Surrogate {
-    int sigmoid;  // 1: sigmoid, 0: atan or rational
-    float alpha;
-    float m, q, num;
-    __device__ void init(int kind, float a)
-    {
-        sigmoid = kind == 0;
-        alpha = a;
-        m = kind == 1 ? 0x1.921fb6p+0f * a : 1.0f;
-        q = kind == 1 ? 1.0f : a;
-        num = kind == 1 ? 0.5f * a : 1.0f;
-    }
-    __device__ __forceinline__ float operator()(float u) const
-    {
-        if (sigmoid) {
-            float a = alpha * fabsf(u);
-            float e = mf_exp_nonpos(-a);
-            float den = 1.0f + e;
-            float nm = alpha * e;
-            float den2 = den * den;
-            return nm / den2;
-        }
-        float z = m * u;
-        float z2 = z * z;
-        float t = q * z2;
-        float den = 1.0f + t;
-        return num / den;
-    }
-};
-
-// Surrogate factor of a potential: float sigma'(H - v_th); Q8.8 the integer
-// L = round-half-even(2^15 sigma'((H - v_th) / 256)).
-__device__ __forceinline__ float sg_factor(const Surrogate& sg, float h, float v_th, int)
-{
-    float u = h - v_th;
-    return sg(u);
-}
-__device__ __forceinline__ int32_t sg_factor_q(const Surrogate& sg, int32_t u)
-{
-    float uf = (float)u * 0.00390625f;
-    float s = sg(uf);
-    return (int32_t)rintf(s * 32768.0f);
-}
-__device__ __forceinline__ int32_t sg_factor(const Surrogate& sg, int32_t h, float, int v_th_q)
-{
-    return sg_factor_q(sg, (int32_t)((uint32_t)h - (uint32_t)v_th_q));
-}
-
 // Q8.8 factors come from a table: u = H - v_th_q is an integer and L(u) is
 // even in u (the float sequence sees |u|, or u only through u*u), so each
 // block evaluates L(0 .. kQTable-1) once into LDS with the same sequence and
@@ -544,14 +463,6 @@ struct QTable {
         return L;
     }
 };
-// dH = grad_spikes * factor (Q8.8: floor((g * L) / 2^15))
-__device__ __forceinline__ float delta_h(float g, float f) { return g * f; }
-__device__ __forceinline__ int32_t delta_h(int32_t g, int32_t L)
-{
-    int64_t p = (int64_t)g * (int64_t)L;
-    return (int32_t)(p >> 15);
-}
-
 // True (wave-uniform) when some lane's value is outside the range in which
 // the exponent-add tap is exact.
 template <int NV>

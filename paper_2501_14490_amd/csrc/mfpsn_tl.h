@@ -9,6 +9,7 @@ namespace mfpsn {
 
 constexpr int kTlWaves = 4;                 // waves per block
 constexpr int kTlMaxHalo = 2048;            // longest history staged in LDS
+constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-column kernel
 
 struct TlArgs {
     const void* x;          // [N][C][S][T] storage type
@@ -26,8 +27,36 @@ struct TlArgs {
     float v_th;
     int32_t v_th_q;
     float fast_lo, fast_hi; // range of |x| in which the exponent-add tap is exact
+    uint32_t tdiv;          // floor(2^32 / T) + 1 (T >= 2; 0 when T = 1): e / T = umulhi(e, tdiv) for e < 64 T
+    int32_t vec_x;          // x is aligned for 4-element vector loads
+    int32_t vec_s;          // spikes are 16-byte aligned
 };
 
 hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t stream);
+
+// Backward in the time-last layout (T <= kTlColsMaxT)
+struct TlBwdArgs {
+    const void* x;          // [N][C][S][T] storage type
+    const void* g;          // grad_spikes, [N][C][S][T] storage type
+    const int8_t* sign;     // [C][k]
+    const int8_t* shift;    // [C][k]
+    const void* bias;       // float[C] or int32[C]
+    void* grad_x;           // [N][C][S][T] float, bfloat16 bits or int32
+    void* acc;              // [k+1][C] double (float data) or int64 (Q8.8): grad_w rows, then grad_b
+    int64_t M;              // columns, N*C*S
+    int32_t T, C, S, k, d;
+    int32_t shift_lo, shift_hi;
+    float v_th;
+    int32_t v_th_q;
+    int32_t sg;             // surrogate kind
+    float alpha;
+    float fast_lo, fast_hi; // range of |x| and |dH| in which the exponent-add tap is exact
+    uint32_t tdiv;          // as TlArgs::tdiv (0 when T = 1)
+    int32_t vec_x;          // x and g aligned for 4-element vector loads
+};
+
+// Zeroes acc, runs the backward, which adds into acc; the caller finalizes
+// acc into grad_w and grad_b.
+hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t stream);
 
 }  // namespace mfpsn

@@ -22,9 +22,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "mfpsn.h"
+#include "mfpsn_surrogate.h"
 #include "mfpsn_tl.h"
 
 namespace mfpsn {
@@ -241,6 +243,442 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_fwd_kernel(TlArgs a)
     }
 }
 
+typedef uint32_t U32x4 __attribute__((ext_vector_type(4)));
+
+// Four consecutive stored elements (one vector load)
+template <int DT> struct TlVec4;
+template <> struct TlVec4<MFPSN_F32> {
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4])
+    {
+        const float4 w = *reinterpret_cast<const float4*>((const float*)p + e);
+        v[0] = w.x, v[1] = w.y, v[2] = w.z, v[3] = w.w;
+    }
+};
+template <> struct TlVec4<MFPSN_BF16> {
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4])
+    {
+        const uint2 w = *reinterpret_cast<const uint2*>((const uint16_t*)p + e);
+        v[0] = __builtin_bit_cast(float, w.x << 16), v[1] = __builtin_bit_cast(float, w.x & 0xffff0000u);
+        v[2] = __builtin_bit_cast(float, w.y << 16), v[3] = __builtin_bit_cast(float, w.y & 0xffff0000u);
+    }
+};
+template <> struct TlVec4<MFPSN_Q8_8> {
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, int32_t (&v)[4])
+    {
+        const uint2 w = *reinterpret_cast<const uint2*>((const int16_t*)p + e);
+        v[0] = (int32_t)(w.x << 16) >> 16, v[1] = (int32_t)w.x >> 16;
+        v[2] = (int32_t)(w.y << 16) >> 16, v[3] = (int32_t)w.y >> 16;
+    }
+};
+
+// The k taps of one lane's channel: for float data the bit-pattern addend
+// kc = (-s) 2^23 + sign 2^31 (mod 2^32) of x * 2^-s with the sign (the
+// exact path takes -s from bits 23..30 and the sign from what remains once
+// (-s) 2^23 is taken away), for Q8.8 the shift and the negation mask.
+template <int DT, int K> struct TlLaneTaps {
+    static constexpr bool kF = DT != MFPSN_Q8_8;
+    using V = typename TlIO<DT>::V;
+    uint32_t kc[kF ? K : 1];
+    int sh[kF ? 1 : K], neg[kF ? 1 : K];
+    __device__ __forceinline__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
+    {
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            int sv = shift[c * K + i];
+            sv = sv < lo ? lo : (sv > hi ? hi : sv);
+            const bool n = sign[c * K + i] < 0;
+            if constexpr (kF)
+                kc[i] = ((uint32_t)(-sv) << 23) ^ (n ? 0x80000000u : 0u);
+            else
+                sh[i] = sv, neg[i] = n ? -1 : 0;
+        }
+    }
+    // sign * in * 2^-s: EXACT by v_ldexp_f32 and a sign flip, else by the
+    // bit-pattern add (exact for |in| in the fast range); Q8.8 floor shift
+    // and negation
+    template <bool EXACT> __device__ __forceinline__ V apply(V in, int i) const
+    {
+        if constexpr (kF) {
+            if constexpr (EXACT) {
+                const int e = (int32_t)(kc[i] << 1) >> 24;
+                const uint32_t sb = (kc[i] - ((uint32_t)e << 23)) & 0x80000000u;
+                return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, ldexpf(in, e)) ^ sb);
+            } else {
+                return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, in) + kc[i]);
+            }
+        } else {
+            return ((in >> sh[i]) ^ neg[i]) - neg[i];
+        }
+    }
+};
+
+constexpr int kTlRow = 65;                             // words per time row of a transposed tile
+constexpr int kTlMaxChunks = 16 * kTlColsMaxT / 64;     // 4-element chunks per lane and group
+
+// Column of the e-th element of a group of columns of length T (e < 64 T)
+__device__ __forceinline__ int tl_col_of(int e, int T, uint32_t tdiv)
+{
+    return T == 1 ? e : (int)__umulhi((uint32_t)e, tdiv);
+}
+
+// Stages a group's ncols * T contiguous elements of src (from element gbase)
+// into the transposed tile tile[tau * kTlRow + col], with 4-element vector
+// loads for a whole group when vec is set.  Returns (wave-uniform) whether
+// some staged float lies outside [lo, hi); always false for Q8.8.
+template <int DT>
+__device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int ncols, int T, uint32_t tdiv, bool vec,
+                                         typename TlIO<DT>::V* tile, float lo, float hi)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    const int lane = (int)threadIdx.x & 63;
+    bool out = false;
+    auto put = [&](int e, V v) {
+        const int c = tl_col_of(e, T, tdiv);
+        tile[(e - c * T) * kTlRow + c] = v;
+        if constexpr (kF) {
+            const float m = __builtin_fabsf(v);
+            out = out || !(m >= lo && m < hi);
+        }
+    };
+    if (ncols == 64 && vec) {
+        const int nch = 16 * T;  // 4-element chunks of the group
+        V v[kTlMaxChunks][4];
+#pragma unroll
+        for (int j = 0; j < kTlMaxChunks; ++j)
+            if (lane + 64 * j < nch)
+                TlVec4<DT>::ld(src, gbase + 4 * (lane + 64 * j), v[j]);
+#pragma unroll
+        for (int j = 0; j < kTlMaxChunks; ++j)
+            if (lane + 64 * j < nch) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    put(4 * (lane + 64 * j) + q, v[j][q]);
+            }
+    } else {
+        for (int e = lane; e < ncols * T; e += 64)
+            put(e, TlIO<DT>::ld(src, gbase + e));
+    }
+    return kF && __builtin_amdgcn_ballot_w64(out) != 0;
+}
+
+// Short columns (T <= kTlColsMaxT): one wave per group of 64 columns,
+// lane = column.  The group's inputs, 64 T contiguous elements, are read with
+// coalesced loads and written transposed into LDS, one row of 64 columns per
+// time step (row stride 65 words: a row read by the 64 lanes touches every
+// bank once).  Each lane then walks its column in time with the taps of its
+// own channel in registers, reading the k inputs of an output from its LDS
+// column, and puts its spikes into a [column][time] byte tile that is
+// written back with 16-byte stores.
+template <int DT, int K>
+__global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    constexpr int kRow = kTlRow;
+    extern __shared__ uint32_t tl_lds[];
+    const int lane = (int)threadIdx.x;
+    const int T = a.T;
+    const int64_t col0 = (int64_t)blockIdx.x * 64;
+    const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
+    const int64_t gbase = col0 * T;
+    V* xt = reinterpret_cast<V*>(tl_lds);
+    uint8_t* st = reinterpret_cast<uint8_t*>(tl_lds) + ((T * kRow * 4 + 15) & ~15);
+    const bool slow = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
+
+    const int64_t col = col0 + (lane < ncols ? lane : 0);
+    const int c = (int)((col / a.S) % a.C);
+    TlLaneTaps<DT, K> taps;
+    taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
+    V bias;
+    if constexpr (kF)
+        bias = ((const float*)a.bias)[c];
+    else
+        bias = ((const int32_t*)a.bias)[c];
+    wave_lds_sync();
+
+    auto tap = [&](V in, int i, auto exact) -> V { return taps.template apply<decltype(exact)::value>(in, i); };
+    const int span = (K - 1) * a.d;
+    const bool pack = (T & 3) == 0;
+    // NO outputs per pass, so that their NO * K LDS reads are in flight together
+    constexpr int NO = K <= 16 ? 4 : 2;
+    auto walk = [&](auto exact) {
+        for (int t0 = 0; t0 < T; t0 += NO) {
+            V acc[NO];
+#pragma unroll
+            for (int j = 0; j < NO; ++j)
+                acc[j] = V(0);
+            if (t0 >= span) {
+                // every tap input exists; outputs past the column's end read
+                // its last step (in the tile) and are not stored
+#pragma unroll
+                for (int j = 0; j < NO; ++j) {
+                    const int t = t0 + j < T ? t0 + j : T - 1;
+                    V in[K];
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        in[i] = xt[(t - (K - 1 - i) * a.d) * kRow + lane];
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc[j] = acc[j] + tap(in[i], i, exact);
+                }
+            } else {
+                // from the first tap whose input exists (time >= 0): the
+                // others read time 0 and are not added
+#pragma unroll
+                for (int j = 0; j < NO; ++j) {
+                    const int t = t0 + j < T ? t0 + j : T - 1;
+                    V in[K];
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const int tau = t - (K - 1 - i) * a.d;
+                        in[i] = xt[(tau > 0 ? tau : 0) * kRow + lane];
+                    }
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc[j] + tap(in[i], i, exact);
+                        acc[j] = t - (K - 1 - i) * a.d >= 0 ? sum : acc[j];
+                    }
+                }
+            }
+            uint32_t s4 = 0;
+#pragma unroll
+            for (int j = 0; j < NO; ++j) {
+                const int t = t0 + j;
+                const V h = acc[j] + bias;
+                bool fire;
+                if constexpr (kF)
+                    fire = h >= a.v_th;
+                else
+                    fire = h >= a.v_th_q;
+                s4 |= (fire ? 1u : 0u) << (8 * j);
+                if (t < T) {
+                    if (!pack)
+                        st[lane * T + t] = fire ? 1 : 0;
+                    if (a.h_out != nullptr && lane < ncols)
+                        reinterpret_cast<V*>(a.h_out)[gbase + (int64_t)lane * T + t] = h;
+                }
+            }
+            if (pack) {  // T and t0 multiples of 4
+                if constexpr (NO == 4) {
+                    *reinterpret_cast<uint32_t*>(st + lane * T + t0) = s4;
+                } else {
+                    *reinterpret_cast<uint16_t*>(st + lane * T + t0) = (uint16_t)s4;
+                }
+            }
+        }
+    };
+    if (slow)
+        walk(std::true_type{});
+    else
+        walk(std::false_type{});
+    wave_lds_sync();
+
+    if (ncols == 64 && a.vec_s) {
+        for (int q = lane; q < 4 * T; q += 64)
+            __builtin_nontemporal_store(reinterpret_cast<const U32x4*>(st)[q],
+                                        reinterpret_cast<U32x4*>(a.spikes + gbase) + q);
+    } else {
+        for (int e = lane; e < ncols * T; e += 64)
+            a.spikes[gbase + e] = st[e];
+    }
+}
+
+// 64-bit values across lanes (two 32-bit shuffles)
+__device__ __forceinline__ double tl_shfl_up(double v, int off)
+{
+    return __shfl_up(v, (unsigned)off, 64);
+}
+__device__ __forceinline__ int64_t tl_shfl_up(int64_t v, int off)
+{
+    const int lo = __shfl_up((int)(uint32_t)v, (unsigned)off, 64);
+    const int hi = __shfl_up((int)(uint32_t)((uint64_t)v >> 32), (unsigned)off, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// bfloat16 bits of a float, round to nearest even (NaN stays NaN)
+__device__ __forceinline__ uint16_t tl_bf16_rne(float v)
+{
+    const uint32_t b = __builtin_bit_cast(uint32_t, v);
+    if ((b & 0x7fffffffu) > 0x7f800000u)
+        return (uint16_t)((b >> 16) | 0x40u);
+    return (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
+}
+
+// Backward (App. A.3: Eqs. backward_X, backward_W, backward_b, generalized
+// to dilation d) for short columns in the time-last layout, lane = column
+// as in tl_cols_kernel.  The group's x and grad_spikes are staged transposed
+// in LDS.  A forward walk recomputes H (the definition's sum), takes
+// dH = grad_spikes * sigma'(H - V_th), writes dH over grad_spikes in the
+// tile and adds the exact products x[t - (k-1-i) d] dH[t] and dH[t] of the
+// lane's column to its grad_w / grad_b sums (double, or int64 for Q8.8).  A
+// second walk forms grad_x[t] = sum over taps i ascending, with
+// t + (k-1-i) d < T, of sign_i dH[t + (k-1-i) d] 2^-s_i into the x tile,
+// which is stored with coalesced writes.  The 64 lanes' sums are reduced per
+// channel (lanes of one channel are consecutive) and added to acc[k+1][C]
+// with atomics.
+template <int DT, int K>
+__global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    using W = std::conditional_t<kF, double, int64_t>;
+    constexpr int kRow = kTlRow;
+    extern __shared__ uint32_t tl_lds[];
+    const int lane = (int)threadIdx.x;
+    const int T = a.T;
+    const int64_t col0 = (int64_t)blockIdx.x * 64;
+    const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
+    const int64_t gbase = col0 * T;
+    V* xt = reinterpret_cast<V*>(tl_lds);  // x, then grad_x
+    V* gt = xt + T * kRow;                 // grad_spikes, then dH
+    const bool slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
+    (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
+
+    const int64_t col = col0 + (lane < ncols ? lane : 0);
+    const int c = (int)((col / a.S) % a.C);
+    TlLaneTaps<DT, K> taps;
+    taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
+    V bias;
+    if constexpr (kF)
+        bias = ((const float*)a.bias)[c];
+    else
+        bias = ((const int32_t*)a.bias)[c];
+    Surrogate sg;
+    sg.init(a.sg, a.alpha);
+    wave_lds_sync();
+
+    // walk 1: H, dH (over grad_spikes in the tile), grad_w and grad_b sums
+    W gw[K], gb = W(0);
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        gw[i] = W(0);
+    bool out_dh = false;
+    auto walk1 = [&](auto exact) {
+        for (int t = 0; t < T; ++t) {
+            V in[K];
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const int tau = t - (K - 1 - i) * a.d;
+                in[i] = xt[(tau > 0 ? tau : 0) * kRow + lane];
+            }
+            const V gv = gt[t * kRow + lane];
+            V acc = V(0);
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const V sum = acc + taps.template apply<decltype(exact)::value>(in[i], i);
+                acc = t - (K - 1 - i) * a.d >= 0 ? sum : acc;
+            }
+            const V h = acc + bias;
+            const V dh = delta_h(gv, sg_factor(sg, h, a.v_th, a.v_th_q));
+            gt[t * kRow + lane] = dh;
+            gb += (W)dh;
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                W p;
+                if constexpr (kF)
+                    p = __builtin_fma((double)in[i], (double)dh, gw[i]);  // exact product, one rounding
+                else
+                    p = gw[i] + (int64_t)in[i] * (int64_t)dh;
+                gw[i] = t - (K - 1 - i) * a.d >= 0 ? p : gw[i];
+            }
+            if constexpr (kF) {
+                const float m = __builtin_fabsf(dh);
+                out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
+            }
+        }
+    };
+    if (slow_x)
+        walk1(std::true_type{});
+    else
+        walk1(std::false_type{});
+    const bool slow_dh = kF && __builtin_amdgcn_ballot_w64(out_dh) != 0;
+    wave_lds_sync();
+
+    // walk 2: grad_x into the x tile
+    auto walk2 = [&](auto exact) {
+        for (int t = 0; t < T; ++t) {
+            V in[K];
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const int tau = t + (K - 1 - i) * a.d;
+                in[i] = gt[(tau < T ? tau : T - 1) * kRow + lane];
+            }
+            V acc = V(0);
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const V sum = acc + taps.template apply<decltype(exact)::value>(in[i], i);
+                acc = t + (K - 1 - i) * a.d < T ? sum : acc;
+            }
+            xt[t * kRow + lane] = acc;
+        }
+    };
+    if (slow_dh)
+        walk2(std::true_type{});
+    else
+        walk2(std::false_type{});
+    wave_lds_sync();
+
+    for (int e = lane; e < ncols * T; e += 64) {
+        const int cc = tl_col_of(e, T, a.tdiv);
+        const V v = xt[(e - cc * T) * kRow + cc];
+        if constexpr (DT == MFPSN_BF16)
+            reinterpret_cast<uint16_t*>(a.grad_x)[gbase + e] = tl_bf16_rne(v);
+        else
+            reinterpret_cast<V*>(a.grad_x)[gbase + e] = v;
+    }
+
+    // per-channel sums: segments of consecutive lanes with one channel
+    // (lanes past the last column form their own and add nothing)
+    const int cl = lane < ncols ? c : -1;
+    const int cprev = __shfl_up(cl, 1u, 64);
+    const uint64_t heads = __builtin_amdgcn_ballot_w64(lane == 0 || cprev != cl);
+    const int seg = __popcll(heads & (lane == 63 ? ~0ull : ((2ull << lane) - 1))) - 1;
+    const int seg_next = __shfl_down(seg, 1u, 64);
+    const bool last = cl >= 0 && (lane == 63 || seg_next != seg);
+    // same[j]: the lane 2^j below is in this lane's segment.  The shuffle
+    // runs on every lane: a lane that sat out of it would hand 0 to the
+    // lane reading it.
+    bool same[6];
+#pragma unroll
+    for (int j = 0; j < 6; ++j) {
+        const int below = __shfl_up(seg, (unsigned)(1 << j), 64);
+        same[j] = (lane >= (1 << j)) & (below == seg);
+    }
+    auto seg_sum = [&](W v) {
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+            const W u = tl_shfl_up(v, 1 << j);
+            v = same[j] ? v + u : v;
+        }
+        return v;
+    };
+    W* acc = reinterpret_cast<W*>(a.acc);
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        const W v = seg_sum(gw[i]);
+        if (last) {
+            if constexpr (kF)
+                atomicAdd(acc + (size_t)i * a.C + cl, v);
+            else
+                atomicAdd(reinterpret_cast<unsigned long long*>(acc) + (size_t)i * a.C + cl, (unsigned long long)v);
+        }
+    }
+    const W v = seg_sum(gb);
+    if (last) {
+        if constexpr (kF)
+            atomicAdd(acc + (size_t)K * a.C + cl, v);
+        else
+            atomicAdd(reinterpret_cast<unsigned long long*>(acc) + (size_t)K * a.C + cl, (unsigned long long)v);
+    }
+}
+
+__global__ void tl_zero_kernel(uint64_t* p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
 template <int DT, int K, int NS, bool LDS>
 void launch_variant(const TlArgs& a, hipStream_t st)
 {
@@ -269,6 +707,13 @@ void launch_variant(const TlArgs& a, hipStream_t st)
 template <int DT, int K>
 void launch_k(const TlArgs& a, hipStream_t st)
 {
+    if (a.T <= kTlColsMaxT) {
+        const size_t lds = ((size_t)a.T * 65 * 4 + 15) / 16 * 16 + (size_t)64 * a.T;
+        const int64_t blocks = (a.M + 63) / 64;
+        auto kern = tl_cols_kernel<DT, K>;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
+        return;
+    }
     const bool lds = a.halo > 0 || (K - 1) * a.d == 0;
     const bool short_steps = a.steps_per_lane == 1;
     if (lds)
@@ -282,6 +727,20 @@ void dispatch_k(const TlArgs& a, hipStream_t st, std::integer_sequence<int, Ks..
     (void)((a.k == Ks + 1 ? (launch_k<DT, Ks + 1>(a, st), true) : false) || ...);
 }
 
+template <int DT, int K>
+void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
+{
+    const size_t lds = (size_t)2 * a.T * kTlRow * 4;
+    const int64_t blocks = (a.M + 63) / 64;
+    auto kern = tl_cols_bwd_kernel<DT, K>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
+}
+template <int DT, int... Ks>
+void dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
+{
+    (void)((a.k == Ks + 1 ? (launch_bwd_k<DT, Ks + 1>(a, st), true) : false) || ...);
+}
+
 }  // namespace
 
 hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t st)
@@ -293,6 +752,28 @@ hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t st)
     case MFPSN_F32: dispatch_k<MFPSN_F32>(a, st, Ks{}); break;
     case MFPSN_BF16: dispatch_k<MFPSN_BF16>(a, st, Ks{}); break;
     default: dispatch_k<MFPSN_Q8_8>(a, st, Ks{}); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mfpsn
+
+namespace mfpsn {
+
+hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t st)
+{
+    const int64_t n = (int64_t)(a.k + 1) * a.C;
+    if (n > 0) {
+        const int64_t blocks = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+        hipLaunchKernelGGL(tl_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (uint64_t*)a.acc, n);
+    }
+    if (a.M == 0 || a.T == 0)
+        return hipGetLastError();
+    using Ks = std::make_integer_sequence<int, MFPSN_MAX_K>;
+    switch (dtype) {
+    case MFPSN_F32: dispatch_bwd_k<MFPSN_F32>(a, st, Ks{}); break;
+    case MFPSN_BF16: dispatch_bwd_k<MFPSN_BF16>(a, st, Ks{}); break;
+    default: dispatch_bwd_k<MFPSN_Q8_8>(a, st, Ks{}); break;
     }
     return hipGetLastError();
 }

@@ -76,6 +76,10 @@ _lib.mfpsn_stream_step.argtypes = [_DP, ctypes.c_int64, _P, _P, _P, _P, _P, _P, 
 _lib.mfpsn_stream_step.restype = ctypes.c_int
 _lib.mfpsn_forward_time_last.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_forward_time_last.restype = ctypes.c_int
+_lib.mfpsn_backward_time_last_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
+_lib.mfpsn_backward_time_last_workspace_size.restype = ctypes.c_int
+_lib.mfpsn_backward_time_last.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_backward_time_last.restype = ctypes.c_int
 _lib.mfpsn_spikes_to_input.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, _P, _P]
 _lib.mfpsn_spikes_to_input.restype = ctypes.c_int
 _lib.mfpsn_sawtooth_dilation.argtypes = [ctypes.c_int32, ctypes.c_int32]
@@ -176,6 +180,21 @@ def mfpsn_quantizer_grad(w, shift, shift_lo: int, shift_hi: int, grad_wq, mode: 
 def mfpsn_forward_time_last(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, stream=None) -> None:
     _check(_lib.mfpsn_forward_time_last(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias),
                                         _ptr(spikes), _ptr(h_out), _stream(stream)), "mfpsn_forward_time_last")
+
+
+def mfpsn_backward_time_last_workspace_size(desc: MfpsnDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.mfpsn_backward_time_last_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
+           "mfpsn_backward_time_last_workspace_size")
+    return int(n.value)
+
+
+def mfpsn_backward_time_last(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
+                             stream=None) -> None:
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(_lib.mfpsn_backward_time_last(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(sign), _ptr(shift),
+                                         _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b), _ptr(workspace),
+                                         nbytes, _stream(stream)), "mfpsn_backward_time_last")
 
 
 def mfpsn_spikes_to_input(spikes, dtype: int, x, stream=None) -> None:
@@ -297,6 +316,24 @@ def forward_time_last(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = Fals
     h = torch.empty(x.shape, dtype=H_OUT[desc.dtype], device=dev) if want_h else None
     mfpsn_forward_time_last(desc, x, sign, shift, bias, spikes, h, stream)
     return (spikes, h) if want_h else spikes
+
+
+def backward_time_last(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None):
+    """Backward for x and grad_spikes in the time-last layout [N, C, *spatial,
+    T] (T <= 64): grad_x in the same layout, grad_w [C, k], grad_b [C]."""
+    dev = x.device
+    _expect(x, STORAGE[desc.dtype], dev, "x")
+    _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
+    if x.shape[-1] != desc.T or x.numel() != desc.T * desc.N * desc.C * desc.S or grad_spikes.shape != x.shape:
+        raise ValueError(f"x of shape {tuple(x.shape)} does not match the descriptor (time last)")
+    grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
+    grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
+    grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
+    need = mfpsn_backward_time_last_workspace_size(desc)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
+    mfpsn_backward_time_last(desc, x, grad_spikes, sign, shift, bias, grad_x, grad_w, grad_b, workspace, stream)
+    return grad_x, grad_w, grad_b
 
 
 def spikes_to_input(spikes, dtype: str = "f32", stream=None):

@@ -73,7 +73,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 8
+    assert lib.mfpsn_abi_version() == 9
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -257,3 +257,33 @@ def test_forward_time_last_validation(lib):
     assert f(ctypes.byref(d), FAKE + 2, FAKE, FAKE, FAKE, FAKE, None, None) == -6
     assert f(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, None) == -6
     assert f(ctypes.byref(good_desc(T=0)), None, None, None, None, None, None, None) == 0
+
+
+def test_backward_time_last_validation(lib):
+    f = lib.mfpsn_backward_time_last
+    f.argtypes = [ctypes.POINTER(Desc)] + [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p]
+    ws = lib.mfpsn_backward_time_last_workspace_size
+    ws.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(ctypes.c_size_t)]
+    n = ctypes.c_size_t(0)
+    d = good_desc()
+    assert ws(ctypes.byref(d), ctypes.byref(n)) == 0 and n.value == (d.k + 1) * d.C * 8
+    assert ws(ctypes.byref(d), None) == -1
+    need = n.value
+    assert f(None, *_bwd_tl_args(), need, None) == -1
+    assert f(ctypes.byref(good_desc(T=65)), *_bwd_tl_args(), need, None) == -2   # T > 64
+    assert f(ctypes.byref(good_desc(k=0)), *_bwd_tl_args(), need, None) == -3
+    assert f(ctypes.byref(good_desc(dtype=7)), *_bwd_tl_args(), need, None) == -4
+    assert f(ctypes.byref(d), *_bwd_tl_args(x=None), need, None) == -1
+    assert f(ctypes.byref(d), *_bwd_tl_args(gw=None), need, None) == -1
+    assert f(ctypes.byref(d), *_bwd_tl_args(x=FAKE + 2), need, None) == -6
+    assert f(ctypes.byref(d), *_bwd_tl_args(gx=FAKE + 2), need, None) == -6
+    assert f(ctypes.byref(good_desc(dtype=2)), *_bwd_tl_args(gw=FAKE + 4), need, None) == -6  # int64 grad_w
+    assert f(ctypes.byref(d), *_bwd_tl_args(), need - 8, None) == -5
+    assert f(ctypes.byref(d), *_bwd_tl_args(ws=None), need, None) == -5
+    assert f(ctypes.byref(d), *_bwd_tl_args(ws=FAKE + 4), need, None) == -5
+
+
+def _bwd_tl_args(**kw):
+    a = dict(x=FAKE, g=FAKE, sign=FAKE, shift=FAKE, bias=FAKE, gx=FAKE, gw=FAKE, gb=FAKE, ws=FAKE)
+    a.update(kw)
+    return [a[k] for k in ("x", "g", "sign", "shift", "bias", "gx", "gw", "gb", "ws")]

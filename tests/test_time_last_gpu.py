@@ -55,6 +55,13 @@ CASES = [
     (257, 1, 3, 2, 1, 1, "q8_8", False),
     (2100, 2, 3, 1, 3, 1100, "f32", False),   # history (k-1)d = 2200: taps from global memory
     (17, 2, 6, 3, 32, 1, "f32", False),
+    # lane-per-column kernel (T <= 64): full groups of 64 columns (vector
+    # loads and stores), T a multiple of 4 or not, a history longer than T
+    (32, 4, 16, 2, 8, 2, "f32", False),
+    (30, 2, 64, 3, 8, 3, "bf16", True),
+    (64, 1, 64, 1, 8, 4, "q8_8", False),
+    (2, 1, 64, 1, 3, 1, "f32", True),
+    (31, 3, 64, 1, 32, 2, "f32", False),
 ]
 
 
@@ -90,6 +97,37 @@ def test_time_last_forward_matches_oracle(orc, T, N, C, S, k, d, dtype, special)
     assert np.array_equal(got_h.view(view), to_time_last(h_tf.cpu().numpy()).view(view))
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
+def test_time_last_unaligned_views(orc, dtype):
+    """x one element past a 16-byte boundary and spikes 3 bytes past one:
+    element loads and byte stores instead of the vector forms."""
+    T, N, C, S, k, d = 30, 2, 64, 1, 8, 3
+    shape, x, w, bias = make(T, N, C, S, k, dtype, seed=11)
+    sign, shift = orc.quantize(w, 0, 7)
+    desc = mfpsn.make_desc(shape, k, d, dtype, "sigmoid", 4.0, 0.4, 100, 0, 7)
+    if dtype == "q8_8":
+        _, s_ref = orc.forward_q88(x, sign, shift, bias, k, d, 100, 0, 7)
+        flat = to_time_last(x).reshape(-1)
+    elif dtype == "bf16":
+        bits = orc.f32_to_bf16_bits_vec(x)
+        _, s_ref = orc.forward_bf16(bits, sign, shift, bias, k, d, 0.4, shift_lo=0, shift_hi=7)
+        flat = to_time_last(bits).view(np.int16).reshape(-1)
+    else:
+        _, s_ref = orc.forward_f32(x, sign, shift, bias, k, d, 0.4, 0, 7)
+        flat = to_time_last(x).reshape(-1)
+    buf = torch.zeros(flat.size + 1, dtype=torch.from_numpy(flat[:1]).dtype, device=DEV)
+    buf[1:] = torch.from_numpy(flat).to(DEV)
+    xt = buf[1:].view(to_time_last(x).shape)
+    if dtype == "bf16":
+        xt = xt.view(torch.bfloat16)
+    sbuf = torch.zeros(flat.size + 3, dtype=torch.uint8, device=DEV)
+    spikes = sbuf[3:].view(xt.shape)
+    sg, sh, b = (torch.from_numpy(a).to(DEV) for a in (sign, shift, bias))
+    mfpsn.mfpsn_forward_time_last(desc, xt, sg, sh, b, spikes, None, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert np.array_equal(spikes.cpu().numpy(), to_time_last(s_ref))
+
+
 def test_time_last_without_h(orc):
     T, N, C, S, k, d = 70, 2, 64, 1, 6, 2
     shape, x, w, bias = make(T, N, C, S, k, "f32", seed=5)
@@ -100,3 +138,87 @@ def test_time_last_without_h(orc):
                                      *(torch.from_numpy(a).to(DEV) for a in (sign, shift, bias)))
     torch.cuda.synchronize()
     assert np.array_equal(spikes.cpu().numpy(), to_time_last(s_ref))
+
+
+# (T, N, C, S, k, d, dtype, special, surrogate, alpha)
+BWD_CASES = [
+    (40, 3, 5, 7, 4, 2, "f32", False, "sigmoid", 4.0),     # ragged last group
+    (32, 4, 16, 2, 8, 2, "f32", False, "atan", 2.0),       # whole groups, vector loads
+    (30, 2, 64, 3, 8, 3, "bf16", True, "sigmoid", 4.0),    # zeros and subnormals: exact taps
+    (64, 1, 64, 1, 8, 4, "q8_8", False, "sigmoid", 4.0),
+    (31, 3, 64, 1, 32, 2, "q8_8", False, "atan", 5.0),
+    (17, 2, 6, 3, 32, 1, "f32", False, "rational", 10.0),  # history longer than T
+    (1, 3, 64, 1, 3, 1, "f32", False, "sigmoid", 4.0),     # one step
+    (20, 8, 3, 1, 5, 1, "f32", True, "sigmoid", 4.0),      # channels alternate across lanes
+    (16, 2, 2, 200, 4, 1, "bf16", False, "sigmoid", 4.0),  # one channel per wave
+    (12, 2, 20, 5, 3, 1, "f32", False, "sigmoid", 4.0),    # a one-lane channel run at lane 0, then five lanes
+]
+
+
+@pytest.mark.parametrize("T,N,C,S,k,d,dtype,special,sg,alpha", BWD_CASES)
+def test_time_last_backward_matches_oracle(orc, T, N, C, S, k, d, dtype, special, sg, alpha):
+    """grad_x bit for bit (every term of the definition, the surrogate's
+    fixed sequence); grad_w, grad_b within 1e-6 absolute + 1e-5 relative of
+    the oracle's double sums (Q8.8: exact integers)."""
+    shape, x, w, bias = make(T, N, C, S, k, dtype, seed=3 * T + k + d, special=special)
+    rng = np.random.default_rng(T * 31 + k)
+    g = rng.normal(0.0, 1.0, x.shape).astype(np.float32)
+    lo, hi = (0, 7) if dtype != "f32" or not special else (-3, 9)
+    sign, shift = orc.quantize(w, lo, hi)
+    v_th, v_th_q = 0.4, 100
+    desc = mfpsn.make_desc(shape, k, d, dtype, sg, alpha, v_th, v_th_q, lo, hi)
+    if dtype == "q8_8":
+        gq = np.clip(np.round(g * 256), -32768, 32767).astype(np.int16)
+        ref = orc.backward_q88(x, gq, sign, shift, bias, k, d, v_th_q, sg, alpha, lo, hi)
+        xt, gt = (torch.from_numpy(to_time_last(a)).to(DEV) for a in (x, gq))
+    elif dtype == "bf16":
+        xb, gb_ = orc.f32_to_bf16_bits_vec(x), orc.f32_to_bf16_bits_vec(g)
+        ref = orc.backward_bf16(xb, gb_, sign, shift, bias, k, d, v_th, surrogate_kind=sg, alpha=alpha,
+                                shift_lo=lo, shift_hi=hi)
+        xt, gt = (torch.from_numpy(to_time_last(a).view(np.int16)).to(DEV).view(torch.bfloat16) for a in (xb, gb_))
+    else:
+        ref = orc.backward_f32(x, g, sign, shift, bias, k, d, v_th, sg, alpha, lo, hi)
+        xt, gt = (torch.from_numpy(to_time_last(a)).to(DEV) for a in (x, g))
+    sg_t, sh_t, b_t = (torch.from_numpy(a).to(DEV) for a in (sign, shift, bias))
+    gx, gw, gb = mfpsn.backward_time_last(desc, xt, gt, sg_t, sh_t, b_t)
+    torch.cuda.synchronize()
+    if dtype == "bf16":
+        got = gx.view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, to_time_last(ref["grad_x_bits"])), "grad_x differs from the oracle"
+    elif dtype == "q8_8":
+        assert np.array_equal(gx.cpu().numpy(), to_time_last(ref["grad_x"])), "grad_x differs from the oracle"
+    else:
+        assert np.array_equal(gx.cpu().numpy().view(np.uint32), to_time_last(ref["grad_x"]).view(np.uint32)), \
+            "grad_x differs from the oracle"
+    if dtype == "q8_8":
+        assert np.array_equal(gw.cpu().numpy(), ref["grad_w"])
+        assert np.array_equal(gb.cpu().numpy(), ref["grad_b"])
+    else:
+        for got, want in ((gw, ref["grad_w"]), (gb, ref["grad_b"])):
+            got = got.cpu().numpy().astype(np.float64)
+            assert np.all(np.abs(got - want) <= 1e-6 + 1e-5 * np.abs(want)), np.max(np.abs(got - want))
+
+
+def test_time_last_backward_repeated_calls_and_empty(orc):
+    """The workspace is cleared by every call (two calls in a row give the
+    same gradients), and N = 0 gives zero gradients."""
+    T, N, C, S, k, d = 24, 2, 64, 2, 6, 2
+    shape, x, w, bias = make(T, N, C, S, k, "f32", seed=21)
+    g = np.random.default_rng(22).normal(0, 1, x.shape).astype(np.float32)
+    sign, shift = orc.quantize(w, 0, 7)
+    desc = mfpsn.make_desc(shape, k, d, "f32", "sigmoid", 4.0, 0.4, 0, 0, 7)
+    args = [torch.from_numpy(to_time_last(a)).to(DEV) for a in (x, g)]
+    args += [torch.from_numpy(a).to(DEV) for a in (sign, shift, bias)]
+    ws = torch.empty(mfpsn.mfpsn_backward_time_last_workspace_size(desc), dtype=torch.uint8, device=DEV)
+    first = [t.clone() for t in mfpsn.backward_time_last(desc, *args, workspace=ws)]
+    second = mfpsn.backward_time_last(desc, *args, workspace=ws)
+    ref = orc.backward_f32(x, g, sign, shift, bias, k, d, 0.4, "sigmoid", 4.0, 0, 7)
+    for a, b in zip(first, second):
+        assert torch.allclose(a, b, rtol=1e-6, atol=0)
+    got = second[1].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(got - ref["grad_w"]) <= 1e-6 + 1e-5 * np.abs(ref["grad_w"]))
+    empty = mfpsn.make_desc((T, 0, C, S), k, d, "f32", "sigmoid", 4.0, 0.4, 0, 0, 7)
+    z = torch.empty((0, C, S, T), dtype=torch.float32, device=DEV)
+    gx, gw, gb = mfpsn.backward_time_last(empty, z, z, *args[2:], workspace=ws)
+    torch.cuda.synchronize()
+    assert gx.numel() == 0 and not gw.any() and not gb.any()
