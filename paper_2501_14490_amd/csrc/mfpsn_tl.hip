@@ -530,8 +530,8 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     const int64_t col0 = (int64_t)blockIdx.x * 64;
     const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
     const int64_t gbase = col0 * T;
-    V* xt = reinterpret_cast<V*>(tl_lds);  // x, then grad_x
-    V* gt = xt + T * kRow;                 // grad_spikes, then dH
+    V* xt = reinterpret_cast<V*>(tl_lds);  // x, then grad_x; row T zeros
+    V* gt = xt + (T + 1) * kRow;           // grad_spikes, then dH; row T zeros
     const bool slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
     (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
 
@@ -548,6 +548,15 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     sg.init(a.sg, a.alpha);
     wave_lds_sync();
 
+    // Taps whose input lies outside the sequence read row T of a tile, which
+    // holds zeros: their grad_w products are zeros, and with the ldexp taps
+    // their terms are zeros too, which leave a sum that starts at +0 as it
+    // is; the exponent-add taps of such inputs are not zeros and are
+    // selected away.
+    xt[T * kRow + lane] = V(0);
+    gt[T * kRow + lane] = V(0);
+    const int span = (K - 1) * a.d;
+
     // walk 1: H, dH (over grad_spikes in the tile), grad_w and grad_b sums
     W gw[K], gb = W(0);
 #pragma unroll
@@ -555,19 +564,27 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
         gw[i] = W(0);
     bool out_dh = false;
     auto walk1 = [&](auto exact) {
+        constexpr bool EX = decltype(exact)::value;
         for (int t = 0; t < T; ++t) {
+            const bool edge = t < span;  // some tap input before time 0
             V in[K];
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const int tau = t - (K - 1 - i) * a.d;
-                in[i] = xt[(tau > 0 ? tau : 0) * kRow + lane];
+                in[i] = xt[(tau >= 0 ? tau : T) * kRow + lane];
             }
             const V gv = gt[t * kRow + lane];
             V acc = V(0);
+            if (!EX && edge) {
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                const V sum = acc + taps.template apply<decltype(exact)::value>(in[i], i);
-                acc = t - (K - 1 - i) * a.d >= 0 ? sum : acc;
+                for (int i = 0; i < K; ++i) {
+                    const V sum = acc + taps.template apply<EX>(in[i], i);
+                    acc = t - (K - 1 - i) * a.d >= 0 ? sum : acc;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    acc = acc + taps.template apply<EX>(in[i], i);
             }
             const V h = acc + bias;
             const V dh = delta_h(gv, sg_factor(sg, h, a.v_th, a.v_th_q));
@@ -575,12 +592,10 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
             gb += (W)dh;
 #pragma unroll
             for (int i = 0; i < K; ++i) {
-                W p;
                 if constexpr (kF)
-                    p = __builtin_fma((double)in[i], (double)dh, gw[i]);  // exact product, one rounding
+                    gw[i] = __builtin_fma((double)in[i], (double)dh, gw[i]);  // exact product, one rounding
                 else
-                    p = gw[i] + (int64_t)in[i] * (int64_t)dh;
-                gw[i] = t - (K - 1 - i) * a.d >= 0 ? p : gw[i];
+                    gw[i] += (int64_t)in[i] * (int64_t)dh;
             }
             if constexpr (kF) {
                 const float m = __builtin_fabsf(dh);
@@ -597,18 +612,26 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 
     // walk 2: grad_x into the x tile
     auto walk2 = [&](auto exact) {
+        constexpr bool EX = decltype(exact)::value;
         for (int t = 0; t < T; ++t) {
+            const bool edge = t + span >= T;  // some tap input past the end
             V in[K];
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const int tau = t + (K - 1 - i) * a.d;
-                in[i] = gt[(tau < T ? tau : T - 1) * kRow + lane];
+                in[i] = gt[(tau < T ? tau : T) * kRow + lane];
             }
             V acc = V(0);
+            if (!EX && edge) {
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                const V sum = acc + taps.template apply<decltype(exact)::value>(in[i], i);
-                acc = t + (K - 1 - i) * a.d < T ? sum : acc;
+                for (int i = 0; i < K; ++i) {
+                    const V sum = acc + taps.template apply<EX>(in[i], i);
+                    acc = t + (K - 1 - i) * a.d < T ? sum : acc;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    acc = acc + taps.template apply<EX>(in[i], i);
             }
             xt[t * kRow + lane] = acc;
         }
@@ -730,7 +753,7 @@ void dispatch_k(const TlArgs& a, hipStream_t st, std::integer_sequence<int, Ks..
 template <int DT, int K>
 void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
 {
-    const size_t lds = (size_t)2 * a.T * kTlRow * 4;
+    const size_t lds = (size_t)2 * (a.T + 1) * kTlRow * 4;
     const int64_t blocks = (a.M + 63) / 64;
     auto kern = tl_cols_bwd_kernel<DT, K>;
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
