@@ -429,8 +429,8 @@ def stack_step(torch, dev, wl, case, mode: str, steps: int, warmup: int):
 def time_last(torch, dev, wl, case, steps: int, warmup: int):
     """The workload's layers in the time-last layout [N][C][S][T], timed beside
     the time-first entry points on the same inputs: the forward (charge and
-    fire, spikes only; mfpsn_forward_time_last) and, for sequences of at most
-    64 steps, the backward (mfpsn_backward_time_last, H recomputed).
+    fire, spikes only; mfpsn_forward_time_last) and the backward
+    (mfpsn_backward_time_last, H recomputed).
     value = layers * T*N*C*S / time of the time-last step; roofline: the
     dominant kernel's algorithmic bytes per launch (backward: x, grad_spikes
     read, grad_x written; forward: x read, spikes written) over its average
@@ -439,7 +439,7 @@ def time_last(torch, dev, wl, case, steps: int, warmup: int):
 
     es = {"f32": 4, "bf16": 2, "q8_8": 2}[wl.dtype]
     gxs = {"f32": 4, "bf16": 2, "q8_8": 4}[wl.dtype]
-    with_bwd = wl.shape[0] <= 64
+    with_bwd = (wl.k - 1) * max(wl.dilations) <= 1024 or wl.shape[0] <= 64
     raw = {}
     for name in ("x", "grad_spikes"):
         a = case[name]

@@ -274,7 +274,7 @@ int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t*
 int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* bytes);
 
 /* Backward (App. A.3 Eqs. backward_X, backward_W, backward_b, with the taps
- * dilated by d) in the time-last layout, for sequences of at most 64 steps:
+ * dilated by d) in the time-last layout:
  *   x, grad_spikes : [N][C][S][T] storage type of desc->dtype
  *   grad_x         : [N][C][S][T] float (F32), bfloat16 (BF16, rounded to
  *                    nearest even) or int32 (Q8.8)
@@ -288,8 +288,9 @@ int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* byte
  * grad_w and grad_b are sums of exact products in double (int64 for Q8.8)
  * rounded once to float; the double sums are added in an order that can
  * change from call to call (the Q8.8 sums are exact).  Errors as
- * mfpsn_backward; MFPSN_ERR_SHAPE also for T > 64 or N*C*S >= 2^37.
- * Asynchronous on `stream`. */
+ * mfpsn_backward; MFPSN_ERR_SHAPE also for N*C*S >= 2^37 and, when T > 64,
+ * for (k-1)*dilation > 1024 or N*C*S*ceil(T/256) >= 2^33.  Asynchronous on
+ * `stream`. */
 int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const int8_t* sign,
                              const int8_t* shift, const void* bias, void* grad_x, void* grad_w, void* grad_b,
                              void* workspace, size_t workspace_bytes, void* stream);

@@ -9,7 +9,9 @@ namespace mfpsn {
 
 constexpr int kTlWaves = 4;                 // waves per block
 constexpr int kTlMaxHalo = 2048;            // longest history staged in LDS
-constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-column kernel
+constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-column kernels
+constexpr int kTlBwdSeg = 256;              // time steps per segment of the long-column backward
+constexpr int kTlBwdMaxSpan = 1024;         // longest history (k-1) d of the long-column backward
 
 struct TlArgs {
     const void* x;          // [N][C][S][T] storage type
@@ -34,7 +36,7 @@ struct TlArgs {
 
 hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t stream);
 
-// Backward in the time-last layout (T <= kTlColsMaxT)
+// Backward in the time-last layout
 struct TlBwdArgs {
     const void* x;          // [N][C][S][T] storage type
     const void* g;          // grad_spikes, [N][C][S][T] storage type
@@ -53,6 +55,7 @@ struct TlBwdArgs {
     float fast_lo, fast_hi; // range of |x| and |dH| in which the exponent-add tap is exact
     uint32_t tdiv;          // as TlArgs::tdiv (0 when T = 1)
     int32_t vec_x;          // x and g aligned for 4-element vector loads
+    int32_t nseg;           // segments of kTlBwdSeg steps per column (T > kTlColsMaxT)
 };
 
 // Zeroes acc, runs the backward, which adds into acc; the caller finalizes

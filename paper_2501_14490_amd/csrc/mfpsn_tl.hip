@@ -696,6 +696,186 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     }
 }
 
+// Sum over the 64 lanes, every lane gets it
+template <typename W> __device__ __forceinline__ W tl_wave_sum(W v)
+{
+#pragma unroll
+    for (int j = 1; j < 64; j <<= 1) {
+        if constexpr (std::is_same_v<W, double>) {
+            v += __shfl_xor(v, j, 64);
+        } else {
+            const int lo = __shfl_xor((int)(uint32_t)v, j, 64);
+            const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), j, 64);
+            v += (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+        }
+    }
+    return v;
+}
+
+// Backward for long columns (T > kTlColsMaxT) in the time-last layout:
+// persistent waves over segments of kTlBwdSeg time steps of one column, lane
+// = time step, so the taps are the same on every lane.  With P = (k-1) d,
+// a segment [t0, t0 + L) stages x over [t0 - P, t0 + L + P) and grad_spikes
+// over [t0, t0 + L + P) in the wave's LDS windows (zeros outside [0, T)),
+// recomputes H and dH over [t0, t0 + L + P) (the dH its grad_x needs), adds
+// the exact products and dH of its own steps to grad_w / grad_b sums, forms
+// grad_x over its own steps from the dH window, and adds the wave's sums to
+// acc[k+1][C] with one atomic per tap.  The dH of the P steps after a
+// segment is recomputed by the next one.
+template <int DT, int K>
+__global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    using W = std::conditional_t<kF, double, int64_t>;
+    constexpr int L = kTlBwdSeg;
+    extern __shared__ uint32_t tl_lds[];
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = (int)threadIdx.x & 63;
+    const int T = a.T, d = a.d, span = (K - 1) * d;
+    const int xw = L + 2 * span, dw = L + span;
+    V* xs = reinterpret_cast<V*>(tl_lds) + (size_t)wave * (xw + dw);
+    V* ds = xs + xw;
+    const int64_t units = a.M * a.nseg, stride = (int64_t)gridDim.x * kTlWaves;
+    Surrogate sg;
+    sg.init(a.sg, a.alpha);
+    W* acc_out = reinterpret_cast<W*>(a.acc);
+    for (int64_t u = (int64_t)blockIdx.x * kTlWaves + wave; u < units; u += stride) {
+        const int64_t col = u / a.nseg;
+        const int t0 = (int)(u - col * a.nseg) * L;
+        const int c = (int)((col / a.S) % a.C);
+        const int64_t cbase = col * (int64_t)T;
+        bool out = false;
+        for (int j = lane; j < xw; j += 64) {
+            const int t = t0 - span + j;
+            V v = V(0);
+            if (t >= 0 && t < T) {
+                v = TlIO<DT>::ld(a.x, cbase + t);
+                if constexpr (kF) {
+                    const float m = __builtin_fabsf(v);
+                    out = out || !(m >= a.fast_lo && m < a.fast_hi);
+                }
+            }
+            xs[j] = v;
+        }
+        for (int j = lane; j < dw; j += 64) {
+            const int t = t0 + j;
+            ds[j] = t < T ? TlIO<DT>::ld(a.g, cbase + t) : V(0);
+        }
+        const bool slow_x = kF && __builtin_amdgcn_ballot_w64(out) != 0;
+        TlLaneTaps<DT, K> taps;
+        taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
+        V bias;
+        if constexpr (kF)
+            bias = ((const float*)a.bias)[c];
+        else
+            bias = ((const int32_t*)a.bias)[c];
+        wave_lds_sync();
+
+        // H and dH over [t0, t0 + L + P); x of time t - (k-1-i) d is xs[j + i d]
+        W gw[K], gb = W(0);
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            gw[i] = W(0);
+        bool out_dh = false;
+        const bool head = t0 < span;  // some tap input before time 0 (zeros in the window)
+        auto walk1 = [&](auto exact) {
+            constexpr bool EX = decltype(exact)::value;
+            for (int j = lane; j < dw; j += 64) {
+                const int t = t0 + j;
+                if (t >= T)
+                    break;
+                V acc = V(0);
+                if (!EX && head) {
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc + taps.template apply<EX>(xs[j + i * d], i);
+                        acc = t - (K - 1 - i) * d >= 0 ? sum : acc;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + taps.template apply<EX>(xs[j + i * d], i);
+                }
+                const V h = acc + bias;
+                const V dh = delta_h(ds[j], sg_factor(sg, h, a.v_th, a.v_th_q));
+                ds[j] = dh;
+                if constexpr (kF) {
+                    const float m = __builtin_fabsf(dh);
+                    out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
+                }
+                if (j < L) {  // this segment's own step
+                    gb += (W)dh;
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        if constexpr (kF)
+                            gw[i] = __builtin_fma((double)xs[j + i * d], (double)dh, gw[i]);
+                        else
+                            gw[i] += (int64_t)xs[j + i * d] * (int64_t)dh;
+                    }
+                }
+            }
+        };
+        if (slow_x)
+            walk1(std::true_type{});
+        else
+            walk1(std::false_type{});
+        const bool slow_dh = kF && __builtin_amdgcn_ballot_w64(out_dh) != 0;
+        wave_lds_sync();
+
+        // grad_x over [t0, t0 + L): dH of time t + (k-1-i) d is ds[j + (k-1-i) d]
+        const bool tail = t0 + L + span > T;  // some tap input past the end (zeros)
+        auto walk2 = [&](auto exact) {
+            constexpr bool EX = decltype(exact)::value;
+            for (int j = lane; j < L; j += 64) {
+                const int t = t0 + j;
+                if (t >= T)
+                    break;
+                V acc = V(0);
+                if (!EX && tail) {
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc + taps.template apply<EX>(ds[j + (K - 1 - i) * d], i);
+                        acc = t + (K - 1 - i) * d < T ? sum : acc;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + taps.template apply<EX>(ds[j + (K - 1 - i) * d], i);
+                }
+                if constexpr (DT == MFPSN_BF16)
+                    reinterpret_cast<uint16_t*>(a.grad_x)[cbase + t] = tl_bf16_rne(acc);
+                else
+                    reinterpret_cast<V*>(a.grad_x)[cbase + t] = acc;
+            }
+        };
+        if (slow_dh)
+            walk2(std::true_type{});
+        else
+            walk2(std::false_type{});
+
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const W v = tl_wave_sum(gw[i]);
+            if (lane == 0) {
+                if constexpr (kF)
+                    atomicAdd(acc_out + (size_t)i * a.C + c, v);
+                else
+                    atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)i * a.C + c,
+                              (unsigned long long)v);
+            }
+        }
+        const W v = tl_wave_sum(gb);
+        if (lane == 0) {
+            if constexpr (kF)
+                atomicAdd(acc_out + (size_t)K * a.C + c, v);
+            else
+                atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)K * a.C + c,
+                          (unsigned long long)v);
+        }
+        wave_lds_sync();  // every read of the windows before the next segment's writes
+    }
+}
+
 __global__ void tl_zero_kernel(uint64_t* p, int64_t n)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
@@ -753,10 +933,26 @@ void dispatch_k(const TlArgs& a, hipStream_t st, std::integer_sequence<int, Ks..
 template <int DT, int K>
 void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
 {
-    const size_t lds = (size_t)2 * (a.T + 1) * kTlRow * 4;
-    const int64_t blocks = (a.M + 63) / 64;
-    auto kern = tl_cols_bwd_kernel<DT, K>;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
+    if (a.T <= kTlColsMaxT) {
+        const size_t lds = (size_t)2 * (a.T + 1) * kTlRow * 4;
+        const int64_t blocks = (a.M + 63) / 64;
+        auto kern = tl_cols_bwd_kernel<DT, K>;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
+        return;
+    }
+    // persistent grid: every resident block slot, at most one segment per wave
+    const int span = (K - 1) * a.d;
+    const size_t lds = (size_t)kTlWaves * (2 * kTlBwdSeg + 3 * (size_t)span) * 4;
+    auto kern = tl_seg_bwd_kernel<DT, K>;
+    int dev = 0, nb = 0, cus = 0;
+    (void)hipGetDevice(&dev);
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, kTlWaves * 64, lds);
+    const int64_t units = a.M * a.nseg;
+    int64_t blocks = (units + kTlWaves - 1) / kTlWaves;
+    const int64_t cap = (int64_t)(nb > 0 ? nb : 1) * (cus > 0 ? cus : 1);
+    blocks = blocks < cap ? blocks : cap;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kTlWaves * 64), lds, st, a);
 }
 template <int DT, int... Ks>
 void dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)

@@ -270,7 +270,7 @@ def test_backward_time_last_validation(lib):
     assert ws(ctypes.byref(d), None) == -1
     need = n.value
     assert f(None, *_bwd_tl_args(), need, None) == -1
-    assert f(ctypes.byref(good_desc(T=65)), *_bwd_tl_args(), need, None) == -2   # T > 64
+    assert f(ctypes.byref(good_desc(T=65, k=32, dilation=34)), *_bwd_tl_args(), need, None) == -2  # history > 1024
     assert f(ctypes.byref(good_desc(k=0)), *_bwd_tl_args(), need, None) == -3
     assert f(ctypes.byref(good_desc(dtype=7)), *_bwd_tl_args(), need, None) == -4
     assert f(ctypes.byref(d), *_bwd_tl_args(x=None), need, None) == -1

@@ -152,6 +152,14 @@ BWD_CASES = [
     (20, 8, 3, 1, 5, 1, "f32", True, "sigmoid", 4.0),      # channels alternate across lanes
     (16, 2, 2, 200, 4, 1, "bf16", False, "sigmoid", 4.0),  # one channel per wave
     (12, 2, 20, 5, 3, 1, "f32", False, "sigmoid", 4.0),    # a one-lane channel run at lane 0, then five lanes
+    # long columns (T > 64): segments of 256 steps, one channel per wave
+    (300, 2, 9, 1, 16, 3, "f32", False, "sigmoid", 4.0),   # two segments, the second ragged
+    (300, 2, 9, 1, 16, 3, "f32", True, "atan", 2.0),       # zeros and subnormals: exact taps
+    (520, 1, 3, 2, 5, 4, "bf16", True, "sigmoid", 4.0),
+    (600, 1, 4, 3, 32, 8, "q8_8", False, "sigmoid", 4.0),  # history of 248 steps
+    (257, 1, 3, 2, 1, 1, "q8_8", False, "rational", 10.0),
+    (65, 3, 5, 1, 8, 20, "f32", False, "sigmoid", 4.0),    # history 140 > T: every step in the head
+    (1100, 1, 2, 1, 32, 33, "f32", False, "sigmoid", 4.0), # history 1023 (the longest), several segments
 ]
 
 
