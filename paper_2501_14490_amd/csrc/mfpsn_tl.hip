@@ -719,9 +719,10 @@ template <typename W> __device__ __forceinline__ W tl_wave_sum(W v)
 // over [t0, t0 + L + P) in the wave's LDS windows (zeros outside [0, T)),
 // recomputes H and dH over [t0, t0 + L + P) (the dH its grad_x needs), adds
 // the exact products and dH of its own steps to grad_w / grad_b sums, forms
-// grad_x over its own steps from the dH window, and adds the wave's sums to
-// acc[k+1][C] with one atomic per tap.  The dH of the P steps after a
-// segment is recomputed by the next one.
+// grad_x over its own steps from the dH window.  A wave takes a contiguous
+// run of segments in channel-major order and adds its sums to acc[k+1][C]
+// (one atomic per tap) when the channel changes and at the end.  The dH of
+// the P steps after a segment is recomputed by the next one.
 template <int DT, int K>
 __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
 {
@@ -735,15 +736,66 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
     const int xw = L + 2 * span, dw = L + span;
     V* xs = reinterpret_cast<V*>(tl_lds) + (size_t)wave * (xw + dw);
     V* ds = xs + xw;
-    const int64_t units = a.M * a.nseg, stride = (int64_t)gridDim.x * kTlWaves;
+    // units in channel-major order (c, n, s, segment); wave w takes the
+    // contiguous run [w chunk, (w+1) chunk), so its sums stay in registers
+    // while the channel stays the same
+    const int64_t units = a.M * a.nseg, per_c = units / a.C;
+    const int64_t nwaves = (int64_t)gridDim.x * kTlWaves;
+    const int64_t chunk = (units + nwaves - 1) / nwaves;
+    const int64_t v0 = ((int64_t)blockIdx.x * kTlWaves + wave) * chunk;
+    const int64_t v1 = v0 + chunk < units ? v0 + chunk : units;
     Surrogate sg;
     sg.init(a.sg, a.alpha);
     W* acc_out = reinterpret_cast<W*>(a.acc);
-    for (int64_t u = (int64_t)blockIdx.x * kTlWaves + wave; u < units; u += stride) {
-        const int64_t col = u / a.nseg;
-        const int t0 = (int)(u - col * a.nseg) * L;
-        const int c = (int)((col / a.S) % a.C);
+    W gw[K], gb = W(0);
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        gw[i] = W(0);
+    TlLaneTaps<DT, K> taps;
+    V bias = V(0);
+    int cur = -1;  // channel of the sums (wave-uniform)
+    auto flush = [&]() {
+        if (cur < 0)
+            return;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const W v = tl_wave_sum(gw[i]);
+            gw[i] = W(0);
+            if (lane == 0) {
+                if constexpr (kF)
+                    atomicAdd(acc_out + (size_t)i * a.C + cur, v);
+                else
+                    atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)i * a.C + cur,
+                              (unsigned long long)v);
+            }
+        }
+        const W v = tl_wave_sum(gb);
+        gb = W(0);
+        if (lane == 0) {
+            if constexpr (kF)
+                atomicAdd(acc_out + (size_t)K * a.C + cur, v);
+            else
+                atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)K * a.C + cur,
+                          (unsigned long long)v);
+        }
+    };
+    for (int64_t u = v0; u < v1; ++u) {
+        const int c = (int)(u / per_c);
+        const int64_t r = u - (int64_t)c * per_c;
+        const int64_t ns = r / a.nseg;  // n S + s
+        const int t0 = (int)(r - ns * a.nseg) * L;
+        const int64_t n = ns / a.S;
+        const int64_t col = (n * a.C + c) * a.S + (ns - n * a.S);
         const int64_t cbase = col * (int64_t)T;
+        if (c != cur) {
+            flush();
+            cur = c;
+            taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
+            if constexpr (kF)
+                bias = ((const float*)a.bias)[c];
+            else
+                bias = ((const int32_t*)a.bias)[c];
+        }
         bool out = false;
         for (int j = lane; j < xw; j += 64) {
             const int t = t0 - span + j;
@@ -762,20 +814,9 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
             ds[j] = t < T ? TlIO<DT>::ld(a.g, cbase + t) : V(0);
         }
         const bool slow_x = kF && __builtin_amdgcn_ballot_w64(out) != 0;
-        TlLaneTaps<DT, K> taps;
-        taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
-        V bias;
-        if constexpr (kF)
-            bias = ((const float*)a.bias)[c];
-        else
-            bias = ((const int32_t*)a.bias)[c];
         wave_lds_sync();
 
         // H and dH over [t0, t0 + L + P); x of time t - (k-1-i) d is xs[j + i d]
-        W gw[K], gb = W(0);
-#pragma unroll
-        for (int i = 0; i < K; ++i)
-            gw[i] = W(0);
         bool out_dh = false;
         const bool head = t0 < span;  // some tap input before time 0 (zeros in the window)
         auto walk1 = [&](auto exact) {
@@ -852,28 +893,9 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
             walk2(std::true_type{});
         else
             walk2(std::false_type{});
-
-#pragma unroll
-        for (int i = 0; i < K; ++i) {
-            const W v = tl_wave_sum(gw[i]);
-            if (lane == 0) {
-                if constexpr (kF)
-                    atomicAdd(acc_out + (size_t)i * a.C + c, v);
-                else
-                    atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)i * a.C + c,
-                              (unsigned long long)v);
-            }
-        }
-        const W v = tl_wave_sum(gb);
-        if (lane == 0) {
-            if constexpr (kF)
-                atomicAdd(acc_out + (size_t)K * a.C + c, v);
-            else
-                atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)K * a.C + c,
-                          (unsigned long long)v);
-        }
         wave_lds_sync();  // every read of the windows before the next segment's writes
     }
+    flush();
 }
 
 __global__ void tl_zero_kernel(uint64_t* p, int64_t n)
