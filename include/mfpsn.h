@@ -289,8 +289,8 @@ int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* byte
  * rounded once to float; the double sums are added in an order that can
  * change from call to call (the Q8.8 sums are exact).  Errors as
  * mfpsn_backward; MFPSN_ERR_SHAPE also for N*C*S >= 2^37 and, when T > 64,
- * for (k-1)*dilation > 1024 or N*C*S*ceil(T/256) >= 2^33.  Asynchronous on
- * `stream`. */
+ * for (k-1)*dilation > 1024 or N*C*S*ceil(T/L) >= 2^33, L = 256 (1024 when
+ * (k-1)*dilation > 64).  Asynchronous on `stream`. */
 int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const int8_t* sign,
                              const int8_t* shift, const void* bias, void* grad_x, void* grad_w, void* grad_b,
                              void* workspace, size_t workspace_bytes, void* stream);

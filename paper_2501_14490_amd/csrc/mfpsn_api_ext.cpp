@@ -344,7 +344,10 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
     if (st != MFPSN_OK)
         return st;
     const int64_t M = (int64_t)desc->N * desc->C * desc->S;
-    const int64_t nseg = ((int64_t)desc->T + kTlBwdSeg - 1) / kTlBwdSeg;
+    // long histories: longer segments, so that the dH recomputed over the
+    // history after each segment is a smaller share of its work
+    const int seg = (int64_t)(desc->k - 1) * desc->dilation > 64 ? kTlBwdSegLong : kTlBwdSeg;
+    const int64_t nseg = ((int64_t)desc->T + seg - 1) / seg;
     if (M >= ((int64_t)1 << 37))
         return MFPSN_ERR_SHAPE;
     if (desc->T > kTlColsMaxT &&
@@ -394,6 +397,7 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
     fast_range(desc, &a.fast_lo, &a.fast_hi);
     a.tdiv = desc->T >= 2 ? (uint32_t)((((uint64_t)1) << 32) / (uint64_t)desc->T + 1) : 0;
     a.vec_x = aligned(x, 4 * es) && aligned(grad_spikes, 4 * es) ? 1 : 0;
+    a.seg = seg;
     a.nseg = (int32_t)nseg;
     hipStream_t s = (hipStream_t)stream;
     if (launch_backward_time_last(a, desc->dtype, s) != hipSuccess)

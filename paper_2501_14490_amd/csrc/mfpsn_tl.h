@@ -11,6 +11,7 @@ constexpr int kTlWaves = 4;                 // waves per block
 constexpr int kTlMaxHalo = 2048;            // longest history staged in LDS
 constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-column kernels
 constexpr int kTlBwdSeg = 256;              // time steps per segment of the long-column backward
+constexpr int kTlBwdSegLong = 1024;         // the same for histories (k-1) d above 64
 constexpr int kTlBwdMaxSpan = 1024;         // longest history (k-1) d of the long-column backward
 
 struct TlArgs {
@@ -55,7 +56,8 @@ struct TlBwdArgs {
     float fast_lo, fast_hi; // range of |x| and |dH| in which the exponent-add tap is exact
     uint32_t tdiv;          // as TlArgs::tdiv (0 when T = 1)
     int32_t vec_x;          // x and g aligned for 4-element vector loads
-    int32_t nseg;           // segments of kTlBwdSeg steps per column (T > kTlColsMaxT)
+    int32_t seg;            // time steps per segment (T > kTlColsMaxT): kTlBwdSeg or kTlBwdSegLong
+    int32_t nseg;           // segments per column, ceil(T / seg)
 };
 
 // Zeroes acc, runs the backward, which adds into acc; the caller finalizes

@@ -713,7 +713,7 @@ template <typename W> __device__ __forceinline__ W tl_wave_sum(W v)
 }
 
 // Backward for long columns (T > kTlColsMaxT) in the time-last layout:
-// persistent waves over segments of kTlBwdSeg time steps of one column, lane
+// persistent waves over segments of L = a.seg time steps of one column, lane
 // = time step, so the taps are the same on every lane.  With P = (k-1) d,
 // a segment [t0, t0 + L) stages x over [t0 - P, t0 + L + P) and grad_spikes
 // over [t0, t0 + L + P) in the wave's LDS windows (zeros outside [0, T)),
@@ -729,10 +729,9 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
     using V = typename TlIO<DT>::V;
     constexpr bool kF = DT != MFPSN_Q8_8;
     using W = std::conditional_t<kF, double, int64_t>;
-    constexpr int L = kTlBwdSeg;
     extern __shared__ uint32_t tl_lds[];
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = (int)threadIdx.x & 63;
-    const int T = a.T, d = a.d, span = (K - 1) * d;
+    const int T = a.T, d = a.d, span = (K - 1) * d, L = a.seg;
     const int xw = L + 2 * span, dw = L + span;
     V* xs = reinterpret_cast<V*>(tl_lds) + (size_t)wave * (xw + dw);
     V* ds = xs + xw;
@@ -964,7 +963,7 @@ void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
     }
     // persistent grid: every resident block slot, at most one segment per wave
     const int span = (K - 1) * a.d;
-    const size_t lds = (size_t)kTlWaves * (2 * kTlBwdSeg + 3 * (size_t)span) * 4;
+    const size_t lds = (size_t)kTlWaves * (2 * (size_t)a.seg + 3 * (size_t)span) * 4;
     auto kern = tl_seg_bwd_kernel<DT, K>;
     int dev = 0, nb = 0, cus = 0;
     (void)hipGetDevice(&dev);

@@ -160,6 +160,7 @@ BWD_CASES = [
     (257, 1, 3, 2, 1, 1, "q8_8", False, "rational", 10.0),
     (65, 3, 5, 1, 8, 20, "f32", False, "sigmoid", 4.0),    # history 140 > T: every step in the head
     (1100, 1, 2, 1, 32, 33, "f32", False, "sigmoid", 4.0), # history 1023 (the longest), several segments
+    (2500, 1, 2, 1, 16, 6, "q8_8", False, "sigmoid", 4.0), # 1024-step segments, the last one ragged
 ]
 
 
