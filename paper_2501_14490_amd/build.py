@@ -62,10 +62,13 @@ def _units():
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
                   [qg_src, os.path.join(CSRC, "mfpsn_qgrad.h")]))
     tl_src = os.path.join(CSRC, "mfpsn_tl.hip")
-    obj = os.path.join(BUILD, "tl.o")
-    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", tl_src, "-o", obj],
-                  [tl_src, os.path.join(CSRC, "mfpsn_tl.h"), os.path.join(CSRC, "mfpsn_surrogate.h"),
-                   os.path.join(INCLUDE, "mfpsn.h")]))
+    tl_deps = [tl_src, os.path.join(CSRC, "mfpsn_tl.h"), os.path.join(CSRC, "mfpsn_surrogate.h"),
+               os.path.join(INCLUDE, "mfpsn.h")]
+    for tag, flag in (("d0", "-DMFPSN_TL_DTYPE=0"), ("d1", "-DMFPSN_TL_DTYPE=1"), ("d2", "-DMFPSN_TL_DTYPE=2"),
+                      ("dispatch", None)):
+        obj = os.path.join(BUILD, f"tl_{tag}.o")
+        units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *([flag] if flag else []),
+                            "-c", tl_src, "-o", obj], tl_deps))
     chain_src = os.path.join(CSRC, "mfpsn_chain.hip")
     obj = os.path.join(BUILD, "chain.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", chain_src, "-o", obj],

@@ -64,4 +64,12 @@ struct TlBwdArgs {
 // acc into grad_w and grad_b.
 hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t stream);
 
+// One storage type's launchers, each in its own translation unit
+void tl_forward_f32(const TlArgs& a, hipStream_t st);
+void tl_forward_bf16(const TlArgs& a, hipStream_t st);
+void tl_forward_q88(const TlArgs& a, hipStream_t st);
+void tl_backward_f32(const TlBwdArgs& a, hipStream_t st);
+void tl_backward_bf16(const TlBwdArgs& a, hipStream_t st);
+void tl_backward_q88(const TlBwdArgs& a, hipStream_t st);
+
 }  // namespace mfpsn

@@ -557,7 +557,10 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     gt[T * kRow + lane] = V(0);
     const int span = (K - 1) * a.d;
 
-    // walk 1: H, dH (over grad_spikes in the tile), grad_w and grad_b sums
+    // walk 1: H, dH (over grad_spikes in the tile), grad_w and grad_b sums.
+    // Steps go in pairs whose LDS reads all issue before either step's
+    // write, so that two independent chains are in flight; steps whose taps
+    // reach before time 0 (t < span) run apart, with the selects they need.
     W gw[K], gb = W(0);
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -565,43 +568,60 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     bool out_dh = false;
     auto walk1 = [&](auto exact) {
         constexpr bool EX = decltype(exact)::value;
-        for (int t = 0; t < T; ++t) {
-            const bool edge = t < span;  // some tap input before time 0
-            V in[K];
+        auto steps = [&](int t, auto npair, auto edge_c) {
+            constexpr int NP = decltype(npair)::value;
+            constexpr bool EDGE = decltype(edge_c)::value && !EX;
+            V in[NP][K], gv[NP], dh[NP];
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                const int tau = t - (K - 1 - i) * a.d;
-                in[i] = xt[(tau >= 0 ? tau : T) * kRow + lane];
-            }
-            const V gv = gt[t * kRow + lane];
-            V acc = V(0);
-            if (!EX && edge) {
+            for (int p = 0; p < NP; ++p) {
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
-                    const V sum = acc + taps.template apply<EX>(in[i], i);
-                    acc = t - (K - 1 - i) * a.d >= 0 ? sum : acc;
+                    const int tau = t + p - (K - 1 - i) * a.d;
+                    in[p][i] = xt[(tau >= 0 ? tau : T) * kRow + lane];
                 }
-            } else {
+                gv[p] = gt[(t + p) * kRow + lane];
+            }
 #pragma unroll
-                for (int i = 0; i < K; ++i)
-                    acc = acc + taps.template apply<EX>(in[i], i);
-            }
-            const V h = acc + bias;
-            const V dh = delta_h(gv, sg_factor(sg, h, a.v_th, a.v_th_q));
-            gt[t * kRow + lane] = dh;
-            gb += (W)dh;
+            for (int p = 0; p < NP; ++p) {
+                V acc = V(0);
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                if constexpr (kF)
-                    gw[i] = __builtin_fma((double)in[i], (double)dh, gw[i]);  // exact product, one rounding
-                else
-                    gw[i] += (int64_t)in[i] * (int64_t)dh;
+                for (int i = 0; i < K; ++i) {
+                    const V sum = acc + taps.template apply<EX>(in[p][i], i);
+                    if constexpr (EDGE)
+                        acc = t + p - (K - 1 - i) * a.d >= 0 ? sum : acc;
+                    else
+                        acc = sum;
+                }
+                const V h = acc + bias;
+                dh[p] = delta_h(gv[p], sg_factor(sg, h, a.v_th, a.v_th_q));
             }
-            if constexpr (kF) {
-                const float m = __builtin_fabsf(dh);
-                out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                gt[(t + p) * kRow + lane] = dh[p];
+                gb += (W)dh[p];
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    if constexpr (kF)
+                        gw[i] = __builtin_fma((double)in[p][i], (double)dh[p], gw[i]);  // exact product, one rounding
+                    else
+                        gw[i] += (int64_t)in[p][i] * (int64_t)dh[p];
+                }
+                if constexpr (kF) {
+                    const float m = __builtin_fabsf(dh[p]);
+                    out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
+                }
             }
-        }
+        };
+        const int te = span < T ? span : T;
+        int t = 0;
+        for (; t + 1 < te; t += 2)
+            steps(t, std::integral_constant<int, 2>{}, std::true_type{});
+        if (t < te)
+            steps(t++, std::integral_constant<int, 1>{}, std::true_type{});
+        for (; t + 1 < T; t += 2)
+            steps(t, std::integral_constant<int, 2>{}, std::false_type{});
+        if (t < T)
+            steps(t, std::integral_constant<int, 1>{}, std::false_type{});
     };
     if (slow_x)
         walk1(std::true_type{});
@@ -610,31 +630,49 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     const bool slow_dh = kF && __builtin_amdgcn_ballot_w64(out_dh) != 0;
     wave_lds_sync();
 
-    // walk 2: grad_x into the x tile
+    // walk 2: grad_x into the x tile, in pairs as walk 1; steps whose taps
+    // reach past T-1 (t >= T - span) run apart with their selects
     auto walk2 = [&](auto exact) {
         constexpr bool EX = decltype(exact)::value;
-        for (int t = 0; t < T; ++t) {
-            const bool edge = t + span >= T;  // some tap input past the end
-            V in[K];
+        auto steps = [&](int t, auto npair, auto edge_c) {
+            constexpr int NP = decltype(npair)::value;
+            constexpr bool EDGE = decltype(edge_c)::value && !EX;
+            V in[NP][K];
 #pragma unroll
-            for (int i = 0; i < K; ++i) {
-                const int tau = t + (K - 1 - i) * a.d;
-                in[i] = gt[(tau < T ? tau : T) * kRow + lane];
-            }
-            V acc = V(0);
-            if (!EX && edge) {
+            for (int p = 0; p < NP; ++p) {
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
-                    const V sum = acc + taps.template apply<EX>(in[i], i);
-                    acc = t + (K - 1 - i) * a.d < T ? sum : acc;
+                    const int tau = t + p + (K - 1 - i) * a.d;
+                    in[p][i] = gt[(tau < T ? tau : T) * kRow + lane];
                 }
-            } else {
-#pragma unroll
-                for (int i = 0; i < K; ++i)
-                    acc = acc + taps.template apply<EX>(in[i], i);
             }
-            xt[t * kRow + lane] = acc;
-        }
+            V acc[NP];
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                acc[p] = V(0);
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    const V sum = acc[p] + taps.template apply<EX>(in[p][i], i);
+                    if constexpr (EDGE)
+                        acc[p] = t + p + (K - 1 - i) * a.d < T ? sum : acc[p];
+                    else
+                        acc[p] = sum;
+                }
+            }
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+                xt[(t + p) * kRow + lane] = acc[p];
+        };
+        const int tb = T - span > 0 ? T - span : 0;  // first step with a tap past T-1
+        int t = 0;
+        for (; t + 1 < tb; t += 2)
+            steps(t, std::integral_constant<int, 2>{}, std::false_type{});
+        if (t < tb)
+            steps(t++, std::integral_constant<int, 1>{}, std::false_type{});
+        for (; t + 1 < T; t += 2)
+            steps(t, std::integral_constant<int, 2>{}, std::true_type{});
+        if (t < T)
+            steps(t, std::integral_constant<int, 1>{}, std::true_type{});
     };
     if (slow_dh)
         walk2(std::true_type{});
@@ -983,22 +1021,32 @@ void dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<in
 
 }  // namespace
 
+// Every storage type's kernels are compiled in a translation unit of their
+// own (MFPSN_TL_DTYPE = 0, 1, 2); the unit without it holds the dispatch.
+#if defined(MFPSN_TL_DTYPE)
+using TlKs = std::make_integer_sequence<int, MFPSN_MAX_K>;
+#if MFPSN_TL_DTYPE == 0
+void tl_forward_f32(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_F32>(a, st, TlKs{}); }
+void tl_backward_f32(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_F32>(a, st, TlKs{}); }
+#elif MFPSN_TL_DTYPE == 1
+void tl_forward_bf16(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_BF16>(a, st, TlKs{}); }
+void tl_backward_bf16(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_BF16>(a, st, TlKs{}); }
+#else
+void tl_forward_q88(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_Q8_8>(a, st, TlKs{}); }
+void tl_backward_q88(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_Q8_8>(a, st, TlKs{}); }
+#endif
+#else
 hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t st)
 {
     if (a.M == 0 || a.T == 0)
         return hipSuccess;
-    using Ks = std::make_integer_sequence<int, MFPSN_MAX_K>;
     switch (dtype) {
-    case MFPSN_F32: dispatch_k<MFPSN_F32>(a, st, Ks{}); break;
-    case MFPSN_BF16: dispatch_k<MFPSN_BF16>(a, st, Ks{}); break;
-    default: dispatch_k<MFPSN_Q8_8>(a, st, Ks{}); break;
+    case MFPSN_F32: tl_forward_f32(a, st); break;
+    case MFPSN_BF16: tl_forward_bf16(a, st); break;
+    default: tl_forward_q88(a, st); break;
     }
     return hipGetLastError();
 }
-
-}  // namespace mfpsn
-
-namespace mfpsn {
 
 hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t st)
 {
@@ -1009,13 +1057,13 @@ hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t 
     }
     if (a.M == 0 || a.T == 0)
         return hipGetLastError();
-    using Ks = std::make_integer_sequence<int, MFPSN_MAX_K>;
     switch (dtype) {
-    case MFPSN_F32: dispatch_bwd_k<MFPSN_F32>(a, st, Ks{}); break;
-    case MFPSN_BF16: dispatch_bwd_k<MFPSN_BF16>(a, st, Ks{}); break;
-    default: dispatch_bwd_k<MFPSN_Q8_8>(a, st, Ks{}); break;
+    case MFPSN_F32: tl_backward_f32(a, st); break;
+    case MFPSN_BF16: tl_backward_bf16(a, st); break;
+    default: tl_backward_q88(a, st); break;
     }
     return hipGetLastError();
 }
+#endif
 
 }  // namespace mfpsn
