@@ -264,7 +264,7 @@ const char* mfpsn_status_string(int status);
  * sign, shift, bias, desc (sizes T, N, C, S as for mfpsn_forward) and the
  * values computed are those of mfpsn_forward: the outputs are its outputs
  * with the time axis moved last, bit for bit.  Same alignment and errors as
- * mfpsn_forward; MFPSN_ERR_SHAPE also when N*C*S*ceil(T/256) >= 2^33.  The
+ * mfpsn_forward; MFPSN_ERR_SHAPE also when N*C*S*ceil(T/64) >= 2^33.  The
  * library keeps no state; the call is asynchronous on `stream`. */
 int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
                             const void* bias, uint8_t* spikes, void* h_out, void* stream);

@@ -283,10 +283,14 @@ int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t*
     if (st != MFPSN_OK)
         return st;
     const int64_t M = (int64_t)desc->N * desc->C * desc->S;
-    // segments of 256 time steps, or of 64 for short sequences (fewer idle lanes)
+    // long columns with histories of at most kTlBwdMaxSpan steps: segments of
+    // 256 steps (1024 for histories above 64); longer histories: segments of
+    // 256 time steps, or of 64 for short sequences (fewer idle lanes)
+    const int64_t span = (int64_t)(desc->k - 1) * desc->dilation;
+    const int seg = desc->T > kTlColsMaxT && span <= kTlBwdMaxSpan ? (span > 64 ? kTlBwdSegLong : kTlBwdSeg) : 0;
     const int spl = desc->T > 96 ? 4 : 1;
-    const int64_t nseg = ((int64_t)desc->T + 64 * spl - 1) / (64 * spl);
-    if (M * nseg >= ((int64_t)1 << 33))  // blocks of kTlWaves segments must fit the grid
+    const int64_t nseg = seg > 0 ? ((int64_t)desc->T + seg - 1) / seg : ((int64_t)desc->T + 64 * spl - 1) / (64 * spl);
+    if (M * (((int64_t)desc->T + 63) / 64) >= ((int64_t)1 << 33))  // segments must fit the grid
         return MFPSN_ERR_SHAPE;
     if (M == 0 || desc->T == 0)
         return MFPSN_OK;
@@ -309,8 +313,8 @@ int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t*
     a.k = desc->k;
     a.d = desc->dilation;
     a.steps_per_lane = spl;
+    a.seg = seg;
     a.nseg = (int32_t)nseg;
-    const int64_t span = (int64_t)(desc->k - 1) * desc->dilation;
     a.halo = span <= kTlMaxHalo ? (int32_t)span : 0;
     a.shift_lo = desc->shift_lo;
     a.shift_hi = desc->shift_hi;

@@ -23,8 +23,9 @@ struct TlArgs {
     void* h_out;            // nullable, float or int32 [N][C][S][T]
     int64_t M;              // columns, N*C*S
     int32_t T, C, S, k, d;
-    int32_t steps_per_lane; // 1 or 4: segments of 64 or 256 time steps
-    int32_t nseg;           // segments per column, ceil(T / (64 * steps_per_lane))
+    int32_t steps_per_lane; // 1 or 4: segments of 64 or 256 time steps (seg = 0)
+    int32_t seg;            // > 0: segment length of tl_seg_fwd_kernel (T > kTlColsMaxT, history <= kTlBwdMaxSpan)
+    int32_t nseg;           // segments per column, ceil(T / seg), else ceil(T / (64 * steps_per_lane))
     int32_t halo;           // LDS history slots per wave (0: taps read from global memory)
     int32_t shift_lo, shift_hi;
     float v_th;

@@ -734,6 +734,42 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     }
 }
 
+// dst[j] = src[cbase + t_first + j] for j in [0, n), 0 where the time
+// t_first + j lies outside [0, T); the loads go in batches of eight per lane,
+// all issued before their LDS writes.  With CHECK, returns (wave-uniform)
+// whether some staged float lies outside [lo, hi).
+template <int DT, bool CHECK>
+__device__ __forceinline__ bool tl_stage_window(const void* src, int64_t cbase, int t_first, int n, int T,
+                                                typename TlIO<DT>::V* dst, float lo, float hi)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr int B = 8;
+    const int lane = (int)threadIdx.x & 63;
+    bool out = false;
+    for (int base = 0; base < n; base += 64 * B) {
+        V v[B];
+#pragma unroll
+        for (int q = 0; q < B; ++q) {
+            const int j = base + lane + 64 * q;
+            const int t = t_first + j;
+            v[q] = j < n && t >= 0 && t < T ? TlIO<DT>::ld(src, cbase + t) : V(0);
+        }
+#pragma unroll
+        for (int q = 0; q < B; ++q) {
+            const int j = base + lane + 64 * q;
+            if (j < n) {
+                dst[j] = v[q];
+                if constexpr (CHECK && DT != MFPSN_Q8_8) {
+                    const int t = t_first + j;
+                    const float m = __builtin_fabsf(v[q]);
+                    out = out || (t >= 0 && t < T && !(m >= lo && m < hi));
+                }
+            }
+        }
+    }
+    return CHECK && DT != MFPSN_Q8_8 && __builtin_amdgcn_ballot_w64(out) != 0;
+}
+
 // Sum over the 64 lanes, every lane gets it
 template <typename W> __device__ __forceinline__ W tl_wave_sum(W v)
 {
@@ -833,24 +869,8 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
             else
                 bias = ((const int32_t*)a.bias)[c];
         }
-        bool out = false;
-        for (int j = lane; j < xw; j += 64) {
-            const int t = t0 - span + j;
-            V v = V(0);
-            if (t >= 0 && t < T) {
-                v = TlIO<DT>::ld(a.x, cbase + t);
-                if constexpr (kF) {
-                    const float m = __builtin_fabsf(v);
-                    out = out || !(m >= a.fast_lo && m < a.fast_hi);
-                }
-            }
-            xs[j] = v;
-        }
-        for (int j = lane; j < dw; j += 64) {
-            const int t = t0 + j;
-            ds[j] = t < T ? TlIO<DT>::ld(a.g, cbase + t) : V(0);
-        }
-        const bool slow_x = kF && __builtin_amdgcn_ballot_w64(out) != 0;
+        const bool slow_x = tl_stage_window<DT, true>(a.x, cbase, t0 - span, xw, T, xs, a.fast_lo, a.fast_hi);
+        (void)tl_stage_window<DT, false>(a.g, cbase, t0, dw, T, ds, 0.0f, 0.0f);
         wave_lds_sync();
 
         // H and dH over [t0, t0 + L + P); x of time t - (k-1-i) d is xs[j + i d]
@@ -941,6 +961,87 @@ __global__ void tl_zero_kernel(uint64_t* p, int64_t n)
         p[i] = 0;
 }
 
+// Forward for long columns (T > kTlColsMaxT) with histories P = (k-1) d of
+// at most kTlBwdMaxSpan steps: persistent waves over segments [t0, t0 + L)
+// of one column (L = a.seg), lane = time step, in channel-major runs as in
+// tl_seg_bwd_kernel (the taps are loaded again only when the channel
+// changes).  A segment stages x over [t0 - P, t0 + L) in the wave's LDS
+// window (zeros before time 0), so the input of tap i for step t0 + j is
+// xs[j + i d]; only the first segment of a column, whose taps reach before
+// time 0, selects the exponent-add terms of those zeros away.
+template <int DT, int K>
+__global__ __launch_bounds__(kTlWaves * 64) void tl_seg_fwd_kernel(TlArgs a)
+{
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    extern __shared__ uint32_t tl_lds[];
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = (int)threadIdx.x & 63;
+    const int T = a.T, d = a.d, span = (K - 1) * d, L = a.seg;
+    const int xw = L + span;
+    V* xs = reinterpret_cast<V*>(tl_lds) + (size_t)wave * xw;
+    const int64_t units = a.M * a.nseg, per_c = units / a.C;
+    const int64_t nwaves = (int64_t)gridDim.x * kTlWaves;
+    const int64_t chunk = (units + nwaves - 1) / nwaves;
+    const int64_t v0 = ((int64_t)blockIdx.x * kTlWaves + wave) * chunk;
+    const int64_t v1 = v0 + chunk < units ? v0 + chunk : units;
+    TlLaneTaps<DT, K> taps;
+    V bias = V(0);
+    int cur = -1;
+    for (int64_t u = v0; u < v1; ++u) {
+        const int c = (int)(u / per_c);
+        const int64_t r = u - (int64_t)c * per_c;
+        const int64_t ns = r / a.nseg;  // n S + s
+        const int t0 = (int)(r - ns * a.nseg) * L;
+        const int64_t n = ns / a.S;
+        const int64_t cbase = ((n * a.C + c) * a.S + (ns - n * a.S)) * (int64_t)T;
+        if (c != cur) {
+            cur = c;
+            taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
+            if constexpr (kF)
+                bias = ((const float*)a.bias)[c];
+            else
+                bias = ((const int32_t*)a.bias)[c];
+        }
+        const bool slow = tl_stage_window<DT, true>(a.x, cbase, t0 - span, xw, T, xs, a.fast_lo, a.fast_hi);
+        wave_lds_sync();
+        const bool head = t0 < span;
+        auto walk = [&](auto exact) {
+            constexpr bool EX = decltype(exact)::value;
+            for (int j = lane; j < L; j += 64) {
+                const int t = t0 + j;
+                if (t >= T)
+                    break;
+                V acc = V(0);
+                if (!EX && head) {
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc + taps.template apply<EX>(xs[j + i * d], i);
+                        acc = t - (K - 1 - i) * d >= 0 ? sum : acc;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = acc + taps.template apply<EX>(xs[j + i * d], i);
+                }
+                const V h = acc + bias;
+                bool fire;
+                if constexpr (kF)
+                    fire = h >= a.v_th;
+                else
+                    fire = h >= a.v_th_q;
+                a.spikes[cbase + t] = fire ? 1 : 0;
+                if (a.h_out != nullptr)
+                    reinterpret_cast<V*>(a.h_out)[cbase + t] = h;
+            }
+        };
+        if (slow)
+            walk(std::true_type{});
+        else
+            walk(std::false_type{});
+        wave_lds_sync();  // every read of the window before the next segment's writes
+    }
+}
+
 template <int DT, int K, int NS, bool LDS>
 void launch_variant(const TlArgs& a, hipStream_t st)
 {
@@ -974,6 +1075,20 @@ void launch_k(const TlArgs& a, hipStream_t st)
         const int64_t blocks = (a.M + 63) / 64;
         auto kern = tl_cols_kernel<DT, K>;
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
+        return;
+    }
+    if (a.seg > 0) {  // histories of at most kTlBwdMaxSpan steps
+        const size_t lds = (size_t)kTlWaves * ((size_t)a.seg + (size_t)(K - 1) * a.d) * 4;
+        auto kern = tl_seg_fwd_kernel<DT, K>;
+        int dev = 0, nb = 0, cus = 0;
+        (void)hipGetDevice(&dev);
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, kTlWaves * 64, lds);
+        const int64_t units = a.M * a.nseg;
+        int64_t blocks = (units + kTlWaves - 1) / kTlWaves;
+        const int64_t cap = (int64_t)(nb > 0 ? nb : 1) * (cus > 0 ? cus : 1);
+        blocks = blocks < cap ? blocks : cap;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kTlWaves * 64), lds, st, a);
         return;
     }
     const bool lds = a.halo > 0 || (K - 1) * a.d == 0;

@@ -62,6 +62,11 @@ CASES = [
     (64, 1, 64, 1, 8, 4, "q8_8", False),
     (2, 1, 64, 1, 3, 1, "f32", True),
     (31, 3, 64, 1, 32, 2, "f32", False),
+    # long columns: 1024-step segments (history above 64), a history longer
+    # than T, and a history of 1200 steps (the LDS-window segment kernel)
+    (2500, 1, 3, 1, 16, 6, "q8_8", False),
+    (65, 3, 5, 1, 8, 20, "bf16", True),
+    (1500, 1, 2, 1, 3, 600, "f32", True),
 ]
 
 
