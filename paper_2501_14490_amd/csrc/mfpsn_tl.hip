@@ -570,14 +570,15 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
         constexpr bool EX = decltype(exact)::value;
         auto steps = [&](int t, auto npair, auto edge_c) {
             constexpr int NP = decltype(npair)::value;
-            constexpr bool EDGE = decltype(edge_c)::value && !EX;
+            constexpr bool NEAR = decltype(edge_c)::value;  // some tap before time 0
+            constexpr bool EDGE = NEAR && !EX;              // ... whose term must be selected away
             V in[NP][K], gv[NP], dh[NP];
 #pragma unroll
             for (int p = 0; p < NP; ++p) {
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
                     const int tau = t + p - (K - 1 - i) * a.d;
-                    in[p][i] = xt[(tau >= 0 ? tau : T) * kRow + lane];
+                    in[p][i] = xt[(NEAR && tau < 0 ? T : tau) * kRow + lane];
                 }
                 gv[p] = gt[(t + p) * kRow + lane];
             }
@@ -636,14 +637,15 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
         constexpr bool EX = decltype(exact)::value;
         auto steps = [&](int t, auto npair, auto edge_c) {
             constexpr int NP = decltype(npair)::value;
-            constexpr bool EDGE = decltype(edge_c)::value && !EX;
+            constexpr bool NEAR = decltype(edge_c)::value;  // some tap past T-1
+            constexpr bool EDGE = NEAR && !EX;
             V in[NP][K];
 #pragma unroll
             for (int p = 0; p < NP; ++p) {
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
                     const int tau = t + p + (K - 1 - i) * a.d;
-                    in[p][i] = gt[(tau < T ? tau : T) * kRow + lane];
+                    in[p][i] = gt[(NEAR && tau >= T ? T : tau) * kRow + lane];
                 }
             }
             V acc[NP];
