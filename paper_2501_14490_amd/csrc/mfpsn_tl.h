@@ -1,5 +1,5 @@
-// Internal interface of the time-last forward kernel (mfpsn_tl.hip) for the
-// C-ABI layer.  Not installed; not part of the ABI.
+// Internal interface of the time-last kernels (mfpsn_tl.hip: forward and
+// backward) for the C-ABI layer.  Not installed; not part of the ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -8,11 +8,11 @@
 namespace mfpsn {
 
 constexpr int kTlWaves = 4;                 // waves per block
-constexpr int kTlMaxHalo = 2048;            // longest history staged in LDS
+constexpr int kTlMaxHalo = 2048;            // longest history tl_fwd_kernel stages in LDS
 constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-column kernels
-constexpr int kTlBwdSeg = 256;              // time steps per segment of the long-column backward
+constexpr int kTlBwdSeg = 256;              // time steps per segment of the zero-window segment kernels
 constexpr int kTlBwdSegLong = 1024;         // the same for histories (k-1) d above 64
-constexpr int kTlBwdMaxSpan = 1024;         // longest history (k-1) d of the long-column backward
+constexpr int kTlBwdMaxSpan = 1024;         // longest history (k-1) d of the zero-window segment kernels
 
 struct TlArgs {
     const void* x;          // [N][C][S][T] storage type

@@ -1,16 +1,17 @@
-// gfx950 forward of the mul-free channel-wise neuron (arXiv 2501.14490,
-// Eqs. mfdpsn_charge, mfdpsn_fire) for the time-last layout [N][C][S][T]
-// (time innermost, the paper's second layout).
+// gfx950 kernels of the mul-free channel-wise neuron (arXiv 2501.14490,
+// Eqs. mfdpsn_charge, mfdpsn_fire; App. A.3 Eqs. backward_X, backward_W,
+// backward_b) for the time-last layout [N][C][S][T] (time innermost, the
+// paper's second layout).
 //
-// A wave takes segments of 64 or 256 consecutive time steps of one column
-// (lane l: steps t0 + l + 64 v), so its channel, and with it the k taps, are
-// the same on every lane and sit in scalar registers.  The wave stages the
-// inputs its taps read, x[t0 - (k-1)d .. t0 + 64 NS - 1] of its column, in
-// its own LDS window with coalesced loads; every tap then reads its input
-// from LDS at t - (k-1-i) d (consecutive lanes, consecutive addresses).
-// Waves are persistent, and the loads of a wave's next segment are in flight
-// while it computes the current one.  A history longer than the LDS slots
-// reads the taps from global memory instead.
+// Short columns (T <= 64): one wave per group of 64 columns, lane = column,
+// the group transposed through LDS (tl_cols_kernel, tl_cols_bwd_kernel).
+// Long columns: a wave per segment of consecutive time steps of one column,
+// lane = time step, so the channel and its k taps are the same on every lane;
+// the segment's inputs and the history its taps read are staged in the
+// wave's LDS window with coalesced loads (tl_seg_fwd_kernel,
+// tl_seg_bwd_kernel; tl_fwd_kernel for histories above 1024 steps, with the
+// next segment's loads in flight while it computes and the taps read from
+// global memory past 2048 steps).
 //
 // The arithmetic is the definition's, as in the time-first kernels: taps in
 // ascending order starting from the first one whose input exists (time >= 0),
@@ -67,10 +68,15 @@ struct TlUnit {
     int t0, ws, we, c;
 };
 
+// Forward for histories above kTlBwdMaxSpan steps (and T > kTlColsMaxT).
 // Persistent waves: wave w takes segments w, w + W, ... (W waves in the
-// grid); NS time steps per lane and segment (64 NS per segment); LDS: the
-// window in LDS, the first NS+2 loads of the next segment's window in
-// flight while the current one computes.
+// grid) of 64 NS consecutive time steps of one column, lane l taking steps
+// t0 + l + 64 v; the taps are wave-uniform and sit in scalar registers.
+// LDS: the segment and the (k-1) d steps before it in the wave's window
+// (every tap then reads its input at t - (k-1-i) d: consecutive lanes,
+// consecutive addresses), the first NS+2 loads of the next segment's window
+// in flight while the current one computes; without LDS (histories above
+// kTlMaxHalo) the taps read global memory.
 template <int DT, int K, int NS, bool LDS>
 __global__ __launch_bounds__(kTlWaves * 64) void tl_fwd_kernel(TlArgs a)
 {
