@@ -286,18 +286,41 @@ template <int DT, int K> struct TlLaneTaps {
     using V = typename TlIO<DT>::V;
     uint32_t kc[kF ? K : 1];
     int sh[kF ? 1 : K], neg[kF ? 1 : K];
+    int nneg;  // Q8.8: number of negative taps
     __device__ __forceinline__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
     {
+        nneg = 0;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             int sv = shift[c * K + i];
             sv = sv < lo ? lo : (sv > hi ? hi : sv);
             const bool n = sign[c * K + i] < 0;
-            if constexpr (kF)
+            if constexpr (kF) {
                 kc[i] = ((uint32_t)(-sv) << 23) ^ (n ? 0x80000000u : 0u);
-            else
+            } else {
                 sh[i] = sv, neg[i] = n ? -1 : 0;
+                nneg += n ? 1 : 0;
+            }
         }
+    }
+    // A sum over all k taps (every input exists) as start() followed by
+    // accumulate() per tap in ascending order.  Float: +0 and one rounded add
+    // per term, as apply().  Q8.8: ((v >> s) ^ m) is +(v >> s) or -(v >> s) - 1,
+    // so the sum starts at the number of negative taps and adds it unchanged
+    // (integers: the same value).
+    __device__ __forceinline__ V start() const
+    {
+        if constexpr (kF)
+            return V(0);
+        else
+            return nneg;
+    }
+    template <bool EXACT> __device__ __forceinline__ V accumulate(V acc, V in, int i) const
+    {
+        if constexpr (kF)
+            return acc + apply<EXACT>(in, i);
+        else
+            return ((in >> sh[i]) ^ neg[i]) + acc;
     }
     // sign * in * 2^-s: EXACT by v_ldexp_f32 and a sign flip, else by the
     // bit-pattern add (exact for |in| in the fast range); Q8.8 floor shift
@@ -424,9 +447,10 @@ __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
 #pragma unroll
                     for (int i = 0; i < K; ++i)
                         in[i] = xt[(t - (K - 1 - i) * a.d) * kRow + lane];
+                    acc[j] = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc[j] = acc[j] + tap(in[i], i, exact);
+                        acc[j] = taps.template accumulate<decltype(exact)::value>(acc[j], in[i], i);
                 }
             } else {
                 // from the first tap whose input exists (time >= 0): the
@@ -590,14 +614,20 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
             }
 #pragma unroll
             for (int p = 0; p < NP; ++p) {
-                V acc = V(0);
+                V acc;
+                if constexpr (EDGE) {
+                    acc = V(0);
 #pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    const V sum = acc + taps.template apply<EX>(in[p][i], i);
-                    if constexpr (EDGE)
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc + taps.template apply<EX>(in[p][i], i);
                         acc = t + p - (K - 1 - i) * a.d >= 0 ? sum : acc;
-                    else
-                        acc = sum;
+                    }
+                } else {
+                    // every term counts (the zero rows' terms are zeros)
+                    acc = taps.start();
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc = taps.template accumulate<EX>(acc, in[p][i], i);
                 }
                 const V h = acc + bias;
                 dh[p] = delta_h(gv[p], sg_factor(sg, h, a.v_th, a.v_th_q));
@@ -657,14 +687,18 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
             V acc[NP];
 #pragma unroll
             for (int p = 0; p < NP; ++p) {
-                acc[p] = V(0);
+                if constexpr (EDGE) {
+                    acc[p] = V(0);
 #pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    const V sum = acc[p] + taps.template apply<EX>(in[p][i], i);
-                    if constexpr (EDGE)
+                    for (int i = 0; i < K; ++i) {
+                        const V sum = acc[p] + taps.template apply<EX>(in[p][i], i);
                         acc[p] = t + p + (K - 1 - i) * a.d < T ? sum : acc[p];
-                    else
-                        acc[p] = sum;
+                    }
+                } else {
+                    acc[p] = taps.start();
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        acc[p] = taps.template accumulate<EX>(acc[p], in[p][i], i);
                 }
             }
 #pragma unroll
@@ -898,9 +932,10 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
                         acc = t - (K - 1 - i) * d >= 0 ? sum : acc;
                     }
                 } else {
+                    acc = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc = acc + taps.template apply<EX>(xs[j + i * d], i);
+                        acc = taps.template accumulate<EX>(acc, xs[j + i * d], i);
                 }
                 const V h = acc + bias;
                 const V dh = delta_h(ds[j], sg_factor(sg, h, a.v_th, a.v_th_q));
@@ -944,9 +979,10 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
                         acc = t + (K - 1 - i) * d < T ? sum : acc;
                     }
                 } else {
+                    acc = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc = acc + taps.template apply<EX>(ds[j + (K - 1 - i) * d], i);
+                        acc = taps.template accumulate<EX>(acc, ds[j + (K - 1 - i) * d], i);
                 }
                 if constexpr (DT == MFPSN_BF16)
                     reinterpret_cast<uint16_t*>(a.grad_x)[cbase + t] = tl_bf16_rne(acc);
@@ -1027,9 +1063,10 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_fwd_kernel(TlArgs a)
                         acc = t - (K - 1 - i) * d >= 0 ? sum : acc;
                     }
                 } else {
+                    acc = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc = acc + taps.template apply<EX>(xs[j + i * d], i);
+                        acc = taps.template accumulate<EX>(acc, xs[j + i * d], i);
                 }
                 const V h = acc + bias;
                 bool fire;
