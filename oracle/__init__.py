@@ -14,9 +14,13 @@ and ``tests/test_golden.py``):
   forward_*       k=1 closed form, np.convolve (sliding PSN), dense Toeplitz
                   matrix of App. A.2, causality, time-shift, zero input,
                   power-of-two scaling, Fraction brute force, the op counts of
-                  Table "params and shape" / Table "energy"
+                  Table "params and shape" / Table "energy"; per-channel
+                  thresholds: equal values reproduce the shared threshold bit
+                  for bit, each channel equals its own scalar run, firing at
+                  equality
   backward_*      transposed Toeplitz, adjoint identity, finite differences
-                  of the smoothed loss, exact big-integer sums (Q8.8)
+                  of the smoothed loss (also in the per-channel thresholds:
+                  grad_vth = -sum dH), exact big-integer sums (Q8.8)
   surrogate, exp  closed forms at 0, symmetry, unit integral, 2-ulp bound
                   against double exp
   sawtooth        the printed sequence and receptive-field example of Sec. 4.1
@@ -79,14 +83,14 @@ def _load():
             lib.orc_quantize.argtypes = [P, i64, i32, i32, P, P]
             lib.orc_quantize.restype = None
             geo = [i32] * 6  # T N C S k d
-            lib.orc_forward_f32.argtypes = [P, *geo, P, P, i32, i32, P, f32, P, P, P]
+            lib.orc_forward_f32.argtypes = [P, *geo, P, P, i32, i32, P, f32, P, P, P, P]
             lib.orc_forward_f32.restype = None
-            lib.orc_forward_q88.argtypes = [P, *geo, P, P, i32, i32, P, ctypes.c_int32, P, P, P]
+            lib.orc_forward_q88.argtypes = [P, *geo, P, P, i32, i32, P, ctypes.c_int32, P, P, P, P]
             lib.orc_forward_q88.restype = None
-            lib.orc_backward_f32.argtypes = [P, P, *geo, P, P, i32, i32, P, f32, i32, f32, P, P, P, P, P]
+            lib.orc_backward_f32.argtypes = [P, P, *geo, P, P, i32, i32, P, f32, P, i32, f32, P, P, P, P, P, P]
             lib.orc_backward_f32.restype = None
-            lib.orc_backward_q88.argtypes = [P, P, *geo, P, P, i32, i32, P, ctypes.c_int32, i32, f32,
-                                             P, P, P, P, P]
+            lib.orc_backward_q88.argtypes = [P, P, *geo, P, P, i32, i32, P, ctypes.c_int32, P, i32, f32,
+                                             P, P, P, P, P, P]
             lib.orc_backward_q88.restype = None
             lib.orc_bn_forward_stats.argtypes = [P, *geo, P, P, P, f32, P, P, P, P]
             lib.orc_bn_forward_stats.restype = None
@@ -233,39 +237,51 @@ def quantizer_grad(w, shift, grad_wq, mode: int, shift_lo: int, shift_hi: int) -
 # ---------------------------------------------------------------------------
 # forward
 # ---------------------------------------------------------------------------
+def _thresholds(v_th_c, C, dtype):
+    """Per-channel thresholds [C] as a contiguous array, or None (the scalar
+    threshold applies to every channel)."""
+    if v_th_c is None:
+        return None
+    return _c(v_th_c, dtype).reshape(C)
+
+
 def forward_f32(x, sign, shift, bias, k: int, d: int, v_th: float, shift_lo: int = -127,
-                shift_hi: int = 127, with_tap_count: bool = False):
-    """Float potentials H and spikes for x [T, N, C, ...] float32."""
+                shift_hi: int = 127, with_tap_count: bool = False, v_th_c=None):
+    """Float potentials H and spikes for x [T, N, C, ...] float32.  v_th_c:
+    optional per-channel thresholds [C] (then v_th is not used)."""
     x = _c(x, np.float32)
     T, N, C, S = _geometry(x)
     sign = _c(sign, np.int8).reshape(C, k)
     shift = _c(shift, np.int8).reshape(C, k)
     bias = _c(bias, np.float32).reshape(C)
+    vc = _thresholds(v_th_c, C, np.float32)
     H = np.empty(x.shape, np.float32)
     spk = np.empty(x.shape, np.uint8)
     taps = ctypes.c_int64(0)
     _load().orc_forward_f32(_ptr(x), T, N, C, S, int(k), int(d), _ptr(sign), _ptr(shift),
-                            int(shift_lo), int(shift_hi), _ptr(bias), float(v_th), _ptr(H), _ptr(spk),
-                            ctypes.byref(taps))
+                            int(shift_lo), int(shift_hi), _ptr(bias), float(v_th),
+                            None if vc is None else _ptr(vc), _ptr(H), _ptr(spk), ctypes.byref(taps))
     if with_tap_count:
         return H, spk, int(taps.value)
     return H, spk
 
 
 def forward_q88(x, sign, shift, bias, k: int, d: int, v_th: int, shift_lo: int = 0,
-                shift_hi: int = 31, with_tap_count: bool = False):
-    """Q8.8 potentials H (int32) and spikes for x [T, N, C, ...] int16."""
+                shift_hi: int = 31, with_tap_count: bool = False, v_th_c=None):
+    """Q8.8 potentials H (int32) and spikes for x [T, N, C, ...] int16.
+    v_th_c: optional per-channel Q8.8 thresholds [C] (int32)."""
     x = _c(x, np.int16)
     T, N, C, S = _geometry(x)
     sign = _c(sign, np.int8).reshape(C, k)
     shift = _c(shift, np.int8).reshape(C, k)
     bias = _c(bias, np.int32).reshape(C)
+    vc = _thresholds(v_th_c, C, np.int32)
     H = np.empty(x.shape, np.int32)
     spk = np.empty(x.shape, np.uint8)
     taps = ctypes.c_int64(0)
     _load().orc_forward_q88(_ptr(x), T, N, C, S, int(k), int(d), _ptr(sign), _ptr(shift),
-                            int(shift_lo), int(shift_hi), _ptr(bias), int(v_th), _ptr(H), _ptr(spk),
-                            ctypes.byref(taps))
+                            int(shift_lo), int(shift_hi), _ptr(bias), int(v_th),
+                            None if vc is None else _ptr(vc), _ptr(H), _ptr(spk), ctypes.byref(taps))
     if with_tap_count:
         return H, spk, int(taps.value)
     return H, spk
@@ -316,8 +332,9 @@ def stream_forward(x, sign, shift, bias, k: int, d: int, v_th, dtype: str = "f32
 # backward
 # ---------------------------------------------------------------------------
 def backward_f32(x, g, sign, shift, bias, k: int, d: int, v_th: float, surrogate_kind="sigmoid",
-                 alpha: float = 4.0, shift_lo: int = -127, shift_hi: int = 127):
-    """Returns dict with H, dH, grad_x (float32), grad_w, grad_b (float64 sums)."""
+                 alpha: float = 4.0, shift_lo: int = -127, shift_hi: int = 127, v_th_c=None):
+    """Returns dict with H, dH, grad_x (float32), grad_w, grad_b, grad_vth
+    (float64 sums).  v_th_c: optional per-channel thresholds [C]."""
     x = _c(x, np.float32)
     g = _c(g, np.float32)
     T, N, C, S = _geometry(x)
@@ -325,20 +342,24 @@ def backward_f32(x, g, sign, shift, bias, k: int, d: int, v_th: float, surrogate
     sign = _c(sign, np.int8).reshape(C, k)
     shift = _c(shift, np.int8).reshape(C, k)
     bias = _c(bias, np.float32).reshape(C)
+    vc = _thresholds(v_th_c, C, np.float32)
     H = np.empty(x.shape, np.float32)
     dH = np.empty(x.shape, np.float32)
     gx = np.empty(x.shape, np.float32)
     gw = np.empty((C, k), np.float64)
     gb = np.empty((C,), np.float64)
+    gv = np.empty((C,), np.float64)
     _load().orc_backward_f32(_ptr(x), _ptr(g), T, N, C, S, int(k), int(d), _ptr(sign), _ptr(shift),
-                             int(shift_lo), int(shift_hi), _ptr(bias), float(v_th), _sg(surrogate_kind),
-                             float(alpha), _ptr(H), _ptr(dH), _ptr(gx), _ptr(gw), _ptr(gb))
-    return {"H": H, "dH": dH, "grad_x": gx, "grad_w": gw, "grad_b": gb}
+                             int(shift_lo), int(shift_hi), _ptr(bias), float(v_th),
+                             None if vc is None else _ptr(vc), _sg(surrogate_kind), float(alpha), _ptr(H),
+                             _ptr(dH), _ptr(gx), _ptr(gw), _ptr(gb), _ptr(gv))
+    return {"H": H, "dH": dH, "grad_x": gx, "grad_w": gw, "grad_b": gb, "grad_vth": gv}
 
 
 def backward_q88(x, g, sign, shift, bias, k: int, d: int, v_th: int, surrogate_kind="sigmoid",
-                 alpha: float = 4.0, shift_lo: int = 0, shift_hi: int = 31):
-    """Returns dict with H, dH, grad_x (int32), grad_w, grad_b (int64)."""
+                 alpha: float = 4.0, shift_lo: int = 0, shift_hi: int = 31, v_th_c=None):
+    """Returns dict with H, dH, grad_x (int32), grad_w, grad_b, grad_vth
+    (int64).  v_th_c: optional per-channel Q8.8 thresholds [C] (int32)."""
     x = _c(x, np.int16)
     g = _c(g, np.int16)
     T, N, C, S = _geometry(x)
@@ -346,15 +367,18 @@ def backward_q88(x, g, sign, shift, bias, k: int, d: int, v_th: int, surrogate_k
     sign = _c(sign, np.int8).reshape(C, k)
     shift = _c(shift, np.int8).reshape(C, k)
     bias = _c(bias, np.int32).reshape(C)
+    vc = _thresholds(v_th_c, C, np.int32)
     H = np.empty(x.shape, np.int32)
     dH = np.empty(x.shape, np.int32)
     gx = np.empty(x.shape, np.int32)
     gw = np.empty((C, k), np.int64)
     gb = np.empty((C,), np.int64)
+    gv = np.empty((C,), np.int64)
     _load().orc_backward_q88(_ptr(x), _ptr(g), T, N, C, S, int(k), int(d), _ptr(sign), _ptr(shift),
-                             int(shift_lo), int(shift_hi), _ptr(bias), int(v_th), _sg(surrogate_kind),
-                             float(alpha), _ptr(H), _ptr(dH), _ptr(gx), _ptr(gw), _ptr(gb))
-    return {"H": H, "dH": dH, "grad_x": gx, "grad_w": gw, "grad_b": gb}
+                             int(shift_lo), int(shift_hi), _ptr(bias), int(v_th),
+                             None if vc is None else _ptr(vc), _sg(surrogate_kind), float(alpha), _ptr(H),
+                             _ptr(dH), _ptr(gx), _ptr(gw), _ptr(gb), _ptr(gv))
+    return {"H": H, "dH": dH, "grad_x": gx, "grad_w": gw, "grad_b": gb, "grad_vth": gv}
 
 
 # bf16 storage: inputs are bfloat16 bit patterns (uint16); they widen exactly

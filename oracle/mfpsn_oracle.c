@@ -211,15 +211,32 @@ static int64_t floor_div_pow2(int64_t v, int s)
     return q;
 }
 
+/* Threshold of channel c: the learnable channel-wise V_th[c] of
+ * Eq. mfdpsn_fire when a per-channel array is given, else the one scalar
+ * threshold shared by every channel (Sec. 3.1, Eq. fire). */
+static float thr_f32(const float* v_th_c, float v_th, int c)
+{
+    return v_th_c ? v_th_c[c] : v_th;
+}
+
+static int32_t thr_q88(const int32_t* v_th_c, int32_t v_th, int c)
+{
+    return v_th_c ? v_th_c[c] : v_th;
+}
+
 /* Float potentials and spikes.
  *   H[t,n,c,s] = (sum_{i=0..k-1, tau>=0} sign[c,i] * ldexp(x[tau,n,c,s], -shift[c,i])) + bias[c],
- *   tau = t - (k-1-i) d;   spike = (H >= v_th) ? 1 : 0   (Heaviside, Theta(0) = 1, Sec. 3.1).
+ *   tau = t - (k-1-i) d;   spike = (H >= V_th) ? 1 : 0   (Heaviside, Theta(0) = 1, Sec. 3.1),
+ * with V_th = v_th_c[c] when v_th_c is given (the channel-wise threshold of
+ * Eq. mfdpsn_fire), else the scalar v_th.  The threshold is compared with H
+ * as is: it is not folded into the bias, so the comparison sees the rounded
+ * sum acc + bias[c] itself.
  * Shifts are clamped into [lo, hi].  *tap_count receives the number of
  * (non-omitted) tap terms evaluated, i.e. the SHIFT count of Table
  * "params and shape" summed over all columns. */
 void orc_forward_f32(const float* x, int T, int N, int C, int S, int k, int d,
                      const int8_t* sign, const int8_t* shift, int lo, int hi,
-                     const float* bias, float v_th, float* H, uint8_t* spikes,
+                     const float* bias, float v_th, const float* v_th_c, float* H, uint8_t* spikes,
                      int64_t* tap_count)
 {
     int64_t taps = 0;
@@ -244,7 +261,7 @@ void orc_forward_f32(const float* x, int T, int N, int C, int S, int k, int d,
                     if (H)
                         H[t * M + col] = h;
                     if (spikes)
-                        spikes[t * M + col] = (h >= v_th) ? 1 : 0;
+                        spikes[t * M + col] = (h >= thr_f32(v_th_c, v_th, c)) ? 1 : 0;
                 }
     if (tap_count)
         *tap_count = taps;
@@ -253,10 +270,11 @@ void orc_forward_f32(const float* x, int T, int N, int C, int S, int k, int d,
 /* Q8.8 fixed-point potentials and spikes: every term is the arithmetic right
  * shift (floor) of the int16 input, negated for a negative tap; the int32
  * accumulator starts at the Q8.8 bias.  Shifts are clamped into [lo, hi]
- * (lo >= 0). */
+ * (lo >= 0).  The spike compares H with v_th_c[c] (Q8.8) when given, else
+ * with the scalar v_th. */
 void orc_forward_q88(const int16_t* x, int T, int N, int C, int S, int k, int d,
                      const int8_t* sign, const int8_t* shift, int lo, int hi,
-                     const int32_t* bias, int32_t v_th, int32_t* H, uint8_t* spikes,
+                     const int32_t* bias, int32_t v_th, const int32_t* v_th_c, int32_t* H, uint8_t* spikes,
                      int64_t* tap_count)
 {
     int64_t taps = 0;
@@ -278,7 +296,7 @@ void orc_forward_q88(const int16_t* x, int T, int N, int C, int S, int k, int d,
                     if (H)
                         H[t * M + col] = (int32_t)acc;
                     if (spikes)
-                        spikes[t * M + col] = (acc >= v_th) ? 1 : 0;
+                        spikes[t * M + col] = (acc >= thr_q88(v_th_c, v_th, c)) ? 1 : 0;
                 }
     if (tap_count)
         *tap_count = taps;
@@ -289,8 +307,9 @@ void orc_forward_q88(const int16_t* x, int T, int N, int C, int S, int k, int d,
 /* dilation d carried through).                                               */
 /* ------------------------------------------------------------------------ */
 
-/* Float path.  dH = grad_spikes * sigma'(H - v_th) (surrogate gradient of the
- * Heaviside); H is recomputed by orc_forward_f32 into the caller's H buffer.
+/* Float path.  dH = grad_spikes * sigma'(H - V_th) (surrogate gradient of the
+ * Heaviside), V_th the channel's threshold (v_th_c[c] when given, else v_th);
+ * H is recomputed by orc_forward_f32 into the caller's H buffer.
  *   grad_x[t] = sum_{i ascending, t+(k-1-i)d < T} sign*ldexp(dH[t+(k-1-i)d], -shift)
  *                (transposed dilated convolution; float, same rules as the charge)
  *   grad_w[c,i] = sum_{t,n,s, tau>=0} x[tau] * dH[t]     (double; products of two
@@ -298,17 +317,22 @@ void orc_forward_q88(const int16_t* x, int T, int N, int C, int S, int k, int d,
  *   grad_b[c]   = sum_{t,n,s} dH[t]                      (double)
  * grad_w is the gradient of the quantized weight, which the whole-quantizer
  * straight-through estimator passes unchanged to the latent weight
- * (Sec. 4.2).  grad_b is also minus the gradient of a per-channel threshold. */
+ * (Sec. 4.2).
+ *   grad_vth[c] = sum_{t,n,s} -dH[t]                     (double; optional)
+ * is the gradient of the channel's threshold: H - V_th[c] enters the
+ * surrogate with V_th[c] negated (Eq. mfdpsn_fire). */
 void orc_backward_f32(const float* x, const float* grad_spikes, int T, int N, int C, int S,
                       int k, int d, const int8_t* sign, const int8_t* shift, int lo, int hi,
-                      const float* bias, float v_th, int kind, float alpha,
-                      float* H, float* dH, float* grad_x, double* grad_w, double* grad_b)
+                      const float* bias, float v_th, const float* v_th_c, int kind, float alpha,
+                      float* H, float* dH, float* grad_x, double* grad_w, double* grad_b,
+                      double* grad_vth)
 {
     const int64_t M = (int64_t)N * C * S;
     const int64_t total = (int64_t)T * M;
-    orc_forward_f32(x, T, N, C, S, k, d, sign, shift, lo, hi, bias, v_th, H, NULL, NULL);
+    orc_forward_f32(x, T, N, C, S, k, d, sign, shift, lo, hi, bias, v_th, v_th_c, H, NULL, NULL);
     for (int64_t e = 0; e < total; ++e) {
-        const float u = H[e] - v_th;
+        const int c = (int)((e / S) % C);
+        const float u = H[e] - thr_f32(v_th_c, v_th, c);
         dH[e] = grad_spikes[e] * orc_surrogate(kind, alpha, u);
     }
     for (int t = 0; t < T; ++t)
@@ -343,12 +367,17 @@ void orc_backward_f32(const float* x, const float* grad_spikes, int T, int N, in
             }
             grad_w[c * k + i] = sum;
         }
-        double sb = 0.0;
+        double sb = 0.0, sv = 0.0;
         for (int t = 0; t < T; ++t)
             for (int n = 0; n < N; ++n)
-                for (int s = 0; s < S; ++s)
-                    sb += (double)dH[t * M + ((int64_t)n * C + c) * S + s];
+                for (int s = 0; s < S; ++s) {
+                    const double v = (double)dH[t * M + ((int64_t)n * C + c) * S + s];
+                    sb += v;
+                    sv += -v;
+                }
         grad_b[c] = sb;
+        if (grad_vth)
+            grad_vth[c] = sv;
     }
 }
 
@@ -362,20 +391,24 @@ int32_t orc_surrogate_q15(int kind, float alpha, int32_t u)
     return (int32_t)rintf(sg * 32768.0f);
 }
 
-/* Q8.8 path.  dH = floor(grad_spikes * L(H - v_th) / 2^15) with L the Q0.15
- * surrogate factor above (grad_spikes and dH are Q8.8); grad_x uses the same
+/* Q8.8 path.  dH = floor(grad_spikes * L(H - V_th) / 2^15) with L the Q0.15
+ * surrogate factor above (grad_spikes and dH are Q8.8) and V_th the channel's
+ * threshold (v_th_c[c] when given, else v_th); grad_x uses the same
  * floor-shift taps as the charge (int32, Q8.8); grad_w = sum x*dH exactly in
- * int64 (Q16.16); grad_b = sum dH in int64 (Q8.8). */
+ * int64 (Q16.16); grad_b = sum dH in int64 (Q8.8); grad_vth = sum -dH
+ * (optional). */
 void orc_backward_q88(const int16_t* x, const int16_t* grad_spikes, int T, int N, int C, int S,
                       int k, int d, const int8_t* sign, const int8_t* shift, int lo, int hi,
-                      const int32_t* bias, int32_t v_th, int kind, float alpha,
-                      int32_t* H, int32_t* dH, int32_t* grad_x, int64_t* grad_w, int64_t* grad_b)
+                      const int32_t* bias, int32_t v_th, const int32_t* v_th_c, int kind, float alpha,
+                      int32_t* H, int32_t* dH, int32_t* grad_x, int64_t* grad_w, int64_t* grad_b,
+                      int64_t* grad_vth)
 {
     const int64_t M = (int64_t)N * C * S;
     const int64_t total = (int64_t)T * M;
-    orc_forward_q88(x, T, N, C, S, k, d, sign, shift, lo, hi, bias, v_th, H, NULL, NULL);
+    orc_forward_q88(x, T, N, C, S, k, d, sign, shift, lo, hi, bias, v_th, v_th_c, H, NULL, NULL);
     for (int64_t e = 0; e < total; ++e) {
-        const int32_t L = orc_surrogate_q15(kind, alpha, H[e] - v_th);
+        const int c = (int)((e / S) % C);
+        const int32_t L = orc_surrogate_q15(kind, alpha, H[e] - thr_q88(v_th_c, v_th, c));
         dH[e] = (int32_t)floor_div_pow2((int64_t)grad_spikes[e] * (int64_t)L, 15);
     }
     for (int t = 0; t < T; ++t)
@@ -408,12 +441,17 @@ void orc_backward_q88(const int16_t* x, const int16_t* grad_spikes, int T, int N
             }
             grad_w[c * k + i] = sum;
         }
-        int64_t sb = 0;
+        int64_t sb = 0, sv = 0;
         for (int t = 0; t < T; ++t)
             for (int n = 0; n < N; ++n)
-                for (int s = 0; s < S; ++s)
-                    sb += dH[t * M + ((int64_t)n * C + c) * S + s];
+                for (int s = 0; s < S; ++s) {
+                    const int64_t v = dH[t * M + ((int64_t)n * C + c) * S + s];
+                    sb += v;
+                    sv -= v;
+                }
         grad_b[c] = sb;
+        if (grad_vth)
+            grad_vth[c] = sv;
     }
 }
 
@@ -514,7 +552,8 @@ static double bn_conv_value(const float* x, int64_t M, int64_t t, int64_t col, i
 
 /* Training-mode statistics and fusion.  Per channel c, over all (t, n, s):
  *   mean mu = sum Tv / n_c,  biased variance var = sum (Tv - mu)^2 / n_c,
- *   n_c = T*N*S (the mean and biased variance of the input sequence, App. C);
+ *   n_c = T*N*S (App. C normalizes with these per-channel batch statistics,
+ *   the variance divided by the count, not by the count minus one);
  *   s = gamma / sqrt(var + eps),  W_f = s * W,  b_f = beta - s * mu
  * (Eq. weight fuse, Eq. bias fuse).  The sums are sequential in (t, n, s)
  * order, in double; the variance takes the two-pass form.  W_f and b_f are

@@ -382,6 +382,118 @@ def test_backward_matches_finite_differences(orc, kind, alpha, d):
         assert abs(fd - out["grad_x"][idx]) <= 2e-4 * scale_x + 1e-6, (idx, fd, out["grad_x"][idx])
 
 
+# ---------------------------------------------------------------------------
+# learnable channel-wise threshold V_th[c] (Sec. 4.2, Eq. mfdpsn_fire)
+# ---------------------------------------------------------------------------
+def test_per_channel_threshold_equal_to_scalar_is_the_scalar_path(orc):
+    # one value in every channel: the same neuron as the shared threshold,
+    # bit for bit (float and Q8.8, forward and backward)
+    k, d = 4, 2
+    c = small_case(T=17, N=3, C=5, S=3, k=k, seed=41)
+    v = 0.37
+    vc = np.full(5, v, np.float32)
+    H0, S0 = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, v)
+    H1, S1 = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, -99.0, v_th_c=vc)
+    assert np.array_equal(H0.view(np.uint32), H1.view(np.uint32)) and np.array_equal(S0, S1)
+    b0 = orc.backward_f32(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, v)
+    b1 = orc.backward_f32(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, -99.0, v_th_c=vc)
+    for name in ("dH", "grad_x"):
+        assert np.array_equal(b0[name].view(np.uint32), b1[name].view(np.uint32)), name
+    for name in ("grad_w", "grad_b"):
+        assert np.array_equal(b0[name], b1[name]), name
+    q = workloads.make_small(17, 3, 5, (3,), k=k, dtype="q8_8", seed=42)
+    H0, S0 = orc.forward_q88(q["x"], q["sign"], q["shift"], q["bias"], k, d, 95, 0, 7)
+    H1, S1 = orc.forward_q88(q["x"], q["sign"], q["shift"], q["bias"], k, d, -7, 0, 7,
+                             v_th_c=np.full(5, 95, np.int32))
+    assert np.array_equal(H0, H1) and np.array_equal(S0, S1)
+    b0 = orc.backward_q88(q["x"], q["grad_spikes"], q["sign"], q["shift"], q["bias"], k, d, 95, "sigmoid", 4.0, 0, 7)
+    b1 = orc.backward_q88(q["x"], q["grad_spikes"], q["sign"], q["shift"], q["bias"], k, d, -7, "sigmoid", 4.0, 0, 7,
+                          v_th_c=np.full(5, 95, np.int32))
+    for name in ("dH", "grad_x", "grad_w", "grad_b"):
+        assert np.array_equal(b0[name], b1[name]), name
+
+
+@pytest.mark.parametrize("dtype", ["f32", "q8_8"])
+def test_per_channel_threshold_is_each_channel_with_its_own_scalar(orc, dtype):
+    # channels are independent neurons: channel c with thresholds V_th[c] is
+    # the shared-threshold neuron run on that channel alone with V_th[c]
+    k, d, C = 5, 3, 6
+    c = workloads.make_small(23, 2, C, (4,), k=k, dtype=dtype, seed=43)
+    rng = np.random.default_rng(44)
+    if dtype == "q8_8":
+        vc = rng.integers(-300, 300, C).astype(np.int32)
+        fw, bw, extra = orc.forward_q88, orc.backward_q88, (0, 7)
+        bargs = ("sigmoid", 4.0, 0, 7)
+    else:
+        vc = rng.normal(0.2, 0.5, C).astype(np.float32)
+        fw, bw, extra = orc.forward_f32, orc.backward_f32, ()
+        bargs = ()
+    H, S = fw(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0, *extra, v_th_c=vc)
+    b = bw(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, 0, *bargs, v_th_c=vc)
+    for ch in range(C):
+        one = {n: (np.ascontiguousarray(v[:, :, ch:ch + 1]) if n in ("x", "grad_spikes") else v[ch:ch + 1])
+               for n, v in c.items()}
+        v = vc[ch].item()
+        H1, S1 = fw(one["x"], one["sign"], one["shift"], one["bias"], k, d, v, *extra)
+        b1 = bw(one["x"], one["grad_spikes"], one["sign"], one["shift"], one["bias"], k, d, v, *bargs)
+        assert np.array_equal(H[:, :, ch:ch + 1], H1) and np.array_equal(S[:, :, ch:ch + 1], S1), ch
+        for name in ("dH", "grad_x"):
+            assert np.array_equal(b[name][:, :, ch:ch + 1], b1[name]), (ch, name)
+        for name in ("grad_w", "grad_b"):
+            assert np.array_equal(b[name][ch], b1[name][0]), (ch, name)
+        assert b["grad_vth"][ch] == -b1["grad_b"][0], ch
+
+
+def test_per_channel_threshold_fires_at_equality(orc):
+    # Theta(0) = 1: a channel whose threshold equals one of its potentials
+    # exactly fires there, and one just above it does not
+    k, d = 3, 1
+    c = small_case(T=9, N=1, C=2, S=1, k=k, seed=45)
+    H, _ = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0.0)
+    h = H[4, 0, 1]
+    vc = np.array([np.inf, h], np.float32)
+    _, S = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0.0, v_th_c=vc)
+    assert S[4, 0, 1] == 1 and not S[:, :, 0].any()
+    vc[1] = np.nextafter(h, np.float32(np.inf))
+    _, S = orc.forward_f32(c["x"], c["sign"], c["shift"], c["bias"], k, d, 0.0, v_th_c=vc)
+    assert S[4, 0, 1] == 0
+
+
+@pytest.mark.parametrize("kind,alpha", [("sigmoid", 4.0), ("atan", 2.0)])
+def test_per_channel_threshold_gradient_matches_finite_differences(orc, kind, alpha):
+    # L = sum g * step(H - V_th[c]) with a smooth step whose derivative is the
+    # surrogate: dL/dV_th[c] = -sum dH over the channel
+    k, d = 3, 2
+    c = small_case(T=12, N=2, C=3, S=2, k=k, seed=46)
+    x = c["x"].astype(np.float64)
+    g = c["grad_spikes"].astype(np.float64)
+    wq = tap_weights(c["sign"], c["shift"])
+    b = c["bias"].astype(np.float64)
+    vc = np.array([0.1, 0.45, -0.2], np.float32)
+    out = orc.backward_f32(c["x"], c["grad_spikes"], c["sign"], c["shift"], c["bias"], k, d, 0.0, kind, alpha,
+                           v_th_c=vc)
+
+    def L(v):
+        T = x.shape[0]
+        H = np.zeros(x.shape)
+        for i in range(k):
+            lag = (k - 1 - i) * d
+            if lag < T:
+                H[lag:] += wq[:, i].reshape(1, 1, -1, 1) * x[:T - lag]
+        H += b.reshape(1, 1, -1, 1)
+        return float(np.sum(g * primitive(kind, alpha, H - v.reshape(1, 1, -1, 1))))
+
+    h = 1e-6
+    scale = np.abs(out["grad_vth"]).max()
+    for ch in range(3):
+        vp, vm = vc.astype(np.float64), vc.astype(np.float64)
+        vp[ch] += h
+        vm[ch] -= h
+        fd = (L(vp) - L(vm)) / (2 * h)
+        assert abs(fd - out["grad_vth"][ch]) <= 2e-4 * scale + 1e-6, (ch, fd, out["grad_vth"][ch])
+        assert out["grad_vth"][ch] == -out["grad_b"][ch]
+
+
 def test_grad_w_exact_in_double_against_fraction(orc):
     # grad_w sums products of two floats, each exact in double; the double sum
     # of a few hundred terms is within n*eps of the exact rational sum.
