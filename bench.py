@@ -4,21 +4,33 @@
 A step is one training pass of a sawtooth stack of P neuron layers over one
 batch: the forward of every layer (dilations d = 1..P in layer order), then
 the backward of every layer in reverse order, as autograd would run them.
-Each layer reads its own x and grad_spikes tensors (the batch rolled along N),
-so no layer finds another layer's inputs in cache.  Inputs are resident in
-HBM when the timed region starts.
+Each layer reads its own x and grad_spikes tensors (the batch rolled along N).
+Inputs are resident in HBM, and the last-level cache is cold for every call:
+before each forward and backward a 1 GiB scratch buffer is read on the same
+stream, outside the HIP events that time the call.
+
+The headline workload (default) is the event-vision shape x[30,32,64,44,44],
+bf16 storage with f32 arithmetic, k = 8, sawtooth period 3 (the largest
+single-GPU workload); the same run measures the audio-spike, sequential-image
+and long fixed-point workloads under "configs".
 
 Prints ONE JSON line on stdout (everything else goes to stderr):
-  value      = P * T*N*C*S / step time   (elements/s, whole job)
-  roofline   = the backward kernel (the dominant one): algorithmic bytes per
-               launch (read x, read grad_spikes, write grad_x) / its average
-               duration from HIP events recorded on the launch stream inside
-               the timed region, against 8 TB/s.  The events are created
-               without the system-scope fence (hipEventDisableSystemFence), so
-               recording them does not write back and invalidate the caches
-               between launches.
+  value      = P * T*N*C*S / step time, the step time being the sum of the
+               per-call durations (HIP events on the launch stream, cold
+               cache) of the P forwards and P backwards (elements/s)
+  roofline   = the dominant kernel, mfpsn_backward (bwd_kernel + fin_kernel):
+               algorithmic bytes per launch (read x, read grad_spikes, write
+               grad_x) / its average event-timed duration, against 8 TB/s;
+               traffic = HBM bytes per launch from the committed rocprofv3
+               counter summary (null when it was taken on other kernel
+               sources); fwd_bwd = the same for forward + backward together
+  configs    = the other workloads, each with per-dilation call times and
+               algorithmic-bandwidth fractions
   cpu_baseline = the oracle (single-threaded C) timed on this host on a
-               channel slice of the same workload
+               channel slice of the headline workload
+The events are created without the system-scope fence
+(hipEventDisableSystemFence), so recording them does not write back and
+invalidate the caches between launches.
 """
 from __future__ import annotations
 
@@ -54,25 +66,41 @@ def alg_bytes(wl):
     return es + 1, es + es + gxs
 
 
+KERNEL_SOURCES = ("mfpsn_kernels.hip", "mfpsn_api.cpp", "mfpsn_internal.h", "mfpsn_surrogate.h")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters.json")
+SIMDS, CLOCK_HZ = 1024, 2.4e9   # MI355X: 256 CUs x 4 SIMDs, peak engine clock
+VALU_CYCLES = 2                 # cycles per plain wave64 VALU instruction on one SIMD
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("mfpsn_kernels.hip", "mfpsn_api.cpp", "mfpsn_internal.h"):
+    for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2501_14490_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(wl_name, mode):
-    """HBM bytes per backward launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "bwd_traffic.json")
+def committed_counters(wl_name, mode):
+    """The committed rocprofv3 counter summary of a workload (HBM bytes and
+    VALU instructions per launch), if it was taken on the current kernel
+    sources; else None."""
     try:
-        rec = json.load(open(path))
+        rec = json.load(open(COUNTERS_FILE))
     except (OSError, ValueError):
         return None
     ent = rec.get(f"{wl_name}|{mode}")
     if not ent or ent.get("kernel_source") != kernel_source_hash():
         return None
-    return ent.get("bytes_per_launch")
+    return ent
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 class HipEvents:
@@ -138,9 +166,9 @@ def cpu_baseline(wl, case, channels: int):
     dt = time.perf_counter() - t0
     elems = wl.T * wl.N * channels * wl.S * len(wl.dilations)
     return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
+            "cpu": cpu_model(), "nproc": os.cpu_count(),
             "sample": f"{channels} of {wl.C} channels ({elems} element-layers, every dilation), "
-                      f"fwd+bwd in {dt:.1f} s on {platform.processor() or platform.machine()} "
-                      f"(nproc {os.cpu_count()})"}
+                      f"fwd+bwd in {dt:.1f} s, single thread"}
 
 
 def memory_ceiling(torch, dev, wl):
@@ -311,14 +339,14 @@ def bn_step(torch, dev, wl, case, steps: int, warmup: int):
             mfpsn.mfpsn_quantize_weights(L["w_f"], 0, wl.s_max, L["sign"], L["shift"], stream)
             mark("quantize", li, 1)
             mark("forward", li, 0)
-            mfpsn.mfpsn_forward(L["desc"], L["x"], L["sign"], L["shift"], L["b_f"], L["spikes"], None, L["sg"],
+            mfpsn.mfpsn_forward(L["desc"], L["x"], L["sign"], L["shift"], L["b_f"], None, L["spikes"], None, L["sg"],
                                 stream)
             mark("forward", li, 1)
         for li in reversed(range(P)):
             L = layers[li]
             mark("backward", li, 0)
-            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], None, L["sg"], L["sign"], L["shift"], L["b_f"], L["gx"],
-                                 L["gwf"], L["gbf"], L["ws"], stream=stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], None, L["sg"], L["sign"], L["shift"], L["b_f"], None,
+                                 L["gx"], L["gwf"], L["gbf"], None, L["ws"], stream=stream)
             mark("backward", li, 1)
             mark("bn_backward", li, 0)
             mfpsn.mfpsn_bn_backward(L["desc"], L["x"], L["w"], L["aux"], eps, L["gwf"], L["gbf"], L["gx"], L["gw"],
@@ -393,14 +421,14 @@ def stack_step(torch, dev, wl, case, mode: str, steps: int, warmup: int):
 
     def step():
         for li, L in enumerate(layers):
-            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], L["sg"], stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, None, L["spikes"], L["h"], L["sg"], stream)
             if li + 1 < P:
                 mfpsn.mfpsn_spikes_to_input(L["spikes"], dt, layers[li + 1]["x"], stream)
         g = g_top
         for li in reversed(range(P)):
             L = layers[li]
-            mfpsn.mfpsn_backward(L["desc"], L["x"], g, L["h"], L["sg"], sign, shift, bias, L["gx"], L["gw"],
-                                 L["gb"], L["ws"], stream=stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], g, L["h"], L["sg"], sign, shift, bias, None, L["gx"], L["gw"],
+                                 L["gb"], None, L["ws"], stream=stream)
             g = L["gx"]
 
     for _ in range(warmup):
@@ -473,7 +501,7 @@ def time_last(torch, dev, wl, case, steps: int, warmup: int):
             if layout == "tl":
                 mfpsn.mfpsn_forward_time_last(desc, xs["tl"], sign, shift, bias, spk["tl"], None, stream)
             else:
-                mfpsn.mfpsn_forward(desc, xs["tf"], sign, shift, bias, spk["tf"], None, None, stream)
+                mfpsn.mfpsn_forward(desc, xs["tf"], sign, shift, bias, None, spk["tf"], None, None, stream)
             if ev is not None:
                 hev.record(ev[li][1], stream)
         if not with_bwd:
@@ -486,8 +514,8 @@ def time_last(torch, dev, wl, case, steps: int, warmup: int):
                 mfpsn.mfpsn_backward_time_last(desc, xs["tl"], gs["tl"], sign, shift, bias, gx["tl"], gw, gb, ws,
                                                stream)
             else:
-                mfpsn.mfpsn_backward(desc, xs["tf"], gs["tf"], None, None, sign, shift, bias, gx["tf"], gw, gb, ws,
-                                     stream=stream)
+                mfpsn.mfpsn_backward(desc, xs["tf"], gs["tf"], None, None, sign, shift, bias, None, gx["tf"], gw, gb, None,
+                                     ws, stream=stream)
             if ev is not None:
                 hev.record(ev[li][3], stream)
 
@@ -539,14 +567,264 @@ def time_last(torch, dev, wl, case, steps: int, warmup: int):
     print(json.dumps(rec), flush=True)
 
 
+class Flush:
+    """A 1 GiB device buffer read before every timed call (on the call's
+    stream, outside its events), so no call finds its inputs in the 256 MB
+    last-level (memory-side) cache or the L2s: every timed byte comes from
+    HBM.  The buffer is read, not written: a write would leave up to 256 MB
+    of dirty lines that the timed kernel would then have to write back,
+    charging it for the flush's own traffic; after a read every line is
+    clean."""
+
+    BYTES = 1 << 30
+
+    def __init__(self, torch, dev):
+        self.buf = torch.ones(self.BYTES // 4, dtype=torch.int32, device=dev)
+        self.acc = torch.zeros((), dtype=torch.int64, device=dev)
+
+    def __call__(self):
+        self.acc += self.buf.sum(dtype=torch.int64)
+
+
+def measure(torch, dev, wl, mode, steps: int, warmup: int, flush, hev):
+    """Time `steps` training steps of the workload's sawtooth stack (P layers,
+    forward of every layer then backward in reverse), every call cold.
+    Returns the per-call averages and the derived rates."""
+    from paper_2501_14490_amd import mfpsn, workloads
+
+    t0 = time.time()
+    case = workloads.make_inputs(wl)
+    log(f"{wl.name}: inputs drawn in {time.time() - t0:.1f}s")
+
+    def dev_tensor(a, storage):
+        if wl.dtype == "bf16" and storage:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x0 = dev_tensor(case["x"], True)
+    g0 = dev_tensor(case["grad_spikes"], True)
+    sign = dev_tensor(case["sign"], False)
+    shift = dev_tensor(case["shift"], False)
+    bias = dev_tensor(case["bias"], False)
+    del case
+    P = len(wl.dilations)
+    layers = []
+    for li, d in enumerate(wl.dilations):
+        x = torch.roll(x0, shifts=7 * li, dims=1).contiguous() if li else x0
+        g = torch.roll(g0, shifts=11 * li, dims=1).contiguous() if li else g0
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        ws = torch.empty(max(mfpsn.mfpsn_backward_workspace_size(desc), 8), dtype=torch.uint8, device=dev)
+        layers.append({
+            "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
+            "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
+            "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
+            "h": torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev) if mode == "h" else None,
+            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if mode == "sg" else None,
+            "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+            "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
+        })
+    del x0, g0
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        for li, L in enumerate(layers):
+            flush()
+            if events is not None:
+                hev.record(events[("fwd", li)][0], stream)
+            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, None, L["spikes"], L["h"], L["sg"], stream)
+            if events is not None:
+                hev.record(events[("fwd", li)][1], stream)
+        for li in reversed(range(P)):
+            L = layers[li]
+            flush()
+            if events is not None:
+                hev.record(events[("bwd", li)][0], stream)
+            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["h"], L["sg"], sign, shift, bias, None, L["gx"],
+                                 L["gw"], L["gb"], None, L["ws"], stream=stream)
+            if events is not None:
+                hev.record(events[("bwd", li)][1], stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = {(kind, li): [[hev.new(), hev.new()] for _ in range(steps)]
+          for kind in ("fwd", "bwd") for li in range(P)}
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for st in range(steps):
+        step({key: ev[key][st] for key in ev})
+        if st % 10 == 9:
+            log(f"  {wl.name}: step {st + 1}/{steps}")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    def avg_us(kind, li):
+        return 1e3 * float(np.mean([hev.elapsed_ms(a, b) for a, b in ev[(kind, li)]]))
+
+    fb, bb = alg_bytes(wl)
+    elems = wl.elements
+    per_d = {}
+    for li, L in enumerate(layers):
+        f_us, b_us = avg_us("fwd", li), avg_us("bwd", li)
+        per_d[f"d{L['d']}"] = {
+            "fwd_us": round(f_us, 2), "bwd_us": round(b_us, 2),
+            "fwd_frac": round(elems * fb / (f_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "bwd_frac": round(elems * bb / (b_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "fwd_bwd_frac": round(elems * (fb + bb) / ((f_us + b_us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    fwd_us = float(np.mean([v["fwd_us"] for v in per_d.values()]))
+    bwd_us = float(np.mean([v["bwd_us"] for v in per_d.values()]))
+    step_us = P * (fwd_us + bwd_us)
+    for L in layers:
+        L.clear()
+    torch.cuda.empty_cache()
+    return {
+        "wl": wl, "mode": mode, "P": P, "per_d": per_d, "fwd_us": fwd_us, "bwd_us": bwd_us,
+        "step_ms": step_us / 1e3, "wall_ms_per_step": wall * 1e3 / steps,
+        "value": P * elems / (step_us * 1e-6),
+        "fwd_bytes": elems * fb, "bwd_bytes": elems * bb,
+        "fwd_GBs": elems * fb / (fwd_us * 1e-6) / 1e9, "bwd_GBs": elems * bb / (bwd_us * 1e-6) / 1e9,
+        "fwd_bwd_GBs": elems * (fb + bb) / ((fwd_us + bwd_us) * 1e-6) / 1e9,
+    }
+
+
+def describe(wl, P):
+    storage = {"f32": "f32", "bf16": "bf16 storage with f32 arithmetic",
+               "q8_8": "int16 Q8.8 storage with int32 arithmetic"}[wl.dtype]
+    return (f"{wl.name}: x[{','.join(map(str, wl.shape))}] {storage}, k={wl.k}, sawtooth period {P} "
+            f"(one layer per d={wl.dilations}), forward of every layer then backward of every layer")
+
+
+BACKWARD_INPUT_TEXT = {"recompute": "H and sigma'(H - v_th) recomputed from x", "h": "H saved by the forward",
+                       "sg": "sigma'(H - v_th) saved by the forward"}
+
+
+def roofline(r, counters):
+    """Roofline of the dominant kernel (mfpsn_backward) and of forward +
+    backward together, from the event-timed averages; traffic and VALU
+    fraction from the committed counters (None when stale)."""
+    out = {
+        "kernel": "mfpsn_backward (bwd_kernel + fin_kernel)",
+        "bound": "hbm",
+        "achieved": r["bwd_GBs"],
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": r["bwd_GBs"] / HBM_PEAK_GBS,
+        "traffic": None,
+        "alg_bytes_per_launch": r["bwd_bytes"],
+        "avg_launch_us": r["bwd_us"],
+        "fwd_bwd": {"achieved": r["fwd_bwd_GBs"], "frac": r["fwd_bwd_GBs"] / HBM_PEAK_GBS,
+                    "alg_bytes": r["fwd_bytes"] + r["bwd_bytes"], "us": r["fwd_us"] + r["bwd_us"]},
+        "forward": {"achieved": r["fwd_GBs"], "frac": r["fwd_GBs"] / HBM_PEAK_GBS,
+                    "alg_bytes_per_launch": r["fwd_bytes"], "avg_launch_us": r["fwd_us"]},
+    }
+    if counters is not None:
+        out["traffic"] = counters["bwd_bytes_per_launch"]
+        out["traffic_note"] = ("HBM bytes per mfpsn_backward launch: 2*FETCH_SIZE + WRITE_SIZE (KiB -> bytes; "
+                               "FETCH_SIZE reads half of a 1 GiB copy's bytes on this part), averaged over "
+                               f"{counters.get('dispatches_averaged')} dispatches; forward "
+                               f"{counters['fwd_bytes_per_launch']} bytes per launch")
+        if "bwd_valu_insts" in counters:
+            ws = r["wl"].elements / 64
+            out["valu_frac"] = counters["bwd_valu_insts"] * VALU_CYCLES / (SIMDS * CLOCK_HZ * r["bwd_us"] * 1e-6)
+            out["valu_insts_per_wave_step"] = counters["bwd_valu_insts"] / ws
+            out["fwd_valu_frac"] = counters["fwd_valu_insts"] * VALU_CYCLES / (SIMDS * CLOCK_HZ * r["fwd_us"] * 1e-6)
+            out["fwd_valu_insts_per_wave_step"] = counters["fwd_valu_insts"] / ws
+            out["valu_note"] = (f"SQ_INSTS_VALU (wave64 instructions) x {VALU_CYCLES} cycles / ({SIMDS} SIMDs x "
+                                f"{CLOCK_HZ / 1e9:.1f} GHz x event-timed duration): the share of the chip's issue "
+                                "capacity for plain VALU instructions")
+    return out
+
+
+def summarize_counters(out_dir):
+    """Write profiles/counters.json from rocprofv3 --pmc CSV outputs under
+    out_dir: <workload>_<mode>_fetch, _write and _valu runs of
+    `bench.py --workload W --only --steps 2 --warmup 1 --no-cpu-baseline`,
+    plus calibrate_fetch / calibrate_write runs of `bench.py
+    --calibrate-copy` (the byte-counter scale of a plain 1 GiB copy)."""
+    import csv
+    import glob
+
+    def rows(tag):
+        files = glob.glob(os.path.join(out_dir, tag, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {os.path.join(out_dir, tag)}")
+        out = []
+        for f in files:
+            out += list(csv.DictReader(open(f)))
+        return out
+
+    def per_dispatch(tag, counter, name_part):
+        vals = {}
+        for row in rows(tag):
+            if name_part in row["Kernel_Name"] and row["Counter_Name"] == counter:
+                key = row.get("Dispatch_Id") or row.get("Correlation_Id")
+                vals[key] = vals.get(key, 0.0) + float(row["Counter_Value"])
+        if not vals:
+            raise SystemExit(f"{tag}: no {counter} rows for kernels named like {name_part}")
+        return float(np.mean(list(vals.values()))), len(vals)
+
+    def largest(tag, counter):
+        # the 1 GiB copy is the dispatch with the largest count in its run
+        vals = {}
+        for row in rows(tag):
+            if row["Counter_Name"] == counter:
+                key = row.get("Dispatch_Id") or row.get("Correlation_Id")
+                vals[key] = vals.get(key, 0.0) + float(row["Counter_Value"])
+        return max(vals.values())
+
+    copy = 1 << 30
+    fetch_cal = largest("calibrate_fetch", "FETCH_SIZE")
+    write_cal = largest("calibrate_write", "WRITE_SIZE")
+    fscale, wscale = copy / (fetch_cal * 1024), copy / (write_cal * 1024)
+    rec = {"_calibration": {"copy_bytes": copy, "FETCH_SIZE_kib": fetch_cal, "WRITE_SIZE_kib": write_cal,
+                            "fetch_scale": fscale, "write_scale": wscale,
+                            "command": "rocprofv3 --pmc FETCH_SIZE -f csv -d DIR/calibrate_fetch -o p -- python3 "
+                                       "bench.py --calibrate-copy (then WRITE_SIZE into DIR/calibrate_write)"}}
+    from paper_2501_14490_amd import workloads
+    for wid, wl in workloads.WORKLOADS.items():
+        mode = AUTO_BACKWARD_INPUT[wid]
+        tag = f"{wl.name}_{mode}"
+        if not os.path.isdir(os.path.join(out_dir, tag + "_fetch")):
+            continue
+        ent = {"kernel_source": kernel_source_hash(),
+               "command": f"rocprofv3 --pmc FETCH_SIZE -f csv -d DIR/{tag}_fetch -o p -- python3 "
+                          f"bench.py --workload {wid} --only --steps 2 --warmup 1 --no-cpu-baseline "
+                          f"(then WRITE_SIZE into {tag}_write, SQ_INSTS_VALU into {tag}_valu)"}
+        fb = {}
+        for kern in ("bwd_kernel", "fin_kernel", "fwd_kernel"):
+            f, n = per_dispatch(tag + "_fetch", "FETCH_SIZE", kern)
+            w, _ = per_dispatch(tag + "_write", "WRITE_SIZE", kern)
+            fb[kern] = f * 1024 * fscale + w * 1024 * wscale
+            ent[f"{kern}_fetch_kib"] = f
+            ent[f"{kern}_write_kib"] = w
+            ent["dispatches_averaged"] = n
+        ent["bwd_bytes_per_launch"] = fb["bwd_kernel"] + fb["fin_kernel"]
+        ent["fwd_bytes_per_launch"] = fb["fwd_kernel"]
+        fbytes, bbytes = alg_bytes(wl)
+        ent["bwd_alg_bytes_per_launch"] = wl.elements * bbytes
+        ent["fwd_alg_bytes_per_launch"] = wl.elements * fbytes
+        if os.path.isdir(os.path.join(out_dir, tag + "_valu")):
+            ent["bwd_valu_insts"], _ = per_dispatch(tag + "_valu", "SQ_INSTS_VALU", "bwd_kernel")
+            ent["fwd_valu_insts"], _ = per_dispatch(tag + "_valu", "SQ_INSTS_VALU", "fwd_kernel")
+        rec[f"{wl.name}|{mode}"] = ent
+    with open(COUNTERS_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps({k: v.get("bwd_bytes_per_launch") for k, v in rec.items() if "|" in k}))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="1..5 (default 2: audio-spike-shaped)")
+    ap.add_argument("--workload", type=int, default=4,
+                    help="headline workload 1..5 (default 4: event-vision-shaped, the largest)")
+    ap.add_argument("--only", action="store_true", help="measure the headline workload only")
     ap.add_argument("--cpu-channels", type=int, default=None, help="channels in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="do not read the 1 GiB scratch buffer before each call (warm last-level cache)")
     ap.add_argument("--backward-input", choices=("auto",) + BACKWARD_INPUTS, default="auto",
                     help="what the forward saves for the backward: nothing (recompute: the backward "
                          "recomputes H and the surrogate factor from x), the potentials H (h), or the "
@@ -554,6 +832,8 @@ def main():
                          "workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="only write profiles/counters.json from the rocprofv3 --pmc outputs under DIR")
     ap.add_argument("--bn-step", action="store_true",
                     help="only time the batch-normalized-threshold training step of App. C (float workloads)")
     ap.add_argument("--time-last", action="store_true",
@@ -573,10 +853,13 @@ def main():
               f"shards over the batch with one all-reduce of grad_w/grad_b per layer, not built here)",
               file=sys.stderr)
         sys.exit(2)
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
 
     import torch
 
-    from paper_2501_14490_amd import mfpsn, workloads
+    from paper_2501_14490_amd import mfpsn, workloads  # noqa: F401  (loads libmfpsn.so or raises)
 
     if not torch.cuda.is_available():
         log("no GPU visible")
@@ -598,144 +881,77 @@ def main():
         memory_ceiling(torch, dev, wl)
         return
     mode = args.backward_input if args.backward_input != "auto" else AUTO_BACKWARD_INPUT[wl.wid]
-    t0 = time.time()
-    case = workloads.make_inputs(wl)
-    log(f"inputs drawn in {time.time() - t0:.1f}s")
-    if args.stream_inference:
-        stream_inference(torch, dev, wl, case, args.steps, args.warmup)
-        return
-    if args.bn_step:
-        bn_step(torch, dev, wl, case, args.steps, args.warmup)
-        return
-    if args.stack:
-        stack_step(torch, dev, wl, case, mode, args.steps, args.warmup)
-        return
-    if args.time_last:
-        time_last(torch, dev, wl, case, args.steps, args.warmup)
+    if args.stream_inference or args.bn_step or args.stack or args.time_last:
+        case = workloads.make_inputs(wl)
+        if args.stream_inference:
+            stream_inference(torch, dev, wl, case, args.steps, args.warmup)
+        elif args.bn_step:
+            bn_step(torch, dev, wl, case, args.steps, args.warmup)
+        elif args.stack:
+            stack_step(torch, dev, wl, case, mode, args.steps, args.warmup)
+        else:
+            time_last(torch, dev, wl, case, args.steps, args.warmup)
         return
 
-    def dev_tensor(a, storage):
-        if wl.dtype == "bf16" and storage:
-            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
-        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-
-    x0 = dev_tensor(case["x"], True)
-    g0 = dev_tensor(case["grad_spikes"], True)
-    sign = dev_tensor(case["sign"], False)
-    shift = dev_tensor(case["shift"], False)
-    bias = dev_tensor(case["bias"], False)
-    P = len(wl.dilations)
-    layers = []
-    for li, d in enumerate(wl.dilations):
-        x = torch.roll(x0, shifts=7 * li, dims=1).contiguous() if li else x0
-        g = torch.roll(g0, shifts=11 * li, dims=1).contiguous() if li else g0
-        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
-                               wl.s_max)
-        ws = torch.empty(max(mfpsn.mfpsn_backward_workspace_size(desc), 8), dtype=torch.uint8, device=dev)
-        layers.append({
-            "d": d, "desc": desc, "x": x, "g": g, "ws": ws,
-            "spikes": torch.empty(wl.shape, dtype=torch.uint8, device=dev),
-            "gx": torch.empty(wl.shape, dtype=mfpsn.GRAD_X[desc.dtype], device=dev),
-            "h": torch.empty(wl.shape, dtype=mfpsn.H_OUT[desc.dtype], device=dev) if mode == "h" else None,
-            "sg": torch.empty(wl.shape, dtype=mfpsn.SG_OUT[desc.dtype], device=dev) if mode == "sg" else None,
-            "gw": torch.empty((wl.C, wl.k), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
-            "gb": torch.empty((wl.C,), dtype=mfpsn.GRAD_WB[desc.dtype], device=dev),
-        })
-    del x0, g0
-    stream = torch.cuda.current_stream()
     hev = HipEvents()
-
-    def step(events=None):
-        for li, L in enumerate(layers):
-            if events is not None:
-                hev.record(events[("fwd", li)][0], stream)
-            mfpsn.mfpsn_forward(L["desc"], L["x"], sign, shift, bias, L["spikes"], L["h"], L["sg"], stream)
-            if events is not None:
-                hev.record(events[("fwd", li)][1], stream)
-        for li in reversed(range(P)):
-            L = layers[li]
-            if events is not None:
-                hev.record(events[("bwd", li)][0], stream)
-            mfpsn.mfpsn_backward(L["desc"], L["x"], L["g"], L["h"], L["sg"], sign, shift, bias, L["gx"],
-                                 L["gw"], L["gb"], L["ws"], stream=stream)
-            if events is not None:
-                hev.record(events[("bwd", li)][1], stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = {(kind, li): [[hev.new(), hev.new()] for _ in range(args.steps)]
-          for kind in ("fwd", "bwd") for li in range(P)}
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for s in range(args.steps):
-        step({key: ev[key][s] for key in ev})
-        if s % 5 == 4:
-            log(f"  step {s + 1}/{args.steps}")
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    ms_per_step = elapsed * 1e3 / args.steps
-
-    def avg_ms(kind, li):
-        return float(np.mean([hev.elapsed_ms(a, b) for a, b in ev[(kind, li)]]))
-
-    per = {f"{kind}_d{layers[li]['d']}_us": round(avg_ms(kind, li) * 1e3, 2)
-           for kind in ("fwd", "bwd") for li in range(P)}
-    bwd_ms = float(np.mean([avg_ms("bwd", li) for li in range(P)]))
-    fwd_ms = float(np.mean([avg_ms("fwd", li) for li in range(P)]))
-    fb, bb = alg_bytes(wl)
-    elems = wl.elements
-    bwd_bytes = elems * bb
-    achieved = bwd_bytes / (bwd_ms * 1e-3) / 1e9
-    fwd_achieved = elems * fb / (fwd_ms * 1e-3) / 1e9
-    value = P * elems / (elapsed / args.steps)
-    log(f"step {ms_per_step:.3f} ms   fwd {fwd_ms * 1e3:.1f} us ({fwd_achieved:.0f} GB/s alg)   "
-        f"bwd {bwd_ms * 1e3:.1f} us ({achieved:.0f} GB/s alg)   {value / 1e9:.2f} G elements/s")
-    log("per call (us):", per)
-
+    flush = (lambda: None) if args.no_flush else Flush(torch, dev)
+    head = measure(torch, dev, wl, mode, args.steps, args.warmup, flush, hev)
+    log(f"{wl.name}: step {head['step_ms']:.3f} ms (cold calls; wall {head['wall_ms_per_step']:.3f} ms with the "
+        f"flushes)  fwd {head['fwd_us']:.1f} us  bwd {head['bwd_us']:.1f} us  "
+        f"{head['value'] / 1e9:.2f} G elements/s  fwd+bwd {head['fwd_bwd_GBs']:.0f} GB/s alg")
+    log("per dilation:", head["per_d"])
+    others = {}
+    if not args.only:
+        for wid in (2, 3, 4, 5):
+            if wid == wl.wid:
+                continue
+            owl = workloads.WORKLOADS[wid]
+            omode = AUTO_BACKWARD_INPUT[wid]
+            r = measure(torch, dev, owl, omode, args.steps, args.warmup, flush, hev)
+            log(f"{owl.name}: {r['value'] / 1e9:.2f} G elements/s  fwd {r['fwd_us']:.1f} us  bwd "
+                f"{r['bwd_us']:.1f} us  fwd+bwd {r['fwd_bwd_GBs']:.0f} GB/s alg  {r['per_d']}")
+            c = committed_counters(owl.name, omode)
+            others[owl.name] = {
+                "workload": describe(owl, r["P"]), "value": r["value"], "unit": "elements/s",
+                "ms_per_step": r["step_ms"], "backward_input": BACKWARD_INPUT_TEXT[omode],
+                "fwd_us": r["fwd_us"], "bwd_us": r["bwd_us"],
+                "fwd_frac": r["fwd_GBs"] / HBM_PEAK_GBS, "bwd_frac": r["bwd_GBs"] / HBM_PEAK_GBS,
+                "fwd_bwd_frac": r["fwd_bwd_GBs"] / HBM_PEAK_GBS, "per_d": r["per_d"],
+                "traffic": None if c is None else c["bwd_bytes_per_launch"],
+            }
+    P = head["P"]
     result = {
         "metric": "neuron fwd+bwd elements/s (T*N*C*S) and achieved HBM GB/s vs MI355X peak",
-        "value": value,
+        "value": head["value"],
         "unit": "elements/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": head["step_ms"],
+        "wall_ms_per_step_with_flushes": head["wall_ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": {"f32": "f32", "bf16": "bf16", "q8_8": "int16 Q8.8 / int32"}[wl.dtype],
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}: x[{','.join(map(str, wl.shape))}] {wl.dtype}, k={wl.k}, "
-                        f"sawtooth period {P} (one layer per d={wl.dilations}), forward of every layer "
-                        f"then backward of every layer",
-            "elements_per_layer": elems,
+            "workload": describe(wl, P),
+            "elements_per_layer": wl.elements,
             "layers_per_step": P,
             "surrogate": f"{wl.surrogate} alpha={wl.alpha}",
-            "backward_input": {"recompute": "H and sigma'(H - v_th) recomputed from x",
-                               "h": "H saved by the forward",
-                               "sg": "sigma'(H - v_th) saved by the forward"}[mode],
+            "backward_input": BACKWARD_INPUT_TEXT[mode],
             "v_th": wl.v_th,
+            "cache": "cold: 1 GiB read before every call, outside its events" if not args.no_flush
+                     else "warm (no flush)",
         },
-        "roofline": {
-            "kernel": "mfpsn_backward (bwd_kernel + finalize)",
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": measured_traffic(wl.name, mode),
-            "alg_bytes_per_launch": bwd_bytes,
-            "avg_launch_us": bwd_ms * 1e3,
-        },
-        "forward": {"alg_bytes_per_launch": elems * fb, "avg_launch_us": fwd_ms * 1e3,
-                    "achieved_GBs": fwd_achieved, "frac": fwd_achieved / HBM_PEAK_GBS},
-        "per_call_us": per,
+        "roofline": roofline(head, committed_counters(wl.name, mode)),
+        "per_d": head["per_d"],
+        "configs": others,
     }
     if not args.no_cpu_baseline:
-        channels = args.cpu_channels or {1: 128, 2: 320, 3: 64, 4: 8, 5: 48}[wl.wid]
+        channels = args.cpu_channels or {1: 128, 2: 320, 3: 64, 4: 48, 5: 48}[wl.wid]
         log(f"oracle baseline on {channels} channels ...")
+        case = workloads.make_inputs(wl)
         result["cpu_baseline"] = cpu_baseline(wl, case, channels)
         log(f"oracle: {result['cpu_baseline']['value'] / 1e6:.2f} M elements/s")
     print(json.dumps(result), flush=True)

@@ -9,14 +9,18 @@
  *
  *   H[t,n,c,s] = sum_{i=0..k-1, t-(k-1-i)d >= 0} sign[c,i] * 2^-shift[c,i] * x[t-(k-1-i)d, n,c,s]
  *                + bias[c]
- *   spikes     = (H >= v_th)                       (Heaviside, Theta(0) = 1)
- *   dH         = grad_spikes * sigma'(H - v_th)    (surrogate gradient)
+ *   spikes     = (H >= V_th[c])                    (Heaviside, Theta(0) = 1)
+ *   dH         = grad_spikes * sigma'(H - V_th[c]) (surrogate gradient)
  *   grad_x[t]  = sum_{i, t+(k-1-i)d < T} sign[c,i] * 2^-shift[c,i] * dH[t+(k-1-i)d]
  *   grad_w[c,i]= sum_{t,n,s} x[t-(k-1-i)d] * dH[t]  (gradient of the quantized
  *                weight, passed unchanged to the latent weight by the
  *                whole-quantizer straight-through estimator)
- *   grad_b[c]  = sum_{t,n,s} dH[t]                  (minus the gradient of a
- *                per-channel threshold)
+ *   grad_b[c]  = sum_{t,n,s} dH[t]
+ *   grad_vth[c]= -grad_b[c]                        (gradient of the threshold)
+ * V_th[c] is the learnable channel-wise threshold of Eq. mfdpsn_fire when a
+ * per-channel array is passed, else the one scalar threshold of the
+ * descriptor (Sec. 3.1, Eq. fire); the comparison and the surrogate see the
+ * rounded potential H itself (the threshold is not folded into the bias).
  *
  * Every product by a tap is a power-of-two scaling: an exponent move (ldexp)
  * for float data, an arithmetic right shift (floor) for Q8.8 integers
@@ -57,7 +61,7 @@
 extern "C" {
 #endif
 
-#define MFPSN_ABI_VERSION 9
+#define MFPSN_ABI_VERSION 10
 #define MFPSN_MAX_K 32
 
 typedef enum mfpsn_status {
@@ -98,8 +102,9 @@ typedef struct mfpsn_desc {
     int32_t dtype;       /* mfpsn_dtype                                        */
     int32_t surrogate;   /* mfpsn_surrogate                                    */
     float alpha;         /* surrogate parameter, 0 <= alpha <= 1024            */
-    float v_th;          /* threshold, float paths                             */
-    int32_t v_th_q;      /* threshold, Q8.8 path (256 == 1.0)                  */
+    float v_th;          /* threshold, float paths (finite); used when no      */
+                         /* per-channel thresholds are passed                  */
+    int32_t v_th_q;      /* threshold, Q8.8 path (256 == 1.0), |v_th_q| <= 2^30 */
     int32_t shift_lo;    /* shifts are clamped into [shift_lo, shift_hi];      */
     int32_t shift_hi;    /* float: -126..126, Q8.8: 0..31                      */
 } mfpsn_desc;
@@ -107,19 +112,25 @@ typedef struct mfpsn_desc {
 /* Forward: charge (Eq. mfdpsn_charge) and fire (Eq. mfdpsn_fire).
  *   x      : [T][N][C][S] storage type of desc->dtype
  *   sign, shift : int8 [C][k];  bias : float[C] or int32[C] (Q8.8)
- *   spikes : uint8 [T][N][C][S], 1 where H >= v_th else 0 (NaN -> 0)
+ *   v_th_c : optional (may be NULL) per-channel thresholds V_th[c], the
+ *            learnable channel-wise threshold of Eq. mfdpsn_fire: float[C]
+ *            (F32, BF16) or int32[C] Q8.8 (|V_th[c]| <= 2^30); NULL means
+ *            desc->v_th (desc->v_th_q) for every channel.  Device values are
+ *            not validated: a NaN threshold never fires.
+ *   spikes : uint8 [T][N][C][S], 1 where H >= V_th[c] else 0 (NaN -> 0)
  *   h_out  : optional (may be NULL) membrane potential H, float (F32, BF16)
  *            or int32 (Q8.8), [T][N][C][S].  Passed to mfpsn_backward, it
  *            spares the backward the charge.
  *   sg_out : optional (may be NULL) surrogate factor of H, [T][N][C][S]:
- *            float sigma'(H - v_th) (F32, BF16), or int32
- *            L = round_half_even(2^15 * sigma'((H - v_th_q) / 256)) (Q8.8).
+ *            float sigma'(H - V_th[c]) (F32, BF16), or int32
+ *            L = round_half_even(2^15 * sigma'((H - V_th[c]) / 256)) (Q8.8).
  *            Passed to mfpsn_backward, it spares the backward the charge and
  *            the surrogate (dH = grad_spikes * factor there).
- * Alignment: x 4 bytes (F32) / 2 bytes (BF16, Q8.8); h_out, sg_out, bias
- * 4 bytes. */
+ * Alignment: x 4 bytes (F32) / 2 bytes (BF16, Q8.8); h_out, sg_out, bias,
+ * v_th_c 4 bytes. */
 int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
-                  const void* bias, uint8_t* spikes, void* h_out, void* sg_out, void* stream);
+                  const void* bias, const void* v_th_c, uint8_t* spikes, void* h_out, void* sg_out,
+                  void* stream);
 
 /* Bytes of device workspace mfpsn_backward needs for this problem (per-block
  * partial sums of grad_w and grad_b: double, or int64 for Q8.8).  Returns a
@@ -133,26 +144,28 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes);
  *   h           : optional (may be NULL) potentials H of this x, taps and
  *                 bias, as written by mfpsn_forward's h_out
  *   sg          : optional (may be NULL) surrogate factor of this x, taps,
- *                 bias and surrogate, as written by mfpsn_forward's sg_out
+ *                 bias, thresholds and surrogate, as written by
+ *                 mfpsn_forward's sg_out
+ *   v_th_c      : optional per-channel thresholds, as for mfpsn_forward (the
+ *                 same array the forward used)
  *   The backward uses sg if given, else h if given, else recomputes H and
  *   the factor from x.  All three give identical results; a saved tensor
  *   trades 4 bytes per element of memory traffic for the recomputation.
  *   grad_x      : [T][N][C][S] float (F32), bfloat16 (BF16), int32 (Q8.8)
  *   grad_w      : float [C][k] or int64 [C][k] (Q8.8, Q16.16)
  *   grad_b      : float [C]    or int64 [C]    (Q8.8)
+ *   grad_vth    : optional (may be NULL) gradient of the thresholds,
+ *                 -grad_b: float [C] or int64 [C] (Q8.8)
  *   workspace   : >= mfpsn_backward_workspace_size bytes, 8-byte aligned;
  *                 contents on entry are ignored (every word used is written)
- * grad_x follows the sum of the definition exactly, except that a float dH
- * below 2^(shift_hi - 126) in magnitude (a surrogate factor that underflowed)
- * contributes nothing to it: each of its terms is smaller than
- * 2^(shift_hi - shift_lo - 126).
+ * grad_x follows the sum of the definition exactly, every term included.
  * grad_w and grad_b do not depend on the order in which the GPU runs its
  * blocks: partial sums are reduced in a fixed order, so repeated calls give
  * identical bits.  The Q8.8 path is exact (int64 sums); the call fails with
  * MFPSN_ERR_SHAPE when T*N*S*32768*max|dH| could reach 2^62. */
 int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
                    const void* sg, const int8_t* sign, const int8_t* shift, const void* bias,
-                   void* grad_x, void* grad_w, void* grad_b,
+                   const void* v_th_c, void* grad_x, void* grad_w, void* grad_b, void* grad_vth,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* Power-of-two quantizer Q(W) = sign(W) * 2^round(log2|W|) (Sec. 4.2,
@@ -179,7 +192,10 @@ int mfpsn_quantize_weights(const float* w, int64_t count, int32_t shift_lo, int3
  * w_f = s * w (float [C][k]), b_f = beta - s * mu (float [C]),
  * aux = [mu, var, s, 1/sqrt(var + eps)] (double [C][4], for the backward),
  * stats = [sum Tv, sum Tv^2] (double [C][2], optional).  Sums are added in a
- * fixed order (bitwise reproducible); var = sum Tv^2/n - mu^2, at least 0.
+ * fixed order (bitwise reproducible), as sums of the deviations e = Tv - p
+ * from a pivot p (Tv of the channel's last step at its first column):
+ * mu = p + sum e/n, var = sum e^2/n - (sum e/n)^2, at least 0, which keeps
+ * var accurate when |mu| is much larger than the standard deviation.
  * mfpsn_bn_backward: from grad_wf (float [C][k]) and grad_bf (float [C])
  * of the fused weight and bias, adds the statistics path to grad_x (float
  * [T][N][C][S], in: the quantized path's input gradient, out: the total)

@@ -44,8 +44,10 @@ DTYPES = [0, 1, 2]  # f32, bf16, q8.8
 def _units():
     """(object, compile command, sources it depends on) of every translation unit."""
     src = os.path.join(CSRC, "mfpsn_kernels.hip")
-    headers = [os.path.join(CSRC, "mfpsn_internal.h"), os.path.join(CSRC, "mfpsn_surrogate.h"),
-               os.path.join(INCLUDE, "mfpsn.h")]
+    # the headers the kernel source includes (not the public header: the
+    # kernels see only the internal interface)
+    headers = [os.path.join(CSRC, "mfpsn_internal.h"), os.path.join(CSRC, "mfpsn_surrogate.h")]
+    api_headers = [*headers, os.path.join(INCLUDE, "mfpsn.h")]
     units = []
     for dt in DTYPES:
         for lo, hi in K_RANGES:
@@ -56,7 +58,7 @@ def _units():
     bn_src = os.path.join(CSRC, "mfpsn_bn.hip")
     obj = os.path.join(BUILD, "bn.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", bn_src, "-o", obj],
-                  [bn_src, os.path.join(CSRC, "mfpsn_bn.h")]))
+                  [bn_src, os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(INCLUDE, "mfpsn.h")]))
     qg_src = os.path.join(CSRC, "mfpsn_qgrad.hip")
     obj = os.path.join(BUILD, "qgrad.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", qg_src, "-o", obj],
@@ -76,7 +78,7 @@ def _units():
     stream_src = os.path.join(CSRC, "mfpsn_stream.hip")
     obj = os.path.join(BUILD, "stream.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", stream_src, "-o", obj],
-                  [stream_src, os.path.join(CSRC, "mfpsn_stream.h"), *headers]))
+                  [stream_src, os.path.join(CSRC, "mfpsn_stream.h"), *api_headers]))
     obj = os.path.join(BUILD, "kernels_misc.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
                         "-c", src, "-o", obj], [src, *headers]))
@@ -86,7 +88,7 @@ def _units():
         units.append((obj, ["g++", *HOST_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", cpp, "-o", obj],
                       [cpp, os.path.join(CSRC, "mfpsn_stream.h"), os.path.join(CSRC, "mfpsn_qgrad.h"),
                        os.path.join(CSRC, "mfpsn_bn.h"), os.path.join(CSRC, "mfpsn_validate.h"),
-                       os.path.join(CSRC, "mfpsn_chain.h"), os.path.join(CSRC, "mfpsn_tl.h"), *headers]))
+                       os.path.join(CSRC, "mfpsn_chain.h"), os.path.join(CSRC, "mfpsn_tl.h"), *api_headers]))
     return units
 
 

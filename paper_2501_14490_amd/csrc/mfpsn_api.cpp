@@ -4,7 +4,6 @@
 #include "mfpsn.h"
 
 #include <math.h>
-#include <stdlib.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -49,9 +48,12 @@ int validate(const mfpsn_desc* d)
         return MFPSN_ERR_PARAM;
     if ((int64_t)(d->k - 1) * d->dilation > (int64_t)1 << 30)
         return MFPSN_ERR_PARAM;
-    const int64_t M = (int64_t)d->N * d->C * d->S;
-    if (M * 4 >= ((int64_t)1 << 31))  // one time step of any tensor fits a 31-bit offset
+    // one time step of any tensor fits a 31-bit offset (the product of three
+    // int32 sizes is formed in 128 bits, so it cannot overflow)
+    const __int128 cols = (__int128)d->N * d->C * d->S;
+    if (cols * 4 >= ((__int128)1 << 31))
         return MFPSN_ERR_SHAPE;
+    const int64_t M = (int64_t)cols;
     if (d->C > 65535 && !(d->S == 1))  // plane mode puts one channel per grid row
         return MFPSN_ERR_SHAPE;
     if (M > 0 && d->T > 0 && max_chunk(d) == 0)  // k rows of one class do not fit 31-bit offsets
@@ -60,6 +62,8 @@ int validate(const mfpsn_desc* d)
         return MFPSN_ERR_PARAM;
     if (d->dtype == MFPSN_Q8_8) {
         if (d->shift_lo < 0 || d->shift_hi > 31)
+            return MFPSN_ERR_PARAM;
+        if (d->v_th_q < -(1 << 30) || d->v_th_q > (1 << 30))  // H - v_th_q fits int32
             return MFPSN_ERR_PARAM;
     } else {
         if (d->shift_lo < -126 || d->shift_hi > 126)
@@ -79,45 +83,19 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Launch geometry.  Lanes walk residue classes; when the columns alone give
 // too few waves, each class is cut into chunks (multiples of k, of at least
-// 4k steps).  Target number of (wave-sized) work items per pass, overridable
-// for tuning with MFPSN_FWD_ITEMS / MFPSN_BWD_ITEMS.
-int64_t env_int(const char* name, int64_t dflt)
-{
-    const char* e = getenv(name);
-    const long long x = e ? atoll(e) : 0;
-    return x > 0 ? (int64_t)x : dflt;
-}
-
-int64_t target_items(bool backward)
-{
-    // the forward's halo is K-1 loads, so it chunks down to about 8 waves per
-    // SIMD; the backward's halo is K-1 steps of work, so it stops at 2
-    static const int64_t fwd = env_int("MFPSN_FWD_ITEMS", 8192);
-    static const int64_t bwd = env_int("MFPSN_BWD_ITEMS", 2048);
-    return backward ? bwd : fwd;
-}
+// 4k steps), down to a target number of (wave-sized) work items per pass:
+// the forward's halo is k-1 loads, so it chunks down to about 8 waves per
+// SIMD; the backward's halo is k-1 steps of work, so it stops at 2.
+constexpr int64_t kFwdTargetItems = 8192;
+constexpr int64_t kBwdTargetItems = 2048;
 
 // Two adjacent columns per lane (one 2x-wide access per stream and step):
 // plane mode with an even S (a lane's two positions share one row of S
 // columns), orders the two-column kernels are built for, and tensors aligned
-// for the wide accesses.  MFPSN_PAIR=0 turns it off.
+// for the wide accesses.
 bool pair_layout(const mfpsn_desc* d)
 {
-    static const bool on = [] {
-        const char* e = getenv("MFPSN_PAIR");
-        return !(e && strcmp(e, "0") == 0);
-    }();
-    return on && !(d->S == 1 && d->C >= 64) && d->S % 2 == 0 && d->k <= kPairMaxK;
-}
-
-// Line-aligned plane tiles (MFPSN_ROW_TILES=0 turns them off).
-bool row_tiles_enabled()
-{
-    static const bool on = [] {
-        const char* e = getenv("MFPSN_ROW_TILES");
-        return !(e && strcmp(e, "0") == 0);
-    }();
-    return on;
+    return !(d->S == 1 && d->C >= 64) && d->S % 2 == 0 && d->k <= kPairMaxK;
 }
 
 bool pair_aligned(std::initializer_list<const void*> ptrs)
@@ -177,8 +155,7 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
         // own that start on lines, at the price of a few shadow lanes.
         const int64_t width = 64 * nv, line = 128 / g.esize;
         const int64_t per_row = ceil_div(d->S + line - 1, width);
-        if (((int64_t)d->S * g.esize) % 128 != 0 && per_row * width * 8 <= (int64_t)d->S * 9 &&
-            row_tiles_enabled()) {
+        if (((int64_t)d->S * g.esize) % 128 != 0 && per_row * width * 8 <= (int64_t)d->S * 9) {
             g.row_tiles = (int32_t)per_row;
             g.tiles = (int32_t)(per_row * d->N);
         }
@@ -195,7 +172,7 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
         chunk = cap;
     int64_t nchunks = ceil_div(class_len, chunk);
     const int64_t min_chunk = 4 * K;
-    const int64_t target = target_items(backward);
+    const int64_t target = backward ? kBwdTargetItems : kFwdTargetItems;
     while (base * nchunks < target && ceil_div(chunk / 2, K) * K >= min_chunk &&
            ceil_div(chunk / 2, K) * K < chunk) {
         chunk = ceil_div(chunk / 2, K) * K;
@@ -261,7 +238,8 @@ int32_t mfpsn_sawtooth_dilation(int32_t layer, int32_t period)
 }
 
 int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
-                  const void* bias, uint8_t* spikes, void* h_out, void* sg_out, void* stream)
+                  const void* bias, const void* v_th_c, uint8_t* spikes, void* h_out, void* sg_out,
+                  void* stream)
 {
     int st = validate(desc);
     if (st != MFPSN_OK)
@@ -271,8 +249,8 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
         return MFPSN_ERR_NULL;
     if (desc->C > 0 && (!sign || !shift || !bias))
         return MFPSN_ERR_NULL;
-    if (!aligned(x, elem_bytes(desc->dtype)) || !aligned(bias, 4) || !aligned(h_out, 4) ||
-        !aligned(sg_out, 4))
+    if (!aligned(x, elem_bytes(desc->dtype)) || !aligned(bias, 4) || !aligned(v_th_c, 4) ||
+        !aligned(h_out, 4) || !aligned(sg_out, 4))
         return MFPSN_ERR_ALIGN;
     if (total == 0)
         return MFPSN_OK;
@@ -282,6 +260,7 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     a.sign = sign;
     a.shift = shift;
     a.bias = bias;
+    a.v_th_c = v_th_c;
     a.spikes = spikes;
     a.h_out = h_out;
     a.sg_out = sg_out;
@@ -303,8 +282,9 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
 }
 
 int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
-                   const void* sg, const int8_t* sign, const int8_t* shift, const void* bias, void* grad_x,
-                   void* grad_w, void* grad_b, void* workspace, size_t ws_bytes, void* stream)
+                   const void* sg, const int8_t* sign, const int8_t* shift, const void* bias,
+                   const void* v_th_c, void* grad_x, void* grad_w, void* grad_b, void* grad_vth,
+                   void* workspace, size_t ws_bytes, void* stream)
 {
     int st = validate(desc);
     if (st != MFPSN_OK)
@@ -316,8 +296,9 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
         return MFPSN_ERR_NULL;
     const int es = elem_bytes(desc->dtype);
     if (!aligned(x, es) || !aligned(grad_spikes, es) || !aligned(grad_x, grad_x_bytes(desc->dtype)) ||
-        !aligned(bias, 4) || !aligned(h, 4) || !aligned(sg, 4) || !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
-        !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
+        !aligned(bias, 4) || !aligned(v_th_c, 4) || !aligned(h, 4) || !aligned(sg, 4) ||
+        !aligned(grad_w, desc->dtype == MFPSN_Q8_8 ? 8 : 4) || !aligned(grad_b, desc->dtype == MFPSN_Q8_8 ? 8 : 4) ||
+        !aligned(grad_vth, desc->dtype == MFPSN_Q8_8 ? 8 : 4))
         return MFPSN_ERR_ALIGN;
     if (desc->dtype == MFPSN_Q8_8) {
         // every partial sum of grad_w must fit int64
@@ -337,6 +318,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     a.sign = sign;
     a.shift = shift;
     a.bias = bias;
+    a.v_th_c = v_th_c;
     a.grad_x = grad_x;
     a.partial = (double*)workspace;
     hipStream_t s = (hipStream_t)stream;
@@ -350,6 +332,7 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     f.partial = (const double*)workspace;
     f.grad_w = grad_w;
     f.grad_b = grad_b;
+    f.grad_vth = grad_vth;
     if (launch_finalize(f, s) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;

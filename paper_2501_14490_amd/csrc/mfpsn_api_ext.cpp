@@ -60,7 +60,7 @@ int validate_bn(const mfpsn_desc* d, BnGeom* g)
     // items (each chunk at least 2k steps), and a thread count that spreads
     // the items evenly and keeps every thread in one channel
     constexpr int64_t kTarget = 256 * 4 * 3 * 64;
-    const int64_t L = (d->T + d->dilation - 1) / d->dilation;
+    const int64_t L = ((int64_t)d->T + d->dilation - 1) / d->dilation;
     const int64_t walks = (int64_t)g->M * d->dilation;
     int64_t nch = walks > 0 ? (2 * kTarget + walks - 1) / walks : 1;
     const int64_t max_nch = L / (2 * (int64_t)d->k);
@@ -414,6 +414,7 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
     f.partial = (const double*)workspace;
     f.grad_w = grad_w;
     f.grad_b = grad_b;
+    f.grad_vth = nullptr;
     if (launch_finalize(f, s) != hipSuccess)
         return MFPSN_ERR_HIP;
     return MFPSN_OK;

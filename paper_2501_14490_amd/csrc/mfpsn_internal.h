@@ -63,6 +63,7 @@ struct FwdArgs {
     const int8_t* sign;
     const int8_t* shift;
     const void* bias;
+    const void* v_th_c;  // nullable: per-channel thresholds, float or int32 [C]
     uint8_t* spikes;
     void* h_out;       // nullable: potentials H
     void* sg_out;      // nullable: surrogate factor of H
@@ -77,6 +78,7 @@ struct BwdArgs {
     const int8_t* sign;
     const int8_t* shift;
     const void* bias;
+    const void* v_th_c;  // nullable: per-channel thresholds, float or int32 [C]
     void* grad_x;
     double* partial;   // [blocks][k+1][C]
 };
@@ -86,6 +88,7 @@ struct FinArgs {
     const double* partial;
     void* grad_w;
     void* grad_b;
+    void* grad_vth;    // nullable: -grad_b
 };
 
 // The launchers size the persistent grid from the kernel's occupancy and

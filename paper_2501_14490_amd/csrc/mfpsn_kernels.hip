@@ -43,11 +43,11 @@
 // scattered into the k open grad_x accumulators it feeds (outputs j-k+1..j);
 // contributions reach every output in ascending tap order, so the sum order
 // is the definition's.  Output j is complete after step j and is stored.
-// Lanes whose dH is zero or below the exponent-add range skip the scatter:
-// their terms are zeros or smaller than 2^(shift_hi-shift_lo-126), and they
-// would otherwise force the exact path on the whole wave wherever the
-// surrogate gradient underflows.  grad_x therefore equals the sequential
-// definition bit for bit, except that such tiny dH values count as zero.
+// Lanes whose dH is zero skip the scatter (their terms are zeros, which change
+// no bit of an accumulator that starts at +0); lanes whose dH lies outside the
+// exponent-add range (tiny, huge, infinite, NaN) take the exact ldexp taps, on
+// their own lanes only.  grad_x therefore equals the sequential definition
+// bit for bit.
 // grad_w / grad_b are accumulated from exact products: double for float data
 // (the x ring is kept in double), int64 for Q8.8; they are reduced inside the
 // block in a fixed order and written as per-block partials, which a finalize
@@ -603,6 +603,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         bias = ((const int32_t*)a.bias)[c];
         start = bias + tp.cneg;
     }
+    // the channel's threshold (Eq. mfdpsn_fire): V_th[c] when given, else the
+    // one shared by every channel
+    float vth = g.v_th;
+    int vthq = g.v_th_q;
+    if (a.v_th_c != nullptr) {
+        if constexpr (kF)
+            vth = ((const float*)a.v_th_c)[c];
+        else
+            vthq = ((const int32_t*)a.v_th_c)[c];
+    }
     const uint32_t M = g.M;
     const int d = g.d;
     const uint64_t xrow = (uint64_t)M * es;
@@ -702,7 +712,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                 }
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
-                    spk |= (h.v[e] >= g.v_th ? 1u : 0u) << (8 * e);
+                    spk |= (h.v[e] >= vth ? 1u : 0u) << (8 * e);
             } else {
 #pragma unroll
                 for (int e = 0; e < NV; ++e) {
@@ -715,7 +725,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                         pin(acc);
                     }
                     h.v[e] = acc;
-                    spk |= (h.v[e] >= g.v_th_q ? 1u : 0u) << (8 * e);
+                    spk |= (h.v[e] >= vthq ? 1u : 0u) << (8 * e);
                 }
             }
             st_bytes<NV>(ss, vs, so_s, spk);
@@ -731,9 +741,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
                     if constexpr (kF)
-                        w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], g.v_th, g.v_th_q));
+                        w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], vth, vthq));
                     else
-                        w.v[e] = (uint32_t)qt(sg, h.v[e], g.v_th_q);
+                        w.v[e] = (uint32_t)qt(sg, h.v[e], vthq);
                 st_words<NV>(gs, vh, so_h, w);
             }
             advance(so_s, sstep);
@@ -834,6 +844,14 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         start = bias + tp.cneg;
         reset = tp.cneg;
     }
+    float vth = g.v_th;  // the channel's threshold, as in the forward
+    int vthq = g.v_th_q;
+    if (a.v_th_c != nullptr) {
+        if constexpr (kF)
+            vth = ((const float*)a.v_th_c)[c];
+        else
+            vthq = ((const int32_t*)a.v_th_c)[c];
+    }
     Surrogate sg;
     sg.init(g.sg, g.alpha);
     constexpr bool kQT = !kF && HS != kSavedFactor;  // Q8.8 factors from the table
@@ -845,9 +863,9 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     }
     auto factor = [&](V h) __attribute__((always_inline)) {
         if constexpr (kQT)
-            return qt(sg, h, g.v_th_q);
+            return qt(sg, h, vthq);
         else
-            return sg_factor(sg, h, g.v_th, g.v_th_q);
+            return sg_factor(sg, h, vth, vthq);
     };
 
     const uint32_t M = g.M;
@@ -1074,20 +1092,21 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 }
                 // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k).  Lanes
                 // whose dH is in the exponent-add range take the fast taps;
-                // lanes above it (or infinite, NaN) the exact taps.  A dH below
-                // the range (zero, or a surrogate gradient that underflowed to
-                // under 2^(shift_hi-126)) adds nothing: its terms are zeros or
-                // smaller than 2^(shift_hi-shift_lo-126).
+                // every other nonzero dH (one whose scaled terms would leave the
+                // normal range: tiny, huge, infinite or NaN) the exact taps.  A
+                // zero dH adds nothing: its terms are zeros, and an accumulator
+                // that starts at +0 is never -0, so adding them changes no bit.
 #pragma unroll
                 for (int e = 0; e < NV; ++e) {
                     if constexpr (kF) {
                         const float m = __builtin_fabsf(dh.v[e]);
-                        if (m >= g.fast_lo && m < g.fast_hi) {
+                        const bool fast = m >= g.fast_lo && m < g.fast_hi;
+                        if (fast) {
 #pragma unroll
                             for (int i = imin; i < K; ++i)
                                 gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply_fast(dh.v[e], i);
                         }
-                        if (__builtin_expect(!(m < g.fast_hi), 0)) {
+                        if (__builtin_expect(!fast && m != 0.0f, 0)) {
 #pragma unroll
                             for (int i = imin; i < K; ++i)
                                 gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply(dh.v[e], i);
@@ -1229,17 +1248,24 @@ __device__ __forceinline__ void fin_body(const FinArgs& a)
     for (int q = 1; q < kFinWaves; ++q)
         t += red[q][lane];
     const int i = e / a.C, c = e % a.C;
+    // grad_vth = -grad_b: V_th[c] enters the surrogate as H - V_th[c]
     if constexpr (std::is_same_v<W, int64_t>) {
-        if (i < a.k)
+        if (i < a.k) {
             ((int64_t*)a.grad_w)[c * a.k + i] = t;
-        else
+        } else {
             ((int64_t*)a.grad_b)[c] = t;
+            if (a.grad_vth != nullptr)
+                ((int64_t*)a.grad_vth)[c] = -t;
+        }
     } else {
         const float v = (float)t;
-        if (i < a.k)
+        if (i < a.k) {
             ((float*)a.grad_w)[c * a.k + i] = v;
-        else
+        } else {
             ((float*)a.grad_b)[c] = v;
+            if (a.grad_vth != nullptr)
+                ((float*)a.grad_vth)[c] = -v;
+        }
     }
 }
 

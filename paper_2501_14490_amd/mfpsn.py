@@ -53,11 +53,11 @@ class MfpsnDesc(ctypes.Structure):
 
 _P = ctypes.c_void_p
 _DP = ctypes.POINTER(MfpsnDesc)
-_lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_forward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.mfpsn_forward.restype = ctypes.c_int
 _lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
-_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
 _lib.mfpsn_backward.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
@@ -145,8 +145,9 @@ def mfpsn_sawtooth_dilation(layer: int, period: int) -> int:
     return int(_lib.mfpsn_sawtooth_dilation(int(layer), int(period)))
 
 
-def mfpsn_forward(desc: MfpsnDesc, x, sign, shift, bias, spikes, h_out=None, sg_out=None, stream=None) -> None:
-    _check(_lib.mfpsn_forward(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias),
+def mfpsn_forward(desc: MfpsnDesc, x, sign, shift, bias, v_th_c, spikes, h_out=None, sg_out=None,
+                  stream=None) -> None:
+    _check(_lib.mfpsn_forward(ctypes.byref(desc), _ptr(x), _ptr(sign), _ptr(shift), _ptr(bias), _ptr(v_th_c),
                               _ptr(spikes), _ptr(h_out), _ptr(sg_out), _stream(stream)), "mfpsn_forward")
 
 
@@ -157,13 +158,14 @@ def mfpsn_backward_workspace_size(desc: MfpsnDesc) -> int:
     return int(n.value)
 
 
-def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b,
-                   workspace, workspace_bytes=None, stream=None) -> None:
+def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sg, sign, shift, bias, v_th_c, grad_x, grad_w, grad_b,
+                   grad_vth, workspace, workspace_bytes=None, stream=None) -> None:
     if workspace_bytes is None:
         workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(_lib.mfpsn_backward(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(h), _ptr(sg), _ptr(sign),
-                               _ptr(shift), _ptr(bias), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
-                               _ptr(workspace), int(workspace_bytes), _stream(stream)), "mfpsn_backward")
+                               _ptr(shift), _ptr(bias), _ptr(v_th_c), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
+                               _ptr(grad_vth), _ptr(workspace), int(workspace_bytes), _stream(stream)),
+           "mfpsn_backward")
 
 
 def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=None) -> None:
@@ -251,24 +253,33 @@ def _expect(t, dtype, device, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, want_sg: bool = False, stream=None):
-    """spikes, plus H (want_h) and the surrogate factor (want_sg) in that order."""
+def forward(desc: MfpsnDesc, x, sign, shift, bias, want_h: bool = False, want_sg: bool = False, stream=None,
+            v_th_c=None):
+    """spikes, plus H (want_h) and the surrogate factor (want_sg) in that order.
+    v_th_c: optional per-channel thresholds [C] (float, int32 for Q8.8)."""
     dev = x.device
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(bias, BIAS[desc.dtype], dev, "bias")
+    if v_th_c is not None:
+        _expect(v_th_c, BIAS[desc.dtype], dev, "v_th_c")
     spikes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
     h = torch.empty(x.shape, dtype=H_OUT[desc.dtype], device=dev) if want_h else None
     sg = torch.empty(x.shape, dtype=SG_OUT[desc.dtype], device=dev) if want_sg else None
-    mfpsn_forward(desc, x, sign, shift, bias, spikes, h, sg, stream)
+    mfpsn_forward(desc, x, sign, shift, bias, v_th_c, spikes, h, sg, stream)
     out = (spikes,) + ((h,) if want_h else ()) + ((sg,) if want_sg else ())
     return out if len(out) > 1 else spikes
 
 
-def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, sg=None, h=None):
+def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None, stream=None, sg=None, h=None,
+             v_th_c=None, want_vth: bool = False):
     """sg: optional surrogate factor saved by forward(..., want_sg=True); h:
     optional potentials saved by forward(..., want_h=True).  sg is used if
-    given, else h, else both are recomputed from x."""
+    given, else h, else both are recomputed from x.  v_th_c: the per-channel
+    thresholds the forward used; want_vth: also return the threshold gradient.
+    Returns grad_x, grad_w, grad_b (and grad_vth)."""
     dev = x.device
+    if v_th_c is not None:
+        _expect(v_th_c, BIAS[desc.dtype], dev, "v_th_c")
     _expect(x, STORAGE[desc.dtype], dev, "x")
     _expect(grad_spikes, STORAGE[desc.dtype], dev, "grad_spikes")
     if sg is not None:
@@ -278,12 +289,13 @@ def backward(desc: MfpsnDesc, x, grad_spikes, sign, shift, bias, workspace=None,
     grad_x = torch.empty(x.shape, dtype=GRAD_X[desc.dtype], device=dev)
     grad_w = torch.empty((desc.C, desc.k), dtype=GRAD_WB[desc.dtype], device=dev)
     grad_b = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev)
+    grad_vth = torch.empty((desc.C,), dtype=GRAD_WB[desc.dtype], device=dev) if want_vth else None
     need = mfpsn_backward_workspace_size(desc)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
-    mfpsn_backward(desc, x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b, workspace,
-                   stream=stream)
-    return grad_x, grad_w, grad_b
+    mfpsn_backward(desc, x, grad_spikes, h, sg, sign, shift, bias, v_th_c, grad_x, grad_w, grad_b, grad_vth,
+                   workspace, stream=stream)
+    return (grad_x, grad_w, grad_b, grad_vth) if want_vth else (grad_x, grad_w, grad_b)
 
 
 def quantize(w, shift_lo: int, shift_hi: int, stream=None):
@@ -410,7 +422,7 @@ class StreamState:
 
 
 class MfPSNFunction(torch.autograd.Function):
-    """spikes = Theta(conv_{Q(W)}(x) + b - v_th) with the surrogate-gradient
+    """spikes = Theta(conv_{Q(W)}(x) + b - V_th) with the surrogate-gradient
     backward (Sec. 4.2, App. A.3).  Float storage paths (f32, bf16).
 
     ste="whole" (default): the gradient of W is the gradient of Q(W) (the
@@ -418,34 +430,34 @@ class MfPSNFunction(torch.autograd.Function):
     ste="round": only round()'s derivative is replaced by 1, so the gradient
     of W is that of Q(W) times |Q(W)|/|W| (Eq. ste_q).
     v_th: a float, or a per-channel tensor [C] (the learnable channel-wise
-    threshold of Eq. mfdpsn_fire).  A per-channel threshold folds into the
-    bias, b - v_th, compared with 0; its gradient is minus the bias gradient."""
+    threshold of Eq. mfdpsn_fire), passed to the library as is; its gradient
+    comes from the library's backward."""
 
     @staticmethod
     def forward(ctx, x, w, b, k, dilation, v_th, surrogate, alpha, shift_lo, shift_hi, ste="whole"):
         dtype = "bf16" if x.dtype == torch.bfloat16 else "f32"
         per_channel = torch.is_tensor(v_th)
         bc = b.detach().float().contiguous()
-        if per_channel:
-            bc = (bc - v_th.detach().float().reshape(bc.shape)).contiguous()
+        vc = v_th.detach().float().reshape(bc.shape).contiguous() if per_channel else None
         desc = make_desc(x.shape, k, dilation, dtype, surrogate, alpha, 0.0 if per_channel else v_th, 0,
                          shift_lo, shift_hi)
         wc = w.detach().contiguous()
         sign, shift = quantize(wc, shift_lo, shift_hi)
         xc = x.detach().contiguous()
-        spikes, sg = forward(desc, xc, sign, shift, bc, want_sg=True)
-        ctx.save_for_backward(xc, wc, sign, shift, bc, sg)
+        spikes, sg = forward(desc, xc, sign, shift, bc, want_sg=True, v_th_c=vc)
+        ctx.save_for_backward(xc, wc, sign, shift, bc, sg, vc)
         ctx.desc, ctx.per_channel, ctx.ste = desc, per_channel, ste
         ctx.shift_range = (shift_lo, shift_hi)
         return spikes.to(x.dtype)
 
     @staticmethod
     def backward(ctx, grad_spikes):
-        xc, wc, sign, shift, bc, sg = ctx.saved_tensors
+        xc, wc, sign, shift, bc, sg, vc = ctx.saved_tensors
         g = grad_spikes.to(xc.dtype).contiguous()
-        grad_x, grad_wq, grad_b = backward(ctx.desc, xc, g, sign, shift, bc, sg=sg)
+        out = backward(ctx.desc, xc, g, sign, shift, bc, sg=sg, v_th_c=vc, want_vth=ctx.per_channel)
+        grad_x, grad_wq, grad_b = out[:3]
+        grad_vth = out[3] if ctx.per_channel else None
         grad_w = grad_wq if ctx.ste == "whole" else quantizer_grad(wc, shift, grad_wq, ctx.ste, *ctx.shift_range)
-        grad_vth = -grad_b if ctx.per_channel else None
         return grad_x, grad_w, grad_b, None, None, grad_vth, None, None, None, None, None
 
 

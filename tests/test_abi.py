@@ -37,8 +37,8 @@ def lib():
     L = ctypes.CDLL(LIB)
     P = ctypes.c_void_p
     DP = ctypes.POINTER(Desc)
-    L.mfpsn_forward.argtypes = [DP, P, P, P, P, P, P, P, P]
-    L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    L.mfpsn_forward.argtypes = [DP, P, P, P, P, P, P, P, P, P]
+    L.mfpsn_backward.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.mfpsn_backward_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
     L.mfpsn_quantize_weights.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
     L.mfpsn_bn_workspace_size.argtypes = [DP, ctypes.POINTER(ctypes.c_size_t)]
@@ -73,7 +73,7 @@ def test_struct_layout_matches_header():
 
 
 def test_version_and_status_strings(lib):
-    assert lib.mfpsn_abi_version() == 9
+    assert lib.mfpsn_abi_version() == 10
     for s in range(-7, 1):
         assert lib.mfpsn_status_string(s)
     assert lib.mfpsn_status_string(-99) == b"unknown status"
@@ -96,24 +96,33 @@ FAKE = 0x100000  # never dereferenced: validation fails first
 ])
 def test_forward_rejects_bad_descriptors(lib, kw, status):
     d = good_desc(**kw)
-    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None) == status
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == status
 
 
 def test_forward_rejects_null_and_misaligned(lib):
-    assert lib.mfpsn_forward(None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None) == -1
+    assert lib.mfpsn_forward(None, FAKE, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -1
     d = good_desc()
-    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, FAKE, None, None, None) == -1
-    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, None, None) == -1
-    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 2, None) == -6
-    assert lib.mfpsn_forward(ctypes.byref(d), FAKE + 2, FAKE, FAKE, FAKE, FAKE, None, None, None) == -6
-    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE + 1, FAKE, None, None, None) == -6
+    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -1
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, None, None, None) == -1
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, FAKE, None, FAKE + 2, None) == -6
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE + 2, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -6
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE + 1, None, FAKE, None, None, None) == -6
     d16 = good_desc(dtype=1)
-    assert lib.mfpsn_forward(ctypes.byref(d16), FAKE + 1, FAKE, FAKE, FAKE, FAKE, None, None, None) == -6
+    assert lib.mfpsn_forward(ctypes.byref(d16), FAKE + 1, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -6
+
+
+def test_forward_rejects_misaligned_thresholds_and_bad_q88_threshold(lib):
+    d = good_desc()
+    assert lib.mfpsn_forward(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE + 2, FAKE, None, None, None) == -6
+    q = good_desc(dtype=2, v_th_q=(1 << 30) + 1)
+    assert lib.mfpsn_forward(ctypes.byref(q), FAKE, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -3
+    q = good_desc(dtype=2, v_th_q=-(1 << 30) - 1)
+    assert lib.mfpsn_forward(ctypes.byref(q), FAKE, FAKE, FAKE, FAKE, None, FAKE, None, None, None) == -3
 
 
 def test_empty_forward_is_a_no_op(lib):
     d = good_desc(T=0)
-    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, None, None, None, None) == 0
+    assert lib.mfpsn_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, None, None, None, None, None) == 0
 
 
 def test_backward_workspace_and_validation(lib):
@@ -127,15 +136,16 @@ def test_backward_workspace_and_validation(lib):
     # too small / misaligned / missing workspace
     need = ctypes.c_size_t(0)
     lib.mfpsn_backward_workspace_size(ctypes.byref(d), ctypes.byref(need))
-    args = [FAKE] * 10  # x, grad_spikes, h, sg, sign, shift, bias, grad_x, grad_w, grad_b
+    # x, grad_spikes, h, sg, sign, shift, bias, v_th_c, grad_x, grad_w, grad_b, grad_vth
+    args = [FAKE] * 12
     assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE, need.value - 8, None) == -5
     assert lib.mfpsn_backward(ctypes.byref(d), *args, FAKE + 4, need.value, None) == -5
     assert lib.mfpsn_backward(ctypes.byref(d), *args, None, need.value, None) == -5
     # null tensors (h and sg may be NULL; grad_w may not)
     bad = list(args)
-    bad[8] = None  # grad_w
+    bad[9] = None  # grad_w
     assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -1
-    for i in (2, 3):  # misaligned h, sg
+    for i in (2, 3, 7, 11):  # misaligned h, sg, v_th_c, grad_vth
         bad = list(args)
         bad[i] = FAKE + 2
         assert lib.mfpsn_backward(ctypes.byref(d), *bad, FAKE, need.value, None) == -6

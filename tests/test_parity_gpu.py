@@ -2,12 +2,10 @@
 
 Bar: spikes, Q8.8 potentials and all Q8.8 gradients bit-exact; float
 potentials and grad_x bit-exact (both sides follow the same pinned float
-sequence); bf16 grad_x bit-exact after round-to-nearest-even; grad_w and
-grad_b within 1e-6 absolute + 1e-5 relative of the oracle's double sums
-(only the order of the double additions differs).  The one documented
-exception: the kernel drops the grad_x terms of a dH below the exponent-add
-range (|dH| < 2^(shift_hi-126), where the surrogate gradient underflows), so
-an output fed by such a dH is only required to be within 1e-30 of the oracle.
+sequence, every term included, also those of a dH below the exponent-add
+range); bf16 grad_x bit-exact after round-to-nearest-even; grad_w and grad_b
+within 1e-6 absolute + 1e-5 relative of the oracle's double sums (only the
+order of the double additions differs).
 """
 import numpy as np
 import pytest
@@ -42,19 +40,20 @@ def to_dev(a, dtype, offset=0):
 
 
 def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256, saved=None,
-            offset=0):
+            offset=0, v_th_c=None):
     x = to_dev(case["x"], dtype, offset)
     g = to_dev(case["grad_spikes"], dtype, offset)
     sign = to_dev(case["sign"], None)
     shift = to_dev(case["shift"], None)
     bias = to_dev(case["bias"], None)
+    vc = to_dev(v_th_c, None) if v_th_c is not None else None
     desc = mfpsn.make_desc(case["x"].shape, k, d, dtype, surrogate, alpha, v_th, v_th_q, lo, hi)
-    spikes, h, sg = mfpsn.forward(desc, x, sign, shift, bias, want_h=True, want_sg=True)
-    gx, gw, gb = mfpsn.backward(desc, x, g, sign, shift, bias, sg=sg if saved == "sg" else None,
-                                h=h if saved == "h" else None)
+    spikes, h, sg = mfpsn.forward(desc, x, sign, shift, bias, want_h=True, want_sg=True, v_th_c=vc)
+    gx, gw, gb, gv = mfpsn.backward(desc, x, g, sign, shift, bias, sg=sg if saved == "sg" else None,
+                                    h=h if saved == "h" else None, v_th_c=vc, want_vth=True)
     torch.cuda.synchronize()
     out = {"spikes": spikes.cpu().numpy(), "H": h.cpu().numpy(), "SG": sg.cpu().numpy(),
-           "grad_w": gw.cpu().numpy(), "grad_b": gb.cpu().numpy()}
+           "grad_w": gw.cpu().numpy(), "grad_b": gb.cpu().numpy(), "grad_vth": gv.cpu().numpy()}
     if dtype == "bf16":
         out["grad_x_bits"] = gx.view(torch.int16).cpu().numpy().view(np.uint16)
     else:
@@ -62,52 +61,44 @@ def gpu_run(case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7,
     return out
 
 
-def oracle_run(orc, case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256):
+def oracle_run(orc, case, k, d, dtype, v_th, surrogate="sigmoid", alpha=4.0, lo=0, hi=7, v_th_q=256,
+               v_th_c=None):
     if dtype == "q8_8":
-        H, spk = orc.forward_q88(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th_q, lo, hi)
+        H, spk = orc.forward_q88(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th_q, lo, hi,
+                                 v_th_c=v_th_c)
         b = orc.backward_q88(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
-                             v_th_q, surrogate, alpha, lo, hi)
+                             v_th_q, surrogate, alpha, lo, hi, v_th_c=v_th_c)
     elif dtype == "bf16":
         H, spk = orc.forward_bf16(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th,
-                                  shift_lo=lo, shift_hi=hi)
+                                  shift_lo=lo, shift_hi=hi, v_th_c=v_th_c)
         b = orc.backward_bf16(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
-                              v_th, surrogate_kind=surrogate, alpha=alpha, shift_lo=lo, shift_hi=hi)
+                              v_th, surrogate_kind=surrogate, alpha=alpha, shift_lo=lo, shift_hi=hi, v_th_c=v_th_c)
     else:
-        H, spk = orc.forward_f32(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th, lo, hi)
+        H, spk = orc.forward_f32(case["x"], case["sign"], case["shift"], case["bias"], k, d, v_th, lo, hi,
+                                 v_th_c=v_th_c)
         b = orc.backward_f32(case["x"], case["grad_spikes"], case["sign"], case["shift"], case["bias"], k, d,
-                             v_th, surrogate, alpha, lo, hi)
+                             v_th, surrogate, alpha, lo, hi, v_th_c=v_th_c)
     b["spikes"], b["Hf"] = spk, H
-    # the surrogate factor the forward saves, by the oracle's own surrogate
+    # the surrogate factor the forward saves, by the oracle's own surrogate,
+    # at the threshold of each element's channel
+    C = case["x"].shape[2]
+    bshape = (1, 1, C) + (1,) * (case["x"].ndim - 3)
     if dtype == "q8_8":
-        b["SG"] = orc.surrogate_q15(surrogate, alpha, (H.astype(np.int64) - v_th_q).astype(np.int32))
+        thr = (np.asarray(v_th_c, np.int64) if v_th_c is not None else np.full(C, v_th_q, np.int64)).reshape(bshape)
+        b["SG"] = orc.surrogate_q15(surrogate, alpha, (H.astype(np.int64) - thr).astype(np.int32))
     else:
-        b["SG"] = orc.surrogate(surrogate, alpha, (H - np.float32(v_th)).astype(np.float32))
+        thr = (np.asarray(v_th_c, np.float32) if v_th_c is not None else np.full(C, v_th, np.float32)).reshape(bshape)
+        b["SG"] = orc.surrogate(surrogate, alpha, (H - thr).astype(np.float32))
     return b
 
 
-def tiny_dh_outputs(dH, k, d, hi):
-    """Mask of grad_x outputs that receive a term from a nonzero dH below the
-    exponent-add range 2^(max(1, hi+1) - 127)."""
-    lo_bound = np.float32(2.0 ** (max(1, hi + 1) - 127))
-    tiny = (dH != 0) & (np.abs(dH) < lo_bound)
-    T = dH.shape[0]
-    hit = np.zeros(dH.shape, dtype=bool)
-    for m in range(k):
-        s = m * d
-        if s < T:
-            hit[:T - s] |= tiny[s:]
-    return hit
-
-
-def check_grad_x(g, r, hit, label):
-    """bit-exact outside `hit`; within 1e-30 on it; NaN matches NaN."""
+def check_grad_x(g, r, label):
+    """bit-exact; NaN matches NaN whatever its payload."""
     nan = np.isnan(r)
     assert np.array_equal(np.isnan(g), nan), f"{label}: grad_x NaN pattern differs"
-    exact = ~hit & ~nan
     diff = np.abs(g.astype(np.float64) - r.astype(np.float64))
-    assert np.array_equal(g[exact].view(np.uint32), r[exact].view(np.uint32)), (
-        f"{label}: grad_x differs, max |diff| {np.nanmax(np.where(exact, diff, 0))}")
-    assert np.all(diff[hit & ~nan] <= 1e-30), f"{label}: grad_x near a tiny dH differs by {diff[hit & ~nan].max()}"
+    assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), (
+        f"{label}: grad_x differs, max |diff| {np.nanmax(np.where(~nan, diff, 0))}")
 
 
 def compare(got, ref, dtype, label, k=None, d=None, hi=7):
@@ -125,17 +116,20 @@ def compare(got, ref, dtype, label, k=None, d=None, hi=7):
         assert np.array_equal(got["grad_x"], ref["grad_x"]), f"{label}: grad_x differs"
         assert np.array_equal(got["grad_w"], ref["grad_w"]), f"{label}: grad_w differs"
         assert np.array_equal(got["grad_b"], ref["grad_b"]), f"{label}: grad_b differs"
+        if "grad_vth" in got:
+            assert np.array_equal(got["grad_vth"], ref["grad_vth"]), f"{label}: grad_vth differs"
         return
     assert np.array_equal(got["H"].view(np.uint32), ref["Hf"].view(np.uint32)), (
         f"{label}: H differs, max |diff| {np.abs(got['H'] - ref['Hf']).max()}")
-    hit = tiny_dh_outputs(ref["dH"], k, d, hi)
     if dtype == "bf16":
         gb = got["grad_x_bits"].astype(np.uint32) << 16
         rb = ref["grad_x_bits"].astype(np.uint32) << 16
-        check_grad_x(gb.view(np.float32), rb.view(np.float32), hit, label + " (bf16)")
+        check_grad_x(gb.view(np.float32), rb.view(np.float32), label + " (bf16)")
     else:
-        check_grad_x(got["grad_x"], ref["grad_x"], hit, label)
-    for name in ("grad_w", "grad_b"):
+        check_grad_x(got["grad_x"], ref["grad_x"], label)
+    for name in ("grad_w", "grad_b", "grad_vth"):
+        if name not in got:
+            continue
         g = got[name].astype(np.float64)
         r = ref[name]
         err = np.abs(g - r)
@@ -210,6 +204,38 @@ def test_surrogates(orc, surrogate, alpha, dtype):
     compare(got, ref, dtype, f"{surrogate} {alpha} {dtype}", 4, 2)
 
 
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "q8_8"])
+@pytest.mark.parametrize("shape_i", [0, 1, 5, 8])
+def test_per_channel_threshold(orc, dtype, shape_i, saved):
+    # the learnable channel-wise threshold (Eq. mfdpsn_fire): every channel
+    # fires against its own V_th[c] and the surrogate sees H - V_th[c]; spikes,
+    # H, the factor and grad_x bit for bit, grad_vth = -grad_b to the bar
+    (T, N, C, sp), label = SHAPES[shape_i]
+    k, d = 5, 2
+    case = workloads.make_small(T, N, C, sp, k=k, dtype=dtype, seed=60 + shape_i)
+    rng = np.random.default_rng(61 + shape_i)
+    if dtype == "q8_8":
+        vc = rng.integers(-200, 300, C).astype(np.int32)
+    else:
+        vc = rng.normal(0.2, 0.6, C).astype(np.float32)
+    got = gpu_run(case, k, d, dtype, 99.0, v_th_q=-9999, saved=saved, v_th_c=vc)
+    ref = oracle_run(orc, case, k, d, dtype, 99.0, v_th_q=-9999, v_th_c=vc)
+    assert 0 < ref["spikes"].mean() < 1
+    compare(got, ref, dtype, f"per-channel V_th {label} {dtype} saved={saved}", k, d)
+
+
+def test_per_channel_threshold_at_a_potential_fires(orc):
+    # Theta(0) = 1 with a per-channel threshold placed exactly on a potential
+    case = workloads.make_small(20, 2, 66, (), k=4, dtype="f32", seed=62)
+    H, _ = orc.forward_f32(case["x"], case["sign"], case["shift"], case["bias"], 4, 1, 0.0, 0, 7)
+    vc = H[7, 1, :].astype(np.float32).copy()
+    got = gpu_run(case, 4, 1, "f32", 0.0, v_th_c=vc)
+    assert np.all(got["spikes"][7, 1, :] == 1)
+    ref = oracle_run(orc, case, 4, 1, "f32", 0.0, v_th_c=vc)
+    compare(got, ref, "f32", "threshold on a potential", 4, 1)
+
+
 def test_negative_and_wide_shifts(orc):
     case = workloads.make_small(25, 2, 65, (), k=6, s_lo=-4, s_hi=12, dtype="f32", seed=3)
     got = gpu_run(case, 6, 3, "f32", 0.1, lo=-3, hi=10)
@@ -251,7 +277,7 @@ def compare_nan_aware(got, ref, label, k, d, hi=7):
     nan = np.isnan(r)
     assert np.array_equal(np.isnan(g), nan), f"{label}: H NaN pattern differs"
     assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: H differs"
-    check_grad_x(got["grad_x"], ref["grad_x"], tiny_dh_outputs(ref["dH"], k, d, hi), label)
+    check_grad_x(got["grad_x"], ref["grad_x"], label)
     g, r = got["SG"], ref["SG"]
     nan = np.isnan(r)
     assert np.array_equal(np.isnan(g), nan), f"{label}: surrogate factor NaN pattern differs"
@@ -283,20 +309,40 @@ def test_special_values_take_the_exact_path(orc, k, d, saved):
 
 
 @pytest.mark.parametrize("saved", [None, "h", "sg"])
-def test_tiny_dh_terms(orc, saved):
+@pytest.mark.parametrize("dtype,spatial", [("f32", ()), ("f32", (6,)), ("bf16", (6,))])
+def test_tiny_dh_terms(orc, saved, dtype, spatial):
     # grad_spikes values around 1e-38 make dH fall below the exponent-add
-    # range on many lanes: their grad_x terms are dropped, every other output
-    # stays bit-exact
-    case = workloads.make_small(50, 3, 70, (), k=8, dtype="f32", seed=21)
+    # range on many lanes: those lanes take the exact taps, so every output,
+    # also those fed only by such terms, matches the definition bit for bit
+    C = 70 if not spatial else 3
+    case = workloads.make_small(50, 3, C, spatial, k=8, dtype=dtype, seed=21)
     g = case["grad_spikes"]
     rng = np.random.default_rng(21)
     idx = rng.integers(0, g.size, size=g.size // 5)
-    g.ravel()[idx] = (rng.standard_normal(idx.size) * 1e-37).astype(np.float32)
-    got = gpu_run(case, 8, 2, "f32", 0.25, saved=saved)
-    ref = oracle_run(orc, case, 8, 2, "f32", 0.25)
-    hit = tiny_dh_outputs(ref["dH"], 8, 2, 7)
-    assert hit.any() and not hit.all()
-    compare(got, ref, "f32", "tiny dH", 8, 2)
+    tiny = (rng.standard_normal(idx.size) * 1e-37).astype(np.float32)
+    if dtype == "bf16":
+        g.ravel()[idx] = workloads.to_bf16_bits(tiny)
+    else:
+        g.ravel()[idx] = tiny
+    got = gpu_run(case, 8, 2, dtype, 0.25, saved=saved)
+    ref = oracle_run(orc, case, 8, 2, dtype, 0.25)
+    lo_bound = np.float32(2.0 ** (8 - 127))
+    assert np.any((ref["dH"] != 0) & (np.abs(ref["dH"]) < lo_bound))
+    compare(got, ref, dtype, "tiny dH", 8, 2)
+
+
+@pytest.mark.parametrize("lo,hi", [(0, 126), (-20, 120), (0, 60)])
+def test_wide_shift_ranges_keep_every_term(orc, lo, hi):
+    # with shifts up to 126 almost every dH is below the exponent-add range of
+    # the fast taps: all of them go through the exact taps
+    case = workloads.make_small(40, 3, 70, (), k=6, s_lo=lo, s_hi=hi, dtype="f32", seed=hi)
+    got = gpu_run(case, 6, 2, "f32", 0.25, lo=lo, hi=hi)
+    ref = oracle_run(orc, case, 6, 2, "f32", 0.25, lo=lo, hi=hi)
+    compare(got, ref, "f32", f"shifts [{lo}, {hi}]", 6, 2, hi=hi)
+    case = workloads.make_small(40, 3, 2, (8,), k=6, s_lo=lo, s_hi=hi, dtype="bf16", seed=hi + 1)
+    got = gpu_run(case, 6, 3, "bf16", 0.25, lo=lo, hi=hi)
+    ref = oracle_run(orc, case, 6, 3, "bf16", 0.25, lo=lo, hi=hi)
+    compare(got, ref, "bf16", f"plane shifts [{lo}, {hi}]", 6, 3, hi=hi)
 
 
 def test_negative_shifts_near_overflow(orc):
@@ -357,42 +403,135 @@ def test_quantizer_matches_oracle(orc):
 
 
 # ---------------------------------------------------------------------------
-# the five workloads at full size, every dilation of their period: sampled
-# channels are compared in full (all t, n, s) against the oracle run on the
-# channel slice; the launch is the one bench.py times.
+# the five workloads at full size, every dilation of their period, in the
+# launch configuration bench.py times.  Sampled channels are compared in full
+# (all t, n, s) against the oracle run on the channel slice: channels 0, 63,
+# 64 and C-1, the first and last channel of every 64-channel group (the
+# lane-channel mapping puts 64 channels on one wave), and random ones up to
+# 16.  Every output sits between 4 KiB guard zones that must come back
+# unchanged.  All three backward inputs run at the first dilation.
 # ---------------------------------------------------------------------------
+GUARD = 4096
+PATTERN = 0xA5
+
+
+class Guarded:
+    """A device tensor between two 4 KiB guard zones filled with a pattern."""
+
+    def __init__(self, shape, dtype):
+        self.n = int(np.prod(shape)) if len(shape) else 1
+        es = torch.empty((), dtype=dtype).element_size()
+        nbytes = self.n * es
+        self.buf = torch.full((2 * GUARD + nbytes,), PATTERN, dtype=torch.uint8, device=DEV)
+        self.t = self.buf[GUARD:GUARD + nbytes].view(dtype).view(shape)
+
+    def intact(self):
+        b = self.buf
+        return bool(torch.all(b[:GUARD] == PATTERN)) and bool(torch.all(b[b.numel() - GUARD:] == PATTERN))
+
+
+def sampled_channels(C, rng, at_least=16):
+    ch = {0, C - 1}
+    if C > 64:
+        ch |= {63, 64}
+        for g0 in range(0, C, 64):
+            ch |= {g0, min(C, g0 + 64) - 1}
+    rest = [c for c in range(C) if c not in ch]
+    extra = max(0, at_least - len(ch))
+    if extra and rest:
+        ch |= set(rng.choice(rest, size=min(extra, len(rest)), replace=False).tolist())
+    return np.array(sorted(ch))
+
+
+def run_guarded(wl, desc, dev, saved):
+    """One forward (saving H and the factor) and one backward with the given
+    input, every output guarded; returns the outputs and the guards."""
+    spikes = Guarded(wl.shape, torch.uint8)
+    h = Guarded(wl.shape, mfpsn.H_OUT[desc.dtype])
+    sg = Guarded(wl.shape, mfpsn.SG_OUT[desc.dtype])
+    mfpsn.mfpsn_forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], None, spikes.t, h.t, sg.t)
+    gx = Guarded(wl.shape, mfpsn.GRAD_X[desc.dtype])
+    gw = Guarded((wl.C, wl.k), mfpsn.GRAD_WB[desc.dtype])
+    gb = Guarded((wl.C,), mfpsn.GRAD_WB[desc.dtype])
+    gv = Guarded((wl.C,), mfpsn.GRAD_WB[desc.dtype])
+    ws = Guarded((max(mfpsn.mfpsn_backward_workspace_size(desc), 8),), torch.uint8)
+    mfpsn.mfpsn_backward(desc, dev["x"], dev["grad_spikes"], h.t if saved == "h" else None,
+                         sg.t if saved == "sg" else None, dev["sign"], dev["shift"], dev["bias"], None, gx.t, gw.t,
+                         gb.t, gv.t, ws.t)
+    torch.cuda.synchronize()
+    guards = {"spikes": spikes, "h": h, "sg": sg, "grad_x": gx, "grad_w": gw, "grad_b": gb, "grad_vth": gv,
+              "workspace": ws}
+    return {n: g.t for n, g in guards.items()}, guards
+
+
 @pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_workloads_full_size(orc, wid):
     wl = workloads.WORKLOADS[wid]
     case = workloads.make_inputs(wl)
     dev = {n: to_dev(case[n], wl.dtype if n in ("x", "grad_spikes") else None) for n in case}
     rng = np.random.default_rng(wid)
-    chans = np.sort(rng.choice(wl.C, size=min(wl.C, 6), replace=False))
+    chans = sampled_channels(wl.C, rng)
     chans_t = torch.from_numpy(chans).to(DEV)
+    sub = {"x": np.ascontiguousarray(case["x"][:, :, chans]),
+           "grad_spikes": np.ascontiguousarray(case["grad_spikes"][:, :, chans]),
+           "sign": case["sign"][chans], "shift": case["shift"][chans], "bias": case["bias"][chans]}
     for d in wl.dilations:
         desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
                                wl.s_max)
-        spikes, h, sg = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True,
-                                      want_sg=True)
-        # the backward recomputes H, or reads the saved factor or the saved H,
-        # by dilation
-        saved = (None, "sg", "h")[d % 3]
-        gx, gw, gb = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"], dev["bias"],
-                                    sg=sg if saved == "sg" else None, h=h if saved == "h" else None)
-        torch.cuda.synchronize()
-        got = {"spikes": spikes.index_select(2, chans_t).cpu().numpy(),
-               "H": h.index_select(2, chans_t).cpu().numpy(),
-               "SG": sg.index_select(2, chans_t).cpu().numpy(),
-               "grad_w": gw.index_select(0, chans_t).cpu().numpy(),
-               "grad_b": gb.index_select(0, chans_t).cpu().numpy()}
-        gxs = gx.index_select(2, chans_t)
-        if wl.dtype == "bf16":
-            got["grad_x_bits"] = gxs.view(torch.int16).cpu().numpy().view(np.uint16)
-        else:
-            got["grad_x"] = gxs.cpu().numpy()
-        sub = {"x": np.ascontiguousarray(case["x"][:, :, chans]),
-               "grad_spikes": np.ascontiguousarray(case["grad_spikes"][:, :, chans]),
-               "sign": case["sign"][chans], "shift": case["shift"][chans], "bias": case["bias"][chans]}
         ref = oracle_run(orc, sub, wl.k, d, wl.dtype, wl.v_th, wl.surrogate, wl.alpha, 0, wl.s_max, wl.v_th_q)
-        compare(got, ref, wl.dtype, f"{wl.name} d={d}", wl.k, d, hi=wl.s_max)
-        del spikes, h, sg, gx, gw, gb
+        # the backward recomputes H, or reads the saved factor or the saved H:
+        # all three at the first dilation, one by rotation at the others
+        modes = [None, "sg", "h"] if d == wl.dilations[0] else [(None, "sg", "h")[d % 3]]
+        for saved in modes:
+            out, guards = run_guarded(wl, desc, dev, saved)
+            for name, g in guards.items():
+                assert g.intact(), f"{wl.name} d={d} saved={saved}: guard zone of {name} overwritten"
+            got = {"spikes": out["spikes"].index_select(2, chans_t).cpu().numpy(),
+                   "H": out["h"].index_select(2, chans_t).cpu().numpy(),
+                   "SG": out["sg"].index_select(2, chans_t).cpu().numpy(),
+                   "grad_w": out["grad_w"].index_select(0, chans_t).cpu().numpy(),
+                   "grad_b": out["grad_b"].index_select(0, chans_t).cpu().numpy(),
+                   "grad_vth": out["grad_vth"].index_select(0, chans_t).cpu().numpy()}
+            gxs = out["grad_x"].index_select(2, chans_t)
+            if wl.dtype == "bf16":
+                got["grad_x_bits"] = gxs.view(torch.int16).cpu().numpy().view(np.uint16)
+            else:
+                got["grad_x"] = gxs.cpu().numpy()
+            compare(got, ref, wl.dtype, f"{wl.name} d={d} saved={saved}", wl.k, d, hi=wl.s_max)
+            del out, guards
+
+
+@pytest.mark.parametrize("wid", [2, 3, 4, 5])
+def test_workloads_full_size_time_last(wid):
+    # the time-last entry points at full size and every dilation, against the
+    # time-first ones on the same inputs (which the test above pins to the
+    # oracle): spikes, H and grad_x bit for bit on every element, grad_w and
+    # grad_b to the double-sum bar
+    wl = workloads.WORKLOADS[wid]
+    case = workloads.make_inputs(wl)
+    dev = {n: to_dev(case[n], wl.dtype if n in ("x", "grad_spikes") else None) for n in case}
+    perm = (1, 2) + tuple(range(3, len(wl.shape))) + (0,)
+    back = (len(wl.shape) - 1,) + tuple(range(len(wl.shape) - 1))
+    x_tl = dev["x"].permute(perm).contiguous()
+    g_tl = dev["grad_spikes"].permute(perm).contiguous()
+    for d in wl.dilations:
+        desc = mfpsn.make_desc(wl.shape, wl.k, d, wl.dtype, wl.surrogate, wl.alpha, wl.v_th, wl.v_th_q, 0,
+                               wl.s_max)
+        spk_tf, h_tf = mfpsn.forward(desc, dev["x"], dev["sign"], dev["shift"], dev["bias"], want_h=True)
+        gx_tf, gw_tf, gb_tf = mfpsn.backward(desc, dev["x"], dev["grad_spikes"], dev["sign"], dev["shift"],
+                                             dev["bias"])
+        spk_tl, h_tl = mfpsn.forward_time_last(desc, x_tl, dev["sign"], dev["shift"], dev["bias"], want_h=True)
+        gx_tl, gw_tl, gb_tl = mfpsn.backward_time_last(desc, x_tl, g_tl, dev["sign"], dev["shift"], dev["bias"])
+        torch.cuda.synchronize()
+        label = f"{wl.name} d={d}"
+        assert torch.equal(spk_tl.permute(back), spk_tf), f"{label}: time-last spikes differ"
+        assert torch.equal(h_tl.permute(back).view(torch.int32), h_tf.view(torch.int32)), f"{label}: H differs"
+        ix = torch.int16 if gx_tf.element_size() == 2 else torch.int32
+        assert torch.equal(gx_tl.permute(back).view(ix), gx_tf.view(ix)), f"{label}: time-last grad_x differs"
+        for a, b, name in ((gw_tl, gw_tf, "grad_w"), (gb_tl, gb_tf, "grad_b")):
+            if wl.dtype == "q8_8":
+                assert torch.equal(a, b), f"{label}: {name} differs"
+            else:
+                a64, b64 = a.double().cpu().numpy(), b.double().cpu().numpy()
+                assert np.all(np.abs(a64 - b64) <= 2 * (GW_ABS + GW_REL * np.abs(b64))), f"{label}: {name}"
+        del spk_tf, h_tf, gx_tf, spk_tl, h_tl, gx_tl
