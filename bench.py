@@ -94,6 +94,16 @@ def committed_counters(wl_name, mode):
 
 
 def cpu_model() -> str:
+    """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
+    import subprocess
+
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.strip().startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
@@ -579,11 +589,12 @@ class Flush:
     BYTES = 1 << 30
 
     def __init__(self, torch, dev):
+        self.torch = torch
         self.buf = torch.ones(self.BYTES // 4, dtype=torch.int32, device=dev)
         self.acc = torch.zeros((), dtype=torch.int64, device=dev)
 
     def __call__(self):
-        self.acc += self.buf.sum(dtype=torch.int64)
+        self.acc += self.buf.sum(dtype=self.torch.int64)
 
 
 def measure(torch, dev, wl, mode, steps: int, warmup: int, flush, hev):

@@ -88,6 +88,12 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // SIMD; the backward's halo is k-1 steps of work, so it stops at 2.
 constexpr int64_t kFwdTargetItems = 8192;
 constexpr int64_t kBwdTargetItems = 2048;
+// Waves take every nw-th item rather than a contiguous range, so the waves
+// that run at the same time walk neighbouring tiles (see ItemRange in the
+// kernels).
+constexpr bool kStridedItems = true;
+// Items of one group (channel or channel group) are counted in 31 bits.
+constexpr int64_t kMaxItems = ((int64_t)1 << 31) - 1;
 
 // Two adjacent columns per lane (one 2x-wide access per stream and step):
 // plane mode with an even S (a lane's two positions share one row of S
@@ -165,7 +171,10 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
     // fewer items than the target (or a class spans too many bytes).
     const int64_t K = d->k;
     const int64_t class_len = d->T > 0 ? ceil_div(d->T, d->dilation) : 0;
-    const int64_t base = (int64_t)g.groups * g.tiles * g.d;
+    // residue classes that hold a step: d, or T when the dilation exceeds the
+    // sequence (classes r >= T are empty)
+    g.ncls = d->dilation < d->T ? d->dilation : (d->T > 0 ? d->T : 1);
+    const int64_t base = (int64_t)g.groups * g.tiles * g.ncls;
     const int64_t cap = max_chunk(d);
     int64_t chunk = ceil_div(class_len > 0 ? class_len : 1, K) * K;
     if (chunk > cap)
@@ -182,7 +191,8 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
         nchunks = 1;
     g.chunk = (int32_t)chunk;
     g.nchunks = (int32_t)nchunks;
-    g.items = (int64_t)g.tiles * g.d * g.nchunks;
+    g.items = (int64_t)g.tiles * g.ncls * g.nchunks;
+    g.strided = kStridedItems ? 1 : 0;
     // upper bound of the persistent grid (the launcher picks the actual size)
     int64_t blocks = ceil_div(kMaxResidentBlocks, g.groups);
     const int64_t need = ceil_div(g.items, kWaves);
@@ -256,6 +266,8 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
         return MFPSN_OK;
     FwdArgs a;
     a.g = plan(desc, false, pair_layout(desc) && pair_aligned({x, spikes, h_out, sg_out}) ? 2 : 1);
+    if (a.g.items > kMaxItems)
+        return MFPSN_ERR_SHAPE;
     a.x = x;
     a.sign = sign;
     a.shift = shift;
@@ -277,6 +289,8 @@ int mfpsn_backward_workspace_size(const mfpsn_desc* desc, size_t* bytes)
     if (!bytes)
         return MFPSN_ERR_NULL;
     const int64_t total = (int64_t)desc->T * desc->N * desc->C * desc->S;
+    if (total > 0 && (plan(desc, true, 1).items > kMaxItems || plan(desc, true, 2).items > kMaxItems))
+        return MFPSN_ERR_SHAPE;
     *bytes = total > 0 ? backward_workspace(desc) : 0;
     return MFPSN_OK;
 }
@@ -308,6 +322,8 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
     }
     BwdArgs a;
     a.g = plan(desc, true, pair_layout(desc) && pair_aligned({x, grad_spikes, h, sg, grad_x}) ? 2 : 1);
+    if (total > 0 && a.g.items > kMaxItems)
+        return MFPSN_ERR_SHAPE;
     const size_t need = total > 0 ? backward_workspace(desc) : 0;
     if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
         return MFPSN_ERR_WORKSPACE;

@@ -139,8 +139,28 @@ __device__ __forceinline__ void forward_walk(const BnGeom& g, const WalkItem& it
         }
 }
 
-// statistics partials: thread t's sums of Tv and Tv^2 over the steps of
-// all its items (one channel), written to part[t] and part[G + t]
+// The shift of channel c's statistics: Tv of the channel's last time step at
+// its first column (n = 0, s = 0), taps in ascending order.  Every element of
+// the channel is summed as Tv - pivot, so the variance comes from sums of
+// deviations from a value near the mean instead of the difference of two
+// large sums (which would cancel when |mean| >> standard deviation).
+__device__ __forceinline__ double pivot_tv(const BnGeom& g, const float* __restrict__ x,
+                                           const float* __restrict__ w, int c)
+{
+    const int t = g.T - 1;
+    const size_t col = (size_t)c * g.S;
+    double acc = 0.0;
+    for (int i = 0; i < g.k; ++i) {
+        const int64_t tau = (int64_t)t - (int64_t)(g.k - 1 - i) * g.d;
+        if (tau >= 0)
+            acc = __builtin_fma((double)w[(size_t)c * g.k + i], (double)x[(size_t)tau * g.M + col], acc);
+    }
+    return acc;
+}
+
+// statistics partials: thread t's sums of Tv - pivot and (Tv - pivot)^2 over
+// the steps of all its items (one channel), written to part[t] and
+// part[G + t]
 template <int K>
 __global__ __launch_bounds__(kBnThreads) void bn_stats_walk(BnGeom g, const float* __restrict__ x,
                                                             const float* __restrict__ w, double* __restrict__ part)
@@ -152,9 +172,11 @@ __global__ __launch_bounds__(kBnThreads) void bn_stats_walk(BnGeom g, const floa
         if (it.j1 > it.j0) {
             double wd[K], ring[K];
             load_weights<K>(w + (size_t)it.c * K, wd);
+            const double p = pivot_tv(g, x, w, it.c);
             forward_walk<K>(g, it, x, wd, ring, [&](double v, int) {
-                s1 = s1 + v;
-                s2 = __builtin_fma(v, v, s2);
+                const double e = v - p;
+                s1 = s1 + e;
+                s2 = __builtin_fma(e, e, s2);
             });
         }
     }
@@ -198,6 +220,7 @@ __device__ __forceinline__ double channel_sum(const BnGeom& g, const double* __r
 
 // one block per channel: the sums, the statistics and the fusion
 __global__ __launch_bounds__(kBnThreads) void bn_fuse(BnGeom g, const double* __restrict__ inter,
+                                                      const float* __restrict__ x,
                                                       const float* __restrict__ w, const float* __restrict__ gamma,
                                                       const float* __restrict__ beta, float eps,
                                                       float* __restrict__ w_f, float* __restrict__ b_f,
@@ -205,12 +228,14 @@ __global__ __launch_bounds__(kBnThreads) void bn_fuse(BnGeom g, const double* __
 {
     __shared__ double red[kBnThreads];
     for (int c = blockIdx.x; c < g.C; c += gridDim.x) {
-        const double s1 = channel_sum(g, inter, 0, c, red);
-        const double s2 = channel_sum(g, inter, 1, c, red);
+        const double s1 = channel_sum(g, inter, 0, c, red);  // sum of Tv - pivot
+        const double s2 = channel_sum(g, inter, 1, c, red);  // sum of (Tv - pivot)^2
         if (threadIdx.x == 0) {
             const double nc = (double)g.T * g.N * g.S;
-            const double mu = s1 / nc;
-            double var = s2 / nc - mu * mu;
+            const double p = nc > 0 ? pivot_tv(g, x, w, c) : 0.0;
+            const double dm = nc > 0 ? s1 / nc : 0.0;  // mean - pivot
+            const double mu = p + dm;
+            double var = nc > 0 ? s2 / nc - dm * dm : 0.0;
             var = var > 0.0 ? var : 0.0;
             const double inv = 1.0 / sqrt(var + (double)eps);
             const double sc = (double)gamma[c] * inv;
@@ -222,8 +247,9 @@ __global__ __launch_bounds__(kBnThreads) void bn_fuse(BnGeom g, const double* __
             aux[4 * (size_t)c + 2] = sc;
             aux[4 * (size_t)c + 3] = inv;
             if (stats != nullptr) {
-                stats[2 * (size_t)c + 0] = s1;
-                stats[2 * (size_t)c + 1] = s2;
+                // sum Tv and sum Tv^2 from the shifted sums
+                stats[2 * (size_t)c + 0] = nc * p + s1;
+                stats[2 * (size_t)c + 1] = s2 + 2.0 * p * s1 + nc * p * p;
             }
         }
     }
@@ -427,7 +453,7 @@ hipError_t launch_bn_forward_stats(const BnGeom& g, const float* x, const float*
     stats_dispatch(g, x, w, ws.part, st, BnOrders{});
     hipLaunchKernelGGL(bn_rows, dim3(grid_for((size_t)2 * g.NG * g.S * g.C)), dim3(kBnThreads), 0, st, g, 2, ws.part,
                        ws.inter);
-    hipLaunchKernelGGL(bn_fuse, dim3(blocks_for(g.C)), dim3(kBnThreads), 0, st, g, ws.inter, w, gamma, beta, eps,
+    hipLaunchKernelGGL(bn_fuse, dim3(blocks_for(g.C)), dim3(kBnThreads), 0, st, g, ws.inter, x, w, gamma, beta, eps,
                        w_f, b_f, aux, stats);
     return hipGetLastError();
 }

@@ -30,12 +30,15 @@ struct Geom {
                        // within each row (0: tiles run over the flattened (n, s) plane)
     int32_t line_elems;// elements per 128-byte line (128 / esize)
     int32_t tq, tr;    // T = tq * d + tr
+    int32_t ncls;      // residue classes with a step: min(d, T) (at least 1)
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk
     int32_t groups;    // gridDim.y: channel groups (lane-channel) or channels (plane)
     int32_t blocks;    // gridDim.x: blocks per group (set by the launcher; the
                        // planner's value is the upper bound the workspace is sized for)
-    int64_t items;     // items per group = tiles * d * nchunks
+    int64_t items;     // items per group = tiles * d * nchunks (< 2^31)
+    int32_t strided;   // 1: wave w takes items w, w + nw, ... (nw waves per group);
+                       // 0: a contiguous range of items
     uint32_t M;        // N*C*S, columns per time step
     int32_t esize;     // bytes per stored element of x / grad_spikes
     int32_t shift_lo, shift_hi;

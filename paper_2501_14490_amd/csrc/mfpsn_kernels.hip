@@ -107,6 +107,16 @@ constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
 constexpr int kBwdPrefetchHighK = MFPSN_BWD_PREFETCH_HIGH_K;  // orders 24 and up
 constexpr int kBwdPairBytes = MFPSN_BWD_PAIR_BYTES;  // plane mode, two columns per lane
 
+// What the scheduler may move across the end of a step (the mask of
+// __builtin_amdgcn_sched_barrier): 0 keeps every instruction in its step, so
+// no later step's loads are hoisted and held in registers for a whole block.
+#ifndef MFPSN_FWD_STEP_BARRIER
+#define MFPSN_FWD_STEP_BARRIER 0
+#endif
+#ifndef MFPSN_BWD_STEP_BARRIER
+#define MFPSN_BWD_STEP_BARRIER 0
+#endif
+
 // Highest order built with unguarded full blocks (higher orders walk only
 // guarded blocks: smaller code, a few scalar instructions more per step).
 #ifndef MFPSN_FULL_BLOCK_MAX_K
@@ -482,8 +492,37 @@ __device__ __forceinline__ bool any_slow(const Pk<int32_t, NV>&, const Geom&)
     return false;
 }
 
+// Q8.8 charge of one column: start + sum_i ((x_i >> s_i) ^ m_i), an exact
+// integer sum, so it may be split into kQ88Sums independent partial sums
+// (taps i, i + kQ88Sums, ...) that the hardware can issue interleaved; each
+// partial sum is pinned, so it stays one shift and one xor-add per tap.
+#ifndef MFPSN_Q88_SUMS
+#define MFPSN_Q88_SUMS 1
+#endif
+constexpr int kQ88Sums = MFPSN_Q88_SUMS;
+template <int K, typename TP, typename X>
+__device__ __forceinline__ int32_t q88_charge(const TP& tp, int32_t start, X x)
+{
+    constexpr int NS = kQ88Sums < K ? kQ88Sums : K;
+    int32_t part[NS];
+#pragma unroll
+    for (int p = 0; p < NS; ++p)
+        part[p] = p == 0 ? start : 0;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        part[i % NS] = part[i % NS] + tp.apply(x(i), i);
+        pin(part[i % NS]);
+    }
+    int32_t acc = part[0];
+#pragma unroll
+    for (int p = 1; p < NS; ++p)
+        acc += part[p];
+    return acc;
+}
+
 // ---------------------------------------------------------------------------
-// items.  Item q of a group: q = (tile * d + r) * nchunks + chunk.
+// items.  Item q of a group: q = (tile * ncls + r) * nchunks + chunk, over
+// the ncls = min(d, T) residue classes that hold a step.
 // Lane -> column.  Lane-channel tiles: 64 consecutive channels of one sample.
 // Plane tiles: 64 consecutive positions p = n*S + s of one channel's (n, s)
 // plane.  A lane whose column does not exist reads and writes the column of
@@ -492,21 +531,53 @@ __device__ __forceinline__ bool any_slow(const Pk<int32_t, NV>&, const Geom&)
 // ---------------------------------------------------------------------------
 struct Cursor {
     int tile, r, chunk;
-    __device__ Cursor(const Geom& g, int64_t q)
+    __device__ Cursor(const Geom& g, int64_t q) { set(g, q); }
+    __device__ void set(const Geom& g, int64_t q)
     {
-        chunk = (int)(q % g.nchunks);
-        q /= g.nchunks;
-        r = (int)(q % g.d);
-        tile = (int)(q / g.d);
+        const uint32_t u = (uint32_t)q;  // items per group < 2^31 (planner)
+        const uint32_t rc = u / (uint32_t)g.nchunks;
+        chunk = (int)(u - rc * (uint32_t)g.nchunks);
+        const uint32_t t = rc / (uint32_t)g.ncls;
+        r = (int)(rc - t * (uint32_t)g.ncls);
+        tile = (int)t;
     }
     __device__ void next(const Geom& g)
     {
         if (++chunk == g.nchunks) {
             chunk = 0;
-            if (++r == g.d) {
+            if (++r == g.ncls) {
                 r = 0;
                 ++tile;
             }
+        }
+    }
+    // to item q of a walk with item step `step` (1: the next item)
+    __device__ void advance(const Geom& g, int64_t q, int64_t step)
+    {
+        if (step == 1)
+            next(g);
+        else
+            set(g, q);
+    }
+};
+
+// The items of a wave: a contiguous range [q0, q1) (strided = 0), or every
+// nw-th item from its wave index (strided = 1), so that the waves running
+// at the same time walk neighbouring tiles and their accesses at each step
+// fall into a few contiguous stretches of memory instead of being spread over
+// the whole tensor.  Either way the waves' item counts differ by at most one.
+struct ItemRange {
+    int64_t q0, q1, step;
+    __device__ ItemRange(const Geom& g, int wid, int nw)
+    {
+        if (g.strided) {
+            q0 = wid;
+            q1 = g.items;
+            step = nw;
+        } else {
+            q0 = g.items * wid / nw;
+            q1 = g.items * (wid + 1) / nw;
+            step = 1;
         }
     }
 };
@@ -576,8 +647,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const int grp = blockIdx.y;
     const int wid = (int)blockIdx.x * kWaves + uniform((int)threadIdx.x >> 6);
     const int nw = (int)gridDim.x * kWaves;
-    const int64_t q0 = g.items * wid / nw;
-    const int64_t q1 = g.items * (wid + 1) / nw;
+    const ItemRange range(g, wid, nw);
+    const int64_t q0 = range.q0, q1 = range.q1, qstep = range.step;
     Surrogate sg;
     sg.init(g.sg, g.alpha);
     __shared__ int32_t qtab[kF ? 1 : kQTable];
@@ -625,7 +696,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     Cursor cur(g, q0);
     int tile_cached = -1;
     Cols cols{};
-    for (int64_t q = q0; q < q1; ++q, cur.next(g)) {
+    for (int64_t q = q0; q < q1; q += qstep, cur.advance(g, q, qstep)) {
         // item scalars, pinned to SGPRs
         const int r = uniform(cur.r);
         const int Lr = uniform(class_len(g, r));
@@ -718,13 +789,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                 for (int e = 0; e < NV; ++e) {
                     // (pinned partial sums: one shift and one xor-add per tap,
                     // instead of the reassociated shift, xor, add3 sequence)
-                    V acc = start;
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        acc = acc + tp.apply(ring[(u + 1 + i) % K].v[e], i);
-                        pin(acc);
-                    }
-                    h.v[e] = acc;
+                    h.v[e] = q88_charge<K>(tp, start, [&](int i) { return ring[(u + 1 + i) % K].v[e]; });
                     spk |= (h.v[e] >= vthq ? 1u : 0u) << (8 * e);
                 }
             }
@@ -748,7 +813,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             }
             advance(so_s, sstep);
             advance(so_h, hstep);
-            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_sched_barrier(MFPSN_FWD_STEP_BARRIER);
         };
         auto block = [&](int jb0, auto kc_) __attribute__((always_inline)) {
             constexpr int kind = decltype(kc_)::value;
@@ -829,8 +894,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     const int grp = blockIdx.y;
     const int wid = (int)blockIdx.x * kWaves + wave;
     const int nw = (int)gridDim.x * kWaves;
-    const int64_t q0 = g.items * wid / nw;
-    const int64_t q1 = g.items * (wid + 1) / nw;
+    const ItemRange range(g, wid, nw);
+    const int64_t q0 = range.q0, q1 = range.q1, qstep = range.step;
     const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
 
     TP tp;
@@ -884,7 +949,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     Cursor cur(g, q0);
     int tile_cached = -1;
     Cols cols{};
-    for (int64_t q = q0; q < q1; ++q, cur.next(g)) {
+    for (int64_t q = q0; q < q1; q += qstep, cur.advance(g, q, qstep)) {
         // item scalars, pinned to SGPRs
         const int r = uniform(cur.r);
         const int Lr = uniform(class_len(g, r));
@@ -1048,13 +1113,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                     } else {
 #pragma unroll
                         for (int e = 0; e < NV; ++e) {
-                            V acc = start;
-#pragma unroll
-                            for (int i = 0; i < K; ++i) {
-                                acc = acc + tp.apply(xf[(sj + 1 + i) % K].v[e], i);
-                                pin(acc);
-                            }
-                            h.v[e] = acc;
+                            h.v[e] = q88_charge<K>(tp, start, [&](int i) { return xf[(sj + 1 + i) % K].v[e]; });
                         }
                     }
 #pragma unroll
@@ -1133,7 +1192,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             advance(so_gx, -gxstep);
             // keep the scheduler from hoisting later steps' loads above this
             // step (which would hold them in registers for a whole block)
-            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_sched_barrier(MFPSN_BWD_STEP_BARRIER);
         };
         auto block = [&](int b, auto kc_) __attribute__((always_inline)) {
             constexpr int kind = decltype(kc_)::value;

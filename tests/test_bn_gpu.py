@@ -173,3 +173,68 @@ def test_bn_autograd_function_equals_the_stages(orc):
     for got, want in ((xt.grad, staged["grad_x"]), (wt.grad, staged["grad_w"]), (gt.grad, staged["grad_gamma"]),
                       (bt.grad, staged["grad_beta"])):
         assert torch.equal(got, want)
+
+
+@pytest.mark.parametrize("d", [1, 4])
+def test_bn_variance_when_the_mean_dwarfs_the_spread(orc, d):
+    """The whole audio-spike layer with inputs around 3000 and a dominant
+    "now" tap, so that every channel's |mu|/sigma of Tv is at least 10^3: the
+    variance (and s, W_f, b_f after it) must still match the oracle's
+    two-pass variance within 1e-9 relative."""
+    T, N, C, S, k = 250, 256, 512, 1, 16
+    rng = np.random.default_rng(500 + d)
+    x = (3000.0 + rng.normal(0.0, 1.0, (T, N, C))).astype(np.float32)
+    w = rng.normal(0.0, 1e-4, (C, k)).astype(np.float32)
+    w[:, k - 1] = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    gamma = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    beta = rng.normal(-1.0, 0.3, C).astype(np.float32)
+    desc = mfpsn.make_desc(x.shape, k, d, "f32", "sigmoid", 4.0, 0.0, 0, 0, 7)
+    ws = mfpsn.bn_workspace(desc, DEV)
+    w_f, b_f, aux, stats = mfpsn.bn_forward_stats(desc, dev(x), dev(w), dev(gamma), dev(beta), EPS, ws,
+                                                  want_stats=True)
+    torch.cuda.synchronize()
+    ch = np.array([0, 1, 63, 64, 200, 383, 384, 511])
+    ref = orc.bn_forward_stats(np.ascontiguousarray(x[:, :, ch]), w[ch], gamma[ch], beta[ch], EPS, k, d)
+    ratio = np.abs(ref["aux"][:, 0]) / np.sqrt(ref["aux"][:, 1])
+    assert np.all(ratio >= 1e3), ratio
+    a = aux.cpu().numpy()[ch]
+    rel_close(a[:, 0], ref["aux"][:, 0], 1e-12)
+    rel_close(a[:, 1], ref["aux"][:, 1], 1e-9)
+    rel_close(a[:, 2:], ref["aux"][:, 2:], 1e-9)
+    rel_close(stats.cpu().numpy()[ch], ref["stats"], 1e-12)
+    rel_close(w_f.cpu().numpy()[ch], ref["w_f"], 1e-6)
+    rel_close(b_f.cpu().numpy()[ch], ref["b_f"], 1e-6, 1e-5)
+
+
+def test_bn_step_from_raw_inputs_on_both_sides(orc):
+    """The whole fused step from the same raw x, W, gamma, beta and
+    grad_spikes on both sides (each side quantizes its own W_f and fires on
+    its own b_f): spikes equal except where the oracle's potential lies
+    within 1e-5 of the threshold, gradients within the float tolerance."""
+    T, N, C, S, k, d = 24, 4, 70, 1, 5, 2
+    x, w, gamma, beta, g = make_case(T, N, C, S, k, seed=901)
+    desc = mfpsn.make_desc(x.shape, k, d, "f32", "sigmoid", 4.0, 0.0, 0, 0, 7)
+    xt = dev(x)
+    ws = mfpsn.bn_workspace(desc, DEV)
+    w_f, b_f, aux = mfpsn.bn_forward_stats(desc, xt, dev(w), dev(gamma), dev(beta), EPS, ws)
+    sign, shift = mfpsn.quantize(w_f, 0, 7)
+    spikes, sg = mfpsn.forward(desc, xt, sign, shift, b_f, want_sg=True)
+    gx, gwf, gbf = mfpsn.backward(desc, xt, dev(g), sign, shift, b_f, sg=sg)
+    grad_w, grad_gamma, grad_beta = mfpsn.bn_backward(desc, xt, dev(w), aux, gwf, gbf, gx, EPS, ws)
+    torch.cuda.synchronize()
+    # the oracle, from the raw inputs only
+    ref = orc.bn_forward_stats(x, w, gamma, beta, EPS, k, d)
+    s_o, sh_o = orc.quantize(ref["w_f"], 0, 7)
+    H, S_o = orc.forward_f32(x, s_o, sh_o, ref["b_f"], k, d, 0.0, 0, 7)
+    b = orc.backward_f32(x, g, s_o, sh_o, ref["b_f"], k, d, 0.0, "sigmoid", 4.0, 0, 7)
+    gwf_o = b["grad_w"].astype(np.float32).astype(np.float64)
+    gbf_o = b["grad_b"].astype(np.float32).astype(np.float64)
+    rb = orc.bn_backward(x, w, gamma, EPS, ref["aux"], gwf_o, gbf_o, b["grad_x"].astype(np.float64), k, d)
+    assert np.array_equal(sign.cpu().numpy(), s_o) and np.array_equal(shift.cpu().numpy(), sh_o)
+    near = np.abs(H) < 1e-5
+    got_s = spikes.cpu().numpy()
+    assert np.array_equal(got_s[~near], S_o[~near])
+    rel_close(gx.cpu().numpy(), rb["grad_x"], 1e-5, 1e-6)
+    rel_close(grad_w.cpu().numpy(), rb["grad_w"], 1e-5, 1e-6)
+    rel_close(grad_gamma.cpu().numpy(), rb["grad_gamma"], 1e-5, 1e-6)
+    rel_close(grad_beta.cpu().numpy(), rb["grad_beta"], 1e-5, 1e-6)
