@@ -168,6 +168,24 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
                    const void* v_th_c, void* grad_x, void* grad_w, void* grad_b, void* grad_vth,
                    void* workspace, size_t workspace_bytes, void* stream);
 
+/* mfpsn_backward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments and results as mfpsn_backward, without the
+ * workspace arguments.  Its workspace is a fixed array of
+ * MFPSN_NO_ALLOC_WORKSPACE_BYTES of device memory inside the library, one per
+ * GPU, held until the process ends; the call allocates nothing.  Problems
+ * whose mfpsn_backward_workspace_size exceeds that size fail with
+ * MFPSN_ERR_WORKSPACE before anything is launched.  Every word of the array
+ * a call uses is written by that call before it is read, so nothing carries
+ * over between calls; but all calls on one GPU share the array, so calls
+ * that may overlap on one GPU (different streams, or host threads without an
+ * order between their streams) race and must not be issued. */
+#define MFPSN_NO_ALLOC_WORKSPACE_BYTES (64u << 20)
+int mfpsn_backward_no_alloc(const mfpsn_desc* desc, const void* x, const void* grad_spikes, const void* h,
+                            const void* sg, const int8_t* sign, const int8_t* shift, const void* bias,
+                            const void* v_th_c, void* grad_x, void* grad_w, void* grad_b, void* grad_vth,
+                            void* stream);
+
 /* Power-of-two quantizer Q(W) = sign(W) * 2^round(log2|W|) (Sec. 4.2,
  * Eq. round_w), applied elementwise to `count` (< 2^31) floats w (device):
  *   sign  = -1 if w < 0 else +1 (so sign(0) = +1)

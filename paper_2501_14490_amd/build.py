@@ -79,6 +79,10 @@ def _units():
     obj = os.path.join(BUILD, "stream.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", stream_src, "-o", obj],
                   [stream_src, os.path.join(CSRC, "mfpsn_stream.h"), *api_headers]))
+    na_src = os.path.join(CSRC, "mfpsn_noalloc.hip")
+    obj = os.path.join(BUILD, "noalloc.o")
+    units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", na_src, "-o", obj],
+                  [na_src, os.path.join(INCLUDE, "mfpsn.h")]))
     obj = os.path.join(BUILD, "kernels_misc.o")
     units.append((obj, [HIPCC, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-DMFPSN_TU_MISC",
                         "-c", src, "-o", obj], [src, *headers]))

@@ -59,6 +59,8 @@ _lib.mfpsn_backward_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size
 _lib.mfpsn_backward_workspace_size.restype = ctypes.c_int
 _lib.mfpsn_backward.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]
 _lib.mfpsn_backward.restype = ctypes.c_int
+_lib.mfpsn_backward_no_alloc.argtypes = [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.mfpsn_backward_no_alloc.restype = ctypes.c_int
 _lib.mfpsn_quantize_weights.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P]
 _lib.mfpsn_quantize_weights.restype = ctypes.c_int
 _lib.mfpsn_bn_workspace_size.argtypes = [_DP, ctypes.POINTER(ctypes.c_size_t)]
@@ -166,6 +168,14 @@ def mfpsn_backward(desc: MfpsnDesc, x, grad_spikes, h, sg, sign, shift, bias, v_
                                _ptr(shift), _ptr(bias), _ptr(v_th_c), _ptr(grad_x), _ptr(grad_w), _ptr(grad_b),
                                _ptr(grad_vth), _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "mfpsn_backward")
+
+
+def mfpsn_backward_no_alloc(desc: MfpsnDesc, x, grad_spikes, h, sg, sign, shift, bias, v_th_c, grad_x, grad_w,
+                            grad_b, grad_vth, stream=None) -> None:
+    _check(_lib.mfpsn_backward_no_alloc(ctypes.byref(desc), _ptr(x), _ptr(grad_spikes), _ptr(h), _ptr(sg),
+                                        _ptr(sign), _ptr(shift), _ptr(bias), _ptr(v_th_c), _ptr(grad_x),
+                                        _ptr(grad_w), _ptr(grad_b), _ptr(grad_vth), _stream(stream)),
+           "mfpsn_backward_no_alloc")
 
 
 def mfpsn_quantize_weights(w, shift_lo: int, shift_hi: int, sign, shift, stream=None) -> None:
