@@ -88,10 +88,12 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // SIMD; the backward's halo is k-1 steps of work, so it stops at 2.
 constexpr int64_t kFwdTargetItems = 8192;
 constexpr int64_t kBwdTargetItems = 2048;
-// Waves take every nw-th item rather than a contiguous range, so the waves
-// that run at the same time walk neighbouring tiles (see ItemRange in the
-// kernels).
-constexpr bool kStridedItems = true;
+// Waves take contiguous ranges of items.  Taking every nw-th item instead
+// (so that the waves running together walk neighbouring tiles) measured
+// slower on MI355X for three of the four workloads (event vision 215 against
+// 226 G elements/s, long fixed point 123 against 131), and faster only for
+// the sequential-image shape (201 against 195).
+constexpr bool kStridedItems = false;
 // Items of one group (channel or channel group) are counted in 31 bits.
 constexpr int64_t kMaxItems = ((int64_t)1 << 31) - 1;
 

@@ -473,6 +473,24 @@ struct QTable {
         return L;
     }
 };
+// True (this lane) when one of its values is outside the range in which the
+// exponent-add tap is exact.
+template <int NV>
+__device__ __forceinline__ bool lane_slow(const Pk<float, NV>& v, const Geom& g)
+{
+    bool out = false;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        const float m = __builtin_fabsf(v.v[e]);
+        out = out || !(m >= g.fast_lo && m < g.fast_hi);
+    }
+    return out;
+}
+template <int NV>
+__device__ __forceinline__ bool lane_slow(const Pk<int32_t, NV>&, const Geom&)
+{
+    return false;
+}
 // True (wave-uniform) when some lane's value is outside the range in which
 // the exponent-add tap is exact.
 template <int NV>
@@ -725,21 +743,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 #pragma unroll
             for (int e = 0; e < NV; ++e)
                 ring[i].v[e] = V(0);
+        // The halo x[j0-k+1 .. j0-1] (chunks after the first; j0 is a multiple
+        // of k) and x[j0 .. j0+P-1] at prefetch slot j mod P, kept as loaded
+        // (converted in the step that uses them, so no step waits for the
+        // loads it issues itself).  Every load is issued before any value is
+        // looked at: an item starts after one memory round trip.  A halo input
+        // outside the exponent-add range keeps the exact taps on for the steps
+        // whose window holds it.
         if (j0 > 0) {
-            // halo x[j0-k+1 .. j0-1]; j0 is a multiple of k
 #pragma unroll
-            for (int m = 0; m < K - 1; ++m) {
+            for (int m = 0; m < K - 1; ++m)
                 ring[(m + 1) % K] = IO<DT>::template load<NV>(xs, vx, m * xstep);
-                if (TP::kHasFast && any_slow(ring[(m + 1) % K], g))
-                    slow = m + 1;
-            }
         }
-        // x[j] at slot j mod P, as loaded: converted in the step that uses it,
-        // so no step waits for the loads it issues itself
         typename IO<DT>::template Raw<NV> pf[P];
 #pragma unroll
         for (int p = 0; p < P; ++p)
             pf[p] = IO<DT>::template load_raw<NV>(xs, vx, min((j0 + p - jb) * xstep, so_xlast));
+        if constexpr (TP::kHasFast) {
+            if (j0 > 0) {
+#pragma unroll
+                for (int m = 0; m < K - 1; ++m) {
+                    const bool bad = __builtin_amdgcn_ballot_w64(lane_slow(ring[(m + 1) % K], g)) != 0;
+                    slow = bad ? m + 1 : slow;
+                }
+            }
+        }
         int32_t so_xp = (j0 + P - jb) * xstep;  // prefetch of step j + P
         int32_t so_s = 0, so_h = 0;
 
@@ -964,7 +992,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         const bool partial = cols.partial;
         const bool active = cols.active;
         // steps j1..jtop are the halo of a lower chunk: their dH feeds outputs
-        // below j1; the walk starts at the top of jtop's block
+        // below j1; the walk starts at the top of jtop's block (the steps
+        // above jtop only move the loads along)
         const int jtop = uniform(min(j1 + K - 1, Lr) - 1);
         const int jstart = uniform((jtop / K) * K + K - 1);
         const int jb = uniform(max(0, j0 - (K - 1) - P));  // lowest row any stream touches
@@ -997,20 +1026,6 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         Pk<double, NV> xd[kXD ? K : 1];
         PV xf[kXV ? K : 1];
         int slow_x = 0;  // live steps left on the exact recompute path
-#pragma unroll
-        for (int m = 0; m < K - 1; ++m) {
-            const int t = jstart - m;  // slot k-1-m; values past jtop are never used
-            const PV v = IO<DT>::template load<NV>(xs, vx, (min(t, Lr - 1) - jb) * xstep);
-            if constexpr (kXD)
-#pragma unroll
-                for (int e = 0; e < NV; ++e)
-                    xd[K - 1 - m].v[e] = (double)v.v[e];
-            if constexpr (kXV)
-                xf[K - 1 - m] = v;
-            // x[t] (t <= jtop) is in the window of at most k live steps
-            if (kRe && TP::kHasFast && t <= jtop && any_slow(v, g))
-                slow_x = K;
-        }
         // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P, as loaded
         // (converted in the step that uses them)
         typename IO<DT>::template Raw<NV> pg[P], px[P];
@@ -1023,15 +1038,42 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 v.v[e] = __builtin_bit_cast(V, w.v[e]);
             return v;
         };
+        // Preload: the ring's inputs x[jstart-k+2 .. jstart] (slot t mod k;
+        // values past jtop are never used) and the first P steps' streams.
+        // Every load is issued before any value is looked at, so an item
+        // starts after one memory round trip, not one per ring slot.
+        {
+            typename IO<DT>::template Raw<NV> rr[K - 1 > 0 ? K - 1 : 1];
 #pragma unroll
-        for (int p = 0; p < P; ++p) {
-            const int jp = jstart - p;
-            const int js = (K - 1 - p) % P;
-            const int rowg = min(jp, Lr - 1);
-            pg[js] = IO<DT>::template load_raw<NV>(gsb, vx, (rowg - jb) * xstep);
-            if constexpr (HS)
-                ph[js] = load_h((rowg - jb) * hstep);
-            px[js] = IO<DT>::template load_raw<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
+            for (int m = 0; m < K - 1; ++m)
+                rr[m] = IO<DT>::template load_raw<NV>(xs, vx, (min(jstart - m, Lr - 1) - jb) * xstep);
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+                const int jp = jstart - p;
+                const int js = (K - 1 - p) % P;
+                const int rowg = min(jp, Lr - 1);
+                pg[js] = IO<DT>::template load_raw<NV>(gsb, vx, (rowg - jb) * xstep);
+                if constexpr (HS)
+                    ph[js] = load_h((rowg - jb) * hstep);
+                px[js] = IO<DT>::template load_raw<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
+            }
+            bool out = false;  // some live input of this lane outside the exponent-add range
+#pragma unroll
+            for (int m = 0; m < K - 1; ++m) {
+                const PV v = IO<DT>::template cvt<NV>(rr[m]);
+                if constexpr (kXD)
+#pragma unroll
+                    for (int e = 0; e < NV; ++e)
+                        xd[K - 1 - m].v[e] = (double)v.v[e];
+                if constexpr (kXV)
+                    xf[K - 1 - m] = v;
+                // x[t] (t <= jtop) is in the window of at most k live steps
+                if constexpr (kRe && TP::kHasFast)
+                    if (jstart - m <= jtop)
+                        out = out || lane_slow(v, g);
+            }
+            if (kRe && TP::kHasFast && __builtin_amdgcn_ballot_w64(out) != 0)
+                slow_x = K;
         }
         int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
         int32_t so_hp = (jstart - P - jb) * hstep;           // factor or H of step j - P
