@@ -303,8 +303,11 @@ const char* mfpsn_status_string(int status);
 int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t* sign, const int8_t* shift,
                             const void* bias, uint8_t* spikes, void* h_out, void* stream);
 
-/* Bytes of device workspace mfpsn_backward_time_last needs: (k+1)*C
- * 8-byte sums.  Returns a status; *bytes is written on success. */
+/* Bytes of device workspace mfpsn_backward_time_last needs: 8-byte sums,
+ * (k+1)*C of them plus (k+1) per partial-sum slot; the slots are
+ * ceil(N*C*S/64) + N*C when T <= 64, else C plus the segment kernel's
+ * waves (at most 4 * min(ceil(N*C*S*ceil(T/L)/4), 8192), L as below).
+ * Depends on desc only.  Returns a status; *bytes is written on success. */
 int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* bytes);
 
 /* Backward (App. A.3 Eqs. backward_X, backward_W, backward_b, with the taps
@@ -320,8 +323,9 @@ int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* byte
  * sigma'(H - v_th) with the surrogate of mfpsn_backward, and grad_x is the
  * definition's sum over the taps in ascending order, every term included.
  * grad_w and grad_b are sums of exact products in double (int64 for Q8.8)
- * rounded once to float; the double sums are added in an order that can
- * change from call to call (the Q8.8 sums are exact).  Errors as
+ * rounded once to float; the double sums are added in a fixed order for a
+ * given desc and device, so repeated calls give the same bits (the Q8.8
+ * sums are exact).  Errors as
  * mfpsn_backward; MFPSN_ERR_SHAPE also for N*C*S >= 2^37 and, when T > 64,
  * for (k-1)*dilation > 1024 or N*C*S*ceil(T/L) >= 2^33, L = 256 (1024 when
  * (k-1)*dilation > 64).  Asynchronous on `stream`. */

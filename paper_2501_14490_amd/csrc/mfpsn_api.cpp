@@ -114,7 +114,24 @@ bool pair_aligned(std::initializer_list<const void*> ptrs)
     return true;
 }
 
-Geom plan(const mfpsn_desc* d, bool backward, int nv)
+// The flat forward (16- or 8-byte accesses over the flattened rows): an
+// order it is built for, S a multiple of its columns per lane, and tensors
+// aligned for its accesses.
+int flat_layout(const mfpsn_desc* d, const void* x, const void* spikes, const void* h_out, const void* sg_out)
+{
+    const int nv = flat_nv(d->k, d->dtype);
+    if (nv == 0 || d->S % nv != 0)
+        return 0;
+    const uintptr_t wx = (uintptr_t)nv * elem_bytes(d->dtype), ws = (uintptr_t)nv;
+    const uintptr_t ww = 4u * nv < 16u ? 4u * nv : 16u;
+    if (((uintptr_t)x % wx) != 0 || ((uintptr_t)spikes % ws) != 0 || ((uintptr_t)h_out % ww) != 0 ||
+        ((uintptr_t)sg_out % ww) != 0)
+        return 0;
+    return nv;
+}
+
+// flat: the flat forward's columns per lane (0: lane-channel or plane mode)
+Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0)
 {
     Geom g;
     memset(&g, 0, sizeof(g));
@@ -147,7 +164,12 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv)
             g.fast_hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
         }
     }
-    if (d->S == 1 && d->C >= 64) {
+    if (flat > 0) {
+        g.mode = kFlat;
+        g.nv = flat;
+        g.groups = 1;
+        g.tiles = (int32_t)ceil_div((int64_t)g.M, 64 * flat);
+    } else if (d->S == 1 && d->C >= 64) {
         g.mode = kLaneChannel;
         g.nv = 1;
         g.groups = (int32_t)ceil_div(d->C, 64);
@@ -267,7 +289,8 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
     if (total == 0)
         return MFPSN_OK;
     FwdArgs a;
-    a.g = plan(desc, false, pair_layout(desc) && pair_aligned({x, spikes, h_out, sg_out}) ? 2 : 1);
+    a.g = plan(desc, false, pair_layout(desc) && pair_aligned({x, spikes, h_out, sg_out}) ? 2 : 1,
+               flat_layout(desc, x, spikes, h_out, sg_out));
     if (a.g.items > kMaxItems)
         return MFPSN_ERR_SHAPE;
     a.x = x;

@@ -329,6 +329,17 @@ int mfpsn_forward_time_last(const mfpsn_desc* desc, const void* x, const int8_t*
     return MFPSN_OK;
 }
 
+// Workspace of the time-last backward: the [k+1][C] sums, then the
+// partial-sum slots (tl_bwd_slots) of k+1 sums each, 8 bytes per sum.
+static size_t tl_bwd_workspace(const mfpsn_desc* desc)
+{
+    const int64_t M = (int64_t)desc->N * desc->C * desc->S;
+    const int seg = (int64_t)(desc->k - 1) * desc->dilation > 64 ? kTlBwdSegLong : kTlBwdSeg;
+    const int64_t nseg = ((int64_t)desc->T + seg - 1) / seg;
+    const int64_t slots = tl_bwd_slots(M, desc->T, desc->C, desc->N, nseg);
+    return (size_t)(desc->k + 1) * ((size_t)desc->C + (size_t)slots) * 8;
+}
+
 int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* bytes)
 {
     const int st = validate(desc);
@@ -336,7 +347,7 @@ int mfpsn_backward_time_last_workspace_size(const mfpsn_desc* desc, size_t* byte
         return st;
     if (!bytes)
         return MFPSN_ERR_NULL;
-    *bytes = (size_t)(desc->k + 1) * (size_t)desc->C * 8;
+    *bytes = tl_bwd_workspace(desc);
     return MFPSN_OK;
 }
 
@@ -373,7 +384,7 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
         if (reach >= 4611686018427387904.0)
             return MFPSN_ERR_SHAPE;
     }
-    const size_t need = (size_t)(desc->k + 1) * (size_t)desc->C * 8;
+    const size_t need = tl_bwd_workspace(desc);
     if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 8)))
         return MFPSN_ERR_WORKSPACE;
     if (desc->C == 0)
@@ -386,6 +397,7 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
     a.bias = bias;
     a.grad_x = grad_x;
     a.acc = workspace;
+    a.part = (char*)workspace + (size_t)(desc->k + 1) * (size_t)desc->C * 8;
     a.M = M;
     a.T = desc->T;
     a.C = desc->C;
@@ -403,6 +415,7 @@ int mfpsn_backward_time_last(const mfpsn_desc* desc, const void* x, const void* 
     a.vec_x = aligned(x, 4 * es) && aligned(grad_spikes, 4 * es) ? 1 : 0;
     a.seg = seg;
     a.nseg = (int32_t)nseg;
+    a.chunk = 0;
     hipStream_t s = (hipStream_t)stream;
     if (launch_backward_time_last(a, desc->dtype, s) != hipSuccess)
         return MFPSN_ERR_HIP;

@@ -16,16 +16,21 @@ enum Dtype : int32_t { kF32 = 0, kBF16 = 1, kQ88 = 2 };
 //   kPlane (S >= 2, or C < 64): every lane of a block shares one channel c
 //       (taps are wave-uniform); a wave covers 64 consecutive positions
 //       n*S + s of the channel's (n, s) plane.
-enum Mode : int32_t { kLaneChannel = 0, kPlane = 1 };
+//   kFlat (forward, S a multiple of nv): a wave covers 64*nv consecutive
+//       columns of the flattened row of M = N*C*S columns, 16 (or 8) bytes
+//       per lane; every lane loads the taps of its own channel (S % nv == 0
+//       keeps a lane's nv columns in one channel).
+enum Mode : int32_t { kLaneChannel = 0, kPlane = 1, kFlat = 2 };
 
 // Launch geometry, computed on the host by plan() and passed by value.
 struct Geom {
     int32_t T, N, C, S;
     int32_t k, d;
     int32_t mode;
-    int32_t nv;        // adjacent columns per lane: 1, or 2 (plane mode, S even)
+    int32_t nv;        // adjacent columns per lane: 1, or 2 (plane mode, S even), or
+                       // 2, 4, 8 (flat mode)
     int32_t tiles;     // tiles per group: lane-channel N; plane ceil(N*S/(64*nv)),
-                       // or N * row_tiles with line-aligned rows
+                       // or N * row_tiles with line-aligned rows; flat ceil(M/(64*nv))
     int32_t row_tiles; // plane tiles per (n, c) row when tiles follow 128-byte lines
                        // within each row (0: tiles run over the flattened (n, s) plane)
     int32_t line_elems;// elements per 128-byte line (128 / esize)
@@ -33,7 +38,7 @@ struct Geom {
     int32_t ncls;      // residue classes with a step: min(d, T) (at least 1)
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk
-    int32_t groups;    // gridDim.y: channel groups (lane-channel) or channels (plane)
+    int32_t groups;    // gridDim.y: channel groups (lane-channel), channels (plane) or 1 (flat)
     int32_t blocks;    // gridDim.x: blocks per group (set by the launcher; the
                        // planner's value is the upper bound the workspace is sized for)
     int64_t items;     // items per group = tiles * d * nchunks (< 2^31)
@@ -51,6 +56,15 @@ struct Geom {
     // subnormal, infinite, NaN, near-limit) take the exact ldexp path.
     float fast_lo, fast_hi;
 };
+
+// Columns per lane of the flat forward: 16 bytes of x per lane up to order
+// 8, 8 bytes up to order 16 (the ring holds k*nv values per lane); 0: none
+// (higher orders).
+constexpr int flat_nv(int k, int dtype)
+{
+    const int es = dtype == kF32 ? 4 : 2;
+    return k <= 8 ? 16 / es : (k <= 16 ? 8 / es : 0);
+}
 
 constexpr int kWaves = 4;          // waves per block
 constexpr int kPairMaxK = 16;      // highest order with two-column (nv = 2) kernels

@@ -92,6 +92,9 @@ constexpr int prefetch_depth(int K, int cap)
 #ifndef MFPSN_FWD_PREFETCH_F32_PAIR
 #define MFPSN_FWD_PREFETCH_F32_PAIR 2
 #endif
+#ifndef MFPSN_FWD_PREFETCH_WIDE
+#define MFPSN_FWD_PREFETCH_WIDE 4
+#endif
 #ifndef MFPSN_BWD_PREFETCH
 #define MFPSN_BWD_PREFETCH 2
 #endif
@@ -103,6 +106,7 @@ constexpr int prefetch_depth(int K, int cap)
 #endif
 constexpr int kFwdPrefetch = MFPSN_FWD_PREFETCH;
 constexpr int kFwdPrefetchF32Pair = MFPSN_FWD_PREFETCH_F32_PAIR;
+constexpr int kFwdPrefetchWide = MFPSN_FWD_PREFETCH_WIDE;  // 16-byte accesses
 constexpr int kBwdPrefetch = MFPSN_BWD_PREFETCH;
 constexpr int kBwdPrefetchHighK = MFPSN_BWD_PREFETCH_HIGH_K;  // orders 24 and up
 constexpr int kBwdPairBytes = MFPSN_BWD_PAIR_BYTES;  // plane mode, two columns per lane
@@ -159,6 +163,11 @@ __device__ __forceinline__ Buf make_buf(const void* tensor, uint64_t tensor_byte
 #define MFPSN_ST_CPOL 2  // nt: streaming stores
 #endif
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 ld128(Buf b, uint32_t v, int32_t s)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(b.rs, v, s, MFPSN_LD_CPOL);
+}
 __device__ __forceinline__ u32x2 ld64(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b64(b.rs, v, s, MFPSN_LD_CPOL);
@@ -170,6 +179,10 @@ __device__ __forceinline__ uint32_t ld32(Buf b, uint32_t v, int32_t s)
 __device__ __forceinline__ uint16_t ld16(Buf b, uint32_t v, int32_t s)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(b.rs, v, s, MFPSN_LD_CPOL);
+}
+__device__ __forceinline__ void st128(Buf b, uint32_t v, int32_t s, u32x4 x)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 __device__ __forceinline__ void st64(Buf b, uint32_t v, int32_t s, u32x2 x)
 {
@@ -188,9 +201,9 @@ __device__ __forceinline__ void st8(Buf b, uint32_t v, int32_t s, uint8_t x)
     __builtin_amdgcn_raw_buffer_store_b8(x, b.rs, v, s, MFPSN_ST_CPOL);
 }
 
-// The NV adjacent columns a lane holds (NV = 1, or 2 in plane mode when the
-// two columns are neighbours in memory): every stream moves them with one
-// access, so a wave's access covers 64 * NV elements.
+// The NV adjacent columns a lane holds (NV = 1, 2, 4 or 8, neighbours in
+// memory): every stream moves them with one access (two for eight 32-bit
+// words), so a wave's access covers 64 * NV elements.
 template <typename T, int NV> struct Pk {
     T v[NV];
 };
@@ -201,10 +214,19 @@ __device__ __forceinline__ Pk<uint32_t, NV> ld_words(Buf b, uint32_t v, int32_t 
     Pk<uint32_t, NV> r;
     if constexpr (NV == 1) {
         r.v[0] = ld32(b, v, s);
-    } else {
+    } else if constexpr (NV == 2) {
         const u32x2 w = ld64(b, v, s);
         r.v[0] = w.x;
         r.v[1] = w.y;
+    } else {
+#pragma unroll
+        for (int q = 0; q < NV / 4; ++q) {
+            const u32x4 w = ld128(b, v + 16u * q, s);
+            r.v[4 * q] = w.x;
+            r.v[4 * q + 1] = w.y;
+            r.v[4 * q + 2] = w.z;
+            r.v[4 * q + 3] = w.w;
+        }
     }
     return r;
 }
@@ -213,21 +235,83 @@ __device__ __forceinline__ void st_words(Buf b, uint32_t v, int32_t s, const Pk<
 {
     if constexpr (NV == 1) {
         st32(b, v, s, x.v[0]);
-    } else {
+    } else if constexpr (NV == 2) {
         u32x2 w;
         w.x = x.v[0];
         w.y = x.v[1];
         st64(b, v, s, w);
+    } else {
+#pragma unroll
+        for (int q = 0; q < NV / 4; ++q) {
+            u32x4 w;
+            w.x = x.v[4 * q];
+            w.y = x.v[4 * q + 1];
+            w.z = x.v[4 * q + 2];
+            w.w = x.v[4 * q + 3];
+            st128(b, v + 16u * q, s, w);
+        }
     }
 }
-// NV adjacent bytes, byte e in bits 8e..8e+7
+// NV adjacent bytes, byte e in bits 8(e mod 4).. of word e / 4
 template <int NV>
-__device__ __forceinline__ void st_bytes(Buf b, uint32_t v, int32_t s, uint32_t x)
+__device__ __forceinline__ void st_bytes(Buf b, uint32_t v, int32_t s, const uint32_t (&x)[(NV + 3) / 4])
 {
-    if constexpr (NV == 1)
-        st8(b, v, s, (uint8_t)x);
-    else
-        st16(b, v, s, (uint16_t)x);
+    if constexpr (NV == 1) {
+        st8(b, v, s, (uint8_t)x[0]);
+    } else if constexpr (NV == 2) {
+        st16(b, v, s, (uint16_t)x[0]);
+    } else if constexpr (NV == 4) {
+        st32(b, v, s, x[0]);
+    } else {
+        u32x2 w;
+        w.x = x[0];
+        w.y = x[1];
+        st64(b, v, s, w);
+    }
+}
+// 16-bit values packed two to a 32-bit word (bf16, Q8.8): NV values in
+// (NV + 1) / 2 words
+template <int NV>
+__device__ __forceinline__ Pk<uint32_t, (NV + 1) / 2> ld_halves(Buf b, uint32_t v, int32_t s)
+{
+    Pk<uint32_t, (NV + 1) / 2> r;
+    if constexpr (NV == 1) {
+        r.v[0] = ld16(b, v, s);
+    } else if constexpr (NV == 2) {
+        r.v[0] = ld32(b, v, s);
+    } else if constexpr (NV == 4) {
+        const u32x2 w = ld64(b, v, s);
+        r.v[0] = w.x;
+        r.v[1] = w.y;
+    } else {
+        const u32x4 w = ld128(b, v, s);
+        r.v[0] = w.x;
+        r.v[1] = w.y;
+        r.v[2] = w.z;
+        r.v[3] = w.w;
+    }
+    return r;
+}
+template <int NV>
+__device__ __forceinline__ void st_halves(Buf b, uint32_t v, int32_t s, const Pk<uint32_t, (NV + 1) / 2>& x)
+{
+    if constexpr (NV == 1) {
+        st16(b, v, s, (uint16_t)x.v[0]);
+    } else if constexpr (NV == 2) {
+        st32(b, v, s, x.v[0]);
+    } else if constexpr (NV == 4) {
+        u32x2 w;
+        w.x = x.v[0];
+        w.y = x.v[1];
+        st64(b, v, s, w);
+    } else {
+        u32x4 w;
+        w.x = x.v[0];
+        w.y = x.v[1];
+        w.z = x.v[2];
+        w.w = x.v[3];
+        st128(b, v, s, w);
+    }
 }
 
 // s += inc, kept opaque so the compiler keeps one running SGPR per stream
@@ -293,26 +377,21 @@ template <> struct IO<kBF16> {
     using W = double;
     static constexpr int es = 2;
     static constexpr int gx_es = 2;
-    // NV stored values in one 16-bit (NV = 1) or 32-bit (NV = 2) word, widened
-    // only where they are used
-    template <int NV> using Raw = Pk<std::conditional_t<NV == 1, uint16_t, uint32_t>, 1>;
+    // NV stored values packed two to a 32-bit word, widened only where they
+    // are used
+    template <int NV> using Raw = Pk<uint32_t, (NV + 1) / 2>;
     template <int NV>
     __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
     {
-        Raw<NV> w;
-        if constexpr (NV == 1)
-            w.v[0] = ld16(b, v, s);
-        else
-            w.v[0] = ld32(b, v, s);
-        return w;
+        return ld_halves<NV>(b, v, s);
     }
     template <int NV>
     __device__ static Pk<V, NV> cvt(const Raw<NV>& w)
     {
         Pk<V, NV> r;
-        r.v[0] = __builtin_bit_cast(float, (uint32_t)w.v[0] << 16);
-        if constexpr (NV == 2)
-            r.v[1] = __builtin_bit_cast(float, w.v[0] & 0xFFFF0000u);
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            r.v[e] = __builtin_bit_cast(float, e % 2 == 0 ? w.v[e / 2] << 16 : w.v[e / 2] & 0xFFFF0000u);
         return r;
     }
     template <int NV>
@@ -324,13 +403,15 @@ template <> struct IO<kBF16> {
     __device__ static void store_gx(Buf b, uint32_t v, int32_t s, const Pk<V, NV>& x)
     {
         // round to nearest even
-        const uint16_t h0 = __builtin_bit_cast(uint16_t, (__bf16)x.v[0]);
-        if constexpr (NV == 1) {
-            st16(b, v, s, h0);
-        } else {
-            const uint16_t h1 = __builtin_bit_cast(uint16_t, (__bf16)x.v[1]);
-            st32(b, v, s, (uint32_t)h0 | ((uint32_t)h1 << 16));
+        Pk<uint32_t, (NV + 1) / 2> w;
+#pragma unroll
+        for (int q = 0; q < (NV + 1) / 2; ++q) {
+            const uint32_t h0 = __builtin_bit_cast(uint16_t, (__bf16)x.v[2 * q]);
+            w.v[q] = h0;
+            if (2 * q + 1 < NV)
+                w.v[q] |= (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x.v[2 * q + 1]) << 16;
         }
+        st_halves<NV>(b, v, s, w);
     }
 };
 
@@ -339,24 +420,19 @@ template <> struct IO<kQ88> {
     using W = int64_t;
     static constexpr int es = 2;
     static constexpr int gx_es = 4;
-    template <int NV> using Raw = Pk<std::conditional_t<NV == 1, uint16_t, uint32_t>, 1>;
+    template <int NV> using Raw = Pk<uint32_t, (NV + 1) / 2>;
     template <int NV>
     __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
     {
-        Raw<NV> w;
-        if constexpr (NV == 1)
-            w.v[0] = ld16(b, v, s);
-        else
-            w.v[0] = ld32(b, v, s);
-        return w;
+        return ld_halves<NV>(b, v, s);
     }
     template <int NV>
     __device__ static Pk<V, NV> cvt(const Raw<NV>& w)
     {
         Pk<V, NV> r;
-        r.v[0] = (int32_t)(int16_t)w.v[0];
-        if constexpr (NV == 2)
-            r.v[1] = (int32_t)w.v[0] >> 16;
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            r.v[e] = e % 2 == 0 ? (int32_t)(int16_t)w.v[e / 2] : (int32_t)w.v[e / 2] >> 16;
         return r;
     }
     template <int NV>
@@ -610,7 +686,14 @@ template <int MODE, int NV>
 __device__ __forceinline__ Cols tile_cols(const Geom& g, int tile, int grp, int lane)
 {
     Cols t;
-    if (MODE == kLaneChannel) {
+    if (MODE == kFlat) {
+        // columns 64*NV*tile + NV*lane .. + NV-1 of the flattened row (M is a
+        // multiple of NV)
+        const uint32_t pos = (uint32_t)tile * (64u * NV) + (uint32_t)lane * NV;
+        t.active = pos < g.M;
+        t.partial = (uint64_t)tile * (64u * NV) + 64u * NV > g.M;
+        t.col = min(pos, g.M - NV);
+    } else if (MODE == kLaneChannel) {
         const int c = grp * 64 + lane;
         t.active = c < g.C;
         t.partial = false;
@@ -656,9 +739,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     using PV = Pk<V, NV>;
     using TP = Taps<K, DT, MODE>;
     constexpr int es = IO<DT>::es;
-    // 8 steps of x in flight, but 2 for lanes holding two f32 columns (8
-    // bytes per access): the depths measured fastest on MI355X
-    constexpr int P = prefetch_depth(K, (NV == 2 && es == 4) ? kFwdPrefetchF32Pair : kFwdPrefetch);
+    // 8 steps of x in flight, 2 for lanes holding two f32 columns (8 bytes
+    // per access), 4 for 16-byte accesses: the depths measured fastest on
+    // MI355X
+    constexpr int P = prefetch_depth(K, NV * es >= 16               ? kFwdPrefetchWide
+                                        : (NV == 2 && es == 4) ? kFwdPrefetchF32Pair
+                                                               : kFwdPrefetch);
     constexpr bool kF = DT != kQ88;
     const Geom& g = a.g;
     const int lane = threadIdx.x & 63;
@@ -679,29 +765,33 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     if (q0 >= q1)
         return;
-    const int c = (MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp;
 
+    // the lane's channel: taps, bias and threshold (Eq. mfdpsn_fire: V_th[c]
+    // when given, else the one shared by every channel); flat tiles hold
+    // columns of several channels, so they set it per tile
     TP tp;
-    tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
     V bias, start;
-    if constexpr (kF) {
-        const float b = ((const float*)a.bias)[c];
-        bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
-        start = 0.0f;
-    } else {
-        bias = ((const int32_t*)a.bias)[c];
-        start = bias + tp.cneg;
-    }
-    // the channel's threshold (Eq. mfdpsn_fire): V_th[c] when given, else the
-    // one shared by every channel
     float vth = g.v_th;
     int vthq = g.v_th_q;
-    if (a.v_th_c != nullptr) {
-        if constexpr (kF)
-            vth = ((const float*)a.v_th_c)[c];
-        else
-            vthq = ((const int32_t*)a.v_th_c)[c];
-    }
+    auto set_channel = [&](int c) __attribute__((always_inline)) {
+        tp.load(a.sign, a.shift, c, g.shift_lo, g.shift_hi);
+        if constexpr (kF) {
+            const float b = ((const float*)a.bias)[c];
+            bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
+            start = 0.0f;
+        } else {
+            bias = ((const int32_t*)a.bias)[c];
+            start = bias + tp.cneg;
+        }
+        if (a.v_th_c != nullptr) {
+            if constexpr (kF)
+                vth = ((const float*)a.v_th_c)[c];
+            else
+                vthq = ((const int32_t*)a.v_th_c)[c];
+        }
+    };
+    if constexpr (MODE != kFlat)
+        set_channel((MODE == kLaneChannel) ? min(grp * 64 + lane, g.C - 1) : grp);
     const uint32_t M = g.M;
     const int d = g.d;
     const uint64_t xrow = (uint64_t)M * es;
@@ -725,6 +815,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         if (cur.tile != tile_cached) {
             cols = tile_cols<MODE, NV>(g, cur.tile, grp, lane);
             tile_cached = cur.tile;
+            if constexpr (MODE == kFlat)
+                set_channel((int)((cols.col / (uint32_t)g.S) % (uint32_t)g.C));
         }
         // x rows from jb (the halo of a chunk) on; outputs from j0 on
         const int jb = j0 > 0 ? j0 - (K - 1) : 0;
@@ -785,7 +877,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             advance(so_xp, xstep);
             ring[u] = xv;
             PV h;
-            uint32_t spk = 0;  // spike of column e in byte e
+            uint32_t spk[(NV + 3) / 4] = {};  // spike of column e in byte e mod 4 of word e / 4
             if constexpr (kF) {
                 if (any_slow(xv, g))
                     slow = K;
@@ -811,14 +903,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                 }
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
-                    spk |= (h.v[e] >= vth ? 1u : 0u) << (8 * e);
+                    spk[e / 4] |= (h.v[e] >= vth ? 1u : 0u) << (8 * (e % 4));
             } else {
 #pragma unroll
                 for (int e = 0; e < NV; ++e) {
                     // (pinned partial sums: one shift and one xor-add per tap,
                     // instead of the reassociated shift, xor, add3 sequence)
                     h.v[e] = q88_charge<K>(tp, start, [&](int i) { return ring[(u + 1 + i) % K].v[e]; });
-                    spk |= (h.v[e] >= vthq ? 1u : 0u) << (8 * e);
+                    spk[e / 4] |= (h.v[e] >= vthq ? 1u : 0u) << (8 * (e % 4));
                 }
             }
             st_bytes<NV>(ss, vs, so_s, spk);
@@ -1478,8 +1570,22 @@ template <int K, int DT>
 hipError_t fwd_k(FwdArgs& a, hipStream_t st)
 {
     static int cache[3][16];
+    static int cache_flat[16];
     void (*kern)(FwdArgs) = fwd_kernel<K, DT, kLaneChannel, 1>;
     int slot = 0;
+    if (a.g.mode == kFlat) {
+        constexpr int nv = flat_nv(K, DT);
+        if constexpr (nv > 0) {
+            if (a.g.nv != nv)
+                return hipErrorInvalidValue;
+            kern = fwd_kernel<K, DT, kFlat, nv>;
+            a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache_flat), false);
+            hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if (a.g.mode == kPlane) {
         if (a.g.nv == 2) {
             if constexpr (K <= kPairMaxK) {

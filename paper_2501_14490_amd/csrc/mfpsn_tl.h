@@ -13,6 +13,7 @@ constexpr int kTlColsMaxT = 64;             // longest column of the lane-per-co
 constexpr int kTlBwdSeg = 256;              // time steps per segment of the zero-window segment kernels
 constexpr int kTlBwdSegLong = 1024;         // the same for histories (k-1) d above 64
 constexpr int kTlBwdMaxSpan = 1024;         // longest history (k-1) d of the zero-window segment kernels
+constexpr int kTlSegMaxBlocks = 8192;       // most blocks of the persistent segment backward
 
 struct TlArgs {
     const void* x;          // [N][C][S][T] storage type
@@ -47,6 +48,8 @@ struct TlBwdArgs {
     const void* bias;       // float[C] or int32[C]
     void* grad_x;           // [N][C][S][T] float, bfloat16 bits or int32
     void* acc;              // [k+1][C] double (float data) or int64 (Q8.8): grad_w rows, then grad_b
+    void* part;             // [slots][k+1] of the same type: each block's (T <= kTlColsMaxT) or
+                            // wave's sums of one group of columns, at slot (block or wave) + group
     int64_t M;              // columns, N*C*S
     int32_t T, C, S, k, d;
     int32_t shift_lo, shift_hi;
@@ -59,18 +62,41 @@ struct TlBwdArgs {
     int32_t vec_x;          // x and g aligned for 4-element vector loads
     int32_t seg;            // time steps per segment (T > kTlColsMaxT): kTlBwdSeg or kTlBwdSegLong
     int32_t nseg;           // segments per column, ceil(T / seg)
+    int64_t chunk;          // segments per wave of the segment backward (set by its launcher)
 };
 
-// Zeroes acc, runs the backward, which adds into acc; the caller finalizes
-// acc into grad_w and grad_b.
+// Slots of partial sums the backward writes to TlBwdArgs::part.  The columns
+// fall into groups whose sums are wanted (the (n, c) rows of S columns for
+// T <= kTlColsMaxT, whose blocks take 64 columns each; the channels' runs
+// of N*S*nseg segments for the segment kernel, whose waves take `chunk`
+// segments each).  Both cut the same sequence into consecutive pieces, so
+// the (block, group) pairs that share a column have distinct sums block +
+// group, fewer than blocks + groups.
+inline int64_t tl_bwd_slots(int64_t M, int32_t T, int32_t C, int32_t N, int64_t nseg)
+{
+    if (M == 0 || T == 0)
+        return 0;
+    if (T <= kTlColsMaxT)
+        return (M + 63) / 64 + (int64_t)N * C;
+    int64_t blocks = (M * nseg + kTlWaves - 1) / kTlWaves;
+    blocks = blocks < kTlSegMaxBlocks ? blocks : kTlSegMaxBlocks;
+    return blocks * kTlWaves + C;
+}
+
+// Runs the backward, which writes its partial sums to a.part, then adds
+// each channel's slots in a fixed order into acc (so grad_w and grad_b do
+// not change from call to call); the caller finalizes acc into grad_w and
+// grad_b.
 hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t stream);
 
 // One storage type's launchers, each in its own translation unit
 void tl_forward_f32(const TlArgs& a, hipStream_t st);
 void tl_forward_bf16(const TlArgs& a, hipStream_t st);
 void tl_forward_q88(const TlArgs& a, hipStream_t st);
-void tl_backward_f32(const TlBwdArgs& a, hipStream_t st);
-void tl_backward_bf16(const TlBwdArgs& a, hipStream_t st);
-void tl_backward_q88(const TlBwdArgs& a, hipStream_t st);
+// (the backward launchers return the columns per block, or segments per
+// wave, of the kernel they launched)
+int64_t tl_backward_f32(const TlBwdArgs& a, hipStream_t st);
+int64_t tl_backward_bf16(const TlBwdArgs& a, hipStream_t st);
+int64_t tl_backward_q88(const TlBwdArgs& a, hipStream_t st);
 
 }  // namespace mfpsn

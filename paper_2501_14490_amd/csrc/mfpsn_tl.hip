@@ -545,8 +545,8 @@ __device__ __forceinline__ uint16_t tl_bf16_rne(float v)
 // second walk forms grad_x[t] = sum over taps i ascending, with
 // t + (k-1-i) d < T, of sign_i dH[t + (k-1-i) d] 2^-s_i into the x tile,
 // which is stored with coalesced writes.  The 64 lanes' sums are reduced per
-// channel (lanes of one channel are consecutive) and added to acc[k+1][C]
-// with atomics.
+// (n, c) row (lanes of one row are consecutive) and stored to the row's slot
+// of this block, part[block + n C + c][k+1].
 template <int DT, int K>
 __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 {
@@ -756,24 +756,16 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
         }
         return v;
     };
-    W* acc = reinterpret_cast<W*>(a.acc);
+    W* slot = reinterpret_cast<W*>(a.part) + ((int64_t)blockIdx.x + col / a.S) * (K + 1);
 #pragma unroll
     for (int i = 0; i < K; ++i) {
         const W v = seg_sum(gw[i]);
-        if (last) {
-            if constexpr (kF)
-                atomicAdd(acc + (size_t)i * a.C + cl, v);
-            else
-                atomicAdd(reinterpret_cast<unsigned long long*>(acc) + (size_t)i * a.C + cl, (unsigned long long)v);
-        }
+        if (last)
+            slot[i] = v;
     }
     const W v = seg_sum(gb);
-    if (last) {
-        if constexpr (kF)
-            atomicAdd(acc + (size_t)K * a.C + cl, v);
-        else
-            atomicAdd(reinterpret_cast<unsigned long long*>(acc) + (size_t)K * a.C + cl, (unsigned long long)v);
-    }
+    if (last)
+        slot[K] = v;
 }
 
 // dst[j] = src[cbase + t_first + j] for j in [0, n), 0 where the time
@@ -836,9 +828,10 @@ template <typename W> __device__ __forceinline__ W tl_wave_sum(W v)
 // recomputes H and dH over [t0, t0 + L + P) (the dH its grad_x needs), adds
 // the exact products and dH of its own steps to grad_w / grad_b sums, forms
 // grad_x over its own steps from the dH window.  A wave takes a contiguous
-// run of segments in channel-major order and adds its sums to acc[k+1][C]
-// (one atomic per tap) when the channel changes and at the end.  The dH of
-// the P steps after a segment is recomputed by the next one.
+// run of a.chunk segments in channel-major order and stores its sums to
+// its slot of the channel, part[wave + c][k+1], when the channel changes
+// and at the end.  The dH of the P steps after a segment is recomputed by
+// the next one.
 template <int DT, int K>
 __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
 {
@@ -855,13 +848,13 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
     // contiguous run [w chunk, (w+1) chunk), so its sums stay in registers
     // while the channel stays the same
     const int64_t units = a.M * a.nseg, per_c = units / a.C;
-    const int64_t nwaves = (int64_t)gridDim.x * kTlWaves;
-    const int64_t chunk = (units + nwaves - 1) / nwaves;
-    const int64_t v0 = ((int64_t)blockIdx.x * kTlWaves + wave) * chunk;
+    const int64_t chunk = a.chunk;
+    const int64_t wg = (int64_t)blockIdx.x * kTlWaves + wave;
+    const int64_t v0 = wg * chunk;
     const int64_t v1 = v0 + chunk < units ? v0 + chunk : units;
     Surrogate sg;
     sg.init(a.sg, a.alpha);
-    W* acc_out = reinterpret_cast<W*>(a.acc);
+    W* part = reinterpret_cast<W*>(a.part);
     W gw[K], gb = W(0);
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -872,27 +865,18 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
     auto flush = [&]() {
         if (cur < 0)
             return;
+        W* slot = part + (wg + cur) * (K + 1);
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             const W v = tl_wave_sum(gw[i]);
             gw[i] = W(0);
-            if (lane == 0) {
-                if constexpr (kF)
-                    atomicAdd(acc_out + (size_t)i * a.C + cur, v);
-                else
-                    atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)i * a.C + cur,
-                              (unsigned long long)v);
-            }
+            if (lane == 0)
+                slot[i] = v;
         }
         const W v = tl_wave_sum(gb);
         gb = W(0);
-        if (lane == 0) {
-            if constexpr (kF)
-                atomicAdd(acc_out + (size_t)K * a.C + cur, v);
-            else
-                atomicAdd(reinterpret_cast<unsigned long long*>(acc_out) + (size_t)K * a.C + cur,
-                          (unsigned long long)v);
-        }
+        if (lane == 0)
+            slot[K] = v;
     };
     for (int64_t u = v0; u < v1; ++u) {
         const int c = (int)(u / per_c);
@@ -1003,6 +987,39 @@ __global__ void tl_zero_kernel(uint64_t* p, int64_t n)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         p[i] = 0;
+}
+
+// acc[i][c] = the sum of channel c's slots of sum i, in a fixed order.  The
+// channel's groups are g = n C + c, n < ng, each of z consecutive units of
+// a sequence cut into pieces of b units (blocks or waves); group g meets
+// the pieces first = g z / b .. last = (g z + z - 1) / b, whose slots are
+// piece + g.  One wave per (c, i): lane l adds the (n, piece) pairs
+// l + 64 j in four interleaved sums, which are added pairwise, then across
+// the lanes in a fixed tree.
+template <typename W>
+__global__ __launch_bounds__(64) void tl_bwd_reduce_kernel(const W* part, W* acc, int32_t C, int32_t k1, int64_t ng,
+                                                           int64_t z, int64_t b)
+{
+    const int c = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+    const int64_t span = (z + b - 1) / b + 1;  // pieces one group can meet, at most
+    const int64_t total = ng * span;
+    auto term = [&](int64_t q) -> W {
+        if (q >= total)
+            return W(0);
+        const int64_t n = q / span, j = q - n * span;
+        const int64_t g = n * C + c;
+        const int64_t first = g * z / b, last = (g * z + z - 1) / b;
+        return first + j <= last ? part[(first + j + g) * k1 + i] : W(0);
+    };
+    W s[4] = {W(0), W(0), W(0), W(0)};
+    for (int64_t q = lane; q < total; q += 256) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            s[u] += term(q + 64 * u);
+    }
+    const W v = tl_wave_sum((s[0] + s[1]) + (s[2] + s[3]));
+    if (lane == 0)
+        acc[(int64_t)i * C + c] = v;
 }
 
 // Forward for long columns (T > kTlColsMaxT) with histories P = (k-1) d of
@@ -1150,16 +1167,17 @@ void dispatch_k(const TlArgs& a, hipStream_t st, std::integer_sequence<int, Ks..
 }
 
 template <int DT, int K>
-void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
+int64_t launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
 {
     if (a.T <= kTlColsMaxT) {
         const size_t lds = (size_t)2 * (a.T + 1) * kTlRow * 4;
         const int64_t blocks = (a.M + 63) / 64;
         auto kern = tl_cols_bwd_kernel<DT, K>;
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
-        return;
+        return 64;
     }
-    // persistent grid: every resident block slot, at most one segment per wave
+    // persistent grid: every resident block slot (at most kTlSegMaxBlocks,
+    // which bounds the slots), at most one segment per wave
     const int span = (K - 1) * a.d;
     const size_t lds = (size_t)kTlWaves * (2 * (size_t)a.seg + 3 * (size_t)span) * 4;
     auto kern = tl_seg_bwd_kernel<DT, K>;
@@ -1171,12 +1189,19 @@ void launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
     int64_t blocks = (units + kTlWaves - 1) / kTlWaves;
     const int64_t cap = (int64_t)(nb > 0 ? nb : 1) * (cus > 0 ? cus : 1);
     blocks = blocks < cap ? blocks : cap;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kTlWaves * 64), lds, st, a);
+    blocks = blocks < kTlSegMaxBlocks ? blocks : kTlSegMaxBlocks;
+    TlBwdArgs b = a;
+    const int64_t nwaves = blocks * kTlWaves;
+    b.chunk = (units + nwaves - 1) / nwaves;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kTlWaves * 64), lds, st, b);
+    return b.chunk;
 }
 template <int DT, int... Ks>
-void dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
+int64_t dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<int, Ks...>)
 {
-    (void)((a.k == Ks + 1 ? (launch_bwd_k<DT, Ks + 1>(a, st), true) : false) || ...);
+    int64_t piece = 0;
+    (void)((a.k == Ks + 1 ? (piece = launch_bwd_k<DT, Ks + 1>(a, st), true) : false) || ...);
+    return piece;
 }
 
 }  // namespace
@@ -1187,13 +1212,13 @@ void dispatch_bwd_k(const TlBwdArgs& a, hipStream_t st, std::integer_sequence<in
 using TlKs = std::make_integer_sequence<int, MFPSN_MAX_K>;
 #if MFPSN_TL_DTYPE == 0
 void tl_forward_f32(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_F32>(a, st, TlKs{}); }
-void tl_backward_f32(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_F32>(a, st, TlKs{}); }
+int64_t tl_backward_f32(const TlBwdArgs& a, hipStream_t st) { return dispatch_bwd_k<MFPSN_F32>(a, st, TlKs{}); }
 #elif MFPSN_TL_DTYPE == 1
 void tl_forward_bf16(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_BF16>(a, st, TlKs{}); }
-void tl_backward_bf16(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_BF16>(a, st, TlKs{}); }
+int64_t tl_backward_bf16(const TlBwdArgs& a, hipStream_t st) { return dispatch_bwd_k<MFPSN_BF16>(a, st, TlKs{}); }
 #else
 void tl_forward_q88(const TlArgs& a, hipStream_t st) { dispatch_k<MFPSN_Q8_8>(a, st, TlKs{}); }
-void tl_backward_q88(const TlBwdArgs& a, hipStream_t st) { dispatch_bwd_k<MFPSN_Q8_8>(a, st, TlKs{}); }
+int64_t tl_backward_q88(const TlBwdArgs& a, hipStream_t st) { return dispatch_bwd_k<MFPSN_Q8_8>(a, st, TlKs{}); }
 #endif
 #else
 hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t st)
@@ -1211,17 +1236,30 @@ hipError_t launch_forward_time_last(const TlArgs& a, int dtype, hipStream_t st)
 hipError_t launch_backward_time_last(const TlBwdArgs& a, int dtype, hipStream_t st)
 {
     const int64_t n = (int64_t)(a.k + 1) * a.C;
-    if (n > 0) {
+    if (n == 0)
+        return hipSuccess;
+    if (a.M == 0 || a.T == 0) {
         const int64_t blocks = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
         hipLaunchKernelGGL(tl_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (uint64_t*)a.acc, n);
-    }
-    if (a.M == 0 || a.T == 0)
         return hipGetLastError();
-    switch (dtype) {
-    case MFPSN_F32: tl_backward_f32(a, st); break;
-    case MFPSN_BF16: tl_backward_bf16(a, st); break;
-    default: tl_backward_q88(a, st); break;
     }
+    int64_t piece = 0;
+    switch (dtype) {
+    case MFPSN_F32: piece = tl_backward_f32(a, st); break;
+    case MFPSN_BF16: piece = tl_backward_bf16(a, st); break;
+    default: piece = tl_backward_q88(a, st); break;
+    }
+    // groups: the (n, c) rows of S columns, or the channels' runs of segments
+    const bool cols = a.T <= kTlColsMaxT;
+    const int64_t ng = cols ? a.M / ((int64_t)a.C * a.S) : 1;
+    const int64_t z = cols ? (int64_t)a.S : a.M / a.C * a.nseg;
+    const dim3 grid((unsigned)a.C, (unsigned)(a.k + 1));
+    if (dtype == MFPSN_Q8_8)
+        hipLaunchKernelGGL(tl_bwd_reduce_kernel<int64_t>, grid, dim3(64), 0, st, (const int64_t*)a.part,
+                           (int64_t*)a.acc, a.C, a.k + 1, ng, z, piece);
+    else
+        hipLaunchKernelGGL(tl_bwd_reduce_kernel<double>, grid, dim3(64), 0, st, (const double*)a.part,
+                           (double*)a.acc, a.C, a.k + 1, ng, z, piece);
     return hipGetLastError();
 }
 #endif

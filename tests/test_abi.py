@@ -276,8 +276,14 @@ def test_backward_time_last_validation(lib):
     ws.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(ctypes.c_size_t)]
     n = ctypes.c_size_t(0)
     d = good_desc()
-    assert ws(ctypes.byref(d), ctypes.byref(n)) == 0 and n.value == (d.k + 1) * d.C * 8
+    assert ws(ctypes.byref(d), ctypes.byref(n)) == 0 and n.value == _tl_ws_bytes(d)
     assert ws(ctypes.byref(d), None) == -1
+    # the size of every kernel's slots: short columns (one slot per block
+    # and (n, c) row it meets), long columns (the segment kernel's waves)
+    for kw in (dict(T=64, N=3, C=5, S=100), dict(T=65, N=3, C=5, S=100), dict(T=4096, N=16, C=1024, S=1, k=32),
+               dict(T=3000, N=1, C=7, S=1, k=3, dilation=40), dict(T=0), dict(N=0)):
+        e = good_desc(**kw)
+        assert ws(ctypes.byref(e), ctypes.byref(n)) == 0 and n.value == _tl_ws_bytes(e), kw
     need = n.value
     assert f(None, *_bwd_tl_args(), need, None) == -1
     assert f(ctypes.byref(good_desc(T=65, k=32, dilation=34)), *_bwd_tl_args(), need, None) == -2  # history > 1024
@@ -291,6 +297,21 @@ def test_backward_time_last_validation(lib):
     assert f(ctypes.byref(d), *_bwd_tl_args(), need - 8, None) == -5
     assert f(ctypes.byref(d), *_bwd_tl_args(ws=None), need, None) == -5
     assert f(ctypes.byref(d), *_bwd_tl_args(ws=FAKE + 4), need, None) == -5
+
+
+def _tl_ws_bytes(d):
+    """Workspace of the time-last backward as the header states it: (k+1)
+    sums per channel and per partial-sum slot."""
+    M = d.N * d.C * d.S
+    if M == 0 or d.T == 0:
+        slots = 0
+    elif d.T <= 64:
+        slots = -(-M // 64) + d.N * d.C
+    else:
+        L = 1024 if (d.k - 1) * d.dilation > 64 else 256
+        units = M * -(-d.T // L)
+        slots = 4 * min(-(-units // 4), 8192) + d.C
+    return (d.k + 1) * (d.C + slots) * 8
 
 
 def _bwd_tl_args(**kw):

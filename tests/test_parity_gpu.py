@@ -152,6 +152,8 @@ SHAPES = [
     ((7, 8, 2, (4, 4)), "plane, S=16: one full two-column tile"),
     ((9, 3, 2, (44, 44)), "plane, S=1936: tiles on 128-byte lines of each row, two columns per lane"),
     ((7, 2, 3, (5, 387)), "plane, S=1935 (odd): tiles on 128-byte lines of each row, one column per lane"),
+    ((13, 3, 7, (24,)), "flat forward, S=24: a lane group's tile spans channels, ragged last tile"),
+    ((10, 4, 9, (8, 5)), "flat forward, S=40: several tiles, the last one ragged"),
 ]
 
 
