@@ -459,42 +459,26 @@ template <int K, int DT, int MODE> struct Taps;
 
 template <int K, int MODE> struct TapsF {
     static constexpr bool kHasFast = true;
-    // ((-shift) << 23) ^ (sign bit of a negative tap): the value added to a
-    // float's bit pattern to scale it by sign * 2^-shift (shift in -126..126)
-    uint32_t kc[K];
+    // w[i] = sign_i * 2^-shift_i (shift in -126..126: a normal float).  The
+    // product v * w[i] is the exponent move of the tap: exact when v is zero
+    // or normal with a normal result, otherwise rounded once, as the move
+    // itself (ldexp) rounds.
+    float w[K];
     __device__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
     {
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             int s = shift[c * K + i];
             s = s < lo ? lo : (s > hi ? hi : s);
-            uint32_t v = ((uint32_t)(-s) << 23) ^ (sign[c * K + i] < 0 ? 0x80000000u : 0u);
-            kc[i] = MODE == kPlane ? uniform_u(v) : v;
+            uint32_t v = ((uint32_t)(127 - s) << 23) | (sign[c * K + i] < 0 ? 0x80000000u : 0u);
+            w[i] = __builtin_bit_cast(float, MODE == kPlane ? uniform_u(v) : v);
         }
     }
-    // sign * 2^-shift * v for any float: exact exponent move (v_ldexp_f32),
-    // then sign flip.  Bits 23..30 of kc are -shift (sign-extended); bit 31 of
-    // ((-shift) << 23) alone is set exactly when shift > 0, so the tap's sign
-    // bit is bit 31 of kc xor (shift > 0).
-    // (The shift and sign are derived from an opaque copy of kc, so the
-    // compiler cannot hoist them out of the walk and hold 2k more registers
-    // for a path that rarely runs.)
-    __device__ __forceinline__ float apply(float v, int i) const
-    {
-        uint32_t k = kc[i];
-        asm volatile("" : "+v"(k));
-        const int nsh = (int)(k << 1) >> 24;
-        const uint32_t neg = (k ^ (nsh < 0 ? 0x80000000u : 0u)) & 0x80000000u;
-        float y = ldexpf(v, nsh);
-        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, y) ^ neg);
-    }
-    // The same value for a normal v whose result stays normal: adding kc to
-    // the bit pattern subtracts the shift from the exponent field and flips
-    // the sign bit.
-    __device__ __forceinline__ float apply_fast(float v, int i) const
-    {
-        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, v) + kc[i]);
-    }
+    // the tap's term sign * 2^-shift * v, for any float v
+    __device__ __forceinline__ float apply(float v, int i) const { return v * w[i]; }
+    // acc + the tap's term in one rounding: the sum acc + apply(v, i) itself
+    // whenever the term is exact (v in the exponent-add range, or zero)
+    __device__ __forceinline__ float fma(float v, int i, float acc) const { return __builtin_fmaf(v, w[i], acc); }
 };
 template <int K, int MODE> struct Taps<K, kF32, MODE> : TapsF<K, MODE> {};
 template <int K, int MODE> struct Taps<K, kBF16, MODE> : TapsF<K, MODE> {};
@@ -523,7 +507,6 @@ template <int K, int MODE> struct Taps<K, kQ88, MODE> {
     // (v >> s) ^ m equals +(v >> s) or -(v >> s) - 1; the -1s are cancelled by
     // starting the sum at the number of negative taps it contains.
     __device__ __forceinline__ int apply(int v, int i) const { return (v >> sh[i]) ^ m[i]; }
-    __device__ __forceinline__ int apply_fast(int v, int i) const { return apply(v, i); }
 };
 
 // Q8.8 factors come from a table: u = H - v_th_q is an integer and L(u) is
@@ -549,17 +532,21 @@ struct QTable {
         return L;
     }
 };
-// True (this lane) when one of its values is outside the range in which the
-// exponent-add tap is exact.
+// The taps of v are exact products (summed with one fused rounding each):
+// v is zero, or normal far enough from the exponent limits.
+__device__ __forceinline__ bool tap_exact(float v, const Geom& g)
+{
+    const float m = __builtin_fabsf(v);
+    return (m >= g.fast_lo && m < g.fast_hi) || m == 0.0f;
+}
+// True (this lane) when one of its values has an inexact tap product.
 template <int NV>
 __device__ __forceinline__ bool lane_slow(const Pk<float, NV>& v, const Geom& g)
 {
     bool out = false;
 #pragma unroll
-    for (int e = 0; e < NV; ++e) {
-        const float m = __builtin_fabsf(v.v[e]);
-        out = out || !(m >= g.fast_lo && m < g.fast_hi);
-    }
+    for (int e = 0; e < NV; ++e)
+        out = out || !tap_exact(v.v[e], g);
     return out;
 }
 template <int NV>
@@ -572,13 +559,7 @@ __device__ __forceinline__ bool lane_slow(const Pk<int32_t, NV>&, const Geom&)
 template <int NV>
 __device__ __forceinline__ bool any_slow(const Pk<float, NV>& v, const Geom& g)
 {
-    bool out = false;
-#pragma unroll
-    for (int e = 0; e < NV; ++e) {
-        const float m = __builtin_fabsf(v.v[e]);
-        out = out || !(m >= g.fast_lo && m < g.fast_hi);
-    }
-    return __builtin_amdgcn_ballot_w64(out) != 0;
+    return __builtin_amdgcn_ballot_w64(lane_slow(v, g)) != 0;
 }
 template <int NV>
 __device__ __forceinline__ bool any_slow(const Pk<int32_t, NV>&, const Geom&)
@@ -894,10 +875,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                 } else {
 #pragma unroll
                     for (int e = 0; e < NV; ++e) {
-                        V acc = tp.apply_fast(ring[(u + 1 + imin) % K].v[e], imin);
+                        V acc = tp.apply(ring[(u + 1 + imin) % K].v[e], imin);
 #pragma unroll
                         for (int i = imin + 1; i < K; ++i)
-                            acc = acc + tp.apply_fast(ring[(u + 1 + i) % K].v[e], i);
+                            acc = tp.fma(ring[(u + 1 + i) % K].v[e], i, acc);
                         h.v[e] = acc + bias;
                     }
                 }
@@ -1084,10 +1065,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         const bool partial = cols.partial;
         const bool active = cols.active;
         // steps j1..jtop are the halo of a lower chunk: their dH feeds outputs
-        // below j1; the walk starts at the top of jtop's block (the steps
-        // above jtop only move the loads along)
+        // below j1.  The walk runs down from jtop in blocks of k steps: step u
+        // of block b is j = jtop - bk - u, and every value of time t sits in
+        // ring slot (jtop - t) mod k, a compile-time index in every step.
         const int jtop = uniform(min(j1 + K - 1, Lr) - 1);
-        const int jstart = uniform((jtop / K) * K + K - 1);
         const int jb = uniform(max(0, j0 - (K - 1) - P));  // lowest row any stream touches
         const uint64_t brow = (uint64_t)r + (uint64_t)jb * d;
         const Buf xs = make_buf(a.x, xbytes, brow * xrow);
@@ -1097,8 +1078,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         const uint32_t vx = cols.col * es, vh = cols.col * 4u, vgx = cols.col * gxs;
         const int32_t so_last = (Lr - 1 - jb) * xstep, so_hlast = (Lr - 1 - jb) * hstep;
 
-        // grad_x accumulators: output t at slot t mod k, opened with the start
-        // of its sum (Q8.8: the number of negative taps that reach it)
+        // grad_x accumulators: output t at slot (jtop - t) mod k, opened with
+        // the start of its sum (Q8.8: the number of negative taps that reach it)
         PV gxa[K];
 #pragma unroll
         for (int s = 0; s < K; ++s) {
@@ -1106,20 +1087,21 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             if constexpr (kF) {
                 v0 = 0.0f;
             } else {
-                const int t = jtop - (((jtop - s) % K) + K) % K;  // highest output of slot s
-                const int skip = max(0, t + K - Lr);               // taps whose source lies past the end
+                const int t = jtop - s;               // output of slot s
+                const int skip = max(0, t + K - Lr);  // taps whose source lies past the end
                 v0 = __builtin_popcount(tp.negmask >> skip);
             }
 #pragma unroll
             for (int e = 0; e < NV; ++e)
                 gxa[s].v[e] = v0;
         }
-        // x ring: x[t] at slot t mod k, for t in the window of the step
+        // x ring: x[t] at slot (jtop - t) mod k, for t in the window of the
+        // step; zeros for times before 0
         Pk<double, NV> xd[kXD ? K : 1];
         PV xf[kXV ? K : 1];
         int slow_x = 0;  // live steps left on the exact recompute path
-        // prefetch: step j's g[j], h[j], x[j-k+1] at slot j mod P, as loaded
-        // (converted in the step that uses them)
+        // prefetch: step j's g[j], h[j], x[j-k+1] at slot (jtop - j) mod P, as
+        // loaded (converted in the step that uses them)
         typename IO<DT>::template Raw<NV> pg[P], px[P];
         PV ph[HS ? P : 1];
         auto load_h = [&](int32_t so) __attribute__((always_inline)) {
@@ -1130,61 +1112,67 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 v.v[e] = __builtin_bit_cast(V, w.v[e]);
             return v;
         };
-        // Preload: the ring's inputs x[jstart-k+2 .. jstart] (slot t mod k;
-        // values past jtop are never used) and the first P steps' streams.
-        // Every load is issued before any value is looked at, so an item
-        // starts after one memory round trip, not one per ring slot.
+        // Preload: the ring's inputs x[jtop-k+2 .. jtop] (slot jtop - t) and
+        // the first P steps' streams.  Every load is issued before any value
+        // is looked at, so an item starts after one memory round trip, not
+        // one per ring slot.  Rows below jb (times before 0 of a short class,
+        // or steps below the walk) are clamped; their ring values are zeros.
         {
             typename IO<DT>::template Raw<NV> rr[K - 1 > 0 ? K - 1 : 1];
 #pragma unroll
             for (int m = 0; m < K - 1; ++m)
-                rr[m] = IO<DT>::template load_raw<NV>(xs, vx, (min(jstart - m, Lr - 1) - jb) * xstep);
+                rr[m] = IO<DT>::template load_raw<NV>(xs, vx, (max(jtop - m, jb) - jb) * xstep);
 #pragma unroll
             for (int p = 0; p < P; ++p) {
-                const int jp = jstart - p;
-                const int js = (K - 1 - p) % P;
-                const int rowg = min(jp, Lr - 1);
-                pg[js] = IO<DT>::template load_raw<NV>(gsb, vx, (rowg - jb) * xstep);
+                const int rowg = max(jtop - p, jb);
+                pg[p] = IO<DT>::template load_raw<NV>(gsb, vx, (rowg - jb) * xstep);
                 if constexpr (HS)
-                    ph[js] = load_h((rowg - jb) * hstep);
-                px[js] = IO<DT>::template load_raw<NV>(xs, vx, (min(max(jp - K + 1, jb), Lr - 1) - jb) * xstep);
+                    ph[p] = load_h((rowg - jb) * hstep);
+                px[p] = IO<DT>::template load_raw<NV>(xs, vx, (max(jtop - p - K + 1, jb) - jb) * xstep);
             }
-            bool out = false;  // some live input of this lane outside the exponent-add range
+            bool out = false;  // some input of this lane outside the exponent-add range
 #pragma unroll
             for (int m = 0; m < K - 1; ++m) {
-                const PV v = IO<DT>::template cvt<NV>(rr[m]);
+                PV v = IO<DT>::template cvt<NV>(rr[m]);
+                const bool live = jtop - m >= 0;
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    v.v[e] = live ? v.v[e] : V(0);
                 if constexpr (kXD)
 #pragma unroll
                     for (int e = 0; e < NV; ++e)
-                        xd[K - 1 - m].v[e] = (double)v.v[e];
+                        xd[m].v[e] = (double)v.v[e];
                 if constexpr (kXV)
-                    xf[K - 1 - m] = v;
-                // x[t] (t <= jtop) is in the window of at most k live steps
+                    xf[m] = v;
+                // x[t] (0 <= t <= jtop) is in the window of at most k live steps
                 if constexpr (kRe && TP::kHasFast)
-                    if (jstart - m <= jtop)
+                    if (live)
                         out = out || lane_slow(v, g);
             }
             if (kRe && TP::kHasFast && __builtin_amdgcn_ballot_w64(out) != 0)
                 slow_x = K;
         }
-        int32_t so_gp = (jstart - P - jb) * xstep;           // g of step j - P
-        int32_t so_hp = (jstart - P - jb) * hstep;           // factor or H of step j - P
-        int32_t so_xp = (jstart - P - K + 1 - jb) * xstep;   // x of step j - P
-        int32_t so_gx = (jstart - jb) * gxstep;              // grad_x of step j
+        int32_t so_gp = (jtop - P - jb) * xstep;           // g of step j - P
+        int32_t so_hp = (jtop - P - jb) * hstep;           // factor or H of step j - P
+        int32_t so_xp = (jtop - P - K + 1 - jb) * xstep;   // x of step j - P
+        int32_t so_gx = (jtop - jb) * gxstep;              // grad_x of step j
 
-        // one step (u: position in the block, j = bK + k-1-u).  KIND kEdge is
-        // block 0: x[j-k+1] lies before time 0 for u > 0, and the taps
-        // i < u (sources before time 0, outputs before time 0) are left out.
+        // one step (u: position in the block, j = jtop - bk - u).  Time j - k +
+        // 1 + i, the source of tap i and the output that tap i of dH[j]
+        // reaches, sits in slot (u + k - 1 - i) mod k.  Steps j < k - 1 (only
+        // in checked blocks) have sources before time 0: the ring holds zeros
+        // there, whose exact zero terms change no bit of H once the bias is
+        // added (they only lead the sum), and their outputs before time 0
+        // are never stored.
         auto step = [&](auto uc, auto kc_, int j) __attribute__((always_inline)) {
             constexpr int u = decltype(uc)::value;
             constexpr int kind = decltype(kc_)::value;
             constexpr bool full = kind == kFull;
-            constexpr bool edge = kind == kEdge;
-            constexpr int sj = K - 1 - u;  // j mod k
-            constexpr int sp = sj % P;     // j mod P
-            constexpr int imin = edge ? u : 0;
+            constexpr int sp = u % P;  // prefetch slot
+            auto sl = [](int i) constexpr { return (u + K - 1 - i) % K; };  // slot of time j-k+1+i
+            const bool edge = !full && j < K - 1;  // some source before time 0 (wave-uniform)
             const PV gv = IO<DT>::template cvt<NV>(pg[sp]);
-            const PV xv = IO<DT>::template cvt<NV>(px[sp]);
+            PV xv = IO<DT>::template cvt<NV>(px[sp]);
             PV hv;
             if constexpr (HS)
                 hv = ph[sp];
@@ -1196,22 +1184,21 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             if constexpr (HS)
                 advance(so_hp, -hstep);
             advance(so_xp, -xstep);
-            // x[j-k+1] enters the ring (slot (j+1) mod k)
-            if constexpr (!(edge && u > 0)) {
-                if constexpr (kXD)
-#pragma unroll
-                    for (int e = 0; e < NV; ++e)
-                        xd[(sj + 1) % K].v[e] = (double)xv.v[e];
-                if constexpr (kXV)
-                    xf[(sj + 1) % K] = xv;
-                if (kRe && TP::kHasFast && any_slow(xv, g))
-                    slow_x = K;
-            } else if constexpr (!kF) {
+            // x[j-k+1] enters the ring (slot sl(0)); zeros before time 0
+            if (edge) {
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
-                    xf[(sj + 1) % K].v[e] = 0;  // Q8.8: zeros before time 0 (recompute)
+                    xv.v[e] = j - K + 1 >= 0 ? xv.v[e] : V(0);
             }
-            if (full || j <= jtop) {
+            if constexpr (kXD)
+#pragma unroll
+                for (int e = 0; e < NV; ++e)
+                    xd[sl(0)].v[e] = (double)xv.v[e];
+            if constexpr (kXV)
+                xf[sl(0)] = xv;
+            if (kRe && TP::kHasFast && (full || j - K + 1 >= 0) && any_slow(xv, g))
+                slow_x = K;
+            {
                 PV dh;
                 if constexpr (HS == kSavedFactor) {
 #pragma unroll
@@ -1224,30 +1211,29 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                 } else {
                     PV h;
                     if constexpr (kF) {
-                        constexpr int rmin = edge ? u : 0;  // taps reading before time 0 are left out
                         if (__builtin_expect(slow_x > 0, 0)) {
 #pragma unroll
                             for (int e = 0; e < NV; ++e) {
-                                V acc = tp.apply(xf[(sj + 1 + rmin) % K].v[e], rmin);
+                                V acc = tp.apply(xf[sl(0)].v[e], 0);
 #pragma unroll
-                                for (int i = rmin + 1; i < K; ++i)
-                                    acc = acc + tp.apply(xf[(sj + 1 + i) % K].v[e], i);
+                                for (int i = 1; i < K; ++i)
+                                    acc = acc + tp.apply(xf[sl(i)].v[e], i);
                                 h.v[e] = acc + bias;
                             }
                         } else {
 #pragma unroll
                             for (int e = 0; e < NV; ++e) {
-                                V acc = tp.apply_fast(xf[(sj + 1 + rmin) % K].v[e], rmin);
+                                V acc = tp.apply(xf[sl(0)].v[e], 0);
 #pragma unroll
-                                for (int i = rmin + 1; i < K; ++i)
-                                    acc = acc + tp.apply_fast(xf[(sj + 1 + i) % K].v[e], i);
+                                for (int i = 1; i < K; ++i)
+                                    acc = tp.fma(xf[sl(i)].v[e], i, acc);
                                 h.v[e] = acc + bias;
                             }
                         }
                     } else {
 #pragma unroll
                         for (int e = 0; e < NV; ++e) {
-                            h.v[e] = q88_charge<K>(tp, start, [&](int i) { return xf[(sj + 1 + i) % K].v[e]; });
+                            h.v[e] = q88_charge<K>(tp, start, [&](int i) { return xf[sl(i)].v[e]; });
                         }
                     }
 #pragma unroll
@@ -1263,8 +1249,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                             if (MODE == kPlane && partial)
                                 dd = active ? dd : 0.0;  // no contribution from shadow lanes
 #pragma unroll
-                            for (int i = imin; i < K; ++i) {
-                                gw[i] = __builtin_fma(xd[(sj + 1 + i) % K].v[e], dd, gw[i]);
+                            for (int i = 0; i < K; ++i) {
+                                gw[i] = __builtin_fma(xd[sl(i)].v[e], dd, gw[i]);
                                 pin(gw[i]);
                             }
                             gb += dd;
@@ -1274,8 +1260,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                             if (MODE == kPlane && partial)
                                 dq = active ? dq : 0;
 #pragma unroll
-                            for (int i = imin; i < K; ++i) {
-                                gw[i] += (int64_t)xf[(sj + 1 + i) % K].v[e] * (int64_t)dq;
+                            for (int i = 0; i < K; ++i) {
+                                gw[i] += (int64_t)xf[sl(i)].v[e] * (int64_t)dq;
                                 pin(gw[i]);
                             }
                             gb += dq;
@@ -1283,42 +1269,41 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                         }
                     }
                 }
-                // scatter dH[j] into outputs j-k+1+i (slot (j+1+i) mod k).  Lanes
-                // whose dH is in the exponent-add range take the fast taps;
-                // every other nonzero dH (one whose scaled terms would leave the
-                // normal range: tiny, huge, infinite or NaN) the exact taps.  A
-                // zero dH adds nothing: its terms are zeros, and an accumulator
-                // that starts at +0 is never -0, so adding them changes no bit.
+                // scatter dH[j] into outputs j-k+1+i (slot sl(i)).  Lanes whose
+                // dH has exact tap products add them with one fused rounding;
+                // the others (dH whose scaled terms leave the normal range:
+                // tiny, huge, infinite or NaN) round each term, then add.
 #pragma unroll
                 for (int e = 0; e < NV; ++e) {
                     if constexpr (kF) {
-                        const float m = __builtin_fabsf(dh.v[e]);
-                        const bool fast = m >= g.fast_lo && m < g.fast_hi;
+                        const bool fast = tap_exact(dh.v[e], g);
                         if (fast) {
 #pragma unroll
-                            for (int i = imin; i < K; ++i)
-                                gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply_fast(dh.v[e], i);
+                            for (int i = 0; i < K; ++i)
+                                gxa[sl(i)].v[e] = tp.fma(dh.v[e], i, gxa[sl(i)].v[e]);
                         }
-                        if (__builtin_expect(!fast && m != 0.0f, 0)) {
+                        if (__builtin_expect(!fast, 0)) {
 #pragma unroll
-                            for (int i = imin; i < K; ++i)
-                                gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply(dh.v[e], i);
+                            for (int i = 0; i < K; ++i)
+                                gxa[sl(i)].v[e] = gxa[sl(i)].v[e] + tp.apply(dh.v[e], i);
                         }
                     } else {
                         // (integer sums: pinned so they are not reassociated across
                         // steps, which would keep many steps' terms live)
 #pragma unroll
-                        for (int i = imin; i < K; ++i) {
-                            gxa[(sj + 1 + i) % K].v[e] = gxa[(sj + 1 + i) % K].v[e] + tp.apply(dh.v[e], i);
-                            pin(gxa[(sj + 1 + i) % K].v[e]);
+                        for (int i = 0; i < K; ++i) {
+                            gxa[sl(i)].v[e] = gxa[sl(i)].v[e] + tp.apply(dh.v[e], i);
+                            pin(gxa[sl(i)].v[e]);
                         }
                     }
                 }
+                // output j is complete: the k-1 steps above it have scattered
+                // into slot sl(k-1) = u already
                 if (own)
-                    IO<DT>::template store_gx<NV>(gxb, vgx, so_gx, gxa[sj]);
+                    IO<DT>::template store_gx<NV>(gxb, vgx, so_gx, gxa[u]);
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
-                    gxa[sj].v[e] = reset;  // slot now holds output j - k
+                    gxa[u].v[e] = reset;  // slot now holds output j - k
                 if constexpr (kRe && kF)
                     if (slow_x > 0)
                         --slow_x;
@@ -1330,30 +1315,29 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
         };
         auto block = [&](int b, auto kc_) __attribute__((always_inline)) {
             constexpr int kind = decltype(kc_)::value;
-            const int jhi = b * K + K - 1;
+            const int jhi = jtop - b * K;
             [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
                 (void)(((kind == kFull || jhi - U >= j0) ? (step(ic<U>{}, kc_, jhi - U), true) : false) &&
                        ...);
             }(std::make_integer_sequence<int, K>{});
         };
-        // full blocks: b > 0, every step owned and at or below jtop, every
-        // prefetch at or above jb
-        // (block 0, the start of the sequence, is the last one of a walk)
-        int b = jstart / K;
-        const int blo = j0 / K;
-        const int bmin = max(blo, 1);
+        // Blocks b = 0 .. nb-1 cover the steps jtop down to j0.  Full blocks:
+        // every step owned (below j1) with all its sources at or after time
+        // 0, and every prefetch row at or above jb; the others check each step.
+        const int nb = (jtop - j0) / K + 1;
+        int b = 0;
         if constexpr (K <= kFullBlockMaxK) {
-            const int bf_hi = (min(jtop, j1 - 1) - (K - 1)) / K;
-            const int bf_lo = max(bmin, (jb + P + 2 * K - 2) / K);
-            for (; b > bf_hi && b >= bmin; --b)
+            const int bf_lo = (jtop - j1 + K) / K;  // first block below j1
+            const int lmin = max(max(j0, K - 1), jb + P + K - 1);
+            const int span = jtop - (K - 1) - lmin;  // lowest step of block b: jtop - bk - (k-1)
+            const int bf_hi = span >= 0 ? span / K : -1;
+            for (; b < bf_lo && b < nb; ++b)
                 block(b, ic<kChecked>{});
-            for (; b >= bf_lo; --b)
+            for (; b <= bf_hi; ++b)
                 block(b, ic<kFull>{});
         }
-        for (; b >= bmin; --b)
+        for (; b < nb; ++b)
             block(b, ic<kChecked>{});
-        if (blo == 0)
-            block(0, ic<kEdge>{});
     }
     // block reduction in a fixed order, then one partial row per block
     const int C = g.C;
