@@ -129,7 +129,15 @@ constexpr int kBwdPairBytes = MFPSN_BWD_PAIR_BYTES;  // plane mode, two columns 
 constexpr int kFullBlockMaxK = MFPSN_FULL_BLOCK_MAX_K;
 
 template <int V> using ic = std::integral_constant<int, V>;
-enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 };
+// Block kinds (flags): kFull runs every step unguarded; kChecked clamps its
+// prefetches (the backward's also selects what reaches before time 0; the
+// forward's also stops at the item's end); kEdge is the forward's first
+// block, whose taps before time 0 are left out; kLast is the backward's
+// final block, the only one of its walk that stops at the item's end, run
+// outside every loop (a block loop that could stop mid-block carries the
+// registers of prefetches issued but never used, and reconciles them with
+// moves that each wait for the pending load).
+enum BlockKind : int { kFull = 0, kChecked = 1, kEdge = 2 | 1, kLast = 4 | 1 };
 
 // ---------------------------------------------------------------------------
 // buffers: raw buffer resource over [tensor + off, tensor end), per-lane
@@ -844,14 +852,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         int32_t so_xp = (j0 + P - jb) * xstep;  // prefetch of step j + P
         int32_t so_s = 0, so_h = 0;
 
-        // one step (u: position in the block, j = bK + u); KIND kEdge is the
-        // block at the start of the sequence, which leaves out the float taps
-        // that would read before time 0 (Q8.8 keeps them: the ring holds
+        // one step (u: position in the block, j = bK + u); KIND with kEdge is
+        // the block at the start of the sequence, which leaves out the float
+        // taps that would read before time 0 (Q8.8 keeps them: the ring holds
         // zeros there, whose xor-terms the starting value cancels)
         auto step = [&](auto uc, auto kc_, int j) __attribute__((always_inline)) {
             constexpr int u = decltype(uc)::value;
             constexpr int kind = decltype(kc_)::value;
-            constexpr int imin = (kF && kind == kEdge) ? K - 1 - u : 0;
+            constexpr int imin = (kF && (kind & kEdge) == kEdge) ? K - 1 - u : 0;
             (void)j;
             const PV xv = IO<DT>::template cvt<NV>(pf[u % P]);
             pf[u % P] = IO<DT>::template load_raw<NV>(xs, vx, kind == kFull ? so_xp : min(so_xp, so_xlast));
@@ -919,8 +927,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         auto block = [&](int jb0, auto kc_) __attribute__((always_inline)) {
             constexpr int kind = decltype(kc_)::value;
             [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
-                (void)(((kind == kFull || jb0 + U < j1) ? (step(ic<U>{}, kc_, jb0 + U), true) : false) &&
-                       ...);
+                (void)(((kind == kFull || jb0 + U < j1) ? (step(ic<U>{}, kc_, jb0 + U), true) : false) && ...);
             }(std::make_integer_sequence<int, K>{});
         };
         int b = j0 / K;
@@ -963,8 +970,14 @@ __device__ __forceinline__ int64_t wave_sum(int64_t v)
 // surrogate factor, or the forward's saved potentials H.
 enum SavedKind : int { kRecompute = 0, kSavedFactor = 1, kSavedH = 2 };
 
+// Waves per SIMD the backward's register budget must allow (1: no bound).
+#ifndef MFPSN_BWD_WAVES_PER_EU
+#define MFPSN_BWD_WAVES_PER_EU 1
+#endif
+
 template <int K, int DT, int MODE, int HS, int NV>
-__global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MFPSN_BWD_WAVES_PER_EU))) void bwd_kernel(
+    BwdArgs a)
 {
     using V = typename IO<DT>::V;
     using W = typename IO<DT>::W;
@@ -1317,27 +1330,29 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
             constexpr int kind = decltype(kc_)::value;
             const int jhi = jtop - b * K;
             [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
-                (void)(((kind == kFull || jhi - U >= j0) ? (step(ic<U>{}, kc_, jhi - U), true) : false) &&
+                (void)((((kind & kLast) != kLast || jhi - U >= j0) ? (step(ic<U>{}, kc_, jhi - U), true) : false) &&
                        ...);
             }(std::make_integer_sequence<int, K>{});
         };
         // Blocks b = 0 .. nb-1 cover the steps jtop down to j0.  Full blocks:
         // every step owned (below j1) with all its sources at or after time
         // 0, and every prefetch row at or above jb; the others check each step.
-        const int nb = (jtop - j0) / K + 1;
+        // every block before the last runs all its steps
+        const int blast = (jtop - j0) / K;
         int b = 0;
         if constexpr (K <= kFullBlockMaxK) {
             const int bf_lo = (jtop - j1 + K) / K;  // first block below j1
             const int lmin = max(max(j0, K - 1), jb + P + K - 1);
             const int span = jtop - (K - 1) - lmin;  // lowest step of block b: jtop - bk - (k-1)
-            const int bf_hi = span >= 0 ? span / K : -1;
-            for (; b < bf_lo && b < nb; ++b)
+            const int bf_hi = min(span >= 0 ? span / K : -1, blast - 1);
+            for (; b < bf_lo && b < blast; ++b)
                 block(b, ic<kChecked>{});
             for (; b <= bf_hi; ++b)
                 block(b, ic<kFull>{});
         }
-        for (; b < nb; ++b)
+        for (; b < blast; ++b)
             block(b, ic<kChecked>{});
+        block(blast, ic<kLast>{});
     }
     // block reduction in a fixed order, then one partial row per block
     const int C = g.C;
