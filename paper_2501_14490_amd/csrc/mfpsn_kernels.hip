@@ -541,11 +541,13 @@ struct QTable {
     }
 };
 // The taps of v are exact products (summed with one fused rounding each):
-// v is zero, or normal far enough from the exponent limits.
+// v is zero, or normal far enough from the exponent limits.  (Bitwise
+// operators: the short-circuit ones become a branch on the exec mask per
+// operand.)
 __device__ __forceinline__ bool tap_exact(float v, const Geom& g)
 {
     const float m = __builtin_fabsf(v);
-    return (m >= g.fast_lo && m < g.fast_hi) || m == 0.0f;
+    return ((m >= g.fast_lo) & (m < g.fast_hi)) | (m == 0.0f);
 }
 // True (this lane) when one of its values has an inexact tap product.
 template <int NV>
@@ -554,7 +556,7 @@ __device__ __forceinline__ bool lane_slow(const Pk<float, NV>& v, const Geom& g)
     bool out = false;
 #pragma unroll
     for (int e = 0; e < NV; ++e)
-        out = out || !tap_exact(v.v[e], g);
+        out = out | !tap_exact(v.v[e], g);
     return out;
 }
 template <int NV>
@@ -1160,7 +1162,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MFPSN_
                 // x[t] (0 <= t <= jtop) is in the window of at most k live steps
                 if constexpr (kRe && TP::kHasFast)
                     if (live)
-                        out = out || lane_slow(v, g);
+                        out = out | lane_slow(v, g);
             }
             if (kRe && TP::kHasFast && __builtin_amdgcn_ballot_w64(out) != 0)
                 slow_x = K;
