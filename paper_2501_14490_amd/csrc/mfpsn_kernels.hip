@@ -278,11 +278,13 @@ __device__ __forceinline__ void st_bytes(Buf b, uint32_t v, int32_t s, const uin
     }
 }
 // 16-bit values packed two to a 32-bit word (bf16, Q8.8): NV values in
-// (NV + 1) / 2 words
+// (NV + 1) / 2 words.  A single value stays a 16-bit one until it is used:
+// widening it where it is loaded would wait for the load there.
+template <int NV> using Halves = Pk<std::conditional_t<NV == 1, uint16_t, uint32_t>, (NV + 1) / 2>;
 template <int NV>
-__device__ __forceinline__ Pk<uint32_t, (NV + 1) / 2> ld_halves(Buf b, uint32_t v, int32_t s)
+__device__ __forceinline__ Halves<NV> ld_halves(Buf b, uint32_t v, int32_t s)
 {
-    Pk<uint32_t, (NV + 1) / 2> r;
+    Halves<NV> r;
     if constexpr (NV == 1) {
         r.v[0] = ld16(b, v, s);
     } else if constexpr (NV == 2) {
@@ -387,7 +389,7 @@ template <> struct IO<kBF16> {
     static constexpr int gx_es = 2;
     // NV stored values packed two to a 32-bit word, widened only where they
     // are used
-    template <int NV> using Raw = Pk<uint32_t, (NV + 1) / 2>;
+    template <int NV> using Raw = Halves<NV>;
     template <int NV>
     __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
     {
@@ -399,7 +401,8 @@ template <> struct IO<kBF16> {
         Pk<V, NV> r;
 #pragma unroll
         for (int e = 0; e < NV; ++e)
-            r.v[e] = __builtin_bit_cast(float, e % 2 == 0 ? w.v[e / 2] << 16 : w.v[e / 2] & 0xFFFF0000u);
+            r.v[e] = __builtin_bit_cast(float, e % 2 == 0 ? (uint32_t)w.v[e / 2] << 16
+                                                          : (uint32_t)w.v[e / 2] & 0xFFFF0000u);
         return r;
     }
     template <int NV>
@@ -428,7 +431,7 @@ template <> struct IO<kQ88> {
     using W = int64_t;
     static constexpr int es = 2;
     static constexpr int gx_es = 4;
-    template <int NV> using Raw = Pk<uint32_t, (NV + 1) / 2>;
+    template <int NV> using Raw = Halves<NV>;
     template <int NV>
     __device__ static Raw<NV> load_raw(Buf b, uint32_t v, int32_t s)
     {
@@ -440,7 +443,7 @@ template <> struct IO<kQ88> {
         Pk<V, NV> r;
 #pragma unroll
         for (int e = 0; e < NV; ++e)
-            r.v[e] = e % 2 == 0 ? (int32_t)(int16_t)w.v[e / 2] : (int32_t)w.v[e / 2] >> 16;
+            r.v[e] = e % 2 == 0 ? (int32_t)(int16_t)w.v[e / 2] : (int32_t)(uint32_t)w.v[e / 2] >> 16;
         return r;
     }
     template <int NV>
