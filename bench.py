@@ -52,7 +52,7 @@ HBM_PEAK_GBS = 8000.0
 BACKWARD_INPUTS = ("recompute", "h", "sg")
 # what the forward saves for the backward in each workload (the fastest step
 # measured on MI355X)
-AUTO_BACKWARD_INPUT = {1: "recompute", 2: "sg", 3: "recompute", 4: "recompute", 5: "sg"}
+AUTO_BACKWARD_INPUT = {1: "recompute", 2: "recompute", 3: "recompute", 4: "recompute", 5: "sg"}
 
 
 def log(*a):

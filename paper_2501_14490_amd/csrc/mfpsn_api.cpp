@@ -21,9 +21,13 @@ int grad_x_bytes(int dtype) { return dtype == MFPSN_BF16 ? 2 : 4; }
 // Longest chunk of class steps (a multiple of k) whose byte span, with the
 // halo and prefetch rows, still fits the 31-bit scalar offsets the kernels
 // use inside one item (4-byte elements, the widest stream); 0 if none fits.
-int64_t max_chunk(const mfpsn_desc* d)
+// Longest chunk of a residue class (a multiple of k) whose rows, with the
+// halo and prefetch rows around it, keep every 32-bit buffer offset of an
+// item in range; row_es is the widest element of the streams the call
+// moves (4 covers every call).
+int64_t max_chunk(const mfpsn_desc* d, int row_es = 4)
 {
-    const int64_t row = (int64_t)d->N * d->C * d->S * 4 * d->dilation;
+    const int64_t row = (int64_t)d->N * d->C * d->S * row_es * d->dilation;
     if (row <= 0)
         return INT64_MAX;
     const int64_t rows = (((int64_t)1 << 31) - 1) / row - 3 * (int64_t)d->k - 8;
@@ -130,8 +134,9 @@ int flat_layout(const mfpsn_desc* d, const void* x, const void* spikes, const vo
     return nv;
 }
 
-// flat: the flat forward's columns per lane (0: lane-channel or plane mode)
-Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0)
+// flat: the flat forward's columns per lane (0: lane-channel or plane mode);
+// row_es: the widest element of the call's streams (bounds the chunks)
+Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0, int row_es = 4)
 {
     Geom g;
     memset(&g, 0, sizeof(g));
@@ -199,7 +204,7 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0)
     // sequence (classes r >= T are empty)
     g.ncls = d->dilation < d->T ? d->dilation : (d->T > 0 ? d->T : 1);
     const int64_t base = (int64_t)g.groups * g.tiles * g.ncls;
-    const int64_t cap = max_chunk(d);
+    const int64_t cap = max_chunk(d, row_es);
     int64_t chunk = ceil_div(class_len > 0 ? class_len : 1, K) * K;
     if (chunk > cap)
         chunk = cap;
@@ -290,7 +295,8 @@ int mfpsn_forward(const mfpsn_desc* desc, const void* x, const int8_t* sign, con
         return MFPSN_OK;
     FwdArgs a;
     a.g = plan(desc, false, pair_layout(desc) && pair_aligned({x, spikes, h_out, sg_out}) ? 2 : 1,
-               flat_layout(desc, x, spikes, h_out, sg_out));
+               flat_layout(desc, x, spikes, h_out, sg_out),
+               h_out || sg_out ? 4 : elem_bytes(desc->dtype));
     if (a.g.items > kMaxItems)
         return MFPSN_ERR_SHAPE;
     a.x = x;
@@ -346,7 +352,10 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
             return MFPSN_ERR_SHAPE;
     }
     BwdArgs a;
-    a.g = plan(desc, true, pair_layout(desc) && pair_aligned({x, grad_spikes, h, sg, grad_x}) ? 2 : 1);
+    // (narrower rows than the workspace query assumes give longer chunks,
+    // fewer items and no more blocks, so the queried workspace still holds)
+    const int row_es = h || sg ? 4 : (es > grad_x_bytes(desc->dtype) ? es : grad_x_bytes(desc->dtype));
+    a.g = plan(desc, true, pair_layout(desc) && pair_aligned({x, grad_spikes, h, sg, grad_x}) ? 2 : 1, 0, row_es);
     if (total > 0 && a.g.items > kMaxItems)
         return MFPSN_ERR_SHAPE;
     const size_t need = total > 0 ? backward_workspace(desc) : 0;

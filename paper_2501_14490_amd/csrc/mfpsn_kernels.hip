@@ -791,9 +791,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const uint64_t xrow = (uint64_t)M * es;
     const uint64_t xbytes = (uint64_t)g.T * xrow, sbytes = (uint64_t)g.T * M;
     const int32_t xstep = (int32_t)((uint64_t)d * xrow), sstep = (int32_t)((uint64_t)d * M);
-    const int32_t hstep = 4 * sstep;
     const int want_h = a.h_out != nullptr ? 1 : 0;
     const int want_sg = a.sg_out != nullptr ? 1 : 0;
+    // (4-byte rows only when they are written: the planner sizes chunks so
+    // that the offsets of the streams a call moves fit 32 bits)
+    const int32_t hstep = want_h | want_sg ? 4 * sstep : 0;
 
     Cursor cur(g, q0);
     int tile_cached = -1;
@@ -1171,7 +1173,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MFPSN_
                 slow_x = K;
         }
         int32_t so_gp = (jtop - P - jb) * xstep;           // g of step j - P
-        int32_t so_hp = (jtop - P - jb) * hstep;           // factor or H of step j - P
+        int32_t so_hp = HS ? (jtop - P - jb) * hstep : 0;  // factor or H of step j - P
         int32_t so_xp = (jtop - P - K + 1 - jb) * xstep;   // x of step j - P
         int32_t so_gx = (jtop - jb) * gxstep;              // grad_x of step j
 
