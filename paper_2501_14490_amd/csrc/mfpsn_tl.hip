@@ -277,37 +277,42 @@ template <> struct TlVec4<MFPSN_Q8_8> {
     }
 };
 
-// The k taps of one lane's channel: for float data the bit-pattern addend
-// kc = (-s) 2^23 + sign 2^31 (mod 2^32) of x * 2^-s with the sign (the
-// exact path takes -s from bits 23..30 and the sign from what remains once
-// (-s) 2^23 is taken away), for Q8.8 the shift and the negation mask.
+// The k taps of one lane's channel: for float data w = sign 2^-s, a normal
+// float, whose product with an input is the tap's exponent move (exact, or
+// rounded once where the move rounds); for Q8.8 the shift and the negation
+// mask.
 template <int DT, int K> struct TlLaneTaps {
     static constexpr bool kF = DT != MFPSN_Q8_8;
     using V = typename TlIO<DT>::V;
-    uint32_t kc[kF ? K : 1];
+    float w[kF ? K : 1];
     int sh[kF ? 1 : K], neg[kF ? 1 : K];
-    int nneg;  // Q8.8: number of negative taps
+    int nneg;          // Q8.8: number of negative taps
+    uint32_t negmask;  // Q8.8: bit i set for a negative tap i
     __device__ __forceinline__ void load(const int8_t* sign, const int8_t* shift, int c, int lo, int hi)
     {
         nneg = 0;
+        negmask = 0;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             int sv = shift[c * K + i];
             sv = sv < lo ? lo : (sv > hi ? hi : sv);
             const bool n = sign[c * K + i] < 0;
             if constexpr (kF) {
-                kc[i] = ((uint32_t)(-sv) << 23) ^ (n ? 0x80000000u : 0u);
+                w[i] = __builtin_bit_cast(float, ((uint32_t)(127 - sv) << 23) | (n ? 0x80000000u : 0u));
             } else {
                 sh[i] = sv, neg[i] = n ? -1 : 0;
                 nneg += n ? 1 : 0;
+                negmask |= n ? (1u << i) : 0u;
             }
         }
     }
-    // A sum over all k taps (every input exists) as start() followed by
-    // accumulate() per tap in ascending order.  Float: +0 and one rounded add
-    // per term, as apply().  Q8.8: ((v >> s) ^ m) is +(v >> s) or -(v >> s) - 1,
-    // so the sum starts at the number of negative taps and adds it unchanged
-    // (integers: the same value).
+    // A sum over all k taps (every input exists, or is a zero) as start()
+    // followed by accumulate() per tap in ascending order.  Float: +0, then
+    // each term added with one rounding; EXACT rounds the term first (any
+    // input), else one fused rounding (inputs whose terms are exact: zero,
+    // or in the exponent-add range).  Q8.8: ((v >> s) ^ m) is +(v >> s) or
+    // -(v >> s) - 1, so the sum starts at the number of negative taps
+    // (integers: any order, the same value).
     __device__ __forceinline__ V start() const
     {
         if constexpr (kF)
@@ -317,29 +322,33 @@ template <int DT, int K> struct TlLaneTaps {
     }
     template <bool EXACT> __device__ __forceinline__ V accumulate(V acc, V in, int i) const
     {
-        if constexpr (kF)
-            return acc + apply<EXACT>(in, i);
-        else
-            return ((in >> sh[i]) ^ neg[i]) + acc;
-    }
-    // sign * in * 2^-s: EXACT by v_ldexp_f32 and a sign flip, else by the
-    // bit-pattern add (exact for |in| in the fast range); Q8.8 floor shift
-    // and negation
-    template <bool EXACT> __device__ __forceinline__ V apply(V in, int i) const
-    {
         if constexpr (kF) {
-            if constexpr (EXACT) {
-                const int e = (int32_t)(kc[i] << 1) >> 24;
-                const uint32_t sb = (kc[i] - ((uint32_t)e << 23)) & 0x80000000u;
-                return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, ldexpf(in, e)) ^ sb);
-            } else {
-                return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, in) + kc[i]);
-            }
+            if constexpr (EXACT)
+                return acc + in * w[i];
+            else
+                return __builtin_fmaf(in, w[i], acc);
         } else {
-            return ((in >> sh[i]) ^ neg[i]) - neg[i];
+            return ((in >> sh[i]) ^ neg[i]) + acc;
         }
     }
+    // sign * in * 2^-s (float: rounded once, as the exponent move); Q8.8
+    // floor shift and negation
+    template <bool EXACT> __device__ __forceinline__ V apply(V in, int i) const
+    {
+        if constexpr (kF)
+            return in * w[i];
+        else
+            return ((in >> sh[i]) ^ neg[i]) - neg[i];
+    }
 };
+
+// The tap products of v are exact (v zero, or normal far enough from the
+// exponent limits).  Bitwise logic: no branch per operand.
+__device__ __forceinline__ bool tl_tap_exact(float v, float lo, float hi)
+{
+    const float m = __builtin_fabsf(v);
+    return ((m >= lo) & (m < hi)) | (m == 0.0f);
+}
 
 constexpr int kTlRow = 65;                             // words per time row of a transposed tile
 constexpr int kTlMaxChunks = 16 * kTlColsMaxT / 64;     // 4-element chunks per lane and group
@@ -365,10 +374,8 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
     auto put = [&](int e, V v) {
         const int c = tl_col_of(e, T, tdiv);
         tile[(e - c * T) * kTlRow + c] = v;
-        if constexpr (kF) {
-            const float m = __builtin_fabsf(v);
-            out = out || !(m >= lo && m < hi);
-        }
+        if constexpr (kF)
+            out = out | !tl_tap_exact(v, lo, hi);
     };
     if (ncols == 64 && vec) {
         const int nch = 16 * T;  // 4-element chunks of the group
@@ -395,9 +402,12 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
 // lane = column.  The group's inputs, 64 T contiguous elements, are read with
 // coalesced loads and written transposed into LDS, one row of 64 columns per
 // time step (row stride 65 words: a row read by the 64 lanes touches every
-// bank once).  Each lane then walks its column in time with the taps of its
-// own channel in registers, reading the k inputs of an output from its LDS
-// column, and puts its spikes into a [column][time] byte tile that is
+// bank once).  Each lane then walks its column one residue class r of the
+// dilation at a time (times r, r + d, ...: the taps of a step read the k
+// latest steps of its class), reading one input per step from its LDS column
+// into a k-slot register ring (slot j mod k, a compile-time index inside
+// blocks of k unrolled steps), with the taps of its own channel in
+// registers, and puts its spikes into a [column][time] byte tile that is
 // written back with 16-byte stores.
 template <int DT, int K>
 __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
@@ -420,82 +430,66 @@ __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
     TlLaneTaps<DT, K> taps;
     taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
     V bias;
-    if constexpr (kF)
-        bias = ((const float*)a.bias)[c];
-    else
+    if constexpr (kF) {
+        const float b = ((const float*)a.bias)[c];
+        bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
+    } else {
         bias = ((const int32_t*)a.bias)[c];
+    }
     wave_lds_sync();
 
-    auto tap = [&](V in, int i, auto exact) -> V { return taps.template apply<decltype(exact)::value>(in, i); };
-    const int span = (K - 1) * a.d;
-    const bool pack = (T & 3) == 0;
-    // NO outputs per pass, so that their NO * K LDS reads are in flight together
-    constexpr int NO = K <= 16 ? 4 : 2;
+    const int d = a.d;
+    const int ncls = d < T ? d : T;  // residue classes that hold a step
+    V* hrow = a.h_out != nullptr ? reinterpret_cast<V*>(a.h_out) + gbase + (int64_t)lane * T : nullptr;
     auto walk = [&](auto exact) {
-        for (int t0 = 0; t0 < T; t0 += NO) {
-            V acc[NO];
+        constexpr bool EX = decltype(exact)::value;
+        for (int r = 0; r < ncls; ++r) {
+            const int Lr = (T - r + d - 1) / d;
+            V ring[K];  // x of class step j at slot j mod k; zeros before time 0
 #pragma unroll
-            for (int j = 0; j < NO; ++j)
-                acc[j] = V(0);
-            if (t0 >= span) {
-                // every tap input exists; outputs past the column's end read
-                // its last step (in the tile) and are not stored
+            for (int i = 0; i < K; ++i)
+                ring[i] = V(0);
+            // one step (u: its slot; EDGE: the first block, whose float taps
+            // before time 0 are left out -- Q8.8 keeps them: their zeros'
+            // xor-terms are cancelled by the starting value)
+            auto step = [&](auto uc, auto edge_c, int j) __attribute__((always_inline)) {
+                constexpr int u = decltype(uc)::value;
+                constexpr bool EDGE = decltype(edge_c)::value;
+                constexpr int imin = (kF && EDGE) ? K - 1 - u : 0;
+                const int t = r + j * d;
+                ring[u] = xt[t * kRow + lane];
+                V acc;
+                if constexpr (kF) {
+                    acc = taps.template apply<EX>(ring[(u + 1 + imin) % K], imin);
 #pragma unroll
-                for (int j = 0; j < NO; ++j) {
-                    const int t = t0 + j < T ? t0 + j : T - 1;
-                    V in[K];
+                    for (int i = imin + 1; i < K; ++i)
+                        acc = taps.template accumulate<EX>(acc, ring[(u + 1 + i) % K], i);
+                } else {
+                    acc = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        in[i] = xt[(t - (K - 1 - i) * a.d) * kRow + lane];
-                    acc[j] = taps.start();
-#pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc[j] = taps.template accumulate<decltype(exact)::value>(acc[j], in[i], i);
+                        acc = taps.template accumulate<EX>(acc, ring[(u + 1 + i) % K], i);
                 }
-            } else {
-                // from the first tap whose input exists (time >= 0): the
-                // others read time 0 and are not added
-#pragma unroll
-                for (int j = 0; j < NO; ++j) {
-                    const int t = t0 + j < T ? t0 + j : T - 1;
-                    V in[K];
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        const int tau = t - (K - 1 - i) * a.d;
-                        in[i] = xt[(tau > 0 ? tau : 0) * kRow + lane];
-                    }
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        const V sum = acc[j] + tap(in[i], i, exact);
-                        acc[j] = t - (K - 1 - i) * a.d >= 0 ? sum : acc[j];
-                    }
-                }
-            }
-            uint32_t s4 = 0;
-#pragma unroll
-            for (int j = 0; j < NO; ++j) {
-                const int t = t0 + j;
-                const V h = acc[j] + bias;
+                const V h = acc + bias;
                 bool fire;
                 if constexpr (kF)
                     fire = h >= a.v_th;
                 else
                     fire = h >= a.v_th_q;
-                s4 |= (fire ? 1u : 0u) << (8 * j);
-                if (t < T) {
-                    if (!pack)
-                        st[lane * T + t] = fire ? 1 : 0;
-                    if (a.h_out != nullptr && lane < ncols)
-                        reinterpret_cast<V*>(a.h_out)[gbase + (int64_t)lane * T + t] = h;
-                }
-            }
-            if (pack) {  // T and t0 multiples of 4
-                if constexpr (NO == 4) {
-                    *reinterpret_cast<uint32_t*>(st + lane * T + t0) = s4;
-                } else {
-                    *reinterpret_cast<uint16_t*>(st + lane * T + t0) = (uint16_t)s4;
-                }
-            }
+                st[lane * T + t] = fire ? 1 : 0;
+                if (hrow != nullptr && lane < ncols)
+                    hrow[t] = h;
+            };
+            auto block = [&](int b, auto edge_c) __attribute__((always_inline)) {
+                [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
+                    (void)((b * K + U < Lr ? (step(std::integral_constant<int, U>{}, edge_c, b * K + U), true)
+                                           : false) &&
+                           ...);
+                }(std::make_integer_sequence<int, K>{});
+            };
+            block(0, std::true_type{});
+            for (int b = 1; b * K < Lr; ++b)
+                block(b, std::false_type{});
         }
     };
     if (slow)
@@ -538,15 +532,16 @@ __device__ __forceinline__ uint16_t tl_bf16_rne(float v)
 // Backward (App. A.3: Eqs. backward_X, backward_W, backward_b, generalized
 // to dilation d) for short columns in the time-last layout, lane = column
 // as in tl_cols_kernel.  The group's x and grad_spikes are staged transposed
-// in LDS.  A forward walk recomputes H (the definition's sum), takes
-// dH = grad_spikes * sigma'(H - V_th), writes dH over grad_spikes in the
-// tile and adds the exact products x[t - (k-1-i) d] dH[t] and dH[t] of the
-// lane's column to its grad_w / grad_b sums (double, or int64 for Q8.8).  A
-// second walk forms grad_x[t] = sum over taps i ascending, with
-// t + (k-1-i) d < T, of sign_i dH[t + (k-1-i) d] 2^-s_i into the x tile,
-// which is stored with coalesced writes.  The 64 lanes' sums are reduced per
-// (n, c) row (lanes of one row are consecutive) and stored to the row's slot
-// of this block, part[block + n C + c][k+1].
+// in LDS.  Each lane walks every residue class of its column backwards in
+// time, as the time-first backward walks one: a k-slot ring holds the inputs
+// of the step's taps (zeros before time 0), H is recomputed from them, dH =
+// grad_spikes * sigma'(H - V_th), the exact products x dH and dH are added
+// to the lane's grad_w / grad_b sums (double, or int64 for Q8.8), and dH is
+// scattered tap by tap into k grad_x accumulators; an output is complete
+// when the walk reaches its own step, and is written over its grad_spikes in
+// the tile, which is stored with coalesced writes at the end.  The 64
+// lanes' sums are reduced per (n, c) row (lanes of one row are consecutive)
+// and stored to the row's slot of this block, part[block + n C + c][k+1].
 template <int DT, int K>
 __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 {
@@ -560,8 +555,8 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     const int64_t col0 = (int64_t)blockIdx.x * 64;
     const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
     const int64_t gbase = col0 * T;
-    V* xt = reinterpret_cast<V*>(tl_lds);  // x, then grad_x; row T zeros
-    V* gt = xt + (T + 1) * kRow;           // grad_spikes, then dH; row T zeros
+    V* xt = reinterpret_cast<V*>(tl_lds);  // x
+    V* gt = xt + (T + 1) * kRow;           // grad_spikes, then grad_x
     const bool slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
     (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
 
@@ -570,161 +565,131 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     TlLaneTaps<DT, K> taps;
     taps.load(a.sign, a.shift, c, a.shift_lo, a.shift_hi);
     V bias;
-    if constexpr (kF)
-        bias = ((const float*)a.bias)[c];
-    else
+    if constexpr (kF) {
+        const float b = ((const float*)a.bias)[c];
+        bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
+    } else {
         bias = ((const int32_t*)a.bias)[c];
+    }
     Surrogate sg;
     sg.init(a.sg, a.alpha);
     wave_lds_sync();
 
-    // Taps whose input lies outside the sequence read row T of a tile, which
-    // holds zeros: their grad_w products are zeros, and with the ldexp taps
-    // their terms are zeros too, which leave a sum that starts at +0 as it
-    // is; the exponent-add taps of such inputs are not zeros and are
-    // selected away.
-    xt[T * kRow + lane] = V(0);
-    gt[T * kRow + lane] = V(0);
-    const int span = (K - 1) * a.d;
-
-    // walk 1: H, dH (over grad_spikes in the tile), grad_w and grad_b sums.
-    // Steps go in pairs whose LDS reads all issue before either step's
-    // write, so that two independent chains are in flight; steps whose taps
-    // reach before time 0 (t < span) run apart, with the selects they need.
     W gw[K], gb = W(0);
 #pragma unroll
     for (int i = 0; i < K; ++i)
         gw[i] = W(0);
-    bool out_dh = false;
-    auto walk1 = [&](auto exact) {
+    const int d = a.d;
+    const int ncls = d < T ? d : T;  // residue classes that hold a step
+    const bool live = lane < ncols;  // lanes past the last column add nothing
+    // the zero of the grad_x accumulators (Q8.8: one for each negative tap
+    // that reaches the output)
+    const V reset = kF ? V(0) : V(taps.nneg);
+    auto walk = [&](auto exact) {
         constexpr bool EX = decltype(exact)::value;
-        auto steps = [&](int t, auto npair, auto edge_c) {
-            constexpr int NP = decltype(npair)::value;
-            constexpr bool NEAR = decltype(edge_c)::value;  // some tap before time 0
-            constexpr bool EDGE = NEAR && !EX;              // ... whose term must be selected away
-            V in[NP][K], gv[NP], dh[NP];
+        for (int r = 0; r < ncls; ++r) {
+            const int jtop = (T - r + d - 1) / d - 1;  // last step of the class
+            // time of class step j' sits in slot (jtop - j') mod k
+            V xf[K];
+            W xd[kF ? K : 1];
+            V gxa[K];
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-#pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    const int tau = t + p - (K - 1 - i) * a.d;
-                    in[p][i] = xt[(NEAR && tau < 0 ? T : tau) * kRow + lane];
-                }
-                gv[p] = gt[(t + p) * kRow + lane];
+            for (int m = 0; m < K - 1; ++m) {
+                const int jm = jtop - m;
+                xf[m] = jm >= 0 ? xt[(r + jm * d) * kRow + lane] : V(0);
+                if constexpr (kF)
+                    xd[m] = (double)xf[m];
             }
 #pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                V acc;
-                if constexpr (EDGE) {
-                    acc = V(0);
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        const V sum = acc + taps.template apply<EX>(in[p][i], i);
-                        acc = t + p - (K - 1 - i) * a.d >= 0 ? sum : acc;
-                    }
+            for (int s2 = 0; s2 < K; ++s2) {
+                if constexpr (kF) {
+                    gxa[s2] = V(0);
                 } else {
-                    // every term counts (the zero rows' terms are zeros)
+                    const int skip = max(0, (jtop - s2) + K - (jtop + 1));  // taps whose source lies past the end
+                    gxa[s2] = __builtin_popcount(taps.negmask >> skip);
+                }
+            }
+            // one step (u: its position in the block, j = jtop - bk - u); time
+            // j - k + 1 + i, the source of tap i and the output tap i of dH[j]
+            // reaches, sits in slot (u + k - 1 - i) mod k
+            auto step = [&](auto uc, int j) __attribute__((always_inline)) {
+                constexpr int u = decltype(uc)::value;
+                auto sl = [](int i) constexpr { return (u + K - 1 - i) % K; };
+                const int t = r + j * d;
+                const int jn = j - (K - 1);
+                const V xn = jn >= 0 ? xt[(r + jn * d) * kRow + lane] : V(0);
+                const V gv = gt[t * kRow + lane];
+                xf[sl(0)] = xn;
+                if constexpr (kF)
+                    xd[sl(0)] = (double)xn;
+                V acc;
+                if constexpr (kF) {
+                    acc = taps.template apply<EX>(xf[sl(0)], 0);
+#pragma unroll
+                    for (int i = 1; i < K; ++i)
+                        acc = taps.template accumulate<EX>(acc, xf[sl(i)], i);
+                } else {
                     acc = taps.start();
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc = taps.template accumulate<EX>(acc, in[p][i], i);
+                        acc = taps.template accumulate<EX>(acc, xf[sl(i)], i);
                 }
                 const V h = acc + bias;
-                dh[p] = delta_h(gv[p], sg_factor(sg, h, a.v_th, a.v_th_q));
-            }
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                gt[(t + p) * kRow + lane] = dh[p];
-                gb += (W)dh[p];
-#pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    if constexpr (kF)
-                        gw[i] = __builtin_fma((double)in[p][i], (double)dh[p], gw[i]);  // exact product, one rounding
-                    else
-                        gw[i] += (int64_t)in[p][i] * (int64_t)dh[p];
-                }
+                const V dh = delta_h(gv, sg_factor(sg, h, a.v_th, a.v_th_q));
                 if constexpr (kF) {
-                    const float m = __builtin_fabsf(dh[p]);
-                    out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
-                }
-            }
-        };
-        const int te = span < T ? span : T;
-        int t = 0;
-        for (; t + 1 < te; t += 2)
-            steps(t, std::integral_constant<int, 2>{}, std::true_type{});
-        if (t < te)
-            steps(t++, std::integral_constant<int, 1>{}, std::true_type{});
-        for (; t + 1 < T; t += 2)
-            steps(t, std::integral_constant<int, 2>{}, std::false_type{});
-        if (t < T)
-            steps(t, std::integral_constant<int, 1>{}, std::false_type{});
-    };
-    if (slow_x)
-        walk1(std::true_type{});
-    else
-        walk1(std::false_type{});
-    const bool slow_dh = kF && __builtin_amdgcn_ballot_w64(out_dh) != 0;
-    wave_lds_sync();
-
-    // walk 2: grad_x into the x tile, in pairs as walk 1; steps whose taps
-    // reach past T-1 (t >= T - span) run apart with their selects
-    auto walk2 = [&](auto exact) {
-        constexpr bool EX = decltype(exact)::value;
-        auto steps = [&](int t, auto npair, auto edge_c) {
-            constexpr int NP = decltype(npair)::value;
-            constexpr bool NEAR = decltype(edge_c)::value;  // some tap past T-1
-            constexpr bool EDGE = NEAR && !EX;
-            V in[NP][K];
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-#pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    const int tau = t + p + (K - 1 - i) * a.d;
-                    in[p][i] = gt[(NEAR && tau >= T ? T : tau) * kRow + lane];
-                }
-            }
-            V acc[NP];
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                if constexpr (EDGE) {
-                    acc[p] = V(0);
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        const V sum = acc[p] + taps.template apply<EX>(in[p][i], i);
-                        acc[p] = t + p + (K - 1 - i) * a.d < T ? sum : acc[p];
-                    }
-                } else {
-                    acc[p] = taps.start();
+                    const double dd = live ? (double)dh : 0.0;
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        acc[p] = taps.template accumulate<EX>(acc[p], in[p][i], i);
-                }
-            }
+                        gw[i] = __builtin_fma(xd[sl(i)], dd, gw[i]);  // exact product, one rounding
+                    gb += dd;
+                    if (tl_tap_exact(dh, a.fast_lo, a.fast_hi)) {
 #pragma unroll
-            for (int p = 0; p < NP; ++p)
-                xt[(t + p) * kRow + lane] = acc[p];
-        };
-        const int tb = T - span > 0 ? T - span : 0;  // first step with a tap past T-1
-        int t = 0;
-        for (; t + 1 < tb; t += 2)
-            steps(t, std::integral_constant<int, 2>{}, std::false_type{});
-        if (t < tb)
-            steps(t++, std::integral_constant<int, 1>{}, std::false_type{});
-        for (; t + 1 < T; t += 2)
-            steps(t, std::integral_constant<int, 2>{}, std::true_type{});
-        if (t < T)
-            steps(t, std::integral_constant<int, 1>{}, std::true_type{});
+                        for (int i = 0; i < K; ++i)
+                            gxa[sl(i)] = __builtin_fmaf(dh, taps.w[i], gxa[sl(i)]);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            gxa[sl(i)] = gxa[sl(i)] + dh * taps.w[i];
+                    }
+                } else {
+                    const int32_t dq = live ? dh : 0;
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        gw[i] += (int64_t)xf[sl(i)] * (int64_t)dq;
+                    gb += dq;
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        gxa[sl(i)] = taps.template accumulate<true>(gxa[sl(i)], dh, i);
+                }
+                // output j is complete (the k-1 steps above it have scattered
+                // into its slot, sl(k-1) = u): over its grad_spikes
+                gt[t * kRow + lane] = gxa[u];
+                gxa[u] = reset;  // the slot now holds output j - k
+            };
+            auto block = [&](int b, auto last_c) __attribute__((always_inline)) {
+                constexpr bool LAST = decltype(last_c)::value;
+                const int jhi = jtop - b * K;
+                [&]<int... U>(std::integer_sequence<int, U...>) __attribute__((always_inline)) {
+                    (void)(((!LAST || jhi - U >= 0) ? (step(std::integral_constant<int, U>{}, jhi - U), true)
+                                                    : false) &&
+                           ...);
+                }(std::make_integer_sequence<int, K>{});
+            };
+            const int blast = jtop / K;
+            for (int b = 0; b < blast; ++b)
+                block(b, std::false_type{});
+            block(blast, std::true_type{});
+        }
     };
-    if (slow_dh)
-        walk2(std::true_type{});
+    if (slow_x)
+        walk(std::true_type{});
     else
-        walk2(std::false_type{});
+        walk(std::false_type{});
     wave_lds_sync();
 
     for (int e = lane; e < ncols * T; e += 64) {
         const int cc = tl_col_of(e, T, a.tdiv);
-        const V v = xt[(e - cc * T) * kRow + cc];
+        const V v = gt[(e - cc * T) * kRow + cc];
         if constexpr (DT == MFPSN_BF16)
             reinterpret_cast<uint16_t*>(a.grad_x)[gbase + e] = tl_bf16_rne(v);
         else
@@ -795,8 +760,7 @@ __device__ __forceinline__ bool tl_stage_window(const void* src, int64_t cbase, 
                 dst[j] = v[q];
                 if constexpr (CHECK && DT != MFPSN_Q8_8) {
                     const int t = t_first + j;
-                    const float m = __builtin_fabsf(v[q]);
-                    out = out || (t >= 0 && t < T && !(m >= lo && m < hi));
+                    out = out | ((t >= 0) & (t < T) & !tl_tap_exact(v[q], lo, hi));
                 }
             }
         }
@@ -925,8 +889,7 @@ __global__ __launch_bounds__(kTlWaves * 64) void tl_seg_bwd_kernel(TlBwdArgs a)
                 const V dh = delta_h(ds[j], sg_factor(sg, h, a.v_th, a.v_th_q));
                 ds[j] = dh;
                 if constexpr (kF) {
-                    const float m = __builtin_fabsf(dh);
-                    out_dh = out_dh || !(m >= a.fast_lo && m < a.fast_hi);
+                    out_dh = out_dh | !tl_tap_exact(dh, a.fast_lo, a.fast_hi);
                 }
                 if (j < L) {  // this segment's own step
                     gb += (W)dh;
