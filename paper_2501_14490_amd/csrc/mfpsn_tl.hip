@@ -351,6 +351,27 @@ __device__ __forceinline__ bool tl_tap_exact(float v, float lo, float hi)
 }
 
 constexpr int kTlRow = 65;                             // words per time row of a transposed tile
+// The transposed LDS tiles of the short-column kernels hold bf16 data as its
+// 16-bit values (half the LDS per wave, so twice the waves fit on a CU) and
+// other data as the 32-bit values the registers hold.  Rows of 65 words (66
+// halves): a row read by the 64 lanes touches every bank once.
+template <int DT> struct TlTile {
+    using V = typename TlIO<DT>::V;
+    using E = V;
+    static constexpr int kRow = kTlRow;
+    static __device__ __forceinline__ E put(V v) { return v; }
+    static __device__ __forceinline__ V get(E e) { return e; }
+};
+template <> struct TlTile<MFPSN_BF16> {
+    using E = uint16_t;
+    static constexpr int kRow = 2 * kTlRow - 64;
+    static __device__ __forceinline__ E put(float v) { return (uint16_t)(__builtin_bit_cast(uint32_t, v) >> 16); }
+    static __device__ __forceinline__ float get(E e) { return __builtin_bit_cast(float, (uint32_t)e << 16); }
+};
+template <int DT> constexpr size_t tl_tile_bytes(int T)
+{
+    return (size_t)T * TlTile<DT>::kRow * sizeof(typename TlTile<DT>::E);
+}
 constexpr int kTlMaxChunks = 16 * kTlColsMaxT / 64;     // 4-element chunks per lane and group
 
 // Column of the e-th element of a group of columns of length T (e < 64 T)
@@ -360,12 +381,12 @@ __device__ __forceinline__ int tl_col_of(int e, int T, uint32_t tdiv)
 }
 
 // Stages a group's ncols * T contiguous elements of src (from element gbase)
-// into the transposed tile tile[tau * kTlRow + col], with 4-element vector
+// into the transposed tile tile[tau * kRow + col], with 4-element vector
 // loads for a whole group when vec is set.  Returns (wave-uniform) whether
 // some staged float lies outside [lo, hi); always false for Q8.8.
 template <int DT>
 __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int ncols, int T, uint32_t tdiv, bool vec,
-                                         typename TlIO<DT>::V* tile, float lo, float hi)
+                                         typename TlTile<DT>::E* tile, float lo, float hi)
 {
     using V = typename TlIO<DT>::V;
     constexpr bool kF = DT != MFPSN_Q8_8;
@@ -373,7 +394,7 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
     bool out = false;
     auto put = [&](int e, V v) {
         const int c = tl_col_of(e, T, tdiv);
-        tile[(e - c * T) * kTlRow + c] = v;
+        tile[(e - c * T) * TlTile<DT>::kRow + c] = TlTile<DT>::put(v);
         if constexpr (kF)
             out = out | !tl_tap_exact(v, lo, hi);
     };
@@ -413,16 +434,17 @@ template <int DT, int K>
 __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
 {
     using V = typename TlIO<DT>::V;
+    using Tile = TlTile<DT>;
     constexpr bool kF = DT != MFPSN_Q8_8;
-    constexpr int kRow = kTlRow;
+    constexpr int kRow = Tile::kRow;
     extern __shared__ uint32_t tl_lds[];
     const int lane = (int)threadIdx.x;
     const int T = a.T;
     const int64_t col0 = (int64_t)blockIdx.x * 64;
     const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
     const int64_t gbase = col0 * T;
-    V* xt = reinterpret_cast<V*>(tl_lds);
-    uint8_t* st = reinterpret_cast<uint8_t*>(tl_lds) + ((T * kRow * 4 + 15) & ~15);
+    typename Tile::E* xt = reinterpret_cast<typename Tile::E*>(tl_lds);
+    uint8_t* st = reinterpret_cast<uint8_t*>(tl_lds) + ((tl_tile_bytes<DT>(T) + 15) & ~(size_t)15);
     const bool slow = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
 
     const int64_t col = col0 + (lane < ncols ? lane : 0);
@@ -457,7 +479,7 @@ __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
                 constexpr bool EDGE = decltype(edge_c)::value;
                 constexpr int imin = (kF && EDGE) ? K - 1 - u : 0;
                 const int t = r + j * d;
-                ring[u] = xt[t * kRow + lane];
+                ring[u] = Tile::get(xt[t * kRow + lane]);
                 V acc;
                 if constexpr (kF) {
                     acc = taps.template apply<EX>(ring[(u + 1 + imin) % K], imin);
@@ -546,17 +568,19 @@ template <int DT, int K>
 __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 {
     using V = typename TlIO<DT>::V;
+    using Tile = TlTile<DT>;
+    using E = typename Tile::E;
     constexpr bool kF = DT != MFPSN_Q8_8;
     using W = std::conditional_t<kF, double, int64_t>;
-    constexpr int kRow = kTlRow;
+    constexpr int kRow = Tile::kRow;
     extern __shared__ uint32_t tl_lds[];
     const int lane = (int)threadIdx.x;
     const int T = a.T;
     const int64_t col0 = (int64_t)blockIdx.x * 64;
     const int ncols = a.M - col0 < 64 ? (int)(a.M - col0) : 64;
     const int64_t gbase = col0 * T;
-    V* xt = reinterpret_cast<V*>(tl_lds);  // x
-    V* gt = xt + (T + 1) * kRow;           // grad_spikes, then grad_x
+    E* xt = reinterpret_cast<E*>(tl_lds);  // x
+    E* gt = xt + T * kRow;                 // grad_spikes, then grad_x (bf16: its rounded bits)
     const bool slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
     (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
 
@@ -596,7 +620,7 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 #pragma unroll
             for (int m = 0; m < K - 1; ++m) {
                 const int jm = jtop - m;
-                xf[m] = jm >= 0 ? xt[(r + jm * d) * kRow + lane] : V(0);
+                xf[m] = jm >= 0 ? Tile::get(xt[(r + jm * d) * kRow + lane]) : V(0);
                 if constexpr (kF)
                     xd[m] = (double)xf[m];
             }
@@ -617,8 +641,8 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
                 auto sl = [](int i) constexpr { return (u + K - 1 - i) % K; };
                 const int t = r + j * d;
                 const int jn = j - (K - 1);
-                const V xn = jn >= 0 ? xt[(r + jn * d) * kRow + lane] : V(0);
-                const V gv = gt[t * kRow + lane];
+                const V xn = jn >= 0 ? Tile::get(xt[(r + jn * d) * kRow + lane]) : V(0);
+                const V gv = Tile::get(gt[t * kRow + lane]);
                 xf[sl(0)] = xn;
                 if constexpr (kF)
                     xd[sl(0)] = (double)xn;
@@ -663,7 +687,10 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
                 }
                 // output j is complete (the k-1 steps above it have scattered
                 // into its slot, sl(k-1) = u): over its grad_spikes
-                gt[t * kRow + lane] = gxa[u];
+                if constexpr (DT == MFPSN_BF16)
+                    gt[t * kRow + lane] = tl_bf16_rne(gxa[u]);
+                else
+                    gt[t * kRow + lane] = gxa[u];
                 gxa[u] = reset;  // the slot now holds output j - k
             };
             auto block = [&](int b, auto last_c) __attribute__((always_inline)) {
@@ -689,11 +716,7 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
 
     for (int e = lane; e < ncols * T; e += 64) {
         const int cc = tl_col_of(e, T, a.tdiv);
-        const V v = gt[(e - cc * T) * kRow + cc];
-        if constexpr (DT == MFPSN_BF16)
-            reinterpret_cast<uint16_t*>(a.grad_x)[gbase + e] = tl_bf16_rne(v);
-        else
-            reinterpret_cast<V*>(a.grad_x)[gbase + e] = v;
+        reinterpret_cast<E*>(a.grad_x)[gbase + e] = gt[(e - cc * T) * kRow + cc];
     }
 
     // per-channel sums: segments of consecutive lanes with one channel
@@ -1096,7 +1119,7 @@ template <int DT, int K>
 void launch_k(const TlArgs& a, hipStream_t st)
 {
     if (a.T <= kTlColsMaxT) {
-        const size_t lds = ((size_t)a.T * 65 * 4 + 15) / 16 * 16 + (size_t)64 * a.T;
+        const size_t lds = (tl_tile_bytes<DT>(a.T) + 15) / 16 * 16 + (size_t)64 * a.T;
         const int64_t blocks = (a.M + 63) / 64;
         auto kern = tl_cols_kernel<DT, K>;
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
@@ -1133,7 +1156,7 @@ template <int DT, int K>
 int64_t launch_bwd_k(const TlBwdArgs& a, hipStream_t st)
 {
     if (a.T <= kTlColsMaxT) {
-        const size_t lds = (size_t)2 * (a.T + 1) * kTlRow * 4;
+        const size_t lds = 2 * tl_tile_bytes<DT>(a.T);
         const int64_t blocks = (a.M + 63) / 64;
         auto kern = tl_cols_bwd_kernel<DT, K>;
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64), lds, st, a);
