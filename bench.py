@@ -590,11 +590,14 @@ class Flush:
 
     def __init__(self, torch, dev):
         self.torch = torch
-        self.buf = torch.ones(self.BYTES // 4, dtype=torch.int32, device=dev)
-        self.acc = torch.zeros((), dtype=torch.int64, device=dev)
+        self.buf = torch.ones(self.BYTES // 4, dtype=torch.float32, device=dev)
+        self.acc = torch.zeros((), dtype=torch.float32, device=dev)
 
     def __call__(self):
-        self.acc += self.buf.sum(dtype=self.torch.int64)
+        # a float sum reduces the buffer in place (an int32 sum into int64
+        # first writes a converted 2 GiB copy, whose dirty lines the timed
+        # call would then evict)
+        self.acc += self.buf.sum()
 
 
 def measure(torch, dev, wl, mode, steps: int, warmup: int, flush, hev):
