@@ -977,14 +977,8 @@ __device__ __forceinline__ int64_t wave_sum(int64_t v)
 // surrogate factor, or the forward's saved potentials H.
 enum SavedKind : int { kRecompute = 0, kSavedFactor = 1, kSavedH = 2 };
 
-// Waves per SIMD the backward's register budget must allow (1: no bound).
-#ifndef MFPSN_BWD_WAVES_PER_EU
-#define MFPSN_BWD_WAVES_PER_EU 1
-#endif
-
 template <int K, int DT, int MODE, int HS, int NV>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MFPSN_BWD_WAVES_PER_EU))) void bwd_kernel(
-    BwdArgs a)
+__global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 {
     using V = typename IO<DT>::V;
     using W = typename IO<DT>::W;
