@@ -18,9 +18,6 @@ namespace {
 
 int grad_x_bytes(int dtype) { return dtype == MFPSN_BF16 ? 2 : 4; }
 
-// Longest chunk of class steps (a multiple of k) whose byte span, with the
-// halo and prefetch rows, still fits the 31-bit scalar offsets the kernels
-// use inside one item (4-byte elements, the widest stream); 0 if none fits.
 // Longest chunk of a residue class (a multiple of k) whose rows, with the
 // halo and prefetch rows around it, keep every 32-bit buffer offset of an
 // item in range; row_es is the widest element of the streams the call
@@ -168,6 +165,7 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0, int row_es =
             g.fast_lo = ldexpf(1.0f, emin - 127);
             g.fast_hi = emax == 254 ? INFINITY : ldexpf(1.0f, emax - 126);
         }
+        g.x_exact = d->dtype == MFPSN_BF16 && d->shift_lo >= 0 && d->shift_hi <= 16;
     }
     if (flat > 0) {
         g.mode = kFlat;

@@ -50,11 +50,17 @@ struct Geom {
     int32_t sg;        // surrogate kind
     float alpha, v_th;
     int32_t v_th_q;
-    // Float taps move the exponent with one integer add when the input is a
-    // normal number far enough from the exponent limits: fast_lo <= |x| <
-    // fast_hi (derived from [shift_lo, shift_hi]); other inputs (zero,
-    // subnormal, infinite, NaN, near-limit) take the exact ldexp path.
+    // A float tap's product x * (sign 2^-shift) is exact for every shift in
+    // [shift_lo, shift_hi] when x is zero or fast_lo <= |x| < fast_hi; such
+    // inputs add their terms with one fused multiply-add, the others (tiny,
+    // huge, infinite, NaN) round the product first, then add.
     float fast_lo, fast_hi;
+    // 1: every stored input has exact tap products, so the inputs are not
+    // checked (bf16 storage with shifts in [0, 16]: an input is m 2^e with
+    // |m| < 2^8 and e >= -133, so m 2^(e - s) is a float for s <= 16 and
+    // never grows for s >= 0; infinities and NaN give the same result either
+    // way)
+    int32_t x_exact;
 };
 
 // Columns per lane of the flat forward: 16 bytes of x per lane up to order

@@ -567,8 +567,7 @@ __device__ __forceinline__ bool lane_slow(const Pk<int32_t, NV>&, const Geom&)
 {
     return false;
 }
-// True (wave-uniform) when some lane's value is outside the range in which
-// the exponent-add tap is exact.
+// True (wave-uniform) when some lane's value has an inexact tap product.
 template <int NV>
 __device__ __forceinline__ bool any_slow(const Pk<float, NV>& v, const Geom& g)
 {
@@ -578,6 +577,13 @@ template <int NV>
 __device__ __forceinline__ bool any_slow(const Pk<int32_t, NV>&, const Geom&)
 {
     return false;
+}
+// The same for stored inputs, which are not checked where the storage type
+// and shift range make every tap product exact.
+template <typename PV>
+__device__ __forceinline__ bool x_slow(const PV& v, const Geom& g)
+{
+    return !g.x_exact && any_slow(v, g);
 }
 
 // Q8.8 charge of one column: start + sum_i ((x_i >> s_i) ^ m_i), an exact
@@ -851,7 +857,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             if (j0 > 0) {
 #pragma unroll
                 for (int m = 0; m < K - 1; ++m) {
-                    const bool bad = __builtin_amdgcn_ballot_w64(lane_slow(ring[(m + 1) % K], g)) != 0;
+                    const bool bad = x_slow(ring[(m + 1) % K], g);
                     slow = bad ? m + 1 : slow;
                 }
             }
@@ -875,7 +881,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             PV h;
             uint32_t spk[(NV + 3) / 4] = {};  // spike of column e in byte e mod 4 of word e / 4
             if constexpr (kF) {
-                if (any_slow(xv, g))
+                if (x_slow(xv, g))
                     slow = K;
                 if (__builtin_expect(slow > 0, 0)) {
 #pragma unroll
@@ -922,7 +928,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 #pragma unroll
                 for (int e = 0; e < NV; ++e)
                     if constexpr (kF)
-                        w.v[e] = __builtin_bit_cast(uint32_t, sg_factor(sg, h.v[e], vth, vthq));
+                        w.v[e] = __builtin_bit_cast(uint32_t, sg_factor<false>(sg, h.v[e], vth, vthq));
                     else
                         w.v[e] = (uint32_t)qt(sg, h.v[e], vthq);
                 st_words<NV>(gs, vh, so_h, w);
@@ -1163,7 +1169,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                     if (live)
                         out = out | lane_slow(v, g);
             }
-            if (kRe && TP::kHasFast && __builtin_amdgcn_ballot_w64(out) != 0)
+            if (kRe && TP::kHasFast && !g.x_exact && __builtin_amdgcn_ballot_w64(out) != 0)
                 slow_x = K;
         }
         int32_t so_gp = (jtop - P - jb) * xstep;           // g of step j - P
@@ -1210,7 +1216,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                     xd[sl(0)].v[e] = (double)xv.v[e];
             if constexpr (kXV)
                 xf[sl(0)] = xv;
-            if (kRe && TP::kHasFast && (full || j - K + 1 >= 0) && any_slow(xv, g))
+            if (kRe && TP::kHasFast && (full || j - K + 1 >= 0) && x_slow(xv, g))
                 slow_x = K;
             {
                 PV dh;
@@ -1259,9 +1265,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 #pragma unroll
                     for (int e = 0; e < NV; ++e) {
                         if constexpr (kF) {
-                            double dd = (double)dh.v[e];
+                            V de = dh.v[e];
                             if (MODE == kPlane && partial)
-                                dd = active ? dd : 0.0;  // no contribution from shadow lanes
+                                de = active ? de : V(0);  // no contribution from shadow lanes
+                            const double dd = (double)de;
 #pragma unroll
                             for (int i = 0; i < K; ++i) {
                                 gw[i] = __builtin_fma(xd[sl(i)].v[e], dd, gw[i]);

@@ -38,6 +38,25 @@ __device__ __forceinline__ float mf_exp_nonpos(float y)
     return zero ? 0.0f : e;
 }
 
+// n / b rounded to nearest, for b in [1, 4] and n zero or in [2^-100, 2^62]:
+// the reciprocal refined by one Newton step, then the quotient corrected
+// twice by its exact residual.  These are the operations of the general
+// correctly rounded float division, whose operand scaling and special-case
+// fixup leave values in this range unchanged (they act on zero, infinite,
+// subnormal and near-limit operands and quotients only).  b == 1 is exact
+// for any n: the refined reciprocal is 1 and every residual is 0.
+__device__ __forceinline__ float quot_1_4(float n, float b)
+{
+    float r = __builtin_amdgcn_rcpf(b);
+    const float e = __builtin_fmaf(-b, r, 1.0f);
+    r = __builtin_fmaf(e, r, r);
+    float q = n * r;
+    float t = __builtin_fmaf(-b, q, n);
+    q = __builtin_fmaf(t, r, q);
+    t = __builtin_fmaf(-b, q, n);
+    return __builtin_fmaf(t, r, q);
+}
+
 // sigmoid: alpha e / (1 + e)^2 with e = exp(-alpha |u|)
 // atan:    (alpha / 2) / (1 + (pi/2 alpha u)^2)
 // rational: 1 / (1 + alpha u^2)
@@ -45,18 +64,29 @@ __device__ __forceinline__ float mf_exp_nonpos(float y)
 // num / den, with (m, q, num) = (float(pi/2) alpha, 1, alpha/2) or
 // (1, alpha, 1); the multiplications by 1 are exact, so each result is
 // bit-identical to its own formula.
+//
+// The sigmoid's quotient has den^2 in [1, 4] (e in [0, 1]); its numerator
+// alpha e is 0, or at least alpha 2^-24 wherever den^2 > 1 (1 + e rounds to
+// 1 below that).  For alpha = 0 or alpha >= 2^-60 (and alpha <= 1024, which
+// the descriptor's validation guarantees) quot_1_4 therefore gives the
+// correctly rounded quotient; smaller alphas take the general division.
 struct Surrogate {
+    int quick;    // 1: sigmoid with the quotient of quot_1_4
     int sigmoid;  // 1: sigmoid, 0: atan or rational
     float alpha;
     float m, q, num;
     __device__ void init(int kind, float a)
     {
         sigmoid = kind == 0;
+        quick = kind == 0 && (a == 0.0f || a >= 0x1p-60f);
         alpha = a;
         m = kind == 1 ? 0x1.921fb6p+0f * a : 1.0f;
         q = kind == 1 ? 1.0f : a;
         num = kind == 1 ? 0.5f * a : 1.0f;
     }
+    // kQuick = false keeps the general division only (the same results; the
+    // code of both quotients costs registers where a kernel holds many)
+    template <bool kQuick = true>
     __device__ __forceinline__ float operator()(float u) const
     {
         if (sigmoid) {
@@ -65,6 +95,8 @@ struct Surrogate {
             float den = 1.0f + e;
             float nm = alpha * e;
             float den2 = den * den;
+            if (kQuick && __builtin_expect(quick, 1))
+                return quot_1_4(nm, den2);
             return nm / den2;
         }
         float z = m * u;
@@ -77,10 +109,11 @@ struct Surrogate {
 
 // Surrogate factor of a potential: float sigma'(H - v_th); Q8.8 the integer
 // L = round-half-even(2^15 sigma'((H - v_th) / 256)).
+template <bool kQuick = true>
 __device__ __forceinline__ float sg_factor(const Surrogate& sg, float h, float v_th, int)
 {
     float u = h - v_th;
-    return sg(u);
+    return sg.template operator()<kQuick>(u);
 }
 __device__ __forceinline__ int32_t sg_factor_q(const Surrogate& sg, int32_t u)
 {

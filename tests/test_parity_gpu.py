@@ -347,6 +347,77 @@ def test_wide_shift_ranges_keep_every_term(orc, lo, hi):
     compare(got, ref, "bf16", f"plane shifts [{lo}, {hi}]", 6, 3, hi=hi)
 
 
+def _same_or_both_nan(g, r, label):
+    nan = np.isnan(r)
+    assert np.array_equal(np.isnan(g), nan), f"{label}: NaN pattern differs"
+    assert np.array_equal(g[~nan].view(np.uint32), r[~nan].view(np.uint32)), f"{label}: values differ"
+
+
+@pytest.mark.parametrize("saved", [None, "h", "sg"])
+@pytest.mark.parametrize("lo,hi", [(0, 16), (1, 16), (0, 7), (0, 17), (-1, 16)])
+@pytest.mark.parametrize("shape", [(40, 3, 5, (16,)), (30, 4, 3, (6,)), (25, 2, 70, ())])
+def test_bf16_special_inputs(orc, lo, hi, shape, saved):
+    # bf16 inputs: zeros, subnormals, the smallest normals, huge values,
+    # infinities and NaN.  With shifts in [0, 16] every tap product of a bf16
+    # input is exact and the kernels skip the input checks; outside that
+    # range the checks send such inputs to the rounded products.  Either way
+    # H, spikes, the factor and grad_x equal the oracle bit for bit.
+    T, N, C, sp = shape
+    k, d = 6, 2
+    case = workloads.make_small(T, N, C, sp, k=k, s_lo=lo, s_hi=hi, dtype="bf16", seed=hi - lo + T)
+    rng = np.random.default_rng(T + hi)
+    x = case["x"]
+    specials = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x0040, 0x0080, 0x8080, 0x0081, 0x0100,
+                         0x0480, 0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x7FC0], np.uint16)
+    idx = rng.integers(0, x.size, size=x.size // 6)
+    x.ravel()[idx] = specials[rng.integers(0, specials.size, size=idx.size)]
+    got = gpu_run(case, k, d, "bf16", 0.25, lo=lo, hi=hi, saved=saved)
+    ref = oracle_run(orc, case, k, d, "bf16", 0.25, lo=lo, hi=hi)
+    label = f"bf16 specials {shape} shifts [{lo}, {hi}] saved={saved}"
+    assert np.array_equal(got["spikes"], ref["spikes"]), f"{label}: spikes differ"
+    _same_or_both_nan(got["H"], ref["Hf"], label + " H")
+    _same_or_both_nan(got["SG"], ref["SG"], label + " factor")
+    gb = (got["grad_x_bits"].astype(np.uint32) << 16).view(np.float32)
+    rb = (ref["grad_x_bits"].astype(np.uint32) << 16).view(np.float32)
+    check_grad_x(gb, rb, label + " grad_x")
+    for name in ("grad_w", "grad_b"):
+        g = got[name].astype(np.float64)
+        r = ref[name]
+        fin = np.isfinite(r)
+        assert np.array_equal(np.isnan(g), np.isnan(r)), f"{label}: {name} NaN pattern differs"
+        assert np.array_equal(g[~fin & ~np.isnan(r)], r[~fin & ~np.isnan(r)]), f"{label}: {name} infinities differ"
+        err = np.abs(g[fin] - r[fin])
+        assert np.all(err <= GW_ABS + GW_REL * np.abs(r[fin])), f"{label}: {name} max err {err.max()}"
+
+
+@pytest.mark.parametrize("saved", [None, "h"])
+@pytest.mark.parametrize("alpha", [4.0, 1.5, 1e-3, 2.0 ** -59, 2.0 ** -61, 0.0, 1024.0])
+def test_sigmoid_factor_over_its_range(orc, alpha, saved):
+    # order 1, tap +1, zero bias and threshold: H = x and grad_x = dH =
+    # grad_spikes * sigma'(x), with grad_spikes = 1 the factor itself.  The
+    # potentials span the whole sigmoid: the peak, the tails where exp(-alpha
+    # |u|) underflows (alpha |u| near 86) and the range between, where the
+    # backward forms the quotient from a refined reciprocal (alpha 0 or at
+    # least 2^-60) or by the general division (smaller alpha).
+    T, N, C = 64, 16, 64
+    rng = np.random.default_rng(int(alpha * 1000) % 997 + (saved is None))
+    a = np.concatenate([rng.uniform(-100, 100, T * N * C // 2), rng.uniform(60, 90, T * N * C // 4),
+                        rng.standard_normal(T * N * C // 4) * 3])
+    rng.shuffle(a)
+    scale = 1.0 / alpha if alpha > 0 else 1.0
+    x = (a * scale * np.where(rng.random(a.size) < 0.5, -1, 1)).astype(np.float32).reshape(T, N, C)
+    case = {"x": x, "grad_spikes": np.ones_like(x), "sign": np.ones((C, 1), np.int8),
+            "shift": np.zeros((C, 1), np.int8), "bias": np.zeros(C, np.float32)}
+    got = gpu_run(case, 1, 1, "f32", 0.0, alpha=alpha, saved=saved)
+    ref = oracle_run(orc, case, 1, 1, "f32", 0.0, alpha=alpha)
+    assert np.array_equal(got["H"].view(np.uint32), x.view(np.uint32))
+    _same_or_both_nan(got["SG"], ref["SG"], f"alpha {alpha}: forward factor")
+    _same_or_both_nan(got["grad_x"], ref["grad_x"], f"alpha {alpha} saved={saved}: backward factor")
+    _same_or_both_nan(got["grad_x"], ref["SG"], f"alpha {alpha}: grad_x is the factor")
+    if alpha >= 1e-3:
+        assert np.count_nonzero(ref["SG"]) > x.size // 2
+
+
 def test_negative_shifts_near_overflow(orc):
     # left shifts (negative shift) push large inputs toward overflow; the
     # fast range shrinks accordingly and the exact path takes the rest
