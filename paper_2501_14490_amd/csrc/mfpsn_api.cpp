@@ -82,13 +82,7 @@ namespace {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Launch geometry.  Lanes walk residue classes; when the columns alone give
-// too few waves, each class is cut into chunks (multiples of k, of at least
-// 4k steps), down to a target number of (wave-sized) work items per pass:
-// the forward's halo is k-1 loads, so it chunks down to about 8 waves per
-// SIMD; the backward's halo is k-1 steps of work, so it stops at 2.
 constexpr int64_t kFwdTargetItems = 8192;
-constexpr int64_t kBwdTargetItems = 2048;
 // Waves take contiguous ranges of items.  Taking every nw-th item instead
 // (so that the waves running together walk neighbouring tiles) measured
 // slower on MI355X for three of the four workloads (event vision 215 against
@@ -194,35 +188,43 @@ Geom plan(const mfpsn_desc* d, bool backward, int nv, int flat = 0, int row_es =
         }
     }
     g.line_elems = 128 / g.esize;
-    // Cut each residue class into chunks only while the columns alone give
-    // fewer items than the target (or a class spans too many bytes).
+    // Backward: each residue class is one chunk (at most the offset cap), and
+    // the launcher cuts the classes finer for the kernel's resident waves
+    // (balance_chunks), so the block bound allows the finest cut, chunks of k
+    // steps.  Forward: classes are cut into chunks (multiples of k, of at
+    // least 4k steps) only while the columns give fewer than kFwdTargetItems
+    // items over all groups; the halo of a chunk is k-1 loads.
     const int64_t K = d->k;
     const int64_t class_len = d->T > 0 ? ceil_div(d->T, d->dilation) : 0;
     // residue classes that hold a step: d, or T when the dilation exceeds the
     // sequence (classes r >= T are empty)
     g.ncls = d->dilation < d->T ? d->dilation : (d->T > 0 ? d->T : 1);
-    const int64_t base = (int64_t)g.groups * g.tiles * g.ncls;
-    const int64_t cap = max_chunk(d, row_es);
+    const int64_t base = (int64_t)g.tiles * g.ncls;
+    int64_t cap = max_chunk(d, row_es);
+    if (cap > ((int64_t)1 << 30))
+        cap = ((int64_t)1 << 30) / K * K;
     int64_t chunk = ceil_div(class_len > 0 ? class_len : 1, K) * K;
     if (chunk > cap)
         chunk = cap;
     int64_t nchunks = ceil_div(class_len, chunk);
-    const int64_t min_chunk = 4 * K;
-    const int64_t target = backward ? kBwdTargetItems : kFwdTargetItems;
-    while (base * nchunks < target && ceil_div(chunk / 2, K) * K >= min_chunk &&
-           ceil_div(chunk / 2, K) * K < chunk) {
-        chunk = ceil_div(chunk / 2, K) * K;
-        nchunks = ceil_div(class_len, chunk);
+    if (!backward) {
+        while ((int64_t)g.groups * base * nchunks < kFwdTargetItems && ceil_div(chunk / 2, K) * K >= 4 * K &&
+               ceil_div(chunk / 2, K) * K < chunk) {
+            chunk = ceil_div(chunk / 2, K) * K;
+            nchunks = ceil_div(class_len, chunk);
+        }
     }
     if (nchunks < 1)
         nchunks = 1;
+    g.cap = (int32_t)cap;
     g.chunk = (int32_t)chunk;
     g.nchunks = (int32_t)nchunks;
-    g.items = (int64_t)g.tiles * g.ncls * g.nchunks;
+    g.run_max = 1;
+    g.items = base * g.nchunks;
     g.strided = kStridedItems ? 1 : 0;
     // upper bound of the persistent grid (the launcher picks the actual size)
     int64_t blocks = ceil_div(kMaxResidentBlocks, g.groups);
-    const int64_t need = ceil_div(g.items, kWaves);
+    const int64_t need = ceil_div(base * ceil_div(class_len > 0 ? class_len : 1, K), kWaves);
     if (blocks > need)
         blocks = need;
     g.blocks = (int32_t)(blocks > 0 ? blocks : 1);
@@ -350,8 +352,8 @@ int mfpsn_backward(const mfpsn_desc* desc, const void* x, const void* grad_spike
             return MFPSN_ERR_SHAPE;
     }
     BwdArgs a;
-    // (narrower rows than the workspace query assumes give longer chunks,
-    // fewer items and no more blocks, so the queried workspace still holds)
+    // (the block bound, and with it the workspace, does not depend on the
+    // row width: it allows the finest cut of the classes)
     const int row_es = h || sg ? 4 : (es > grad_x_bytes(desc->dtype) ? es : grad_x_bytes(desc->dtype));
     a.g = plan(desc, true, pair_layout(desc) && pair_aligned({x, grad_spikes, h, sg, grad_x}) ? 2 : 1, 0, row_es);
     if (total > 0 && a.g.items > kMaxItems)

@@ -38,6 +38,9 @@ struct Geom {
     int32_t ncls;      // residue classes with a step: min(d, T) (at least 1)
     int32_t nchunks;   // time chunks per residue class
     int32_t chunk;     // class steps per chunk
+    int32_t cap;       // longest run of class steps one walk may span (a multiple
+                       // of k: its rows keep every 32-bit buffer offset in range)
+    int32_t run_max;   // consecutive chunks of one class that one walk takes
     int32_t groups;    // gridDim.y: channel groups (lane-channel), channels (plane) or 1 (flat)
     int32_t blocks;    // gridDim.x: blocks per group (set by the launcher; the
                        // planner's value is the upper bound the workspace is sized for)
@@ -75,6 +78,52 @@ constexpr int flat_nv(int k, int dtype)
 constexpr int kWaves = 4;          // waves per block
 constexpr int kPairMaxK = 16;      // highest order with two-column (nv = 2) kernels
 constexpr int kThreads = 64 * kWaves;
+constexpr int64_t kMaxGroupItems = ((int64_t)1 << 31) - 1;  // items of one group
+
+// Chunks of the residue classes for the backward's `waves` resident waves per
+// group (host).  A wave's items are a contiguous range, and the consecutive
+// chunks of one class in it are walked as one (up to run_max of them), so a
+// chunk costs no halo of its own: the chunk length only decides how evenly
+// the ranges can be cut.  Candidates are the whole class (at most cap steps)
+// and its halvings down to k steps; the estimate of the longest range is
+// ceil(items / waves) chunks of the mean chunk length, plus one halo of k - 1
+// steps when a class is cut.  Ties keep the longer chunk.
+inline void balance_chunks(Geom& g, int64_t waves)
+{
+    const int64_t K = g.k;
+    const int64_t L = g.T > 0 ? ((int64_t)g.T + g.d - 1) / g.d : 0;  // the longest class
+    if (L == 0 || waves < 1 || g.cap < K)
+        return;
+    const int64_t base = (int64_t)g.tiles * g.ncls;
+    const double halo = (double)(K - 1);
+    int64_t c = (L + K - 1) / K * K;
+    if (c > g.cap)
+        c = g.cap;
+    int64_t best_c = 0;
+    double best = 0.0;
+    for (;;) {
+        const int64_t n = (L + c - 1) / c;
+        const int64_t items = base * n;
+        if (items <= kMaxGroupItems) {
+            const double cost =
+                (double)((items + waves - 1) / waves) * ((double)L / (double)n) + (n > 1 ? halo : 0.0);
+            if (best_c == 0 || cost < best) {
+                best = cost;
+                best_c = c;
+            }
+        }
+        const int64_t h = (c / 2 + K - 1) / K * K;
+        if (h < K || h >= c)
+            break;
+        c = h;
+    }
+    if (best_c == 0)
+        return;
+    g.chunk = (int32_t)best_c;
+    g.nchunks = (int32_t)((L + best_c - 1) / best_c);
+    g.items = base * g.nchunks;
+    g.run_max = (int32_t)(g.cap / best_c > 0 ? g.cap / best_c : 1);
+}
 // Upper bound of blocks resident on one GPU at once (8 blocks of 4 waves per
 // CU is 8 waves per SIMD; 320 CUs covers every CDNA part): the persistent grid
 // never exceeds it, so it also bounds the backward's partial rows.

@@ -623,10 +623,12 @@ __device__ __forceinline__ int32_t q88_charge(const TP& tp, int32_t start, X x)
 // the last existing lane of its wave: it computes that lane's values, so its
 // stores duplicate that lane's.  Its grad_w / grad_b contribution is dropped.
 // ---------------------------------------------------------------------------
+// (every member is force-inlined: an out-of-line call puts the cursor on the
+// stack, and the item loop then waits for every pending load to read it)
 struct Cursor {
     int tile, r, chunk;
-    __device__ Cursor(const Geom& g, int64_t q) { set(g, q); }
-    __device__ void set(const Geom& g, int64_t q)
+    __device__ __forceinline__ Cursor(const Geom& g, int64_t q) { set(g, q); }
+    __device__ __forceinline__ void set(const Geom& g, int64_t q)
     {
         const uint32_t u = (uint32_t)q;  // items per group < 2^31 (planner)
         const uint32_t rc = u / (uint32_t)g.nchunks;
@@ -635,7 +637,7 @@ struct Cursor {
         r = (int)(rc - t * (uint32_t)g.ncls);
         tile = (int)t;
     }
-    __device__ void next(const Geom& g)
+    __device__ __forceinline__ void next(const Geom& g)
     {
         if (++chunk == g.nchunks) {
             chunk = 0;
@@ -646,7 +648,7 @@ struct Cursor {
         }
     }
     // to item q of a walk with item step `step` (1: the next item)
-    __device__ void advance(const Geom& g, int64_t q, int64_t step)
+    __device__ __forceinline__ void advance(const Geom& g, int64_t q, int64_t step)
     {
         if (step == 1)
             next(g);
@@ -662,7 +664,7 @@ struct Cursor {
 // the whole tensor.  Either way the waves' item counts differ by at most one.
 struct ItemRange {
     int64_t q0, q1, step;
-    __device__ ItemRange(const Geom& g, int wid, int nw)
+    __device__ __forceinline__ ItemRange(const Geom& g, int wid, int nw)
     {
         if (g.strided) {
             q0 = wid;
@@ -807,11 +809,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     int tile_cached = -1;
     Cols cols{};
     for (int64_t q = q0; q < q1; q += qstep, cur.advance(g, q, qstep)) {
-        // item scalars, pinned to SGPRs
+        // item scalars, pinned to SGPRs; the consecutive chunks of this class
+        // in the range are walked as one
         const int r = uniform(cur.r);
         const int Lr = uniform(class_len(g, r));
         const int j0 = uniform(cur.chunk * g.chunk);
-        const int j1 = uniform(min(Lr, j0 + g.chunk));
+        int more = 0;
+        if (qstep == 1)
+            more = (int)min(min(q1 - 1 - q, (int64_t)(g.nchunks - 1 - cur.chunk)), (int64_t)(g.run_max - 1));
+        more = uniform(more);
+        q += more;
+        cur.chunk += more;
+        const int j1 = uniform(min(Lr, j0 + (more + 1) * g.chunk));
         if (j0 >= j1)
             continue;
         if (cur.tile != tile_cached) {
@@ -1071,11 +1080,18 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
     int tile_cached = -1;
     Cols cols{};
     for (int64_t q = q0; q < q1; q += qstep, cur.advance(g, q, qstep)) {
-        // item scalars, pinned to SGPRs
+        // item scalars, pinned to SGPRs; the consecutive chunks of this class
+        // in the range are walked as one
         const int r = uniform(cur.r);
         const int Lr = uniform(class_len(g, r));
         const int j0 = uniform(cur.chunk * g.chunk);
-        const int j1 = uniform(min(Lr, j0 + g.chunk));
+        int more = 0;
+        if (qstep == 1)
+            more = (int)min(min(q1 - 1 - q, (int64_t)(g.nchunks - 1 - cur.chunk)), (int64_t)(g.run_max - 1));
+        more = uniform(more);
+        q += more;
+        cur.chunk += more;
+        const int j1 = uniform(min(Lr, j0 + (more + 1) * g.chunk));
         if (j0 >= j1)
             continue;
         if (cur.tile != tile_cached) {
@@ -1553,6 +1569,17 @@ int resident_blocks(Kern kern, int (&cache)[16])
 //     share, and a SIMD with more waves issues faster: one wave alone issues
 //     at most one VALU instruction every few cycles and cannot cover its own
 //     dependency latencies (order-32 Q8.8 backward: 384 -> 304 us).
+// Resident waves of one group (the planner's block bound included).
+inline int64_t group_waves(const Geom& g, int resident)
+{
+    int64_t per_group = resident / g.groups;
+    if (per_group < 1)
+        per_group = 1;
+    if (per_group > g.blocks)
+        per_group = g.blocks;
+    return per_group * kWaves;
+}
+
 inline int persistent_blocks(const Geom& g, int resident, bool fill)
 {
     int64_t per_group = resident / g.groups;
@@ -1641,7 +1668,9 @@ hipError_t bwd_k(BwdArgs& a, hipStream_t st)
                                                : bwd_kernel_for<K, DT, kRecompute>(a.g, slot);
     if (kern == nullptr)
         return hipErrorInvalidValue;
-    a.g.blocks = persistent_blocks(a.g, resident_blocks(kern, cache[hs][slot]), true);
+    const int res = resident_blocks(kern, cache[hs][slot]);
+    balance_chunks(a.g, group_waves(a.g, res));
+    a.g.blocks = persistent_blocks(a.g, res, true);
     hipLaunchKernelGGL(kern, dim3(a.g.blocks, a.g.groups), dim3(kThreads), 0, st, a);
     return hipGetLastError();
 }
