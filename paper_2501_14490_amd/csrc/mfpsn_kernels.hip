@@ -6,24 +6,27 @@
 // Work decomposition.  x is time-first, [T][N][C][S]; the M = N*C*S columns
 // are independent time series.  A dilated order-k convolution only couples
 // time steps of one residue class t = r (mod d), so each lane walks one
-// column along one residue class (class step j <-> time r + j*d), optionally
-// restricted to a chunk [j0, j1) of class steps (chunks start at multiples of
-// k).  Each wave owns an equal share of these items (a contiguous range), so
-// the persistent grid finishes together.  Register rings are indexed by
-// j mod k, and the walks are unrolled in blocks of k steps aligned to
-// multiples of k, so every ring slot is a compile-time register.  Block
+// column along one residue class (class step j <-> time r + j*d), or a run of
+// consecutive chunks of it [j0, j1) (chunks start at multiples of k).  Each
+// wave owns a contiguous range of these items whose length differs from the
+// others' by at most one, so the persistent grid finishes together.  Register
+// rings are indexed by the class step mod k, and the walks are unrolled in
+// blocks of k steps, so every ring slot is a compile-time register.  Block
 // variants: full (no bounds checks), checked (per-step uniform guards and
-// clamped prefetches), and the block that touches the start of the sequence,
-// where the taps that would read before time 0 are left out at compile time.
+// clamped prefetches), the forward's block at the start of the sequence,
+// where the taps that would read before time 0 are left out at compile time,
+// and the backward's last block, which stops at the item's end.
 //
 // Memory: one raw buffer resource per tensor and item, a per-lane column
 // offset, and a per-step running scalar offset (one SALU add per stream and
 // step).  Loads run P class steps ahead of their use.
 //
-// Taps never multiply: a float tap moves the exponent, either with one
-// integer add of ((-shift) << 23) ^ sign-bit to the bit pattern (normal
-// values whose result stays normal) or with v_ldexp_f32 and a sign flip (any
-// other value); a Q8.8 tap is an arithmetic right shift and an xor-add (the
+// Taps: a float tap's term is the input times w = sign * 2^-shift, the tap's
+// exponent move, which is exact when the input is zero or far enough from the
+// exponent limits; there fma(x, w, acc) is the definition's sum acc + term
+// with its one rounding.  A wave holding an input outside that range (tiny,
+// huge, infinite, NaN) rounds the product and then adds for the k steps the
+// input reaches.  A Q8.8 tap is an arithmetic right shift and an xor-add (the
 // -1 that xor-negation leaves per negative tap is folded into the starting
 // value).  Sums run in ascending tap order (starting from +0 in the
 // definition; the first term is taken as is, which can only differ in the
@@ -43,9 +46,9 @@
 // scattered into the k open grad_x accumulators it feeds (outputs j-k+1..j);
 // contributions reach every output in ascending tap order, so the sum order
 // is the definition's.  Output j is complete after step j and is stored.
-// Lanes whose dH is zero skip the scatter (their terms are zeros, which change
-// no bit of an accumulator that starts at +0); lanes whose dH lies outside the
-// exponent-add range (tiny, huge, infinite, NaN) take the exact ldexp taps, on
+// Lanes whose dH has exact tap products (zero included: its terms change no
+// bit of an accumulator that starts at +0) add them with fused multiply-adds;
+// lanes whose dH lies outside that range round each product, then add, on
 // their own lanes only.  grad_x therefore equals the sequential definition
 // bit for bit.
 // grad_w / grad_b are accumulated from exact products: double for float data
@@ -488,7 +491,7 @@ template <int K, int MODE> struct TapsF {
     // the tap's term sign * 2^-shift * v, for any float v
     __device__ __forceinline__ float apply(float v, int i) const { return v * w[i]; }
     // acc + the tap's term in one rounding: the sum acc + apply(v, i) itself
-    // whenever the term is exact (v in the exponent-add range, or zero)
+    // whenever the term is exact (v zero or in the range where it is)
     __device__ __forceinline__ float fma(float v, int i, float acc) const { return __builtin_fmaf(v, w[i], acc); }
 };
 template <int K, int MODE> struct Taps<K, kF32, MODE> : TapsF<K, MODE> {};
@@ -840,7 +843,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         const int32_t so_xlast = (Lr - 1 - jb) * xstep;
 
         PV ring[K];  // x[t] at slot t mod k
-        int slow = 0;  // steps left on the exact path
+        int slow = 0;  // steps left with rounded products
 #pragma unroll
         for (int i = 0; i < K; ++i)
 #pragma unroll
@@ -851,7 +854,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         // (converted in the step that uses them, so no step waits for the
         // loads it issues itself).  Every load is issued before any value is
         // looked at: an item starts after one memory round trip.  A halo input
-        // outside the exponent-add range keeps the exact taps on for the steps
+        // with an inexact tap product keeps the rounded products on for the steps
         // whose window holds it.
         if (j0 > 0) {
 #pragma unroll
@@ -1166,7 +1169,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
                     ph[p] = load_h((rowg - jb) * hstep);
                 px[p] = IO<DT>::template load_raw<NV>(xs, vx, (max(jtop - p - K + 1, jb) - jb) * xstep);
             }
-            bool out = false;  // some input of this lane outside the exponent-add range
+            bool out = false;  // some input of this lane with an inexact tap product
 #pragma unroll
             for (int m = 0; m < K - 1; ++m) {
                 PV v = IO<DT>::template cvt<NV>(rr[m]);

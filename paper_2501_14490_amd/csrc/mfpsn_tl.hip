@@ -16,10 +16,12 @@
 // The arithmetic is the definition's, as in the time-first kernels: taps in
 // ascending order starting from the first one whose input exists (time >= 0),
 // bias last, every add rounded; a float tap is x * 2^-shift with the sign
-// applied after the scaling, as an integer add to the bit pattern when every
-// staged input of the wave lies in the range where that is exact, else as
-// v_ldexp_f32 and a sign flip; a Q8.8 tap is an arithmetic right shift and a
-// negation after it (integer sums: any order gives the same value).
+// applied after the scaling, as a fused multiply-add by sign 2^-shift when
+// every staged input of the wave has an exact product (tl_fwd_kernel: an
+// integer add to the bit pattern), else as a rounded product (v_ldexp_f32 and
+// a sign flip in tl_fwd_kernel) and an add; a Q8.8 tap is an arithmetic right
+// shift and a negation after it (integer sums: any order gives the same
+// value).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
