@@ -263,20 +263,28 @@ template <> struct TlVec4<MFPSN_F32> {
     }
 };
 template <> struct TlVec4<MFPSN_BF16> {
-    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4])
+    static __device__ __forceinline__ uint2 ldraw(const void* p, int64_t e)
     {
-        const uint2 w = *reinterpret_cast<const uint2*>((const uint16_t*)p + e);
+        return *reinterpret_cast<const uint2*>((const uint16_t*)p + e);
+    }
+    static __device__ __forceinline__ void cvt(const uint2& w, float (&v)[4])
+    {
         v[0] = __builtin_bit_cast(float, w.x << 16), v[1] = __builtin_bit_cast(float, w.x & 0xffff0000u);
         v[2] = __builtin_bit_cast(float, w.y << 16), v[3] = __builtin_bit_cast(float, w.y & 0xffff0000u);
     }
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4]) { cvt(ldraw(p, e), v); }
 };
 template <> struct TlVec4<MFPSN_Q8_8> {
-    static __device__ __forceinline__ void ld(const void* p, int64_t e, int32_t (&v)[4])
+    static __device__ __forceinline__ uint2 ldraw(const void* p, int64_t e)
     {
-        const uint2 w = *reinterpret_cast<const uint2*>((const int16_t*)p + e);
+        return *reinterpret_cast<const uint2*>((const int16_t*)p + e);
+    }
+    static __device__ __forceinline__ void cvt(const uint2& w, int32_t (&v)[4])
+    {
         v[0] = (int32_t)(w.x << 16) >> 16, v[1] = (int32_t)w.x >> 16;
         v[2] = (int32_t)(w.y << 16) >> 16, v[3] = (int32_t)w.y >> 16;
     }
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, int32_t (&v)[4]) { cvt(ldraw(p, e), v); }
 };
 
 // The k taps of one lane's channel: for float data w = sign 2^-s, a normal
@@ -421,6 +429,64 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
     return kF && __builtin_amdgcn_ballot_w64(out) != 0;
 }
 
+// Stages x and grad_spikes of a group (as tl_stage does each) with every
+// load of both issued before the first LDS write, so the two wait for one
+// memory round trip together; 2-byte types only (their pending vector loads
+// take two registers per lane and chunk).  Returns tl_stage's flag for x.
+template <int DT>
+__device__ __forceinline__ bool tl_stage_pair(const void* x, const void* gsrc, int64_t gbase, int ncols, int T,
+                                              uint32_t tdiv, bool vec, typename TlTile<DT>::E* xt,
+                                              typename TlTile<DT>::E* gt, float lo, float hi)
+{
+    static_assert(DT != MFPSN_F32, "2-byte storage types only");
+    using V = typename TlIO<DT>::V;
+    constexpr bool kF = DT != MFPSN_Q8_8;
+    if (!(ncols == 64 && vec)) {
+        const bool out = tl_stage<DT>(x, gbase, ncols, T, tdiv, vec, xt, lo, hi);
+        (void)tl_stage<DT>(gsrc, gbase, ncols, T, tdiv, vec, gt, 0.0f, 0.0f);
+        return out;
+    }
+    const int lane = (int)threadIdx.x & 63;
+    const int nch = 16 * T;  // 4-element chunks of the group
+    uint2 rx[kTlMaxChunks], rg[kTlMaxChunks];  // as loaded, widened where written
+#pragma unroll
+    for (int j = 0; j < kTlMaxChunks; ++j)
+        if (lane + 64 * j < nch)
+            rx[j] = TlVec4<DT>::ldraw(x, gbase + 4 * (lane + 64 * j));
+#pragma unroll
+    for (int j = 0; j < kTlMaxChunks; ++j)
+        if (lane + 64 * j < nch)
+            rg[j] = TlVec4<DT>::ldraw(gsrc, gbase + 4 * (lane + 64 * j));
+    bool out = false;
+#pragma unroll
+    for (int j = 0; j < kTlMaxChunks; ++j)
+        if (lane + 64 * j < nch) {
+            V v[4];
+            TlVec4<DT>::cvt(rx[j], v);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e = 4 * (lane + 64 * j) + q;
+                const int c = tl_col_of(e, T, tdiv);
+                xt[(e - c * T) * TlTile<DT>::kRow + c] = TlTile<DT>::put(v[q]);
+                if constexpr (kF)
+                    out = out | !tl_tap_exact(v[q], lo, hi);
+            }
+        }
+#pragma unroll
+    for (int j = 0; j < kTlMaxChunks; ++j)
+        if (lane + 64 * j < nch) {
+            V v[4];
+            TlVec4<DT>::cvt(rg[j], v);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e = 4 * (lane + 64 * j) + q;
+                const int c = tl_col_of(e, T, tdiv);
+                gt[(e - c * T) * TlTile<DT>::kRow + c] = TlTile<DT>::put(v[q]);
+            }
+        }
+    return kF && __builtin_amdgcn_ballot_w64(out) != 0;
+}
+
 // Short columns (T <= kTlColsMaxT): one wave per group of 64 columns,
 // lane = column.  The group's inputs, 64 T contiguous elements, are read with
 // coalesced loads and written transposed into LDS, one row of 64 columns per
@@ -447,8 +513,8 @@ __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
     const int64_t gbase = col0 * T;
     typename Tile::E* xt = reinterpret_cast<typename Tile::E*>(tl_lds);
     uint8_t* st = reinterpret_cast<uint8_t*>(tl_lds) + ((tl_tile_bytes<DT>(T) + 15) & ~(size_t)15);
-    const bool slow = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
-
+    // the lane's taps and bias first: their loads then wait with the
+    // staging's instead of after it
     const int64_t col = col0 + (lane < ncols ? lane : 0);
     const int c = (int)((col / a.S) % a.C);
     TlLaneTaps<DT, K> taps;
@@ -460,6 +526,7 @@ __global__ __launch_bounds__(64) void tl_cols_kernel(TlArgs a)
     } else {
         bias = ((const int32_t*)a.bias)[c];
     }
+    const bool slow = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
     wave_lds_sync();
 
     const int d = a.d;
@@ -583,9 +650,8 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     const int64_t gbase = col0 * T;
     E* xt = reinterpret_cast<E*>(tl_lds);  // x
     E* gt = xt + T * kRow;                 // grad_spikes, then grad_x (bf16: its rounded bits)
-    const bool slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
-    (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
-
+    // the lane's taps and bias first: their loads then wait with the
+    // staging's instead of after it
     const int64_t col = col0 + (lane < ncols ? lane : 0);
     const int c = (int)((col / a.S) % a.C);
     TlLaneTaps<DT, K> taps;
@@ -596,6 +662,13 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
         bias = b == 0.0f ? 0.0f : b;  // a zero bias is added as +0
     } else {
         bias = ((const int32_t*)a.bias)[c];
+    }
+    bool slow_x;
+    if constexpr (DT == MFPSN_F32) {
+        slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
+        (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
+    } else {
+        slow_x = tl_stage_pair<DT>(a.x, a.g, gbase, ncols, T, a.tdiv, a.vec_x, xt, gt, a.fast_lo, a.fast_hi);
     }
     Surrogate sg;
     sg.init(a.sg, a.alpha);
