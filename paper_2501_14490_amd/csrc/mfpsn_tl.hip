@@ -408,7 +408,7 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
         if constexpr (kF)
             out = out | !tl_tap_exact(v, lo, hi);
     };
-    if (ncols == 64 && vec) {
+    if (ncols == 64 && vec && DT == MFPSN_F32) {
         const int nch = 16 * T;  // 4-element chunks of the group
         V v[kTlMaxChunks][4];
 #pragma unroll
@@ -422,6 +422,26 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
                 for (int q = 0; q < 4; ++q)
                     put(4 * (lane + 64 * j) + q, v[j][q]);
             }
+    } else if (ncols == 64 && vec) {
+        if constexpr (DT != MFPSN_F32) {
+            // 2-byte types: the chunks stay as loaded (two registers each)
+            // and are widened where they are written
+            const int nch = 16 * T;
+            uint2 w[kTlMaxChunks];
+#pragma unroll
+            for (int j = 0; j < kTlMaxChunks; ++j)
+                if (lane + 64 * j < nch)
+                    w[j] = TlVec4<DT>::ldraw(src, gbase + 4 * (lane + 64 * j));
+#pragma unroll
+            for (int j = 0; j < kTlMaxChunks; ++j)
+                if (lane + 64 * j < nch) {
+                    V v[4];
+                    TlVec4<DT>::cvt(w[j], v);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        put(4 * (lane + 64 * j) + q, v[q]);
+                }
+        }
     } else {
         for (int e = lane; e < ncols * T; e += 64)
             put(e, TlIO<DT>::ld(src, gbase + e));
