@@ -256,11 +256,15 @@ typedef uint32_t U32x4 __attribute__((ext_vector_type(4)));
 // Four consecutive stored elements (one vector load)
 template <int DT> struct TlVec4;
 template <> struct TlVec4<MFPSN_F32> {
-    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4])
+    static __device__ __forceinline__ float4 ldraw(const void* p, int64_t e)
     {
-        const float4 w = *reinterpret_cast<const float4*>((const float*)p + e);
+        return *reinterpret_cast<const float4*>((const float*)p + e);
+    }
+    static __device__ __forceinline__ void cvt(const float4& w, float (&v)[4])
+    {
         v[0] = w.x, v[1] = w.y, v[2] = w.z, v[3] = w.w;
     }
+    static __device__ __forceinline__ void ld(const void* p, int64_t e, float (&v)[4]) { cvt(ldraw(p, e), v); }
 };
 template <> struct TlVec4<MFPSN_BF16> {
     static __device__ __forceinline__ uint2 ldraw(const void* p, int64_t e)
@@ -451,35 +455,37 @@ __device__ __forceinline__ bool tl_stage(const void* src, int64_t gbase, int nco
 
 // Stages x and grad_spikes of a group (as tl_stage does each) with every
 // load of both issued before the first LDS write, so the two wait for one
-// memory round trip together; 2-byte types only (their pending vector loads
-// take two registers per lane and chunk).  Returns tl_stage's flag for x.
-template <int DT>
+// memory round trip together.  The pending vector loads take two registers
+// per lane and chunk for 2-byte types and four for f32, which the callers
+// afford only up to NCH chunks per lane (T <= 4 NCH).  Returns tl_stage's
+// flag for x.
+template <int DT, int NCH>
 __device__ __forceinline__ bool tl_stage_pair(const void* x, const void* gsrc, int64_t gbase, int ncols, int T,
                                               uint32_t tdiv, bool vec, typename TlTile<DT>::E* xt,
                                               typename TlTile<DT>::E* gt, float lo, float hi)
 {
-    static_assert(DT != MFPSN_F32, "2-byte storage types only");
     using V = typename TlIO<DT>::V;
+    using R = decltype(TlVec4<DT>::ldraw(nullptr, 0));
     constexpr bool kF = DT != MFPSN_Q8_8;
-    if (!(ncols == 64 && vec)) {
+    if (!(ncols == 64 && vec) || T > 4 * NCH) {
         const bool out = tl_stage<DT>(x, gbase, ncols, T, tdiv, vec, xt, lo, hi);
         (void)tl_stage<DT>(gsrc, gbase, ncols, T, tdiv, vec, gt, 0.0f, 0.0f);
         return out;
     }
     const int lane = (int)threadIdx.x & 63;
     const int nch = 16 * T;  // 4-element chunks of the group
-    uint2 rx[kTlMaxChunks], rg[kTlMaxChunks];  // as loaded, widened where written
+    R rx[NCH], rg[NCH];  // as loaded, widened where written
 #pragma unroll
-    for (int j = 0; j < kTlMaxChunks; ++j)
+    for (int j = 0; j < NCH; ++j)
         if (lane + 64 * j < nch)
             rx[j] = TlVec4<DT>::ldraw(x, gbase + 4 * (lane + 64 * j));
 #pragma unroll
-    for (int j = 0; j < kTlMaxChunks; ++j)
+    for (int j = 0; j < NCH; ++j)
         if (lane + 64 * j < nch)
             rg[j] = TlVec4<DT>::ldraw(gsrc, gbase + 4 * (lane + 64 * j));
     bool out = false;
 #pragma unroll
-    for (int j = 0; j < kTlMaxChunks; ++j)
+    for (int j = 0; j < NCH; ++j)
         if (lane + 64 * j < nch) {
             V v[4];
             TlVec4<DT>::cvt(rx[j], v);
@@ -493,7 +499,7 @@ __device__ __forceinline__ bool tl_stage_pair(const void* x, const void* gsrc, i
             }
         }
 #pragma unroll
-    for (int j = 0; j < kTlMaxChunks; ++j)
+    for (int j = 0; j < NCH; ++j)
         if (lane + 64 * j < nch) {
             V v[4];
             TlVec4<DT>::cvt(rg[j], v);
@@ -683,13 +689,9 @@ __global__ __launch_bounds__(64) void tl_cols_bwd_kernel(TlBwdArgs a)
     } else {
         bias = ((const int32_t*)a.bias)[c];
     }
-    bool slow_x;
-    if constexpr (DT == MFPSN_F32) {
-        slow_x = tl_stage<DT>(a.x, gbase, ncols, T, a.tdiv, a.vec_x, xt, a.fast_lo, a.fast_hi);
-        (void)tl_stage<DT>(a.g, gbase, ncols, T, a.tdiv, a.vec_x, gt, 0.0f, 0.0f);
-    } else {
-        slow_x = tl_stage_pair<DT>(a.x, a.g, gbase, ncols, T, a.tdiv, a.vec_x, xt, gt, a.fast_lo, a.fast_hi);
-    }
+    // (f32 pairs up to T = 32: eight chunks per lane and array)
+    const bool slow_x = tl_stage_pair<DT, DT == MFPSN_F32 ? kTlMaxChunks / 2 : kTlMaxChunks>(
+        a.x, a.g, gbase, ncols, T, a.tdiv, a.vec_x, xt, gt, a.fast_lo, a.fast_hi);
     Surrogate sg;
     sg.init(a.sg, a.alpha);
     wave_lds_sync();
